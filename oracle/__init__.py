@@ -1,0 +1,278 @@
+"""Plain, slow CPU oracle for Kernel Quantization (KQ): TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the HIP library
+(``paper_2003_05148_amd``) and never imports it.
+
+What each function follows in the paper:
+
+* ``assign`` / ``update`` / ``distortion`` / ``fit`` -- kernel-level
+  quantization, Sec. 3.1, Eq. (1): plain Lloyd k-means over the n = p q kernels
+  of a layer, each a vector of omega^2 = 9 values (C loops in ``kq_oracle.c``).
+* ``cbq_uniform`` / ``cbq_wkmeans`` -- kernel codebook quantization, Sec. 3.2:
+  6-bit quantization of every scalar of a layer's codebook by k-means over those
+  scalars, weighted by how often each codebook entry is used.
+* ``pack_bits`` -- the n * ceil(log2 k)-bit index stream counted by Eq. (4).
+* ``reconstruct`` -- test-time recovery of the weight tensor from the codebook
+  and the indices (end of Sec. 3.2).
+* ``storage_bits`` / ``compression_ratio`` / ``bits_per_param`` -- Eq. (4),
+  Eq. (6) and Eq. (7).
+
+Readings of points the paper leaves open are stated at each function.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kq_oracle.c")
+_LIB = os.path.join(_HERE, "libkq_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the C part of the oracle (plain loops, no FP contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-shared", "-fPIC",
+                        _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        I64, I = ctypes.c_int64, ctypes.c_int
+        lib.kqo_assign.argtypes = [P, I64, I, P, I, P, P, P, P, P]
+        lib.kqo_assign.restype = I
+        lib.kqo_distortion.argtypes = [P, I64, I, P, P]
+        lib.kqo_distortion.restype = ctypes.c_double
+        lib.kqo_update.argtypes = [P, I64, I, P, I, P, P, P]
+        lib.kqo_update.restype = I
+        lib.kqo_fit.argtypes = [P, I64, I, I, P, I, P, P, P, P]
+        lib.kqo_fit.restype = I
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f32(a, shape_last=None):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if shape_last is not None and (a.ndim != 2 or a.shape[1] != shape_last):
+        raise ValueError("expected [*, %d] array" % shape_last)
+    return a
+
+
+# ---- Sec. 3.1: kernel-level quantization (Lloyd k-means, Eq. 1) ----------------------
+
+def assign(X, C):
+    """Nearest codebook entry of every kernel.
+
+    Returns a dict with
+      idx   int32 [n]: decision on fp32 squared distances, ties to the lowest index
+      d32   f32  [n]: that fp32 distance
+      idx64 int32 [n]: decision on fp64 squared distances
+      d1,d2 f64  [n]: best and second-best fp64 squared distances
+    """
+    X = _f32(X)
+    C = _f32(C)
+    n, dim = X.shape
+    k = C.shape[0]
+    out = dict(idx=np.empty(n, np.int32), d32=np.empty(n, np.float32), idx64=np.empty(n, np.int32),
+               d1=np.empty(n, np.float64), d2=np.empty(n, np.float64))
+    rc = _load().kqo_assign(_ptr(X), n, dim, _ptr(C), k, _ptr(out["idx"]), _ptr(out["d32"]),
+                            _ptr(out["idx64"]), _ptr(out["d1"]), _ptr(out["d2"]))
+    if rc:
+        raise ValueError("kqo_assign failed")
+    return out
+
+
+def distortion(X, C, idx) -> float:
+    """Eq. (1) objective of an assignment, fp64, summed in ascending kernel order."""
+    X = _f32(X)
+    C = _f32(C)
+    idx = np.ascontiguousarray(idx, np.int32)
+    return float(_load().kqo_distortion(_ptr(X), X.shape[0], X.shape[1], _ptr(C), _ptr(idx)))
+
+
+def update(X, idx, C_old):
+    """Each entry becomes the mean of its kernel set; an empty set keeps the old entry.
+
+    Returns (C_new float32 [k, dim], counts int32 [k]).
+    """
+    X = _f32(X)
+    C_old = _f32(C_old)
+    idx = np.ascontiguousarray(idx, np.int32)
+    k, dim = C_old.shape
+    C_new = np.empty_like(C_old)
+    counts = np.empty(k, np.int32)
+    rc = _load().kqo_update(_ptr(X), X.shape[0], dim, _ptr(idx), k, _ptr(C_old), _ptr(C_new), _ptr(counts))
+    if rc:
+        raise ValueError("kqo_update failed (index out of range)")
+    return C_new, counts
+
+
+def fit(X, C_init, iters: int):
+    """`iters` Lloyd rounds (assign, update) then a final assignment.
+
+    Returns dict(C [k,dim] after `iters` updates, idx [n] final assignment,
+    counts [k] of the final assignment, J [iters+1] distortion of each assignment).
+    """
+    X = _f32(X)
+    C_init = _f32(C_init)
+    n, dim = X.shape
+    k = C_init.shape[0]
+    C = np.empty_like(C_init)
+    idx = np.empty(n, np.int32)
+    counts = np.empty(k, np.int32)
+    J = np.empty(iters + 1, np.float64)
+    rc = _load().kqo_fit(_ptr(X), n, dim, k, _ptr(C_init), iters, _ptr(C), _ptr(idx), _ptr(counts), _ptr(J))
+    if rc:
+        raise ValueError("kqo_fit failed")
+    return dict(C=C, idx=idx, counts=counts, J=J)
+
+
+# ---- Sec. 3.2: kernel codebook quantization -------------------------------------------
+
+def _nearest_level(v32: np.ndarray, levels32: np.ndarray) -> np.ndarray:
+    """Smallest q minimising |v - L_q|, both widened exactly to fp64."""
+    diff = np.abs(v32.astype(np.float64)[:, None] - levels32.astype(np.float64)[None, :])
+    return np.argmin(diff, axis=1).astype(np.uint8)
+
+
+def uniform_levels(lo: float, hi: float, bits: int) -> np.ndarray:
+    """2^bits levels evenly spaced on [lo, hi]: L_q = fp32(lo + q * delta),
+    delta = (hi - lo) / (2^bits - 1); every operation rounded separately in fp64."""
+    L = 1 << bits
+    delta = (float(hi) - float(lo)) / (L - 1)
+    return np.array([float(lo) + q * delta for q in range(L)], dtype=np.float64).astype(np.float32)
+
+
+def cbq_uniform(C, bits: int = 6):
+    """Uniform-grid quantization of all scalars of one codebook.
+
+    Returns (codes uint8 [k*dim], levels float32 [2^bits], C_hat float32 [k, dim]).
+    A constant codebook gives delta = 0 and every code 0.
+    """
+    C = _f32(C)
+    v = C.reshape(-1)
+    levels = uniform_levels(float(v.min()), float(v.max()), bits)
+    codes = _nearest_level(v, levels)
+    return codes, levels, levels[codes].reshape(C.shape)
+
+
+def _exact_scaled(v32: np.ndarray) -> list:
+    """v * 2^149 as exact Python integers (every fp32 value is a multiple of 2^-149)."""
+    out = []
+    for x in v32.astype(np.float64).tolist():
+        num, den = x.as_integer_ratio()
+        out.append(num * ((1 << 149) // den))
+    return out
+
+
+def cbq_wkmeans(C, weights, bits: int = 6, iters: int = 30):
+    """Weighted 1-D k-means over all scalars of one codebook (Sec. 3.2).
+
+    Scalar r = j*dim + d carries the weight of its entry j (its appearance
+    count).  Initial levels: the uniform grid of ``cbq_uniform``.  Each round:
+      W_q = sum of the weights of the scalars coded q (exact integer);
+      N_q = sum of weight * value over those scalars, computed exactly and
+            rounded once to fp64;
+      L_q = fp32(N_q / W_q) (fp64 division) when W_q > 0, else L_q is kept;
+      codes = nearest level (smallest q on ties).
+    Stops after `iters` rounds or as soon as a round changes no code.
+
+    Returns (codes uint8 [k*dim], levels float32 [2^bits], C_hat float32 [k, dim], rounds).
+    """
+    C = _f32(C)
+    k, dim = C.shape
+    w = np.repeat(np.asarray(weights, dtype=np.int64), dim)
+    if w.shape[0] != k * dim:
+        raise ValueError("weights must have one entry per codebook row")
+    v = C.reshape(-1)
+    codes, levels, _ = cbq_uniform(C, bits)
+    vint = _exact_scaled(v)
+    wl = w.tolist()
+    L = 1 << bits
+    rounds = 0
+    for _ in range(iters):
+        rounds += 1
+        N = [0] * L
+        W = [0] * L
+        for r, q in enumerate(codes.tolist()):
+            N[q] += wl[r] * vint[r]
+            W[q] += wl[r]
+        new_levels = levels.copy()
+        for q in range(L):
+            if W[q] > 0:
+                Nq = N[q] / (1 << 149)          # exact integer ratio, correctly rounded to fp64
+                new_levels[q] = np.float32(Nq / float(W[q]))
+        new_codes = _nearest_level(v, new_levels)
+        changed = bool(np.any(new_codes != codes))
+        levels, codes = new_levels, new_codes
+        if not changed:
+            break
+    return codes, levels, levels[codes].reshape(C.shape), rounds
+
+
+# ---- Eq. (4): the packed index stream, and test-time reconstruction ---------------------
+
+def index_bits(k: int) -> int:
+    """ceil(log2 k) bits per index (Eq. 4); 0 for k == 1."""
+    return 0 if k <= 1 else int(math.ceil(math.log2(k)))
+
+
+def pack_bits(values, bits: int) -> np.ndarray:
+    """Concatenate `bits`-bit values LSB-first: bit t of value i is stream bit i*bits + t,
+    stream bit s is bit (s % 8) of byte s // 8.  Length ceil(n * bits / 8) bytes."""
+    v = np.asarray(values, dtype=np.uint64)
+    if bits == 0 or v.size == 0:
+        return np.zeros(0, np.uint8)
+    bitmat = ((v[:, None] >> np.arange(bits, dtype=np.uint64)[None, :]) & np.uint64(1)).astype(np.uint8)
+    return np.packbits(bitmat.reshape(-1), bitorder="little")
+
+
+def unpack_bits(stream, count: int, bits: int) -> np.ndarray:
+    s = np.unpackbits(np.asarray(stream, np.uint8), bitorder="little")[: count * bits]
+    mat = s.reshape(count, bits).astype(np.int64)
+    return (mat << np.arange(bits, dtype=np.int64)[None, :]).sum(axis=1).astype(np.int32)
+
+
+def reconstruct(idx, C):
+    """W_hat[i] = C[idx[i]] (the codebook may be the 6-bit dequantised one)."""
+    return np.ascontiguousarray(np.asarray(C, np.float32)[np.asarray(idx, np.int64)])
+
+
+# ---- Eq. (4), (6), (7): storage accounting ----------------------------------------------
+
+def storage_bits(n: int, k: int, bc: int, dim: int = 9) -> int:
+    """B = k * omega^2 * b_c + n * ceil(log2 k)   (Eq. 4)."""
+    return k * dim * bc + n * index_bits(k)
+
+
+def compression_ratio(n: int, k: int, bc: int, dim: int = 9, b_fp: int = 32) -> float:
+    """C_KQ = n * omega^2 * b_FP / B   (Eq. 6)."""
+    return n * dim * b_fp / storage_bits(n, k, bc, dim)
+
+
+def bits_per_param(n: int, k: int, bc: int, dim: int = 9) -> float:
+    """beta = B / (n * omega^2)   (Eq. 7)."""
+    return storage_bits(n, k, bc, dim) / (n * dim)
+
+
+def conventional_ratio(n: int, u: int, b1: int, dim: int = 9, b_fp: int = 32) -> float:
+    """C_con = n omega^2 b_FP / (u b_1 + n omega^2 ceil(log2 u))   (Eq. 5)."""
+    return n * dim * b_fp / (u * b1 + n * dim * index_bits(u))

@@ -1,0 +1,255 @@
+/*
+ * kq.h -- C ABI of the MI355X (gfx950) library for the hot path of Kernel
+ * Quantization (Yu, Shi, Huang, Yu: "Kernel Quantization for Efficient Network
+ * Compression").
+ *
+ * The operations:
+ *   kq_assign            Sec. 3.1, Eq. (1): nearest codebook entry of every 3x3 kernel.
+ *   kq_update            Sec. 3.1, Eq. (1): every entry becomes the mean of its kernel set S_i.
+ *   kq_fit_layer         Sec. 3.1: Lloyd k-means on one layer (the "k-means in Eq. (1)"
+ *                        step of Algorithm 1), a fixed number of rounds then a final assignment.
+ *   kq_fit_stack         the same for many layers at once (Sec. 3.1 quantizes layer by layer;
+ *                        layers are independent, so one launch serves all of them).
+ *   kq_quantize_codebook Sec. 3.2: 6-bit quantization of all scalars of a layer's codebook,
+ *                        k-means weighted by how often each entry is used.
+ *   kq_pack_bits         Eq. (4): the n * ceil(log2 k)-bit index stream.
+ *   kq_reconstruct       end of Sec. 3.2: recover the weight tensor from codebook + indices.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - dim is omega^2 and must be 9 (the paper quantizes 3x3 kernels only, Sec. 4.1);
+ *    anything else returns KQ_ERR_UNSUPPORTED.
+ *  - Kernels X are n rows of 9 fp32 values, row-major; for an OIHW weight tensor
+ *    this is the tensor itself (kernel i = o * C_in + c).  Codebooks C are k rows of 9.
+ *  - Pointers named device are device memory (hipMalloc / torch.cuda); pointers named
+ *    host are host memory.  Every buffer belongs to the caller.  The library never
+ *    allocates memory and keeps no global state.
+ *  - stream is a hipStream_t (NULL = the null stream).  Device calls only enqueue work
+ *    on that stream and return; outputs are valid once the stream has been synchronised.
+ *  - Arguments are checked on the host before anything is enqueued.  On an error
+ *    nothing is enqueued and outputs are untouched.  No HIP call is made before the
+ *    checks pass, so argument errors are reported without a GPU.
+ *  - KQ_ERR_HIP: a HIP launch failed; outputs are unspecified.
+ *  - workspace: device scratch of at least the size the matching *_workspace_bytes
+ *    query returns, 256-byte aligned.  It must be all-zero before its first use
+ *    (kq_workspace_init does that); every call leaves it all-zero again when its work
+ *    on the stream completes.  Calls that share a workspace must be ordered on one
+ *    stream.
+ *  - Kernel values must be finite with |x| < 32 for kq_update / kq_fit_* (the member
+ *    sums are exact 64-bit fixed-point sums, see kq_update).  Real CNN weights are
+ *    orders of magnitude smaller.
+ */
+#ifndef KQ_H
+#define KQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kq_status {
+    KQ_OK = 0,
+    KQ_ERR_ARG = 1,          /* null pointer, bad size, misaligned pointer */
+    KQ_ERR_UNSUPPORTED = 2,  /* dim != 9, k above KQ_MAX_K, bits outside 1..16 */
+    KQ_ERR_WORKSPACE = 3,    /* workspace missing, too small or misaligned */
+    KQ_ERR_RANGE = 4,        /* reserved: input outside the supported value range */
+    KQ_ERR_HIP = 5           /* a HIP runtime call failed */
+} kq_status;
+
+#define KQ_DIM 9
+#define KQ_MAX_K 65536
+#define KQ_MAX_STACK 16      /* layers per launch; longer stacks are split by the library */
+
+/* codebook-quantization modes (Sec. 3.2) */
+#define KQ_CBQ_WKMEANS 0     /* weighted k-means over the codebook scalars (the paper's method) */
+#define KQ_CBQ_UNIFORM 1     /* the uniform grid that initialises it, without iterations */
+
+/* workspace queries: op codes */
+#define KQ_OP_ASSIGN 0
+#define KQ_OP_UPDATE 1
+#define KQ_OP_FIT 2
+#define KQ_OP_SQ_ERROR 3     /* n = element count, k = 1 */
+
+/* flags */
+#define KQ_F_COUNTS_ONLY 1u  /* kq_update / kq_update_stack: write counts only, leave C untouched */
+
+/* One layer of a stack.  All pointers are device pointers. */
+typedef struct kq_layer {
+    const float* X;      /* [n][9] kernels */
+    int64_t n;           /* number of kernels, 1 <= n < 2^31 */
+    int32_t k;           /* codebook size, 1 <= k <= min(n, KQ_MAX_K) for fits */
+    float* C;            /* [k][9] codebook: state in, new state out */
+    int32_t* idx;        /* [n] index of the nearest entry */
+    float* best_d;       /* [n] fp32 squared distance to that entry, or NULL */
+    int32_t* counts;     /* [k] kernels per entry (final assignment), or NULL for assign */
+    double* distortion;  /* distortion output(s), or NULL (see each call) */
+} kq_layer;
+
+/* Human-readable name of a status code (static string). */
+const char* kq_status_string(kq_status s);
+
+/* Library ABI version (incremented when a signature changes). */
+int32_t kq_abi_version(void);
+
+/*
+ * Workspace bytes for one layer of n kernels and k entries for op (KQ_OP_*).
+ * Returns 0 for invalid sizes.
+ */
+size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k);
+
+/* Workspace bytes for a stack call (kq_assign_stack / kq_update_stack / kq_fit_stack). */
+size_t kq_stack_workspace_bytes(const kq_layer* layers /* host [n_layers] */, int32_t n_layers);
+
+/* Zero-fill `bytes` of device workspace on `stream` (a fill kernel, no memset node). */
+kq_status kq_workspace_init(void* ws, size_t bytes, void* stream);
+
+/*
+ * kq_assign -- Sec. 3.1, Eq. (1), the assignment half of a Lloyd round.
+ *
+ *   idx[i]    = the entry j minimising the fp32 squared distance
+ *               d(x_i, c_j) = sum_d (x_id - c_jd)^2, evaluated term by term in
+ *               dimension order as t = x - c, acc = fma(t, t, acc); ties go to the
+ *               lowest j.  The result is exactly this argmin.  (Internally the
+ *               distances are screened with matrix-core dot products and every
+ *               kernel whose winner could be in doubt is rescored in that form.)
+ *   best_d[i] = that fp32 distance (device [n], may be NULL).
+ *   *distortion = sum_i best_d[i] in fp64 in a fixed order (device scalar, may be NULL).
+ *
+ *   X device [n][9] fp32, 4-byte aligned; C device [k][9] fp32; idx device [n] int32.
+ *   1 <= n < 2^31, 1 <= k <= KQ_MAX_K (k > n is allowed).
+ */
+kq_status kq_assign(const float* X, int64_t n, int32_t dim, const float* C, int32_t k,
+                    int32_t* idx, float* best_d, double* distortion, uint32_t flags,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kq_update -- Sec. 3.1, Eq. (1), the update half of a Lloyd round.
+ *
+ *   counts[j] = |S_j| = #{i : idx[i] == j}
+ *   C_new[j]  = mean of the kernels in S_j, or C_old[j] when S_j is empty.
+ *   The member sums are exact integer sums of q(x) = rint(x * 2^s), s = 57 -
+ *   ceil(log2 n), so they do not depend on summation order; the mean is
+ *   fp32( (double(sum) * 2^-s) / |S_j| ).
+ *
+ *   X device [n][9]; idx device [n] values in [0, k) (out-of-range indices are
+ *   ignored); C_old, C_new device [k][9] (may alias); counts device [k] or NULL.
+ *   flags: 0, or KQ_F_COUNTS_ONLY to compute only the counts (C_new untouched).
+ */
+kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
+                    const float* C_old, float* C_new, int32_t* counts, uint32_t flags,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kq_fit_layer -- Lloyd k-means on one layer (Sec. 3.1, Eq. 1).
+ *
+ *   C := C_init; repeat iters times { idx := assign(C); C := update(idx, C) };
+ *   then a final idx := assign(C).
+ *   C [k][9] ends as the codebook after `iters` updates, idx [n] the final
+ *   assignment, counts [k] (may be NULL) its member counts, distortion
+ *   device [iters+1] (may be NULL) the distortion of every assignment.
+ *   Requires 1 <= k <= n.  C_init may equal C.
+ */
+kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
+                       int32_t iters, float* C, int32_t* idx, int32_t* counts, double* distortion,
+                       uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Stack versions: one launch per step for up to KQ_MAX_STACK layers (more are split).
+ *   kq_assign_stack: assigns every layer against its C; writes idx, best_d (if set) and
+ *                    distortion[dist_slot] (if distortion is set).
+ *   kq_update_stack: updates every C in place from its idx; writes counts (if set).
+ *   kq_fit_stack:    kq_fit_layer on every layer (C in place, distortion [iters+1]).
+ *   layers is a host array; the pointers in it are device pointers.
+ */
+kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags,
+                          void* ws, size_t ws_bytes, void* stream);
+kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, uint32_t flags,
+                          void* ws, size_t ws_bytes, void* stream);
+kq_status kq_fit_stack(const kq_layer* layers, int32_t n_layers, int32_t iters, uint32_t flags,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kq_quantize_codebook -- Sec. 3.2, 6-bit quantization of one layer's codebook.
+ *
+ *   The k*9 scalars v_r (r = 9 j + d) are coded with 2^bits fp32 levels.
+ *   Grid: lo = min v, hi = max v, delta = (hi - lo) / (2^bits - 1) in fp64,
+ *         L_q = fp32(lo + q * delta) (fp64 multiply, fp64 add).
+ *   code_r = the smallest q minimising |v_r - L_q| (fp64).
+ *   KQ_CBQ_UNIFORM stops there.  KQ_CBQ_WKMEANS then runs up to `iters` rounds of
+ *   weighted 1-D Lloyd, scalar r carrying weight weights[r / 9] (the appearance
+ *   count of its entry; NULL = every weight 1):
+ *     W_q = sum of weights coded q, N_q = exact sum of weight * value over them
+ *     rounded once to fp64, L_q = fp32(N_q / W_q) if W_q > 0 (else kept);
+ *     recompute the codes; stop early when no code changes.
+ *   Every step is exact or correctly rounded, so the result does not depend on
+ *   the order of the work.
+ *
+ *   C device [k][9]; weights device [k] int32 >= 0 or NULL; codes device [k*9] uint8;
+ *   levels device [2^bits] fp32; C_hat device [k][9] (= levels[codes], may be NULL).
+ *   1 <= bits <= 8 here; 1 <= k <= KQ_MAX_K.
+ */
+kq_status kq_quantize_codebook(const float* C, int32_t k, int32_t dim, const int32_t* weights,
+                               int32_t bits, int32_t mode, int32_t iters, uint8_t* codes,
+                               float* levels, float* C_hat, void* stream);
+
+/* One layer for kq_quantize_codebook_stack (device pointers). */
+typedef struct kq_cbq_layer {
+    const float* C;          /* [k][9] */
+    int32_t k;
+    const int32_t* weights;  /* [k] or NULL */
+    uint8_t* codes;          /* [k*9] */
+    float* levels;           /* [2^bits] */
+    float* C_hat;            /* [k][9] or NULL */
+} kq_cbq_layer;
+
+/* kq_quantize_codebook on every layer of a host array, one workgroup per layer. */
+kq_status kq_quantize_codebook_stack(const kq_cbq_layer* layers, int32_t n_layers, int32_t bits,
+                                     int32_t mode, int32_t iters, void* stream);
+
+/*
+ * kq_pack_bits -- the index stream of Eq. (4).
+ *   Value i (its low `bits` bits) occupies stream bits [i*bits, (i+1)*bits), least
+ *   significant bit first; stream bit s is bit (s % 8) of byte s / 8.  Writes exactly
+ *   ceil(count * bits / 8) bytes; unused high bits of the last byte are zero.
+ *   values device [count], elem_bytes 1 (uint8), 2 (uint16) or 4 (int32);
+ *   out device, 4-byte aligned.  0 <= bits <= 16 (bits = 0 writes nothing).
+ */
+kq_status kq_pack_bits(const void* values, int32_t elem_bytes, int64_t count, int32_t bits,
+                       uint8_t* out, void* stream);
+
+/* Inverse of kq_pack_bits: values device [count] int32. */
+kq_status kq_unpack_bits(const uint8_t* in, int64_t count, int32_t bits, int32_t* values, void* stream);
+
+/*
+ * kq_reconstruct -- end of Sec. 3.2: W_hat[i][d] = C[idx[i]][d].
+ *   Pass the 6-bit dequantised codebook (C_hat of kq_quantize_codebook) for K+C.
+ *   idx device [n] values in [0, k) (others give zeros); C device [k][9];
+ *   W_hat device [n][9], 16-byte aligned.
+ */
+kq_status kq_reconstruct(const int32_t* idx, int64_t n, const float* C, int32_t k, int32_t dim,
+                         float* W_hat, void* stream);
+
+/*
+ * kq_reconstruct_packed -- the same from the stored form: indices read from a
+ * kq_pack_bits stream of `bits` = ceil(log2 k) bits each.
+ */
+kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, const float* C,
+                                int32_t k, int32_t dim, float* W_hat, void* stream);
+
+/*
+ * kq_sq_error -- the l2 reconstruction error the paper reports (Sec. 4.2.1):
+ *   *out = sum_i (double(A[i]) - double(B[i]))^2 over `count` fp32 values, in fp64,
+ *   in a fixed order (the same bits on every run).
+ *   A, B device [count] fp32, 4-byte aligned; out device fp64 scalar;
+ *   workspace of kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1) bytes.
+ */
+kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out,
+                      void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KQ_H */

@@ -1,0 +1,362 @@
+"""MI355X (gfx950) hot path of Kernel Quantization (Yu et al., "Kernel Quantization for
+Efficient Network Compression").
+
+Thin Python binding of ``libkq.so`` (C ABI declared in ``include/kq.h``).  Every
+function here only marshals arguments: it checks tensor devices, dtypes and shapes,
+allocates outputs with torch when the caller gives none, and passes device pointers
+and the current HIP stream to the library, where all the work runs.  There is no
+fallback: without the built library, importing this package raises ImportError.
+
+Entry points (same names as the C ABI):
+  kq_assign, kq_update, kq_fit_layer, kq_assign_stack, kq_update_stack, kq_fit_stack,
+  kq_quantize_codebook, kq_quantize_codebook_stack, kq_pack_bits, kq_unpack_bits,
+  kq_reconstruct, kq_reconstruct_packed.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkq.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                      "(or python paper_2003_05148_amd/_build.py)")
+
+_P = ctypes.c_void_p
+_I32, _I64, _U32, _SZ = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t
+
+
+class KqLayer(ctypes.Structure):
+    _fields_ = [("X", _P), ("n", _I64), ("k", _I32), ("C", _P), ("idx", _P), ("best_d", _P),
+                ("counts", _P), ("distortion", _P)]
+
+
+class KqCbqLayer(ctypes.Structure):
+    _fields_ = [("C", _P), ("k", _I32), ("weights", _P), ("codes", _P), ("levels", _P), ("C_hat", _P)]
+
+
+def _load():
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "kq_status_string": ([_I32], ctypes.c_char_p),
+        "kq_abi_version": ([], _I32),
+        "kq_workspace_bytes": ([_I32, _I64, _I32], _SZ),
+        "kq_stack_workspace_bytes": ([_P, _I32], _SZ),
+        "kq_workspace_init": ([_P, _SZ, _P], _I32),
+        "kq_assign": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
+        "kq_update": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
+        "kq_fit_layer": ([_P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
+        "kq_assign_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
+        "kq_update_stack": ([_P, _I32, _U32, _P, _SZ, _P], _I32),
+        "kq_fit_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
+        "kq_quantize_codebook": ([_P, _I32, _I32, _P, _I32, _I32, _I32, _P, _P, _P, _P], _I32),
+        "kq_quantize_codebook_stack": ([_P, _I32, _I32, _I32, _I32, _P], _I32),
+        "kq_pack_bits": ([_P, _I32, _I64, _I32, _P, _P], _I32),
+        "kq_unpack_bits": ([_P, _I64, _I32, _P, _P], _I32),
+        "kq_reconstruct": ([_P, _I64, _P, _I32, _I32, _P, _P], _I32),
+        "kq_reconstruct_packed": ([_P, _I32, _I64, _P, _I32, _I32, _P, _P], _I32),
+        "kq_sq_error": ([_P, _P, _I64, _P, _P, _SZ, _P], _I32),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+lib = _load()
+
+# constants mirrored from include/kq.h
+KQ_OK, KQ_ERR_ARG, KQ_ERR_UNSUPPORTED, KQ_ERR_WORKSPACE, KQ_ERR_RANGE, KQ_ERR_HIP = range(6)
+KQ_DIM = 9
+KQ_MAX_K = 65536
+KQ_MAX_STACK = 16
+KQ_CBQ_WKMEANS, KQ_CBQ_UNIFORM = 0, 1
+KQ_OP_ASSIGN, KQ_OP_UPDATE, KQ_OP_FIT, KQ_OP_SQ_ERROR = 0, 1, 2, 3
+KQ_F_COUNTS_ONLY = 1
+EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
+            "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
+            "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
+            "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error"]
+
+
+class KqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib.kq_status_string(status).decode()} (status {status})")
+
+
+def _check(status: int, where: str):
+    if status != KQ_OK:
+        raise KqError(status, where)
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dev(t: torch.Tensor, dtype, name: str, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _kernels(X: torch.Tensor, name="X"):
+    if X.dim() == 4:  # an OIHW 3x3 conv weight: kernel i = o * C_in + c
+        if X.shape[2] * X.shape[3] != KQ_DIM:
+            raise ValueError("only 3x3 kernels are supported")
+        X = X.reshape(-1, KQ_DIM)
+    _dev(X, torch.float32, name)
+    if X.dim() != 2 or X.shape[1] != KQ_DIM:
+        raise ValueError(f"{name} must be [n, 9] (or an OIHW 3x3 weight)")
+    return X
+
+
+class Workspace:
+    """A zero-initialised device scratch buffer for the library (grown on demand).
+
+    The library returns it to all-zero after every call, so it can be reused by
+    every call ordered on one stream."""
+
+    def __init__(self, device=None):
+        self.device = torch.device(device if device is not None else "cuda")
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+_workspaces: dict = {}
+
+
+def _ws(device, nbytes):
+    key = torch.device(device).index if torch.device(device).index is not None else torch.cuda.current_device()
+    w = _workspaces.get(key)
+    if w is None:
+        w = _workspaces[key] = Workspace(torch.device("cuda", key))
+    return w.get(nbytes)
+
+
+# ---- Sec. 3.1, Eq. (1) ---------------------------------------------------------------
+
+def kq_assign(X, C, idx=None, best_d=None, distortion=None, workspace=None):
+    """Nearest codebook entry of every kernel (exact fp32 argmin, ties to the lowest
+    index).  Returns (idx int32 [n], best_d float32 [n], distortion float64 [1])."""
+    X = _kernels(X)
+    C = _kernels(C, "C")
+    n, k = X.shape[0], C.shape[0]
+    dev = X.device
+    idx = idx if idx is not None else torch.empty(n, dtype=torch.int32, device=dev)
+    best_d = best_d if best_d is not None else torch.empty(n, dtype=torch.float32, device=dev)
+    distortion = distortion if distortion is not None else torch.empty(1, dtype=torch.float64, device=dev)
+    _dev(idx, torch.int32, "idx", (n,))
+    _dev(best_d, torch.float32, "best_d", (n,))
+    _dev(distortion, torch.float64, "distortion")
+    nb = lib.kq_workspace_bytes(KQ_OP_ASSIGN, n, k)
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_assign(X.data_ptr(), n, KQ_DIM, C.data_ptr(), k, idx.data_ptr(), best_d.data_ptr(),
+                         distortion.data_ptr(), 0, ws.data_ptr(), ws.numel(), _stream(dev)), "kq_assign")
+    return idx, best_d, distortion
+
+
+def kq_update(X, idx, C_old, C_new=None, counts=None, workspace=None, counts_only: bool = False):
+    """Mean of every kernel set (empty sets keep their entry).  Returns (C_new, counts)."""
+    X = _kernels(X)
+    C_old = _kernels(C_old, "C_old")
+    n, k = X.shape[0], C_old.shape[0]
+    dev = X.device
+    _dev(idx, torch.int32, "idx", (n,))
+    C_new = C_new if C_new is not None else torch.empty_like(C_old)
+    counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
+    _dev(C_new, torch.float32, "C_new", (k, KQ_DIM))
+    _dev(counts, torch.int32, "counts", (k,))
+    nb = lib.kq_workspace_bytes(KQ_OP_UPDATE, n, k)
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_update(X.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), C_new.data_ptr(),
+                         counts.data_ptr(), KQ_F_COUNTS_ONLY if counts_only else 0, ws.data_ptr(), ws.numel(),
+                         _stream(dev)), "kq_update")
+    return C_new, counts
+
+
+def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):
+    """`iters` Lloyd rounds then a final assignment.  Returns (C, idx, counts, distortion[iters+1])."""
+    X = _kernels(X)
+    C_init = _kernels(C_init, "C_init")
+    n, k = X.shape[0], C_init.shape[0]
+    dev = X.device
+    C = C if C is not None else torch.empty_like(C_init)
+    idx = idx if idx is not None else torch.empty(n, dtype=torch.int32, device=dev)
+    counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
+    distortion = distortion if distortion is not None else torch.empty(iters + 1, dtype=torch.float64, device=dev)
+    _dev(C, torch.float32, "C", (k, KQ_DIM))
+    _dev(idx, torch.int32, "idx", (n,))
+    _dev(counts, torch.int32, "counts", (k,))
+    _dev(distortion, torch.float64, "distortion", (iters + 1,))
+    nb = lib.kq_workspace_bytes(KQ_OP_FIT, n, k)
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_fit_layer(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, C.data_ptr(), idx.data_ptr(),
+                            counts.data_ptr(), distortion.data_ptr(), 0, ws.data_ptr(), ws.numel(),
+                            _stream(dev)), "kq_fit_layer")
+    return C, idx, counts, distortion
+
+
+class Stack:
+    """Device state of a conv stack for the stack calls: per layer X, C, idx, best_d,
+    counts and a distortion history, plus the C descriptor array and a workspace."""
+
+    def __init__(self, Xs, Cs, iters: int = 0, best_d: bool = False):
+        self.X = [_kernels(x) for x in Xs]
+        self.C = [_kernels(c, "C").clone() for c in Cs]
+        dev = self.X[0].device
+        self.idx = [torch.empty(x.shape[0], dtype=torch.int32, device=dev) for x in self.X]
+        self.best_d = [torch.empty(x.shape[0], dtype=torch.float32, device=dev) for x in self.X] if best_d else None
+        self.counts = [torch.empty(c.shape[0], dtype=torch.int32, device=dev) for c in self.C]
+        self.distortion = [torch.zeros(iters + 1, dtype=torch.float64, device=dev) for _ in self.X]
+        arr = (KqLayer * len(self.X))()
+        for i, (x, c) in enumerate(zip(self.X, self.C)):
+            arr[i] = KqLayer(x.data_ptr(), x.shape[0], c.shape[0], c.data_ptr(), self.idx[i].data_ptr(),
+                             self.best_d[i].data_ptr() if best_d else None, self.counts[i].data_ptr(),
+                             self.distortion[i].data_ptr())
+        self.layers = arr
+        self.n_layers = len(self.X)
+        nb = lib.kq_stack_workspace_bytes(ctypes.cast(arr, _P), self.n_layers)
+        if nb == 0:
+            raise ValueError("invalid stack")
+        self.ws = torch.zeros(nb, dtype=torch.uint8, device=dev)
+        self.device = dev
+
+    def set_codebooks(self, Cs):
+        for c, src in zip(self.C, Cs):
+            c.copy_(src)
+
+
+def kq_assign_stack(stack: Stack, dist_slot: int = 0):
+    _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, 0, stack.ws.data_ptr(),
+                               stack.ws.numel(), _stream(stack.device)), "kq_assign_stack")
+
+
+def kq_update_stack(stack: Stack, counts_only: bool = False):
+    _check(lib.kq_update_stack(ctypes.cast(stack.layers, _P), stack.n_layers, KQ_F_COUNTS_ONLY if counts_only else 0,
+                               stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)), "kq_update_stack")
+
+
+def kq_fit_stack(stack: Stack, iters: int):
+    if stack.distortion[0].numel() < iters + 1:
+        raise ValueError("the stack's distortion history is shorter than iters + 1")
+    _check(lib.kq_fit_stack(ctypes.cast(stack.layers, _P), stack.n_layers, iters, 0, stack.ws.data_ptr(),
+                            stack.ws.numel(), _stream(stack.device)), "kq_fit_stack")
+
+
+# ---- Sec. 3.2 --------------------------------------------------------------------------
+
+def kq_quantize_codebook(C, weights=None, bits: int = 6, mode: int = KQ_CBQ_WKMEANS, iters: int = 30,
+                         codes=None, levels=None, C_hat=None):
+    """6-bit (by default) codebook quantization.  Returns (codes uint8 [k*9], levels [2^bits], C_hat)."""
+    C = _kernels(C, "C")
+    k = C.shape[0]
+    dev = C.device
+    if weights is not None:
+        _dev(weights, torch.int32, "weights", (k,))
+    codes = codes if codes is not None else torch.empty(k * KQ_DIM, dtype=torch.uint8, device=dev)
+    levels = levels if levels is not None else torch.empty(1 << bits, dtype=torch.float32, device=dev)
+    C_hat = C_hat if C_hat is not None else torch.empty_like(C)
+    _check(lib.kq_quantize_codebook(C.data_ptr(), k, KQ_DIM, _ptr(weights), bits, mode, iters, codes.data_ptr(),
+                                    levels.data_ptr(), C_hat.data_ptr(), _stream(dev)), "kq_quantize_codebook")
+    return codes, levels, C_hat
+
+
+def kq_quantize_codebook_stack(Cs, weights, bits: int = 6, mode: int = KQ_CBQ_WKMEANS, iters: int = 30, out=None):
+    """kq_quantize_codebook for a list of codebooks in one launch.
+    Returns a list of (codes, levels, C_hat)."""
+    Cs = [_kernels(c, "C") for c in Cs]
+    dev = Cs[0].device
+    if out is None:
+        out = [(torch.empty(c.shape[0] * KQ_DIM, dtype=torch.uint8, device=dev),
+                torch.empty(1 << bits, dtype=torch.float32, device=dev), torch.empty_like(c)) for c in Cs]
+    arr = (KqCbqLayer * len(Cs))()
+    for i, c in enumerate(Cs):
+        w = weights[i] if weights is not None else None
+        if w is not None:
+            _dev(w, torch.int32, "weights", (c.shape[0],))
+        arr[i] = KqCbqLayer(c.data_ptr(), c.shape[0], _ptr(w), out[i][0].data_ptr(), out[i][1].data_ptr(),
+                            out[i][2].data_ptr())
+    _check(lib.kq_quantize_codebook_stack(ctypes.cast(arr, _P), len(Cs), bits, mode, iters, _stream(dev)),
+           "kq_quantize_codebook_stack")
+    return out
+
+
+# ---- Eq. (4) and test-time reconstruction -------------------------------------------------
+
+def index_bits(k: int) -> int:
+    return 0 if k <= 1 else int(math.ceil(math.log2(k)))
+
+
+def kq_pack_bits(values, bits: int, out=None):
+    """LSB-first stream of `bits`-bit fields.  values: int32, uint8 or int16 tensor."""
+    eb = {torch.int32: 4, torch.uint8: 1, torch.int16: 2}.get(values.dtype)
+    if eb is None:
+        raise TypeError("values must be int32, int16 or uint8")
+    _dev(values, values.dtype, "values")
+    count = values.numel()
+    nbytes = (count * bits + 7) // 8
+    out = out if out is not None else torch.empty(max(nbytes, 1), dtype=torch.uint8, device=values.device)
+    _check(lib.kq_pack_bits(values.data_ptr(), eb, count, bits, out.data_ptr(), _stream(values.device)),
+           "kq_pack_bits")
+    return out[:nbytes]
+
+
+def kq_unpack_bits(stream, count: int, bits: int, out=None):
+    _dev(stream, torch.uint8, "stream")
+    out = out if out is not None else torch.empty(count, dtype=torch.int32, device=stream.device)
+    _check(lib.kq_unpack_bits(stream.data_ptr(), count, bits, out.data_ptr(), _stream(stream.device)),
+           "kq_unpack_bits")
+    return out
+
+
+def kq_reconstruct(idx, C, W_hat=None):
+    """W_hat[i] = C[idx[i]]  ([n, 9] float32)."""
+    C = _kernels(C, "C")
+    _dev(idx, torch.int32, "idx")
+    n = idx.numel()
+    W_hat = W_hat if W_hat is not None else torch.empty(n, KQ_DIM, dtype=torch.float32, device=idx.device)
+    _check(lib.kq_reconstruct(idx.data_ptr(), n, C.data_ptr(), C.shape[0], KQ_DIM, W_hat.data_ptr(),
+                              _stream(idx.device)), "kq_reconstruct")
+    return W_hat
+
+
+def kq_reconstruct_packed(packed, bits: int, n: int, C, W_hat=None):
+    C = _kernels(C, "C")
+    _dev(packed, torch.uint8, "packed")
+    W_hat = W_hat if W_hat is not None else torch.empty(n, KQ_DIM, dtype=torch.float32, device=packed.device)
+    _check(lib.kq_reconstruct_packed(packed.data_ptr(), bits, n, C.data_ptr(), C.shape[0], KQ_DIM,
+                                     W_hat.data_ptr(), _stream(packed.device)), "kq_reconstruct_packed")
+    return W_hat
+
+
+def kq_sq_error(A, B, out=None, workspace=None):
+    """sum (A - B)^2 over all elements, fp64, fixed order.  Returns a float64 [1] tensor."""
+    _dev(A, torch.float32, "A")
+    _dev(B, torch.float32, "B", tuple(A.shape))
+    out = out if out is not None else torch.empty(1, dtype=torch.float64, device=A.device)
+    nb = lib.kq_workspace_bytes(KQ_OP_SQ_ERROR, A.numel(), 1)
+    ws = workspace if workspace is not None else _ws(A.device, nb)
+    _check(lib.kq_sq_error(A.data_ptr(), B.data_ptr(), A.numel(), out.data_ptr(), ws.data_ptr(), ws.numel(),
+                           _stream(A.device)), "kq_sq_error")
+    return out

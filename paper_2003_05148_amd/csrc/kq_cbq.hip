@@ -1,0 +1,189 @@
+// Kernel codebook quantization (Sec. 3.2): every scalar of a layer's codebook is
+// coded with one of 2^bits fp32 levels found by k-means over those scalars, each
+// scalar weighted by the appearance count of its codebook entry.
+//
+// One workgroup per layer.  The weighted sums are exact: a scalar v = M 2^e (fp32)
+// times its integer weight w is the integer w M shifted to a fixed position, split
+// into 32-bit digits and added to per-level int64 digit accumulators in LDS
+// (ds_add_u64).  Integer addition makes the sums independent of the order of the
+// work; the exact sum is then rounded once to fp64 (round to nearest even), divided
+// by the exact weight total in fp64 and rounded to fp32.  Grid, codes and level
+// updates use only correctly rounded fp64 operations, so the codes and levels are
+// a pure function of the codebook and the weights.
+#include "kq_internal.h"
+
+namespace kq {
+
+constexpr int kCbqThreads = 1024;
+constexpr int kCbqMaxLevels = 256;
+constexpr int kDigits = 11;  // 32-bit digits: |sum of w v| * 2^149 < 2^328
+
+__device__ __forceinline__ int nearest_level(float v, const float* lev, int nlev) {
+    const double vd = (double)v;
+    double best = fabs(vd - (double)lev[0]);
+    int bq = 0;
+    for (int q = 1; q < nlev; ++q) {
+        const double d = fabs(vd - (double)lev[q]);
+        if (d < best) {
+            best = d;
+            bq = q;
+        }
+    }
+    return bq;
+}
+
+// add w * v * 2^149 (an exact integer) to the digit accumulators of one level
+__device__ __forceinline__ void add_exact(unsigned long long* dig, float v, unsigned w) {
+    const unsigned u = __float_as_uint(v);
+    const unsigned e = (u >> 23) & 0xffu;
+    const unsigned mant = u & 0x7fffffu;
+    const unsigned M = e ? (mant | 0x800000u) : mant;
+    const int sh = e ? (int)e - 1 : 0;  // v * 2^149 = M * 2^sh
+    const unsigned long long P = (unsigned long long)w * M;  // < 2^55
+    if (P == 0) return;
+    const int d0 = sh >> 5, b = sh & 31;
+    const unsigned long long lo = P << b;
+    const unsigned long long hi = b ? (P >> (64 - b)) : 0ull;
+    long long t0 = (long long)(lo & 0xffffffffull), t1 = (long long)(lo >> 32), t2 = (long long)hi;
+    if (u >> 31) {
+        t0 = -t0;
+        t1 = -t1;
+        t2 = -t2;
+    }
+    atomicAdd(&dig[d0], (unsigned long long)t0);
+    atomicAdd(&dig[d0 + 1], (unsigned long long)t1);
+    if (t2) atomicAdd(&dig[d0 + 2], (unsigned long long)t2);
+}
+
+// the exact integer sum_i dig[i] 2^(32 i), times 2^-149, rounded to nearest-even fp64
+__device__ double digits_to_double(const unsigned long long* dig) {
+    unsigned limb[kDigits + 1];
+    long long carry = 0;
+    for (int i = 0; i < kDigits; ++i) {
+        const long long t = (long long)dig[i] + carry;
+        limb[i] = (unsigned)(t & 0xffffffffll);
+        carry = t >> 32;
+    }
+    limb[kDigits] = (unsigned)carry;
+    const bool neg = carry < 0;
+    if (neg) {  // two's complement negate
+        unsigned c = 1;
+        for (int i = 0; i <= kDigits; ++i) {
+            const unsigned long long t = (unsigned long long)(~limb[i]) + c;
+            limb[i] = (unsigned)t;
+            c = (unsigned)(t >> 32);
+        }
+    }
+    int h = kDigits;
+    while (h >= 0 && limb[h] == 0) --h;
+    if (h < 0) return 0.0;
+    const int lz = __clz(limb[h]);
+    const unsigned long long hi64 = ((unsigned long long)limb[h] << 32) | (h >= 1 ? limb[h - 1] : 0u);
+    const unsigned next = h >= 2 ? limb[h - 2] : 0u;
+    unsigned long long win;
+    bool sticky;
+    if (lz) {
+        win = (hi64 << lz) | (unsigned long long)(next >> (32 - lz));
+        sticky = (next << lz) != 0u;
+    } else {
+        win = hi64;
+        sticky = next != 0u;
+    }
+    for (int i = 0; i <= h - 3; ++i) sticky |= limb[i] != 0u;
+    unsigned long long mant = win >> 11;
+    const unsigned rnd = (unsigned)(win & 0x7ffull);
+    if (rnd > 0x400u || (rnd == 0x400u && (sticky || (mant & 1ull)))) ++mant;
+    const int pos = 32 * h + 31 - lz;  // bit index of the leading one
+    const double r = ldexp((double)mant, pos - 52 - 149);
+    return neg ? -r : r;
+}
+
+__global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
+    __shared__ float s_lev[kCbqMaxLevels];
+    __shared__ unsigned long long s_dig[kCbqMaxLevels * kDigits];
+    __shared__ unsigned long long s_w[kCbqMaxLevels];
+    __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave];
+    __shared__ int s_changed;
+
+    const CbqLayer& L = p.L[blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int m = L.k * kDim;
+    const int nlev = 1 << p.bits;
+    const float* __restrict__ v = L.C;
+    uint8_t* __restrict__ codes = L.codes;
+
+    // grid on [min, max]
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+    for (int r = tid; r < m; r += kCbqThreads) {
+        lo = fminf(lo, v[r]);
+        hi = fmaxf(hi, v[r]);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, off));
+        hi = fmaxf(hi, __shfl_xor(hi, off));
+    }
+    if (lane == 0) {
+        s_lo[wave] = lo;
+        s_hi[wave] = hi;
+    }
+    __syncthreads();
+    lo = s_lo[0];
+    hi = s_hi[0];
+    for (int w = 1; w < kCbqThreads / kWave; ++w) {
+        lo = fminf(lo, s_lo[w]);
+        hi = fmaxf(hi, s_hi[w]);
+    }
+    if (tid < nlev) {
+        const double delta = ((double)hi - (double)lo) / (double)(nlev - 1);
+        s_lev[tid] = (float)__dadd_rn((double)lo, __dmul_rn((double)tid, delta));
+    }
+    __syncthreads();
+    for (int r = tid; r < m; r += kCbqThreads) codes[r] = (uint8_t)nearest_level(v[r], s_lev, nlev);
+
+    if (p.mode == KQ_CBQ_WKMEANS) {
+        for (int it = 0; it < p.iters; ++it) {
+            for (int e = tid; e < nlev * kDigits; e += kCbqThreads) s_dig[e] = 0ull;
+            for (int e = tid; e < nlev; e += kCbqThreads) s_w[e] = 0ull;
+            if (tid == 0) s_changed = 0;
+            __syncthreads();
+            for (int r = tid; r < m; r += kCbqThreads) {
+                const int w = L.w ? L.w[r / kDim] : 1;
+                if (w <= 0) continue;
+                const int q = codes[r];
+                add_exact(s_dig + q * kDigits, v[r], (unsigned)w);
+                atomicAdd(&s_w[q], (unsigned long long)w);
+            }
+            __syncthreads();
+            if (tid < nlev && s_w[tid] > 0ull) {
+                const double N = digits_to_double(s_dig + tid * kDigits);
+                s_lev[tid] = (float)(N / (double)s_w[tid]);
+            }
+            __syncthreads();
+            int changed = 0;
+            for (int r = tid; r < m; r += kCbqThreads) {
+                const int q = nearest_level(v[r], s_lev, nlev);
+                if (q != codes[r]) {
+                    codes[r] = (uint8_t)q;
+                    changed = 1;
+                }
+            }
+            if (changed) s_changed = 1;
+            __syncthreads();
+            const int any = s_changed;
+            __syncthreads();
+            if (!any) break;
+        }
+    }
+
+    if (tid < nlev) L.levels[tid] = s_lev[tid];
+    if (L.C_hat)
+        for (int r = tid; r < m; r += kCbqThreads) L.C_hat[r] = s_lev[codes[r]];
+}
+
+hipError_t launch_cbq(const CbqParams& p, hipStream_t s) {
+    hipLaunchKernelGGL(cbq_kernel, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace kq

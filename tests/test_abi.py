@@ -1,0 +1,143 @@
+"""The C-ABI library loads without a GPU, exports every function include/kq.h
+declares, and rejects bad arguments on the host before touching HIP."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kq.h")
+
+kq = pytest.importorskip("paper_2003_05148_amd")
+lib = kq.lib
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kq_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 15
+    raw = ctypes.CDLL(kq.LIB_PATH)
+    for name in names:
+        assert hasattr(raw, name), name
+    assert sorted(kq.EXPORTED) == names
+
+
+def test_status_strings_and_version():
+    assert lib.kq_abi_version() == 1
+    for s in range(6):
+        assert len(lib.kq_status_string(s)) > 0
+    assert lib.kq_status_string(99) == b"unknown status"
+
+
+def test_workspace_sizes():
+    a = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 4096, 256)
+    assert a > 0 and a % 256 == 0
+    assert lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256) == a
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 0, 256) == 0
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, 0) == 0
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, kq.KQ_MAX_K + 1) == 0
+    assert lib.kq_workspace_bytes(7, 10, 4) == 0
+    big = lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 1 << 20, 4096)
+    assert big >= 8 * 10 * 4096
+
+
+FAKE = 0x10000  # a well-aligned non-null pointer value; never dereferenced on these paths
+
+
+def assign(**kw):
+    a = dict(X=FAKE, n=100, dim=9, C=FAKE, k=8, idx=FAKE, best_d=None, dist=None, flags=0, ws=None, wsb=0, s=None)
+    a.update(kw)
+    return lib.kq_assign(a["X"], a["n"], a["dim"], a["C"], a["k"], a["idx"], a["best_d"], a["dist"], a["flags"],
+                         a["ws"], a["wsb"], a["s"])
+
+
+def test_assign_argument_errors():
+    assert assign(dim=8) == kq.KQ_ERR_UNSUPPORTED
+    assert assign(k=kq.KQ_MAX_K + 1) == kq.KQ_ERR_UNSUPPORTED
+    assert assign(n=0) == kq.KQ_ERR_ARG
+    assert assign(n=1 << 31) == kq.KQ_ERR_ARG
+    assert assign(k=0) == kq.KQ_ERR_ARG
+    assert assign(X=None) == kq.KQ_ERR_ARG
+    assert assign(C=None) == kq.KQ_ERR_ARG
+    assert assign(idx=None) == kq.KQ_ERR_ARG
+    assert assign(X=FAKE + 2) == kq.KQ_ERR_ARG
+    assert assign(best_d=FAKE + 1) == kq.KQ_ERR_ARG
+    assert assign(dist=FAKE + 4) == kq.KQ_ERR_ARG
+    assert assign(flags=1) == kq.KQ_ERR_ARG
+    # a distortion output needs a workspace of the queried size
+    assert assign(dist=FAKE) == kq.KQ_ERR_WORKSPACE
+    need = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 100, 8)
+    assert assign(dist=FAKE, ws=FAKE, wsb=need - 1) == kq.KQ_ERR_WORKSPACE
+    assert assign(dist=FAKE, ws=FAKE + 128, wsb=need) == kq.KQ_ERR_WORKSPACE
+
+
+def test_update_and_fit_argument_errors():
+    up = lambda **kw: lib.kq_update(kw.get("X", FAKE), kw.get("n", 100), kw.get("dim", 9), kw.get("idx", FAKE),
+                                    kw.get("k", 8), kw.get("Co", FAKE), kw.get("Cn", FAKE), kw.get("cnt", None), 0,
+                                    kw.get("ws", None), kw.get("wsb", 0), None)
+    assert up(dim=4) == kq.KQ_ERR_UNSUPPORTED
+    assert up(n=-1) == kq.KQ_ERR_ARG
+    assert up(Co=None) == kq.KQ_ERR_ARG
+    assert up(cnt=FAKE + 2) == kq.KQ_ERR_ARG
+    assert up() == kq.KQ_ERR_WORKSPACE
+    fit = lambda **kw: lib.kq_fit_layer(FAKE, kw.get("n", 100), 9, kw.get("k", 8), kw.get("Ci", FAKE),
+                                        kw.get("iters", 3), FAKE, FAKE, None, None, 0, kw.get("ws", None),
+                                        kw.get("wsb", 0), None)
+    assert fit(k=101) == kq.KQ_ERR_ARG          # a fit needs k <= n
+    assert fit(iters=-1) == kq.KQ_ERR_ARG
+    assert fit(Ci=None) == kq.KQ_ERR_ARG
+    assert fit() == kq.KQ_ERR_WORKSPACE
+
+
+def test_stack_argument_errors():
+    arr = (kq.KqLayer * 2)()
+    arr[0] = kq.KqLayer(FAKE, 4096, 256, FAKE, FAKE, None, FAKE, None)
+    arr[1] = kq.KqLayer(FAKE, 100, 200, FAKE, FAKE, None, FAKE, None)
+    p = ctypes.cast(arr, ctypes.c_void_p)
+    need = lib.kq_stack_workspace_bytes(p, 2)
+    assert need == lib.kq_workspace_bytes(0, 4096, 256) + lib.kq_workspace_bytes(0, 100, 200)
+    assert lib.kq_fit_stack(p, 2, 3, 0, FAKE, need, None) == kq.KQ_ERR_ARG      # k > n in layer 1
+    assert lib.kq_assign_stack(p, 2, 0, 0, FAKE, need - 1, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_assign_stack(p, 0, 0, 0, FAKE, need, None) == kq.KQ_ERR_ARG
+    assert lib.kq_assign_stack(None, 2, 0, 0, FAKE, need, None) == kq.KQ_ERR_ARG
+    assert lib.kq_assign_stack(p, 2, -1, 0, FAKE, need, None) == kq.KQ_ERR_ARG
+    arr[1] = kq.KqLayer(FAKE, 100, kq.KQ_MAX_K + 1, FAKE, FAKE, None, FAKE, None)
+    assert lib.kq_update_stack(p, 2, 0, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
+
+
+def test_cbq_pack_reconstruct_argument_errors():
+    q = lambda **kw: lib.kq_quantize_codebook(kw.get("C", FAKE), kw.get("k", 8), kw.get("dim", 9), None,
+                                              kw.get("bits", 6), kw.get("mode", 0), kw.get("iters", 30),
+                                              kw.get("codes", FAKE), kw.get("levels", FAKE), None, None)
+    assert q(dim=3) == kq.KQ_ERR_UNSUPPORTED
+    assert q(bits=9) == kq.KQ_ERR_UNSUPPORTED
+    assert q(bits=0) == kq.KQ_ERR_UNSUPPORTED
+    assert q(mode=5) == kq.KQ_ERR_ARG
+    assert q(iters=-2) == kq.KQ_ERR_ARG
+    assert q(codes=None) == kq.KQ_ERR_ARG
+    assert q(k=0) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits(FAKE, 4, 10, 17, FAKE, None) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_pack_bits(FAKE, 3, 10, 4, FAKE, None) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits(FAKE, 4, 10, 4, FAKE + 2, None) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits(FAKE + 2, 4, 10, 4, FAKE, None) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits(None, 4, 0, 4, None, None) == kq.KQ_OK             # nothing to do
+    assert lib.kq_pack_bits(None, 4, 10, 0, None, None) == kq.KQ_OK            # zero-bit fields
+    assert lib.kq_unpack_bits(None, 10, 4, FAKE, None) == kq.KQ_ERR_ARG
+    assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 9, FAKE + 4, None) == kq.KQ_ERR_ARG   # W_hat 16-B aligned
+    assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 8, FAKE, None) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_reconstruct_packed(None, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG
+    assert lib.kq_workspace_init(FAKE + 8, 100, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_workspace_init(FAKE, 0, None) == kq.KQ_OK
+
+
+def test_python_binding_rejects_cpu_tensors():
+    import torch
+    X = torch.zeros(10, 9)
+    with pytest.raises(TypeError):
+        kq.kq_assign(X, X[:2])

@@ -1,0 +1,289 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bars: assignment indices and fp32 best distances bit-exact (the library returns the
+exact fp32 argmin); distortion within 1e-5 relative of the oracle's fp64 value;
+centroids within 1e-5 relative per codeword; counts, 6-bit codes and levels, packed
+streams and reconstructions bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+kq = pytest.importorskip("paper_2003_05148_amd")
+DEV = torch.device("cuda:0")
+REL = 1e-5
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def check_assign(X, C, tag=""):
+    idx, best_d, dist = kq.kq_assign(dev(X), dev(C))
+    gi, gd, gJ = host(idx), host(best_d), float(host(dist)[0])
+    o = oracle.assign(X, C)
+    bad = np.nonzero(gi != o["idx"])[0]
+    assert bad.size == 0, f"{tag}: {bad.size} indices differ, first {bad[:5]} gpu {gi[bad[:5]]} oracle {o['idx'][bad[:5]]}"
+    assert np.array_equal(gd.view(np.uint32), o["d32"].view(np.uint32)), f"{tag}: best distances differ"
+    J32 = float(np.sum(o["d32"].astype(np.float64)))
+    assert gJ == pytest.approx(J32, rel=1e-12, abs=1e-300), tag
+    J64 = float(np.sum(o["d1"]))
+    assert gJ == pytest.approx(J64, rel=REL, abs=1e-30), tag
+    # against the fp64 decision only near-ties may differ (best and second-best within 1e-5)
+    diff = np.nonzero(o["idx"] != o["idx64"])[0]
+    for i in diff:
+        assert o["d2"][i] - o["d1"][i] <= REL * o["d2"][i], (tag, i)
+    return diff.size
+
+
+def test_assign_single_layer_64x64():
+    L = synth.single_layer(k=256)[0]
+    check_assign(L.X, L.C0, "64x64 k=256 init")
+    check_assign(L.X, synth.random_codebook_state(L.X, 256, 5), "64x64 k=256 jittered")
+
+
+@pytest.mark.parametrize("n,k", [(1, 1), (2, 1), (1, 5), (255, 3), (256, 16), (257, 31), (1000, 33),
+                                 (4133, 256), (3000, 1024), (3001, 1025), (2048, 2100), (700, 4096),
+                                 (300, 7000)])
+def test_assign_shapes(n, k):
+    X = synth.laplace_layer(1, n, 100 + n)[:n]
+    C = synth.random_codebook_state(X, k, k)
+    check_assign(X, C, f"n={n} k={k}")
+
+
+def test_assign_exact_ties_and_near_ties():
+    rng = np.random.default_rng(3)
+    # small integers: many exactly equal distances, duplicated entries
+    X = rng.integers(-2, 3, (3000, 9)).astype(np.float32)
+    C = rng.integers(-2, 3, (200, 9)).astype(np.float32)
+    C[100:150] = C[0:50]
+    check_assign(X, C, "integer grid")
+    # tight clusters far from the origin: strong cancellation in |c|^2 - 2 x.c
+    L = synth.stress_layer(n=20000, k=1024, n_centers=1024, seed=44)[0]
+    check_assign(L.X, L.C0, "clusters")
+    # a point exactly between two entries
+    X = np.zeros((64, 9), np.float32)
+    C = np.zeros((2, 9), np.float32)
+    C[0, 0], C[1, 0] = -1.0, 1.0
+    check_assign(X, C, "midpoint")
+
+
+def test_assign_nonfinite_inputs_match_plain_scan():
+    X = synth.normal_layer(8, 8, 5)
+    X[3, 2] = np.nan
+    X[7, 0] = np.inf
+    C = X[10:30].copy()
+    idx, best_d, _ = kq.kq_assign(dev(X), dev(C))
+    o = oracle.assign(X, C)
+    assert np.array_equal(host(idx), o["idx"])
+
+
+def check_update(X, idx, C_old, tag=""):
+    C_new, counts = kq.kq_update(dev(X), dev(idx), dev(C_old))
+    gc, gz = host(C_new), host(counts)
+    oc, oz = oracle.update(X, idx, C_old)
+    assert np.array_equal(gz, oz), tag
+    empty = oz == 0
+    assert np.array_equal(gc[empty], C_old[empty]), tag
+    err = np.abs(gc.astype(np.float64) - oc.astype(np.float64)).max(axis=1)
+    scale = np.maximum(np.abs(oc.astype(np.float64)).max(axis=1), 1e-30)
+    assert np.all(err <= REL * scale), (tag, float((err / scale).max()))
+    return gc, gz
+
+
+@pytest.mark.parametrize("n,k", [(1, 1), (100, 1), (4096, 16), (4099, 256), (20000, 768), (20000, 769),
+                                 (50000, 4096), (9000, 20000)])
+def test_update_shapes(n, k):
+    X = synth.normal_layer(1, n, 7 + n)[:n]
+    idx = synth.random_indices(n, k, k)
+    if k > 4:
+        idx[idx == 3] = 2        # an empty entry keeps its value
+    C_old = synth.random_codebook_state(X, k, 1)
+    check_update(X, idx, C_old, f"n={n} k={k}")
+
+
+def test_update_in_place_and_ignores_bad_indices():
+    X = synth.normal_layer(16, 16, 3)
+    n, k = X.shape[0], 32
+    idx = synth.random_indices(n, k, 9)
+    C = synth.random_codebook_state(X, k, 2)
+    Cd = dev(C)
+    kq.kq_update(dev(X), dev(idx), Cd, C_new=Cd)
+    oc, _ = oracle.update(X, idx, C)
+    assert np.allclose(host(Cd), oc, rtol=REL, atol=1e-12)
+    bad = idx.copy()
+    bad[:10] = 77
+    bad[10:20] = -1
+    gc, gz = kq.kq_update(dev(X), dev(bad), dev(C))
+    keep = np.arange(n) >= 20
+    oc, oz = oracle.update(X[keep], bad[keep], C)
+    assert np.array_equal(host(gz), oz)
+    assert np.allclose(host(gc), oc, rtol=REL, atol=1e-12)
+
+
+def test_fit_step_locked_single_layer():
+    """At every round both sides start from the oracle's codebook."""
+    L = synth.single_layer(k=256)[0]
+    Xd = dev(L.X)
+    C = L.C0.copy()
+    for t in range(20):
+        idx, best_d, dist = kq.kq_assign(Xd, dev(C))
+        o = oracle.assign(L.X, C)
+        assert np.array_equal(host(idx), o["idx"]), t
+        C_g, z_g = kq.kq_update(Xd, idx, dev(C))
+        C_o, z_o = oracle.update(L.X, o["idx"], C)
+        assert np.array_equal(host(z_g), z_o), t
+        err = np.abs(host(C_g).astype(np.float64) - C_o).max(axis=1)
+        assert np.all(err <= REL * np.maximum(np.abs(C_o).max(axis=1), 1e-30)), t
+        C = C_o
+
+
+def test_fit_layer_free_running():
+    L = synth.single_layer(k=256)[0]
+    iters = 20
+    C, idx, counts, J = kq.kq_fit_layer(dev(L.X), dev(L.C0), iters)
+    gC, gi, gz, gJ = host(C), host(idx), host(counts), host(J)
+    ref = oracle.fit(L.X, L.C0, iters)
+    assert np.all(gJ[1:] <= gJ[:-1] * (1 + 1e-9)), gJ          # Lloyd never increases Eq. (1)
+    a = oracle.assign(L.X, gC)                                  # the final assignment is exact for the final C
+    assert np.array_equal(gi, a["idx"]) and np.array_equal(gz, np.bincount(a["idx"], minlength=L.k))
+    assert gJ[-1] == pytest.approx(float(np.sum(a["d1"])), rel=REL)
+    rel = abs(gJ[-1] - ref["J"][-1]) / ref["J"][-1]
+    assert rel <= 1e-3, rel                                     # trajectories may part at fp32 rounding
+    if np.array_equal(gi, ref["idx"]):
+        assert rel <= REL
+
+
+def test_fit_determinism_and_resume():
+    L = synth.resnet18_stack(k=64, layers=1)[0]
+    Xd, C0 = dev(L.X), dev(L.C0)
+    a = kq.kq_fit_layer(Xd, C0, 10)
+    b = kq.kq_fit_layer(Xd, C0, 10)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    half = kq.kq_fit_layer(Xd, C0, 4)
+    rest = kq.kq_fit_layer(Xd, half[0].clone(), 6)
+    assert torch.equal(rest[0], a[0]) and torch.equal(rest[1], a[1]) and torch.equal(rest[2], a[2])
+    assert torch.equal(rest[3], a[3][4:])
+
+
+def test_stack_full_size_resnet18_sampled():
+    """The ResNet-18-shaped stack at full size and k = 256, in the launch
+    configuration the benchmark times: two Lloyd rounds through the stack calls,
+    checked on sampled kernels (assignment) and in full (update, counts)."""
+    layers = synth.resnet18_stack(k=256)
+    st = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=2, best_d=True)
+    rng = np.random.default_rng(0)
+    for t in range(2):
+        C_before = [host(c) for c in st.C]
+        kq.kq_assign_stack(st, dist_slot=t)
+        idx = [host(i) for i in st.idx]
+        for L, Cb, gi, gd, gJ in zip(layers, C_before, idx, st.best_d, st.distortion):
+            rows = rng.choice(L.n, min(L.n, 1500), replace=False)
+            o = oracle.assign(L.X[rows], Cb)
+            assert np.array_equal(gi[rows], o["idx"]), (L.name, t)
+            assert np.array_equal(host(gd)[rows], o["d32"]), (L.name, t)
+            Jo = oracle.distortion(L.X, Cb, gi)
+            assert float(host(gJ)[t]) == pytest.approx(Jo, rel=REL), (L.name, t)
+        kq.kq_update_stack(st)
+        for L, Cb, gi, gC, gz in zip(layers, C_before, idx, st.C, st.counts):
+            oc, oz = oracle.update(L.X, gi, Cb)
+            assert np.array_equal(host(gz), oz), L.name
+            err = np.abs(host(gC).astype(np.float64) - oc).max(axis=1)
+            assert np.all(err <= REL * np.maximum(np.abs(oc).max(axis=1), 1e-30)), L.name
+
+
+def test_fit_stack_matches_fit_layer():
+    layers = synth.vgg16_stack(k=64, layers=4)
+    st = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=5)
+    kq.kq_fit_stack(st, 5)
+    for i, L in enumerate(layers):
+        C, idx, counts, J = kq.kq_fit_layer(dev(L.X), dev(L.C0), 5)
+        assert torch.equal(C, st.C[i]) and torch.equal(idx, st.idx[i]) and torch.equal(counts, st.counts[i])
+        assert torch.equal(J, st.distortion[i])
+
+
+def test_stress_layer_sampled():
+    """1024 x 1024 kernels from 4096 tight clusters, k = 4096 (several LDS chunks,
+    many guarded kernels): sampled exact parity of one assignment and a full update."""
+    L = synth.stress_layer()[0]
+    Xd = dev(L.X)
+    idx, best_d, dist = kq.kq_assign(Xd, dev(L.C0))
+    gi, gd = host(idx), host(best_d)
+    rows = np.random.default_rng(1).choice(L.n, 3000, replace=False)
+    o = oracle.assign(L.X[rows], L.C0)
+    assert np.array_equal(gi[rows], o["idx"])
+    assert np.array_equal(gd[rows], o["d32"])
+    assert float(host(dist)[0]) == pytest.approx(float(np.sum(gd.astype(np.float64))), rel=1e-12)
+    check_update(L.X, gi, L.C0, "stress update")
+
+
+@pytest.mark.parametrize("mode", [kq.KQ_CBQ_UNIFORM, kq.KQ_CBQ_WKMEANS])
+def test_quantize_codebook_bit_exact(mode):
+    cases = []
+    L = synth.single_layer(k=256)[0]
+    r = oracle.fit(L.X, L.C0, 5)
+    cases.append((r["C"], r["counts"]))
+    rng = np.random.default_rng(2)
+    cases.append((rng.laplace(0, 0.03, (1000, 9)).astype(np.float32), rng.integers(0, 500, 1000)))
+    cases.append((np.full((3, 9), -0.5, np.float32), np.array([1, 2, 3])))
+    tiny = rng.standard_normal((40, 9)).astype(np.float32) * np.float32(1e-30)
+    tiny[0, 0] = np.float32(3e-39)      # a subnormal scalar
+    cases.append((tiny, rng.integers(0, 2 ** 31 - 1, 40)))
+    big = (rng.standard_normal((64, 9)) * 1e30).astype(np.float32)
+    cases.append((big, rng.integers(1, 1000, 64)))
+    for C, w in cases:
+        codes, levels, C_hat = kq.kq_quantize_codebook(dev(C), dev(w.astype(np.int32)), 6, mode, 30)
+        if mode == kq.KQ_CBQ_UNIFORM:
+            oc, ol, oh = oracle.cbq_uniform(C, 6)
+        else:
+            oc, ol, oh, _ = oracle.cbq_wkmeans(C, w, 6, 30)
+        assert np.array_equal(host(codes), oc)
+        assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32))
+        assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32))
+
+
+def test_quantize_codebook_stack_and_unweighted():
+    layers = synth.resnet18_stack(k=16, layers=3)
+    Cs = [oracle.fit(L.X, L.C0, 3)["C"] for L in layers]
+    out = kq.kq_quantize_codebook_stack([dev(c) for c in Cs], None, 6, kq.KQ_CBQ_WKMEANS, 30)
+    for C, (codes, levels, C_hat) in zip(Cs, out):
+        oc, ol, oh, _ = oracle.cbq_wkmeans(C, np.ones(C.shape[0], np.int64), 6, 30)
+        assert np.array_equal(host(codes), oc) and np.array_equal(host(levels), ol)
+
+
+@pytest.mark.parametrize("bits", [1, 3, 4, 6, 8, 9, 11, 12, 16])
+@pytest.mark.parametrize("count", [1, 7, 31, 32, 33, 1000, 4097])
+def test_pack_unpack_bit_exact(bits, count):
+    rng = np.random.default_rng(bits * 1000 + count)
+    v = rng.integers(0, 1 << bits, count).astype(np.int32)
+    s = kq.kq_pack_bits(dev(v), bits)
+    ref = oracle.pack_bits(v, bits)
+    assert np.array_equal(host(s), ref)
+    back = kq.kq_unpack_bits(s, count, bits)
+    assert np.array_equal(host(back), v)
+    if bits <= 8:
+        s8 = kq.kq_pack_bits(dev(v.astype(np.uint8)), bits)
+        assert np.array_equal(host(s8), ref)
+
+
+def test_reconstruct_bit_exact():
+    rng = np.random.default_rng(4)
+    for n, k in [(1, 1), (3, 2), (4097, 256), (262144, 256), (777, 4096)]:
+        C = rng.standard_normal((k, 9)).astype(np.float32)
+        idx = rng.integers(0, k, n).astype(np.int32)
+        W = kq.kq_reconstruct(dev(idx), dev(C))
+        assert np.array_equal(host(W), oracle.reconstruct(idx, C))
+        b = oracle.index_bits(k)
+        packed = kq.kq_pack_bits(dev(idx), b)
+        W2 = kq.kq_reconstruct_packed(packed, b, n, dev(C))
+        assert np.array_equal(host(W2), oracle.reconstruct(idx, C))

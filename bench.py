@@ -109,7 +109,7 @@ def main():
             if record:
                 a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-            kq.kq_assign_stack(st, dist_slot=t)
+            kq.kq_assign_stack(st, dist_slot=t, distortion=False)
             if record:
                 a1.record(stream)
                 ev["assign"].append((a0, a1))
@@ -117,11 +117,11 @@ def main():
                 if record:
                     u0, u1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     u0.record(stream)
-                kq.kq_update_stack(st)
+                kq.kq_update_stack(st, dist_slot=t, distortion_from_assign=True)
                 if record:
                     u1.record(stream)
                     ev["update"].append((u0, u1))
-        kq.kq_update_stack(st, counts_only=True)
+        kq.kq_update_stack(st, dist_slot=T, counts_only=True, distortion_from_assign=True)
         kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30, out=cb_out)
         for i, L in enumerate(layers):
             kq.kq_pack_bits(st.idx[i], bits, out=p_idx[i])

@@ -31,10 +31,9 @@
  *    checks pass, so argument errors are reported without a GPU.
  *  - KQ_ERR_HIP: a HIP launch failed; outputs are unspecified.
  *  - workspace: device scratch of at least the size the matching *_workspace_bytes
- *    query returns, 256-byte aligned.  It must be all-zero before its first use
- *    (kq_workspace_init does that); every call leaves it all-zero again when its work
- *    on the stream completes.  Calls that share a workspace must be ordered on one
- *    stream.
+ *    query returns, 256-byte aligned.  Its contents need no initialisation: every
+ *    call writes what it later reads.  Calls that share a workspace must be ordered on one
+ *    stream (concurrent calls on one workspace race).
  *  - Kernel values must be finite with |x| < 32 for kq_update / kq_fit_* (the member
  *    sums are exact 64-bit fixed-point sums, see kq_update).  Real CNN weights are
  *    orders of magnitude smaller.
@@ -74,6 +73,10 @@ typedef enum kq_status {
 
 /* flags */
 #define KQ_F_COUNTS_ONLY 1u  /* kq_update / kq_update_stack: write counts only, leave C untouched */
+#define KQ_F_DISTORTION_FROM_ASSIGN 2u
+                             /* kq_update_stack: take the distortion from the partial sums the
+                                preceding kq_assign_stack on the same layers and workspace left
+                                (no second pass over the old codebook) */
 
 /* One layer of a stack.  All pointers are device pointers. */
 typedef struct kq_layer {
@@ -133,13 +136,17 @@ kq_status kq_assign(const float* X, int64_t n, int32_t dim, const float* C, int3
  *   ceil(log2 n), so they do not depend on summation order; the mean is
  *   fp32( (double(sum) * 2^-s) / |S_j| ).
  *
+ *   *distortion = the Eq. (1) objective of the given assignment against C_old:
+ *               sum_i d(x_i, C_old[idx[i]]) with d the fp32 distance of kq_assign,
+ *               summed in fp64 in a fixed order (device scalar, may be NULL).
+ *
  *   X device [n][9]; idx device [n] values in [0, k) (out-of-range indices are
  *   ignored); C_old, C_new device [k][9] (may alias); counts device [k] or NULL.
  *   flags: 0, or KQ_F_COUNTS_ONLY to compute only the counts (C_new untouched).
  */
 kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
-                    const float* C_old, float* C_new, int32_t* counts, uint32_t flags,
-                    void* ws, size_t ws_bytes, void* stream);
+                    const float* C_old, float* C_new, int32_t* counts, double* distortion,
+                    uint32_t flags, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * kq_fit_layer -- Lloyd k-means on one layer (Sec. 3.1, Eq. 1).
@@ -159,13 +166,16 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
  * Stack versions: one launch per step for up to KQ_MAX_STACK layers (more are split).
  *   kq_assign_stack: assigns every layer against its C; writes idx, best_d (if set) and
  *                    distortion[dist_slot] (if distortion is set).
- *   kq_update_stack: updates every C in place from its idx; writes counts (if set).
+ *   kq_update_stack: updates every C in place from its idx; writes counts (if set) and
+ *                    the distortion of idx against the old C into distortion[dist_slot]
+ *                    (with KQ_F_DISTORTION_FROM_ASSIGN, the value the preceding
+ *                    kq_assign_stack computed, which is the same objective).
  *   kq_fit_stack:    kq_fit_layer on every layer (C in place, distortion [iters+1]).
  *   layers is a host array; the pointers in it are device pointers.
  */
 kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags,
                           void* ws, size_t ws_bytes, void* stream);
-kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, uint32_t flags,
+kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags,
                           void* ws, size_t ws_bytes, void* stream);
 kq_status kq_fit_stack(const kq_layer* layers, int32_t n_layers, int32_t iters, uint32_t flags,
                        void* ws, size_t ws_bytes, void* stream);

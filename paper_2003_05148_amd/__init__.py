@@ -49,10 +49,10 @@ def _load():
         "kq_stack_workspace_bytes": ([_P, _I32], _SZ),
         "kq_workspace_init": ([_P, _SZ, _P], _I32),
         "kq_assign": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
-        "kq_update": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
+        "kq_update": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
         "kq_fit_layer": ([_P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
         "kq_assign_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
-        "kq_update_stack": ([_P, _I32, _U32, _P, _SZ, _P], _I32),
+        "kq_update_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
         "kq_fit_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
         "kq_quantize_codebook": ([_P, _I32, _I32, _P, _I32, _I32, _I32, _P, _P, _P, _P], _I32),
         "kq_quantize_codebook_stack": ([_P, _I32, _I32, _I32, _I32, _P], _I32),
@@ -79,6 +79,7 @@ KQ_MAX_STACK = 16
 KQ_CBQ_WKMEANS, KQ_CBQ_UNIFORM = 0, 1
 KQ_OP_ASSIGN, KQ_OP_UPDATE, KQ_OP_FIT, KQ_OP_SQ_ERROR = 0, 1, 2, 3
 KQ_F_COUNTS_ONLY = 1
+KQ_F_DISTORTION_FROM_ASSIGN = 2
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
@@ -128,10 +129,8 @@ def _kernels(X: torch.Tensor, name="X"):
 
 
 class Workspace:
-    """A zero-initialised device scratch buffer for the library (grown on demand).
-
-    The library returns it to all-zero after every call, so it can be reused by
-    every call ordered on one stream."""
+    """A device scratch buffer for the library (grown on demand).  Its contents need no
+    initialisation; it can be reused by every call ordered on one stream."""
 
     def __init__(self, device=None):
         self.device = torch.device(device if device is not None else "cuda")
@@ -176,8 +175,9 @@ def kq_assign(X, C, idx=None, best_d=None, distortion=None, workspace=None):
     return idx, best_d, distortion
 
 
-def kq_update(X, idx, C_old, C_new=None, counts=None, workspace=None, counts_only: bool = False):
-    """Mean of every kernel set (empty sets keep their entry).  Returns (C_new, counts)."""
+def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace=None, counts_only: bool = False):
+    """Mean of every kernel set (empty sets keep their entry) and the distortion of the
+    assignment against C_old.  Returns (C_new, counts, distortion float64 [1])."""
     X = _kernels(X)
     C_old = _kernels(C_old, "C_old")
     n, k = X.shape[0], C_old.shape[0]
@@ -187,12 +187,14 @@ def kq_update(X, idx, C_old, C_new=None, counts=None, workspace=None, counts_onl
     counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
     _dev(C_new, torch.float32, "C_new", (k, KQ_DIM))
     _dev(counts, torch.int32, "counts", (k,))
+    distortion = distortion if distortion is not None else torch.empty(1, dtype=torch.float64, device=dev)
+    _dev(distortion, torch.float64, "distortion")
     nb = lib.kq_workspace_bytes(KQ_OP_UPDATE, n, k)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_update(X.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), C_new.data_ptr(),
-                         counts.data_ptr(), KQ_F_COUNTS_ONLY if counts_only else 0, ws.data_ptr(), ws.numel(),
-                         _stream(dev)), "kq_update")
-    return C_new, counts
+                         counts.data_ptr(), distortion.data_ptr(), KQ_F_COUNTS_ONLY if counts_only else 0,
+                         ws.data_ptr(), ws.numel(), _stream(dev)), "kq_update")
+    return C_new, counts, distortion
 
 
 def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):
@@ -247,13 +249,30 @@ class Stack:
             c.copy_(src)
 
 
-def kq_assign_stack(stack: Stack, dist_slot: int = 0):
+def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True):
+    """Assign every layer of the stack; the distortion (if asked) goes to slot dist_slot."""
+    if not distortion:
+        saved = [(l.distortion) for l in stack.layers]
+        for l in stack.layers:
+            l.distortion = None
+        try:
+            _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, 0,
+                                       stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)),
+                   "kq_assign_stack")
+        finally:
+            for l, d in zip(stack.layers, saved):
+                l.distortion = d
+        return
     _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, 0, stack.ws.data_ptr(),
                                stack.ws.numel(), _stream(stack.device)), "kq_assign_stack")
 
 
-def kq_update_stack(stack: Stack, counts_only: bool = False):
-    _check(lib.kq_update_stack(ctypes.cast(stack.layers, _P), stack.n_layers, KQ_F_COUNTS_ONLY if counts_only else 0,
+def kq_update_stack(stack: Stack, dist_slot: int = 0, counts_only: bool = False, distortion_from_assign=False):
+    """Update every codebook of the stack.  The distortion of the assignment goes to slot
+    dist_slot; with distortion_from_assign it is the value the preceding kq_assign_stack
+    left in the workspace (no second pass over the old codebook)."""
+    flags = (KQ_F_COUNTS_ONLY if counts_only else 0) | (KQ_F_DISTORTION_FROM_ASSIGN if distortion_from_assign else 0)
+    _check(lib.kq_update_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, flags,
                                stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)), "kq_update_stack")
 
 

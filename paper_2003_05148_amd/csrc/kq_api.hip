@@ -11,7 +11,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 1;
+constexpr int32_t kAbiVersion = 2;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -30,45 +30,51 @@ kq_status check_ws(void* ws, size_t ws_bytes, size_t need) {
     return KQ_OK;
 }
 
-// fill the device descriptor of one layer; `base` is its workspace region
-void fill_layer(DevLayer& d, const float* X, int64_t n, int32_t k, float* C, const float* C_old, int32_t* idx,
-                float* best_d, int32_t* counts, double* dist, unsigned char* base) {
-    memset(&d, 0, sizeof(d));
-    d.X = X;
-    d.C = C;
-    d.C_old = C_old;
-    d.idx = idx;
-    d.best_d = best_d;
-    d.counts = counts;
-    d.dist = dist;
-    d.n = (int)n;
-    d.k = k;
-    d.shift = fixed_shift(n);
-    d.ctr = (unsigned*)base;
-    d.part = (double*)(base + 256);
-    d.acc = (unsigned long long*)(base + 256 + align256(sizeof(double) * (size_t)assign_blocks(n)));
-}
+enum class Op { Assign, Update };
 
-// the layers [l0, l1) of a stack as launch parameters (assign or update geometry)
-void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, bool for_update,
-                  int32_t dist_slot, bool counts_only) {
+// Launch parameters for layers [l0, l1) of a stack.  `base` points at the workspace
+// of layer 0 (the regions of the layers follow each other in order).
+void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* base, Op op,
+                  int32_t dist_slot, const float* const* C_old, uint32_t kflags, bool from_assign = false) {
     memset(&p, 0, sizeof(p));
     size_t off = 0;
     for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
-    int blk = 0;
+    int unit = 0;
     for (int32_t l = l0; l < l1; ++l) {
         const kq_layer& s = layers[l];
         DevLayer& d = p.L[l - l0];
-        fill_layer(d, s.X, s.n, s.k, s.C, s.C, s.idx, for_update ? nullptr : s.best_d, s.counts,
-                   (!for_update && s.distortion) ? s.distortion + dist_slot : nullptr, ws + off);
-        d.counts_only = counts_only ? 1 : 0;
-        d.blk_begin = blk;
-        d.nblk = for_update ? update_blocks(s.n) : assign_blocks(s.n);
-        blk += d.nblk;
+        unsigned char* w = base + off;
+        d.X = s.X;
+        d.C = s.C;
+        d.C_old = C_old ? C_old[l] : s.C;
+        d.idx = s.idx;
+        d.n = (int)s.n;
+        d.k = s.k;
+        d.shift = fixed_shift(s.n);
+        d.dist = s.distortion ? s.distortion + dist_slot : nullptr;
+        if (op == Op::Assign) {
+            d.best_d = s.best_d;
+            d.part = base ? (double*)w : nullptr;  // partials whenever there is a workspace
+            d.nunits = assign_tiles(s.n);
+        } else {
+            d.counts = s.counts;
+            if (d.dist && from_assign) {
+                d.apart = (const double*)w;
+                d.napart = assign_tiles(s.n) * kAssignWaves;
+            } else if (d.dist) {
+                d.part = (double*)(w + ws_assign_part(s.n));
+            }
+            d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n));
+            d.nunits = update_blocks(s.n);
+            d.flags = (int)kflags | (update_uses_lds(s.k) ? 0 : kFlagAtomicHist) |
+                      ((aligned(s.X, 16) && aligned(s.idx, 16)) ? kFlagVec : 0);
+        }
+        d.unit_begin = unit;
+        unit += d.nunits;
         off += layer_ws_bytes(s.n, s.k);
     }
     p.nlayers = l1 - l0;
-    p.total_blocks = blk;
+    p.total_units = unit;
 }
 
 kq_status check_layers(const kq_layer* layers, int32_t n_layers, bool fit) {
@@ -86,23 +92,57 @@ kq_status check_layers(const kq_layer* layers, int32_t n_layers, bool fit) {
     return KQ_OK;
 }
 
+bool any_distortion(const kq_layer* layers, int32_t l0, int32_t l1) {
+    for (int32_t l = l0; l < l1; ++l)
+        if (layers[l].distortion) return true;
+    return false;
+}
+
+// assignment of layers [l0, l1) (+ the distortion finish when any layer asks for it)
+kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s) {
+    StackParams p;
+    stack_params(p, layers, l0, l1, ws, Op::Assign, slot, nullptr, 0);
+    if (launch_assign(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (any_distortion(layers, l0, l1) && launch_assign_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
+    return KQ_OK;
+}
+
+kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot,
+                     const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false) {
+    StackParams p;
+    stack_params(p, layers, l0, l1, ws, Op::Update, slot, C_old, kflags, from_assign);
+    // large codebooks accumulate with global atomics: clear their accumulators first
+    for (int l = 0; l < p.nlayers; ++l)
+        if ((p.L[l].flags & kFlagAtomicHist) &&
+            launch_fill_zero(p.L[l].hist, sizeof(int64_t) * 10 * (size_t)p.L[l].k, s) != hipSuccess)
+            return KQ_ERR_HIP;
+    if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
+    return KQ_OK;
+}
+
+// Lloyd rounds: assign (leaving distortion partials in the workspace), then update,
+// whose finishing kernel adds those partials; the final assignment is followed by a
+// counts-only update that does the same.
 kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsigned char* ws, hipStream_t s) {
+    kq_layer quiet[KQ_MAX_STACK];
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        StackParams pa, pu;
+        for (int32_t l = l0; l < l1; ++l) {
+            quiet[l - l0] = layers[l];
+            quiet[l - l0].distortion = nullptr;
+        }
+        size_t off = 0;
+        for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
+        bool need_last = false;
+        for (int32_t l = l0; l < l1; ++l) need_last |= layers[l].counts != nullptr || layers[l].distortion != nullptr;
         for (int32_t t = 0; t <= iters; ++t) {
-            stack_params(pa, layers, l0, l1, ws, false, t, false);
-            hipError_t e = launch_assign(pa, s);
-            if (e != hipSuccess) return KQ_ERR_HIP;
+            kq_status st = run_assign(quiet, 0, l1 - l0, ws + off, 0, s);
+            if (st != KQ_OK) return st;
             const bool last = (t == iters);
-            stack_params(pu, layers, l0, l1, ws, true, 0, last);
-            if (last) {
-                bool any_counts = false;
-                for (int32_t l = l0; l < l1; ++l) any_counts |= layers[l].counts != nullptr;
-                if (!any_counts) break;
-            }
-            e = launch_update(pu, s);
-            if (e != hipSuccess) return KQ_ERR_HIP;
+            if (last && !need_last) break;
+            st = run_update(layers, l0, l1, ws, t, nullptr, last ? kFlagCountsOnly : 0, s, true);
+            if (st != KQ_OK) return st;
         }
     }
     return KQ_OK;
@@ -129,7 +169,7 @@ int32_t kq_abi_version(void) { return kAbiVersion; }
 size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k) {
     if (op == KQ_OP_SQ_ERROR) {
         if (n < 1 || n >= (int64_t(1) << 40)) return 0;
-        return 256 + align256(sizeof(double) * (size_t)sq_error_blocks(n));
+        return align256(sizeof(double) * (size_t)sq_error_blocks(n));
     }
     if (!valid_n(n) || !valid_k(k)) return 0;
     if (op != KQ_OP_ASSIGN && op != KQ_OP_UPDATE && op != KQ_OP_FIT) return 0;
@@ -158,32 +198,27 @@ kq_status kq_assign(const float* X, int64_t n, int32_t dim, const float* C, int3
         const kq_status w = check_ws(ws, ws_bytes, layer_ws_bytes(n, k));
         if (w != KQ_OK) return w;
     }
-    kq_layer l = {X, n, k, const_cast<float*>(C), idx, best_d, nullptr, distortion};
-    StackParams p;
-    unsigned char scratch_base[256];  // never dereferenced: without a distortion nothing touches the workspace
-    stack_params(p, &l, 0, 1, ws ? (unsigned char*)ws : scratch_base, false, 0, false);
-    return hip_status(launch_assign(p, (hipStream_t)stream));
+    const kq_layer l = {X, n, k, const_cast<float*>(C), idx, best_d, nullptr, distortion};
+    // without a distortion the workspace (unchecked then) is not touched
+    return run_assign(&l, 0, 1, distortion ? (unsigned char*)ws : nullptr, 0, (hipStream_t)stream);
 }
 
 kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, int32_t k, const float* C_old,
-                    float* C_new, int32_t* counts, uint32_t flags, void* ws, size_t ws_bytes, void* stream) {
+                    float* C_new, int32_t* counts, double* distortion, uint32_t flags, void* ws, size_t ws_bytes,
+                    void* stream) {
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k) || (flags & ~KQ_F_COUNTS_ONLY) != 0) return KQ_ERR_ARG;
     if (!X || !idx || !C_old || !C_new || !aligned(X, 4) || !aligned(idx, 4) || !aligned(C_old, 4) ||
         !aligned(C_new, 4))
         return KQ_ERR_ARG;
-    if (counts && !aligned(counts, 4)) return KQ_ERR_ARG;
+    if ((counts && !aligned(counts, 4)) || (distortion && !aligned(distortion, 8))) return KQ_ERR_ARG;
     const kq_status w = check_ws(ws, ws_bytes, layer_ws_bytes(n, k));
     if (w != KQ_OK) return w;
-    StackParams p;
-    memset(&p, 0, sizeof(p));
-    fill_layer(p.L[0], X, n, k, C_new, C_old, const_cast<int32_t*>(idx), nullptr, counts, nullptr, (unsigned char*)ws);
-    p.L[0].nblk = update_blocks(n);
-    p.L[0].counts_only = (flags & KQ_F_COUNTS_ONLY) ? 1 : 0;
-    p.nlayers = 1;
-    p.total_blocks = p.L[0].nblk;
-    return hip_status(launch_update(p, (hipStream_t)stream));
+    const kq_layer l = {X, n, k, C_new, const_cast<int32_t*>(idx), nullptr, counts, distortion};
+    const float* olds[1] = {C_old};
+    return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0,
+                      (hipStream_t)stream);
 }
 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters, float* C,
@@ -193,7 +228,7 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k) || k > n || iters < 0 || flags != 0) return KQ_ERR_ARG;
     if (!C_init || !aligned(C_init, 4)) return KQ_ERR_ARG;
-    kq_layer l = {X, n, k, C, idx, nullptr, counts, distortion};
+    const kq_layer l = {X, n, k, C, idx, nullptr, counts, distortion};
     kq_status st = check_layers(&l, 1, true);
     if (st != KQ_OK) return st;
     st = check_ws(ws, ws_bytes, layer_ws_bytes(n, k));
@@ -215,25 +250,25 @@ kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
     if (st != KQ_OK) return st;
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        StackParams p;
-        stack_params(p, layers, l0, l1, (unsigned char*)ws, false, dist_slot, false);
-        if (launch_assign(p, (hipStream_t)stream) != hipSuccess) return KQ_ERR_HIP;
+        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, (hipStream_t)stream);
+        if (st != KQ_OK) return st;
     }
     return KQ_OK;
 }
 
-kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, uint32_t flags, void* ws, size_t ws_bytes,
-                          void* stream) {
+kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags, void* ws,
+                          size_t ws_bytes, void* stream) {
     kq_status st = check_layers(layers, n_layers, false);
     if (st != KQ_OK) return st;
-    if ((flags & ~KQ_F_COUNTS_ONLY) != 0) return KQ_ERR_ARG;
+    if (dist_slot < 0 || (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_DISTORTION_FROM_ASSIGN)) != 0) return KQ_ERR_ARG;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        StackParams p;
-        stack_params(p, layers, l0, l1, (unsigned char*)ws, true, 0, (flags & KQ_F_COUNTS_ONLY) != 0);
-        if (launch_update(p, (hipStream_t)stream) != hipSuccess) return KQ_ERR_HIP;
+        st = run_update(layers, l0, l1, (unsigned char*)ws, dist_slot, nullptr,
+                        (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0, (hipStream_t)stream,
+                        (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0);
+        if (st != KQ_OK) return st;
     }
     return KQ_OK;
 }
@@ -283,7 +318,7 @@ kq_status kq_quantize_codebook_stack(const kq_cbq_layer* layers, int32_t n_layer
 kq_status kq_quantize_codebook(const float* C, int32_t k, int32_t dim, const int32_t* weights, int32_t bits,
                                int32_t mode, int32_t iters, uint8_t* codes, float* levels, float* C_hat, void* stream) {
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
-    kq_cbq_layer l = {C, k, weights, codes, levels, C_hat};
+    const kq_cbq_layer l = {C, k, weights, codes, levels, C_hat};
     return kq_quantize_codebook_stack(&l, 1, bits, mode, iters, stream);
 }
 

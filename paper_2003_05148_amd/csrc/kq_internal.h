@@ -16,25 +16,30 @@ constexpr int kWave = 64;
 
 // ---- assignment kernel geometry -----------------------------------------------------
 // A workgroup is 4 waves; each wave scores kAssignTilesPerWave tiles of 32 kernels
-// against 32-entry codebook tiles with v_mfma_f32_32x32x2f32 (K = 10 = 9 dims + norm).
+// against 32-entry codebook tiles with v_mfma_f32_32x32x16_bf16 (a 3-part bf16 split of
+// the K = 10 fp32 contraction, 9 dims + norm).
+// A "tile" of the grid is the 256 kernels one workgroup scores at a time; the grid is
+// persistent (at most kAssignGridMax workgroups, each walking a contiguous run of tiles).
 constexpr int kAssignWaves = 4;
 constexpr int kAssignTilesPerWave = 2;
-constexpr int kAssignKernelsPerBlock = kAssignWaves * kAssignTilesPerWave * 32;   // 256
-constexpr int kAssignChunk = 1024;   // codebook entries staged in LDS at a time
+constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
+constexpr int kAssignChunk = 512;    // codebook entries staged in LDS at a time (64 KB)
+constexpr int kAssignGridMax = 512;  // 2 workgroups (occupancy 2) on each of 256 CUs
 
 // ---- update kernel geometry ---------------------------------------------------------
-constexpr int kUpdateThreads = 256;
+constexpr int kUpdateThreads = 512;
 constexpr int kUpdateKernelsPerBlock = 4096;
 constexpr int kUpdateLdsMaxK = 768;  // LDS histogram [k][9] int64 + [k] u32 up to this k
+constexpr int kFinishEntries = 16;   // codebook entries per finishing workgroup
 
 // ---- squared-error reduction ------------------------------------------------------------
 constexpr int kSqThreads = 256;
 constexpr int kSqPerBlock = 8192;
 
-inline int assign_blocks(int64_t n) { return (int)((n + kAssignKernelsPerBlock - 1) / kAssignKernelsPerBlock); }
+inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1) / kAssignKernelsPerTile); }
 inline int update_blocks(int64_t n) { return (int)((n + kUpdateKernelsPerBlock - 1) / kUpdateKernelsPerBlock); }
-
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
+inline bool update_uses_lds(int32_t k) { return k <= kUpdateLdsMaxK; }
 
 // fixed-point scale of the exact member sums: q(x) = rint(x * 2^s), s = 57 - ceil(log2 n)
 inline int fixed_shift(int64_t n) {
@@ -44,51 +49,82 @@ inline int fixed_shift(int64_t n) {
 }
 
 // ---- per-layer workspace ---------------------------------------------------------------
-//   [0, 256)            : counters (u32 assign, u32 update)
-//   [256, +8*assign_blk): fp64 per-block distortion partials
-//   [.., +8*10*k)       : int64 accumulators, 9 member sums + 1 count per entry
+//   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]   (overwritten each call)
+//   update distortion partials : fp64 [update_blocks(n)]                 (overwritten each call)
+//   update histograms          : int64 [update_blocks(n)][k][10] per-block partial sums
+//                                (k <= kUpdateLdsMaxK, overwritten each call), or int64 [k][10]
+//                                accumulators (larger k; zero-filled before each update)
 inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
-inline size_t layer_ws_bytes(int64_t n, int32_t k) {
-    return 256 + align256(sizeof(double) * (size_t)assign_blocks(n)) + align256(sizeof(int64_t) * 10 * (size_t)k);
+inline size_t ws_assign_part(int64_t n) { return align256(sizeof(double) * (size_t)assign_tiles(n) * kAssignWaves); }
+inline size_t ws_update_part(int64_t n) { return align256(sizeof(double) * (size_t)update_blocks(n)); }
+inline size_t ws_hist(int64_t n, int32_t k) {
+    const size_t copies = update_uses_lds(k) ? (size_t)update_blocks(n) : 1;
+    return align256(sizeof(int64_t) * 10 * (size_t)k * copies);
 }
+inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n) + ws_hist(n, k); }
+
+enum : int { kFlagCountsOnly = 1, kFlagAtomicHist = 2, kFlagVec = 4 };
 
 struct DevLayer {
     const float* X;
-    float* C;                 // codebook read by assign / written by update
-    const float* C_old;       // update: entries kept when empty
+    float* C;                 // assign: the codebook; update: where the new codebook goes
+    const float* C_old;       // update: entries kept when empty; the codebook of the assignment
     int32_t* idx;
     float* best_d;
     int32_t* counts;
-    double* dist;             // assign: where this call's distortion goes (or null)
-    unsigned* ctr;            // [0] assign, [1] update
-    double* part;             // assign partials
-    unsigned long long* acc;  // update accumulators [k][10]
+    double* dist;             // this call's distortion output, or null
+    double* part;             // distortion partials (assign: per wave and tile; update: per block)
+    const double* apart;      // update finish: the assignment's partials to add instead, or null
+    long long* hist;          // update histograms (see the workspace layout)
     int n;
     int k;
-    int blk_begin;            // first workgroup of this layer in the launch
-    int nblk;                 // workgroups of this layer
+    int unit_begin;           // first tile (assign) or workgroup (update) of this layer
+    int nunits;               // tiles or workgroups of this layer
     int shift;                // fixed-point scale (update)
-    int counts_only;          // update: histogram only, C untouched
+    int flags;                // kFlag*
+    int napart;               // number of assignment partials
 };
 
 struct StackParams {
     int nlayers;
-    int total_blocks;
+    int total_units;
     DevLayer L[KQ_MAX_STACK];
 };
 
-// device-side: the layer a workgroup belongs to (layers are laid out in order)
-__device__ __forceinline__ int find_layer(const StackParams& p, int b) {
+// device-side: the layer a unit (tile or workgroup) belongs to (layers are in order)
+__device__ __forceinline__ int find_layer(const StackParams& p, int u) {
     int l = 0;
 #pragma unroll 1
     for (int i = 1; i < p.nlayers; ++i)
-        if (b >= p.L[i].blk_begin) l = i;
+        if (u >= p.L[i].unit_begin) l = i;
     return l;
 }
 
+// Sum of m fp64 values in a fixed order by a workgroup of NT threads (a multiple of 64):
+// thread t adds values t, t + NT, ... in turn, each wave combines its lanes with a
+// butterfly, and thread 0 adds the wave totals in wave order.  Every thread of the
+// workgroup must call it; the result is valid in thread 0.
+template <int NT>
+__device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src, int m, double* s_w) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    double a = 0.0;
+    for (int q = tid; q < m; q += NT) a += src[q];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) a += __shfl_xor(a, off);
+    if (lane == 0) s_w[wave] = a;
+    __syncthreads();
+    double r = 0.0;
+    if (tid == 0)
+        for (int w = 0; w < NT / 64; ++w) r += s_w[w];
+    return r;
+}
+constexpr int kSumThreads = 640;
+
 // launchers (return hipSuccess or the launch error)
 hipError_t launch_assign(const StackParams& p, hipStream_t s);
+hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);
+hipError_t launch_update_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_fill_zero(void* ws, size_t bytes, hipStream_t s);
 
 struct CbqLayer {

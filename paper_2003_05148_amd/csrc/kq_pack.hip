@@ -85,13 +85,11 @@ __global__ void reconstruct_kernel(const int32_t* __restrict__ idx, const uint8_
 }
 
 // sum of squared differences, fp64, fixed order: per-thread strided sums, a
-// butterfly inside each wave, waves in order, then block partials in block order
-// by the last block to finish.
+// butterfly inside each wave, waves in order; a second kernel adds the block
+// partials in block order.
 __global__ __launch_bounds__(kSqThreads) void sq_error_kernel(const float* __restrict__ A, const float* __restrict__ B,
-                                                             long long count, double* out, unsigned* ctr,
-                                                             double* part, int nblk) {
+                                                             long long count, double* part) {
     __shared__ double s_w[kSqThreads / kWave];
-    __shared__ int s_last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const long long base = (long long)blockIdx.x * kSqPerBlock;
     double acc = 0.0;
@@ -111,18 +109,13 @@ __global__ __launch_bounds__(kSqThreads) void sq_error_kernel(const float* __res
         double v = s_w[0];
         for (int w = 1; w < kSqThreads / kWave; ++w) v += s_w[w];
         part[blockIdx.x] = v;
-        __threadfence();
-        const unsigned old = atomicInc(ctr, (unsigned)(nblk - 1));
-        s_last = (old == (unsigned)(nblk - 1));
     }
-    __syncthreads();
-    if (!s_last || wave != 0) return;
-    __threadfence();
+}
+
+__global__ __launch_bounds__(kWave) void sq_finish_kernel(const double* part, int nblk, double* out) {
+    const int lane = threadIdx.x;
     double v = 0.0;
-    for (int q = lane; q < nblk; q += kWave) {
-        v += __builtin_nontemporal_load(part + q);
-        part[q] = 0.0;  // the workspace goes back to all-zero
-    }
+    for (int q = lane; q < nblk; q += kWave) v += part[q];
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
     if (lane == 0) *out = v;
@@ -159,9 +152,11 @@ hipError_t launch_reconstruct(const int32_t* idx, const uint8_t* packed, int bit
 
 hipError_t launch_sq_error(const float* A, const float* B, int64_t count, double* out, void* ws, hipStream_t s) {
     const int nblk = sq_error_blocks(count);
-    unsigned char* base = (unsigned char*)ws;
-    hipLaunchKernelGGL(sq_error_kernel, dim3(nblk), dim3(kSqThreads), 0, s, A, B, (long long)count, out,
-                       (unsigned*)base, (double*)(base + 256), nblk);
+    double* part = (double*)ws;
+    hipLaunchKernelGGL(sq_error_kernel, dim3(nblk), dim3(kSqThreads), 0, s, A, B, (long long)count, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sq_finish_kernel, dim3(1), dim3(kWave), 0, s, (const double*)part, nblk, out);
     return hipGetLastError();
 }
 

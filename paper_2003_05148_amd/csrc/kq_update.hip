@@ -6,107 +6,218 @@
 // overflow int64 (|x| < 32).  Integer addition is associative, so the sums, and with
 // them the new codebook, do not depend on the order in which blocks or lanes add.
 //
-// A block reads 4096 consecutive kernels of one layer (36-byte rows + the index),
-// accumulates a private LDS histogram ([k][9] int64 sums + [k] counts, ds_add_u64),
-// and flushes its non-zero bins into the layer's [k][10] int64 accumulators with
-// global atomics.  Entries above kUpdateLdsMaxK skip the LDS stage and add straight
-// to the global accumulators.  The last block of a layer to finish (atomicInc on a
-// self-resetting counter) divides, writes the codebook and counts and zeroes the
-// accumulators for the next call.
+// update_kernel: a workgroup of 512 threads reads 4096 consecutive kernels of one layer,
+// four kernels (144 bytes: 9 x 16-byte loads, plus one 16-byte load of their indices)
+// per thread step when the rows are 16-byte aligned, accumulates a private LDS
+// histogram ([k][9] int64 sums + [k] counts, ds_add_u64; dynamic LDS sized for the
+// largest k of the launch) and stores it whole as its partial histogram; with more
+// than kUpdateLdsMaxK entries it adds straight into [k][10] global accumulators
+// instead.  Asked for the distortion of a standalone assignment, it also sums, in a
+// fixed order, the fp32 distances of its kernels to their entries of the old codebook.
+// update_finish_kernel: a workgroup of 640 threads owns 16 entries of one layer; four
+// groups of 160 threads add a quarter of the partial histograms each (any order gives
+// the same integers), then it divides and writes the codebook and the counts.  The
+// first workgroup of a layer also adds the distortion partials in a fixed order (those
+// of the assignment kernel when the distortion comes from there).  The kernel boundary
+// orders every partial before its use, so no fence or atomic counter is needed.
 #include "kq_internal.h"
 
 namespace kq {
 
+__device__ __forceinline__ float sqdist9u(const float* x, const float* __restrict__ c) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int d = 0; d < kDim; ++d) {
+        const float t = x[d] - c[d];
+        acc = __fmaf_rn(t, t, acc);
+    }
+    return acc;
+}
+
+struct UpdateCtx {
+    unsigned long long* s_sum;
+    unsigned* s_cnt;
+    unsigned long long* acc;
+    const float* C_old;
+    double scale;
+    int k;
+    bool use_lds, sums, want_dist;
+};
+
+// add one kernel (row x, entry j) to the histogram
+__device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[kDim], int j, double& dacc) {
+    if ((unsigned)j >= (unsigned)c.k) return;
+    if (c.want_dist) dacc += (double)sqdist9u(x, c.C_old + (size_t)j * kDim);
+    if (c.use_lds) {
+        atomicAdd(&c.s_cnt[j], 1u);
+        if (c.sums) {
+#pragma unroll
+            for (int d = 0; d < kDim; ++d)
+                atomicAdd(&c.s_sum[j * kDim + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
+        }
+    } else {
+        atomicAdd(&c.acc[(size_t)j * 10 + 9], 1ull);
+        if (c.sums) {
+#pragma unroll
+            for (int d = 0; d < kDim; ++d)
+                atomicAdd(&c.acc[(size_t)j * 10 + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
+        }
+    }
+}
+
 __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParams p) {
-    __shared__ unsigned long long s_sum[kUpdateLdsMaxK * kDim];
-    __shared__ unsigned s_cnt[kUpdateLdsMaxK];
-    __shared__ int s_last;
+    extern __shared__ unsigned long long s_dyn[];  // [k][9] sums, then [k] u32 counts
+    __shared__ double s_wd[kUpdateThreads / kWave];
 
     const int li = find_layer(p, blockIdx.x);
     const DevLayer& L = p.L[li];
-    const int lb = blockIdx.x - L.blk_begin;
-    const int tid = threadIdx.x;
+    const int lb = blockIdx.x - L.unit_begin;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = L.n, k = L.k;
-    const bool use_lds = k <= kUpdateLdsMaxK;
-    const bool sums = !L.counts_only;
-    const double scale = ldexp(1.0, L.shift);
+    UpdateCtx c;
+    c.s_sum = s_dyn;
+    c.s_cnt = (unsigned*)(s_dyn + (size_t)k * kDim);
+    c.acc = (unsigned long long*)L.hist;
+    c.C_old = L.C_old;
+    c.scale = ldexp(1.0, L.shift);
+    c.k = k;
+    c.use_lds = (L.flags & kFlagAtomicHist) == 0;
+    c.sums = (L.flags & kFlagCountsOnly) == 0;
+    c.want_dist = L.part != nullptr;
+    const bool need_x = c.sums || c.want_dist;
     const float* __restrict__ X = L.X;
     const int32_t* __restrict__ idx = L.idx;
-    unsigned long long* __restrict__ acc = L.acc;
 
-    if (use_lds) {
-        for (int e = tid; e < k * kDim; e += kUpdateThreads) s_sum[e] = 0ull;
-        for (int e = tid; e < k; e += kUpdateThreads) s_cnt[e] = 0u;
+    if (c.use_lds) {
+        for (int e = tid; e < k * kDim; e += kUpdateThreads) c.s_sum[e] = 0ull;
+        for (int e = tid; e < k; e += kUpdateThreads) c.s_cnt[e] = 0u;
         __syncthreads();
     }
 
+    double dacc = 0.0;
     const int i0 = lb * kUpdateKernelsPerBlock;
     const int i1 = min(n, i0 + kUpdateKernelsPerBlock);
-#pragma unroll 2
-    for (int i = i0 + tid; i < i1; i += kUpdateThreads) {
-        const int j = idx[i];
-        if ((unsigned)j >= (unsigned)k) continue;
-        float x[kDim];
-        if (sums) {
+    int iv = i0;  // first row not covered by the vector path
+    if (L.flags & kFlagVec) {
+        // groups of 4 rows: 36 floats = 9 aligned float4 (i0 is a multiple of 4)
+        const int g0 = i0 >> 2, g1 = i1 >> 2;
+        for (int g = g0 + tid; g < g1; g += kUpdateThreads) {
+            const int4 jj = ((const int4*)idx)[g];
+            float f[36];
+            if (need_x) {
+                const float4* src = (const float4*)X + (size_t)g * 9;
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) x[d] = X[(size_t)i * kDim + d];
-        }
-        if (use_lds) {
-            atomicAdd(&s_cnt[j], 1u);
-            if (sums) {
-#pragma unroll
-                for (int d = 0; d < kDim; ++d)
-                    atomicAdd(&s_sum[j * kDim + d], (unsigned long long)__double2ll_rn((double)x[d] * scale));
-            }
-        } else {
-            atomicAdd(&acc[(size_t)j * 10 + 9], 1ull);
-            if (sums) {
-#pragma unroll
-                for (int d = 0; d < kDim; ++d)
-                    atomicAdd(&acc[(size_t)j * 10 + d], (unsigned long long)__double2ll_rn((double)x[d] * scale));
-            }
-        }
-    }
-
-    if (use_lds) {
-        __syncthreads();
-        for (int e = tid; e < k * 10; e += kUpdateThreads) {
-            const int j = e / 10, d = e - 10 * (e / 10);
-            const unsigned long long v = (d == 9) ? (unsigned long long)s_cnt[j] : s_sum[j * kDim + d];
-            if (v) atomicAdd(&acc[e], v);
-        }
-    }
-
-    // the last block of the layer finalises (counter wraps back to 0 by itself)
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const unsigned old = atomicInc(&L.ctr[1], (unsigned)(L.nblk - 1));
-        s_last = (old == (unsigned)(L.nblk - 1));
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    const double inv_scale = ldexp(1.0, -L.shift);
-    for (int j = tid; j < k; j += kUpdateThreads) {
-        unsigned long long* a = acc + (size_t)j * 10;
-        const long long z = (long long)__builtin_nontemporal_load(a + 9);
-        if (L.counts) L.counts[j] = (int32_t)z;
-        if (sums) {
-#pragma unroll
-            for (int d = 0; d < kDim; ++d) {
-                float c;
-                if (z > 0) {
-                    const long long S = (long long)__builtin_nontemporal_load(a + d);
-                    c = (float)(((double)S * inv_scale) / (double)z);
-                } else {
-                    c = L.C_old[(size_t)j * kDim + d];
+                for (int q = 0; q < 9; ++q) {
+                    const float4 v = src[q];
+                    f[4 * q] = v.x;
+                    f[4 * q + 1] = v.y;
+                    f[4 * q + 2] = v.z;
+                    f[4 * q + 3] = v.w;
                 }
-                L.C[(size_t)j * kDim + d] = c;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 36; ++q) f[q] = 0.0f;
+            }
+            const int js[4] = {jj.x, jj.y, jj.z, jj.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float x[kDim];
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) x[d] = f[9 * r + d];
+                add_kernel(c, x, js[r], dacc);
             }
         }
+        iv = g1 << 2;
+    }
+    for (int i = iv + tid; i < i1; i += kUpdateThreads) {
+        float x[kDim];
 #pragma unroll
-        for (int d = 0; d < 10; ++d) a[d] = 0ull;
+        for (int d = 0; d < kDim; ++d) x[d] = need_x ? X[(size_t)i * kDim + d] : 0.0f;
+        add_kernel(c, x, idx[i], dacc);
+    }
+
+    if (c.use_lds) {
+        __syncthreads();
+        unsigned long long* __restrict__ out = c.acc + (size_t)lb * k * 10;
+        for (int e = tid; e < k * 10; e += kUpdateThreads) {
+            const int j = e / 10, d = e - 10 * j;
+            out[e] = (d == 9) ? (unsigned long long)c.s_cnt[j] : c.s_sum[j * kDim + d];
+        }
+    }
+    if (c.want_dist) {
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) dacc += __shfl_xor(dacc, off);
+        if (lane == 0) s_wd[wave] = dacc;
+        __syncthreads();
+        if (tid == 0) {
+            double v = s_wd[0];
+            for (int w = 1; w < kUpdateThreads / kWave; ++w) v += s_wd[w];
+            L.part[lb] = v;
+        }
+    }
+}
+
+constexpr int kFinishGroups = 4;
+constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
+static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
+
+__global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const StackParams p) {
+    __shared__ long long s_S[kFinishGroups][kFinishEntries * 10];
+    __shared__ double s_w[kSumThreads / kWave];
+    // layer and entry range of this workgroup: each layer owns ceil(k / 16) workgroups
+    int li = 0;
+    const int b = blockIdx.x;
+    while (li + 1 < p.nlayers && b >= p.L[li + 1].unit_begin) ++li;
+    const DevLayer& L = p.L[li];
+    const int j0 = (b - L.unit_begin) * kFinishEntries;
+    const int tid = threadIdx.x;
+    const int g = tid / (kFinishEntries * 10), v = tid - g * (kFinishEntries * 10);
+    const int j = j0 + v / 10, d = v - 10 * (v / 10);
+    const bool atomic_hist = (L.flags & kFlagAtomicHist) != 0;
+    const int k = L.k;
+    const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;
+
+    unsigned long long s = 0ull;
+    if (j < k) {
+        if (atomic_hist) {
+            if (g == 0) s = h[(size_t)j * 10 + d];
+        } else {
+            const int nb = L.nunits;
+            const size_t stride = (size_t)k * 10;
+            const unsigned long long* hp = h + (size_t)j * 10 + d;
+            int q = g;
+#pragma unroll 1
+            for (; q + 3 * kFinishGroups < nb; q += 4 * kFinishGroups)
+                s += hp[q * stride] + hp[(q + kFinishGroups) * stride] + hp[(q + 2 * kFinishGroups) * stride] +
+                     hp[(q + 3 * kFinishGroups) * stride];
+            for (; q < nb; q += kFinishGroups) s += hp[q * stride];
+        }
+    }
+    s_S[g][v] = (long long)s;
+    __syncthreads();
+    if (g == 0 && j < k) {
+        long long S = 0, z = 0;
+#pragma unroll
+        for (int q = 0; q < kFinishGroups; ++q) {
+            S += s_S[q][v];
+            z += s_S[q][(v / 10) * 10 + 9];
+        }
+        if (d == 9) {
+            if (L.counts) L.counts[j] = (int32_t)z;
+        } else if ((L.flags & kFlagCountsOnly) == 0) {
+            float c;
+            if (z > 0)
+                c = (float)(((double)S * ldexp(1.0, -L.shift)) / (double)z);
+            else
+                c = L.C_old[(size_t)j * kDim + d];
+            L.C[(size_t)j * kDim + d] = c;
+        }
+    }
+    if (j0 == 0 && L.dist != nullptr) {
+        const double* src = L.apart ? L.apart : L.part;
+        const int m = L.apart ? L.napart : L.nunits;
+        const double a = block_fixed_sum<kSumThreads>(src, m, s_w);
+        if (tid == 0) *L.dist = a;
     }
 }
 
@@ -118,7 +229,26 @@ __global__ void fill_zero_kernel(uint4* p, size_t n16, unsigned char* tail, size
 }
 
 hipError_t launch_update(const StackParams& p, hipStream_t s) {
-    hipLaunchKernelGGL(update_kernel, dim3(p.total_blocks), dim3(kUpdateThreads), 0, s, p);
+    size_t lds = 0;
+    for (int l = 0; l < p.nlayers; ++l)
+        if ((p.L[l].flags & kFlagAtomicHist) == 0) {
+            const size_t b = (size_t)p.L[l].k * (kDim * sizeof(unsigned long long) + sizeof(unsigned));
+            lds = b > lds ? b : lds;
+        }
+    hipLaunchKernelGGL(update_kernel, dim3(p.total_units), dim3(kUpdateThreads), lds, s, p);
+    return hipGetLastError();
+}
+
+// the finishing launch numbers its workgroups per layer: ceil(k / 16) each
+hipError_t launch_update_finish(const StackParams& p, hipStream_t s) {
+    StackParams q = p;
+    int blk = 0;
+    for (int l = 0; l < q.nlayers; ++l) {
+        q.L[l].unit_begin = blk;
+        blk += (q.L[l].k + kFinishEntries - 1) / kFinishEntries;
+    }
+    // nunits keeps the number of update workgroups (partials to add)
+    hipLaunchKernelGGL(update_finish_kernel, dim3(blk), dim3(kFinishThreads), 0, s, q);
     return hipGetLastError();
 }
 

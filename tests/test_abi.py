@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 1
+    assert lib.kq_abi_version() == 2
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -79,12 +79,15 @@ def test_assign_argument_errors():
 
 def test_update_and_fit_argument_errors():
     up = lambda **kw: lib.kq_update(kw.get("X", FAKE), kw.get("n", 100), kw.get("dim", 9), kw.get("idx", FAKE),
-                                    kw.get("k", 8), kw.get("Co", FAKE), kw.get("Cn", FAKE), kw.get("cnt", None), 0,
-                                    kw.get("ws", None), kw.get("wsb", 0), None)
+                                    kw.get("k", 8), kw.get("Co", FAKE), kw.get("Cn", FAKE), kw.get("cnt", None),
+                                    kw.get("dist", None), kw.get("flags", 0), kw.get("ws", None), kw.get("wsb", 0),
+                                    None)
     assert up(dim=4) == kq.KQ_ERR_UNSUPPORTED
     assert up(n=-1) == kq.KQ_ERR_ARG
     assert up(Co=None) == kq.KQ_ERR_ARG
     assert up(cnt=FAKE + 2) == kq.KQ_ERR_ARG
+    assert up(dist=FAKE + 4) == kq.KQ_ERR_ARG
+    assert up(flags=2) == kq.KQ_ERR_ARG
     assert up() == kq.KQ_ERR_WORKSPACE
     fit = lambda **kw: lib.kq_fit_layer(FAKE, kw.get("n", 100), 9, kw.get("k", 8), kw.get("Ci", FAKE),
                                         kw.get("iters", 3), FAKE, FAKE, None, None, 0, kw.get("ws", None),
@@ -108,7 +111,7 @@ def test_stack_argument_errors():
     assert lib.kq_assign_stack(None, 2, 0, 0, FAKE, need, None) == kq.KQ_ERR_ARG
     assert lib.kq_assign_stack(p, 2, -1, 0, FAKE, need, None) == kq.KQ_ERR_ARG
     arr[1] = kq.KqLayer(FAKE, 100, kq.KQ_MAX_K + 1, FAKE, FAKE, None, FAKE, None)
-    assert lib.kq_update_stack(p, 2, 0, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_update_stack(p, 2, 0, 0, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
 
 
 def test_cbq_pack_reconstruct_argument_errors():
@@ -133,6 +136,8 @@ def test_cbq_pack_reconstruct_argument_errors():
     assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 8, FAKE, None) == kq.KQ_ERR_UNSUPPORTED
     assert lib.kq_reconstruct_packed(None, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG
     assert lib.kq_workspace_init(FAKE + 8, 100, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_sq_error(FAKE, FAKE, 0, FAKE, FAKE, 1 << 20, None) == kq.KQ_ERR_ARG
+    assert lib.kq_sq_error(FAKE, FAKE, 100, FAKE, FAKE, 0, None) == kq.KQ_ERR_WORKSPACE
     assert lib.kq_workspace_init(FAKE, 0, None) == kq.KQ_OK
 
 

@@ -88,9 +88,12 @@ def test_assign_nonfinite_inputs_match_plain_scan():
 
 
 def check_update(X, idx, C_old, tag=""):
-    C_new, counts = kq.kq_update(dev(X), dev(idx), dev(C_old))
+    C_new, counts, J = kq.kq_update(dev(X), dev(idx), dev(C_old))
     gc, gz = host(C_new), host(counts)
     oc, oz = oracle.update(X, idx, C_old)
+    ok = (idx >= 0) & (idx < C_old.shape[0])
+    Jo = oracle.distortion(X[ok], C_old, idx[ok])
+    assert float(host(J)[0]) == pytest.approx(Jo, rel=REL, abs=1e-30), tag
     assert np.array_equal(gz, oz), tag
     empty = oz == 0
     assert np.array_equal(gc[empty], C_old[empty]), tag
@@ -123,7 +126,7 @@ def test_update_in_place_and_ignores_bad_indices():
     bad = idx.copy()
     bad[:10] = 77
     bad[10:20] = -1
-    gc, gz = kq.kq_update(dev(X), dev(bad), dev(C))
+    gc, gz, _ = kq.kq_update(dev(X), dev(bad), dev(C))
     keep = np.arange(n) >= 20
     oc, oz = oracle.update(X[keep], bad[keep], C)
     assert np.array_equal(host(gz), oz)
@@ -139,7 +142,8 @@ def test_fit_step_locked_single_layer():
         idx, best_d, dist = kq.kq_assign(Xd, dev(C))
         o = oracle.assign(L.X, C)
         assert np.array_equal(host(idx), o["idx"]), t
-        C_g, z_g = kq.kq_update(Xd, idx, dev(C))
+        C_g, z_g, J_g = kq.kq_update(Xd, idx, dev(C))
+        assert float(host(J_g)[0]) == pytest.approx(float(np.sum(o["d1"])), rel=REL), t
         C_o, z_o = oracle.update(L.X, o["idx"], C)
         assert np.array_equal(host(z_g), z_o), t
         err = np.abs(host(C_g).astype(np.float64) - C_o).max(axis=1)
@@ -187,6 +191,7 @@ def test_stack_full_size_resnet18_sampled():
         C_before = [host(c) for c in st.C]
         kq.kq_assign_stack(st, dist_slot=t)
         idx = [host(i) for i in st.idx]
+        Ja = [float(host(d)[t]) for d in st.distortion]
         for L, Cb, gi, gd, gJ in zip(layers, C_before, idx, st.best_d, st.distortion):
             rows = rng.choice(L.n, min(L.n, 1500), replace=False)
             o = oracle.assign(L.X[rows], Cb)
@@ -194,7 +199,12 @@ def test_stack_full_size_resnet18_sampled():
             assert np.array_equal(host(gd)[rows], o["d32"]), (L.name, t)
             Jo = oracle.distortion(L.X, Cb, gi)
             assert float(host(gJ)[t]) == pytest.approx(Jo, rel=REL), (L.name, t)
-        kq.kq_update_stack(st)
+        kq.kq_update_stack(st, dist_slot=t)
+        for Jassign, gJ in zip(Ja, st.distortion):           # update measures the same objective
+            assert float(host(gJ)[t]) == pytest.approx(Jassign, rel=1e-12)
+        kq.kq_update_stack(st, dist_slot=t, counts_only=True, distortion_from_assign=True)
+        for Jassign, gJ in zip(Ja, st.distortion):           # the assignment's own partials: same bits
+            assert float(host(gJ)[t]) == Jassign
         for L, Cb, gi, gC, gz in zip(layers, C_before, idx, st.C, st.counts):
             oc, oz = oracle.update(L.X, gi, Cb)
             assert np.array_equal(host(gz), oz), L.name

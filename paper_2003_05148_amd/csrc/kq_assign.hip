@@ -5,81 +5,61 @@
 //
 // Screening on the matrix cores.  Up to the constant |x|^2, d(x, c_j) is the score
 //     s_j = |c_j|^2 - 2 x . c_j = sum_{d < 10} w_jd y_d,  w_j = (-2 c_j, |c_j|^2), y = (x, 1).
-// Every fp32 value v is split into three bf16 parts v = v_h + v_m + v_l (each part the
-// round-to-nearest bf16 of what the previous ones leave), and the six cross terms that
-// carry fp32 precision, w_h y_h + w_h y_m + w_m y_h + w_h y_l + w_l y_h + w_m y_m, form a
-// K = 60 (padded to 64) bf16 contraction: four v_mfma_f32_32x32x16_bf16 per 32 x 32
-// tile of (codebook entries, kernels), products exact and sums in fp32.  In the 32x32
-// D layout lane l holds column (kernel) l % 32 and 16 rows (entries); per register slot
-// it keeps the best and the second-best score, the best carrying its codebook tile in
-// its low mantissa bits (3 VALU ops per score: and-or and two med3).
+// Every fp32 value v is split exactly into v = v_h + v_m + v_l with v_h = bf16(v) and
+// v_m = bf16(v - v_h) (round to nearest), and the three cross terms w_h y_h + w_h y_m +
+// w_m y_h form a K = 30 (padded to 32) bf16 contraction: two v_mfma_f32_32x32x16_bf16
+// per 32 x 32 tile of (codebook entries, kernels), products exact and sums in fp32.  In
+// the 32x32 D layout lane l holds column (kernel) l % 32 and 16 of its rows (entries);
+// the 32 rows of a kernel are its "slots", slot r holding entries r, r + 32, r + 64, ...
+// Each lane keeps the minimum score of each slot, one v_min3 per two scores.
 //
-// Exactness guard.  Let Q = (|x| + max_j |c_j|)^2 and u = 2^-24.  A screened score is
-// within 84 u Q of its exact value (dropped cross terms and split remainders 7 u Q, at
-// most 68 fp32 roundings in the MFMA sums, 9 u Q in the fp32 norm) plus 32 u Q for the
-// packed tile bits, and the fp32 distance of any entry is within 12 u of its exact value.
-// So when the two best screened scores are more than theta = 2^-15 Q + 2^-100 apart
-// (512 u Q, against 257 u Q needed) the screened winner is the fp32 argmin.  Kernels
-// below that gap are rescored over the whole codebook in the exact fp32 form by their
-// wave.  The output is therefore the plain fp32 argmin, bit for bit.
+// Exactness.  Let Q = (|x| + max_j |c_j|)^2 and u = 2^-24; every |s_j| <= Q.  A screened
+// score is within 842 u Q of its exact value (dropped cross terms 3 * 2^-16 Q, at most
+// 33 fp32 roundings in the MFMA sums, 9 u Q in the fp32 norm) plus 32 u Q where a slot
+// minimum carries its slot number in its 4 lowest mantissa bits, and the fp32 distance
+// of any entry is within 12 u Q of its exact value.  The entries of the slot with the
+// smallest minimum are rescored in the plain fp32 form; when every other slot's minimum
+// exceeds it by more than theta = 2^-13 Q + 2^-100 (2048 u Q, against
+// 2 (842 + 32 + 12) u Q = 1772 u Q needed), no entry outside that slot can reach the
+// slot's fp32 minimum, so the slot's fp32 argmin (lowest index on ties) is the answer.
+// Kernels below that gap are rescored over the whole codebook in the exact fp32 form by
+// their wave.  The output is therefore the plain fp32 argmin, bit for bit.
 //
 // Grid.  Kernels are cut into tiles of 256 (one per workgroup pass); tiles of all
 // layers of a stack are numbered layer after layer and a persistent grid of at most
-// kAssignGridMax workgroups walks contiguous runs of them.  A codebook of up to 512
-// entries is split and staged once per layer in LDS in the MFMA A-operand order
-// [tile][k-step][lane][8 x bf16] (one conflict-free ds_read_b128 per MFMA); larger
-// ones are streamed through LDS in 512-entry chunks.  The next tile's kernels are
-// loaded while the current one is scored.  After the scoring each wave settles its own
-// 64 kernels (no workgroup barrier) and, when asked, writes an fp64 distortion
-// partial; a second kernel sums the partials in a fixed order.
+// kAssignGridMax workgroups walks contiguous runs of them.  A codebook of up to
+// kAssignChunk entries is split and staged once per layer in LDS, in the MFMA A-operand
+// order [tile][k-step][lane][8 x bf16] (one conflict-free ds_read_b128 per MFMA
+// operand) and as fp32 rows for the slot rescoring; larger ones are streamed through LDS
+// chunk by chunk.  Each lane splits its own kernel; the B operands of the two 32-kernel
+// tiles of a wave are exchanged between the lane halves with v_permlane32_swap.  The next
+// tile's kernels are loaded while the current one is scored.  After the scoring each wave
+// settles its own 64 kernels (no workgroup barrier) and, when asked, writes an fp64
+// distortion partial; a second kernel sums the partials in a fixed order.
 #include "kq_internal.h"
 
 namespace kq {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-// ---- the bf16 contraction ----------------------------------------------------------------
-// term k < 60 of the contraction: dimension k % 10 of cross term k / 10; the cross terms
-// (entry part, kernel part) are (h,h), (h,m), (m,h), (h,l), (l,h), (m,m); k >= 60 is zero.
-__host__ __device__ constexpr int term_dim(int k) { return k % 10; }
-__host__ __device__ constexpr int term_wpart(int k) { return (k / 10 == 2 || k / 10 == 5) ? 1 : (k / 10 == 4 ? 2 : 0); }
-__host__ __device__ constexpr int term_ypart(int k) { return (k / 10 == 1 || k / 10 == 5) ? 1 : (k / 10 == 3 ? 2 : 0); }
+constexpr int kRowFloats = 12;      // fp32 codebook rows in LDS: 9 values, padded to 48 bytes
+constexpr float kPadScore = 1e38f;  // score of padding entries: finite and above any trusted score
+constexpr float kTrustQ = 1e37f;    // Q at or above this: no screening result is trusted
+static_assert(kAssignChunk % 64 == 0, "chunks hold whole pairs of 32-entry tiles");
 
-__device__ __forceinline__ float bf16_round(float v) { return (float)(__bf16)v; }
-
-// v = h + m + l with h, m, l representable in bf16 (up to a remainder below 2^-25 |v|)
-__device__ __forceinline__ void split3(float v, float& h, float& m, float& l) {
-    h = bf16_round(v);
-    const float r = v - h;  // exact
-    m = bf16_round(r);
-    l = bf16_round(r - m);  // r - m exact
+// two fp32 values split exactly: v = h + m + l with h = bf16(v), m = bf16(v - h); H and M
+// hold (h(a), h(b)) and (m(a), m(b)) packed, a in the low half
+__device__ __forceinline__ void split2(float a, float b, unsigned& H, unsigned& M) {
+    const f32x2 v = {a, b};
+    H = __builtin_bit_cast(unsigned, __builtin_convertvector(v, bf16x2));
+    const f32x2 r = {a - __uint_as_float(H << 16), b - __uint_as_float(H & 0xffff0000u)};  // exact
+    M = __builtin_bit_cast(unsigned, __builtin_convertvector(r, bf16x2));
 }
-
-// B operands (kernel side) of one kernel: lane half `half` holds terms 16 kk + 8 half + e
-__device__ __forceinline__ void build_b(const float (&x)[kDim], bool valid, int half, bf16x8 (&b)[4]) {
-    float p[3][10];
-#pragma unroll
-    for (int d = 0; d < kDim; ++d) split3(valid ? x[d] : 0.0f, p[0][d], p[1][d], p[2][d]);
-    p[0][9] = valid ? 1.0f : 0.0f;
-    p[1][9] = 0.0f;
-    p[2][9] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int k0 = 16 * kk + e, k1 = 16 * kk + 8 + e;
-            const float v0 = k0 < 60 ? p[term_ypart(k0)][term_dim(k0)] : 0.0f;
-            const float v1 = k1 < 60 ? p[term_ypart(k1)][term_dim(k1)] : 0.0f;
-            b[kk][e] = (__bf16)(half ? v1 : v0);
-        }
-}
-
-// Scores are folded with the codebook tile (0..15 within a 512-entry chunk) packed into
-// their 5 lowest mantissa bits, so one med3 keeps the best score and its tile.  The
-// packing moves a score by less than 2^-19 of its magnitude; the guard allows for it.
-constexpr unsigned kTileMask = 31u;
-constexpr float kPadScore = 1e38f;  // score of padding entries: finite, so packing keeps a number
 
 __device__ __forceinline__ float sqdist9(const float* x, const float* c) {
     float acc = 0.0f;
@@ -91,47 +71,17 @@ __device__ __forceinline__ float sqdist9(const float* x, const float* c) {
     return acc;
 }
 
-// merge two (best, index, second) summaries; exact ties of the screened best are always
-// caught by the guard (the second then equals the best), so any winner is fine here
-__device__ __forceinline__ void merge_top2(float& b, int& j, float& s, float ob, int oj, float os) {
-    const float mx = __builtin_amdgcn_fmed3f(b, ob, __builtin_inff());
-    s = __builtin_amdgcn_fmed3f(__builtin_amdgcn_fmed3f(s, os, -__builtin_inff()), mx, -__builtin_inff());
-    const bool lt = ob < b;
-    b = lt ? ob : b;
-    j = lt ? oj : j;
+__device__ __forceinline__ float min2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, -3.402823466e38f); }
+
+// A operands (entries) of codebook tiles 2 p and 2 p + 1
+__device__ __forceinline__ void lds_a(u32x4 (&a)[2][2], const u32x4* s_a, int p, int lane) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) a[t][kk] = s_a[((2 * p + t) * 2 + kk) * kWave + lane];
 }
 
-// the 32 x 32 scores of one codebook tile (A operands a) against the wave's R kernel tiles
-template <int R>
-__device__ __forceinline__ void score_tile(f32x16 (&acc)[R], const bf16x8 (&a)[4], const bf16x8 (&b)[R][4]) {
-    const f32x16 zero = {0.0f};
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[r][0], zero, 0, 0, 0);
-#pragma unroll
-    for (int kk = 1; kk < 4; ++kk)
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-            acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], b[r][kk], acc[r], 0, 0, 0);
-}
-
-// per register slot: second = med3(best, second, s), best = med3(best, s, -FLT_MAX)
-// = min(best, s) -- 3 VALU ops (v_and_or_b32 with the tile held in a VGPR, 2 v_med3_f32)
-template <int R>
-__device__ __forceinline__ void fold_tile(const f32x16 (&acc)[R], unsigned tile, float (&best)[R][16],
-                                          float (&sec)[R][16]) {
-    unsigned vt;
-    asm("v_mov_b32 %0, %1" : "=v"(vt) : "s"(tile));
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const float sp = __uint_as_float((__float_as_uint(acc[r][q]) & ~kTileMask) | vt);
-            sec[r][q] = __builtin_amdgcn_fmed3f(best[r][q], sec[r][q], sp);
-            best[r][q] = __builtin_amdgcn_fmed3f(best[r][q], sp, -3.402823466e38f);
-        }
-}
-
-// this lane's kernel (kernel 256 t + 64 wave + lane of the layer); zeros past the end
+// this lane's kernel (kernel 256 t + 64 wave + lane of the layer); a valid row past the end
 __device__ __forceinline__ void load_kernel(const DevLayer& L, int tile, int wave, int lane, float (&x)[kDim]) {
     const int i = tile * kAssignKernelsPerTile + wave * kWave + lane;
     const int ic = i < L.n ? i : L.n - 1;
@@ -139,20 +89,28 @@ __device__ __forceinline__ void load_kernel(const DevLayer& L, int tile, int wav
     for (int d = 0; d < kDim; ++d) x[d] = L.X[(size_t)ic * kDim + d];
 }
 
-__device__ __forceinline__ void global_entry(const float* __restrict__ C, int j, float (&c)[kDim]) {
-#pragma unroll
-    for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)j * kDim + d];
+// (best, second, index, distance) summaries; a tie of the screened bests makes the second
+// equal to the best, which the guard rejects, so either winner may be kept
+__device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d, float ob, float os, int oj,
+                                           float od) {
+    const float mx = fmaxf(b, ob);
+    s = fminf(fminf(s, os), mx);
+    const bool lt = ob < b;
+    b = lt ? ob : b;
+    j = lt ? oj : j;
+    d = lt ? od : d;
 }
 
 template <int R>
 __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const StackParams p) {
-    static_assert(R == 2, "one kernel per lane in the epilogue needs R == 2");
-    __shared__ bf16x8 s_a[kAssignChunk / 32 * 4 * kWave];  // [tile][k-step][lane] A operands
-    __shared__ float s_wmax[kAssignWaves];                  // per-wave max |c|^2 of the staged codebook
+    static_assert(R == 2, "one kernel per lane and the half exchange need two kernel tiles per wave");
+    __shared__ u32x4 s_a[kAssignChunk / 32 * 2 * kWave];  // [tile][k-step][lane] A operands
+    __shared__ f32x4 s_c[kAssignChunk * kRowFloats / 4];   // fp32 rows of the staged entries
+    __shared__ float s_wmax[kAssignWaves];                 // per-wave max |c|^2 of the staged codebook
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int col = lane & 31, half = lane >> 5;
+    const int half = lane >> 5;
     const long long T = p.total_units;
     int t = (int)((long long)blockIdx.x * T / gridDim.x);
     const int t_end = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);
@@ -162,6 +120,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
     int staged = -1;  // layer whose whole codebook is resident in LDS
     float xo[kDim];   // this lane's kernel of the current tile
     load_kernel(p.L[li], t - p.L[li].unit_begin, wave, lane, xo);
+    const float* s_cf = reinterpret_cast<const float*>(s_c);
 
 #pragma unroll 1
     for (; t < t_end; ++t) {
@@ -181,35 +140,40 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
             load_kernel(p.L[ln], t + 1 - p.L[ln].unit_begin, wave, lane, xn);
         }
 
-        // B operands: kernel tile r of this wave is kernels 64 wave + 32 r + col, i.e. the
-        // kernel of lane col + 32 r; lanes swap kernels with their partner half
-        bf16x8 bop[R][4];
+        // B operands.  Kernel tile r of this wave is kernels 64 wave + 32 r + (lane % 32), the
+        // kernels of lanes 32 r .. 32 r + 31.  Lane (col, half) needs, for k-step kk, dwords
+        // 8 kk + 4 half .. + 3 of the column's kernel; dword e packs terms 2e, 2e + 1:
+        // [y_h pairs 0..4 | y_m pairs 0..4 | y_h pairs 0..4 | 0].
+        u32x4 bop[R][2];
         {
-            float xp[kDim];
+            unsigned H[5], M[5];
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) xp[d] = __shfl_xor(xo[d], 32);
-            const bool vp = __shfl_xor((int)valid, 32) != 0;
-            // tile `half` is this lane's own kernel, tile 1 - half the partner's
-            bf16x8 own[4], par[4];
-            build_b(xo, valid, half, own);
-            build_b(xp, vp, half, par);
+            for (int q = 0; q < 4; ++q)
+                split2(valid ? xo[2 * q] : 0.0f, valid ? xo[2 * q + 1] : 0.0f, H[q], M[q]);
+            split2(valid ? xo[8] : 0.0f, valid ? 1.0f : 0.0f, H[4], M[4]);
+            unsigned D[16];
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                bop[0][kk] = half ? par[kk] : own[kk];
-                bop[1][kk] = half ? own[kk] : par[kk];
+            for (int q = 0; q < 5; ++q) {
+                D[q] = H[q];
+                D[5 + q] = M[q];
+                D[10 + q] = H[q];
             }
-        }
-
-        float rb[R], rs[R];
-        int rj[R];
+            D[15] = 0u;
+            // lanes < 32 own tile 0 and lanes >= 32 tile 1: swapping (D[8kk+e], D[8kk+4+e])
+            // across the halves leaves tile 0's operand in the first result, tile 1's in the second
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            rb[r] = __builtin_inff();
-            rs[r] = __builtin_inff();
-            rj[r] = 0x7fffffff;
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const auto sw = __builtin_amdgcn_permlane32_swap(D[8 * kk + e], D[8 * kk + 4 + e], false, false);
+                    bop[0][kk][e] = sw[0];
+                    bop[1][kk][e] = sw[1];
+                }
         }
 
-        const int kpad = (k + 31) & ~31;
+        float rb = __builtin_inff(), rs = __builtin_inff(), rd = __builtin_inff();  // running summary
+        int rj = 0x7fffffff;
+        const int kpad = (k + 63) & ~63;
         const bool resident = kpad <= kAssignChunk;
         float tmax = 0.0f;
 #pragma unroll 1
@@ -219,36 +183,47 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
                 __syncthreads();  // every wave is done with the previous contents
                 for (int jl = tid; jl < cn; jl += kAssignWaves * kWave) {
                     const int j = c0 + jl;
-                    float w[3][10];
+                    float c[kDim], w[10];
                     if (j < k) {
-                        float c[kDim];
-                        global_entry(C, j, c);
+#pragma unroll
+                        for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)j * kDim + d];
                         float nn = 0.0f;
 #pragma unroll
                         for (int d = 0; d < kDim; ++d) {
                             nn = __fmaf_rn(c[d], c[d], nn);
-                            split3(-2.0f * c[d], w[0][d], w[1][d], w[2][d]);
+                            w[d] = -2.0f * c[d];
                         }
-                        split3(nn, w[0][9], w[1][9], w[2][9]);
+                        w[9] = nn;
                         tmax = fmaxf(tmax, nn);
                     } else {
 #pragma unroll
-                        for (int d = 0; d < kDim; ++d) w[0][d] = w[1][d] = w[2][d] = 0.0f;
-                        split3(kPadScore, w[0][9], w[1][9], w[2][9]);
+                        for (int d = 0; d < kDim; ++d) c[d] = w[d] = 0.0f;
+                        w[9] = kPadScore;
                     }
+                    unsigned H[5], M[5], A[16];
+#pragma unroll
+                    for (int q = 0; q < 5; ++q) split2(w[2 * q], w[2 * q + 1], H[q], M[q]);
+                    // [w_h pairs 0..4 | w_h pairs 0..4 | w_m pairs 0..4 | 0]
+#pragma unroll
+                    for (int q = 0; q < 5; ++q) {
+                        A[q] = H[q];
+                        A[5 + q] = H[q];
+                        A[10 + q] = M[q];
+                    }
+                    A[15] = 0u;
                     const int tl = jl >> 5, row = jl & 31;
 #pragma unroll
-                    for (int kk = 0; kk < 4; ++kk)
+                    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
-                            bf16x8 v;
-#pragma unroll
-                            for (int e = 0; e < 8; ++e) {
-                                const int kt = 16 * kk + 8 * h + e;
-                                v[e] = (__bf16)(kt < 60 ? w[term_wpart(kt)][term_dim(kt)] : 0.0f);
-                            }
-                            s_a[(tl * 4 + kk) * kWave + row + 32 * h] = v;
+                            const int e0 = 8 * kk + 4 * h;
+                            const u32x4 v = {A[e0], A[e0 + 1], A[e0 + 2], A[e0 + 3]};
+                            s_a[(tl * 2 + kk) * kWave + row + 32 * h] = v;
                         }
+                    const f32x4 r0 = {c[0], c[1], c[2], c[3]}, r1 = {c[4], c[5], c[6], c[7]}, r2 = {c[8], 0.f, 0.f, 0.f};
+                    s_c[jl * 3 + 0] = r0;
+                    s_c[jl * 3 + 1] = r1;
+                    s_c[jl * 3 + 2] = r2;
                 }
                 if (c0 + cn >= kpad) {  // last chunk: publish this wave's max norm
                     float wm = tmax;
@@ -260,51 +235,84 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
                 staged = resident ? li : -1;
             }
 
-            float best[R][16], sec[R][16];
+            // slot minima over the chunk, two codebook tiles per step
+            float best[R][16];
 #pragma unroll
             for (int r = 0; r < R; ++r)
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    best[r][q] = __builtin_inff();
-                    sec[r][q] = __builtin_inff();
-                }
-            const int ntile = cn >> 5;
+                for (int q = 0; q < 16; ++q) best[r][q] = 3.402823466e38f;  // finite: packing keeps a number
+            const int npair = cn >> 6;
+            u32x4 aN[2][2];
+            lds_a(aN, s_a, 0, lane);
 #pragma unroll 1
-            for (int tt = 0; tt < ntile; ++tt) {
-                bf16x8 a[4];
+            for (int tp = 0; tp < npair; ++tp) {
+                u32x4 a[2][2];
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) a[kk] = s_a[(tt * 4 + kk) * kWave + lane];
-                f32x16 acc[R];
-                score_tile<R>(acc, a, bop);
-                fold_tile<R>(acc, (unsigned)tt, best, sec);
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int kk = 0; kk < 2; ++kk) a[u][kk] = aN[u][kk];
+                lds_a(aN, s_a, min(tp + 1, npair - 1), lane);  // the next pair's operands
+                const f32x16 zero = {0.0f};
+                f32x16 acc[2][R];
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        acc[u][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8, a[u][0]), __builtin_bit_cast(bf16x8, bop[r][0]), zero, 0, 0, 0);
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        acc[u][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8, a[u][1]), __builtin_bit_cast(bf16x8, bop[r][1]), acc[u][r], 0,
+                            0, 0);
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q)
+                        best[r][q] = __builtin_fminf(__builtin_fminf(best[r][q], acc[0][r][q]), acc[1][r][q]);
             }
-            // fold this chunk's 16 slots into the running summaries
+
+            // per kernel tile: smallest and second smallest slot minimum, the slot number q
+            // (rows 8 (q / 4) + 4 half + q % 4) packed into the low bits
+            float m1[R], m2[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r)
+            for (int r = 0; r < R; ++r) {
+                float a1 = __builtin_inff(), a2 = __builtin_inff();
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
-                    const int j = c0 + (int)(__float_as_uint(best[r][q]) & kTileMask) * 32 + 8 * (q >> 2) + 4 * half +
-                                  (q & 3);
-                    merge_top2(rb[r], rj[r], rs[r], best[r][q], j, sec[r][q]);
+                    const float pq = __uint_as_float((__float_as_uint(best[r][q]) & ~15u) | (unsigned)q);
+                    a2 = __builtin_amdgcn_fmed3f(a1, a2, pq);
+                    a1 = min2(a1, pq);
                 }
-        }
-
-        // the two half-waves; lane l then owns kernel 64 wave + l (tile r = half)
-        float fb = __builtin_inff(), fs = __builtin_inff();
-        int fj = 0x7fffffff;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            float b = rb[r], s2 = rs[r];
-            int j = rj[r];
-            const float ob = __shfl_xor(b, 32);
-            const int oj = __shfl_xor(j, 32);
-            const float os = __shfl_xor(s2, 32);
-            merge_top2(b, j, s2, ob, oj, os);
-            if (r == half) {
-                fb = b;
-                fj = j;
-                fs = s2;
+                m1[r] = a1;
+                m2[r] = a2;
             }
+            // own kernel: lanes < 32 tile 0, lanes >= 32 tile 1; first from the lower half's rows
+            const auto x1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m1[0]), __float_as_uint(m1[1]), false, false);
+            const auto x2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m2[0]), __float_as_uint(m2[1]), false, false);
+            const float lo1 = __uint_as_float(x1[0]), hi1 = __uint_as_float(x1[1]);
+            const float lo2 = __uint_as_float(x2[0]), hi2 = __uint_as_float(x2[1]);
+            const float M1 = min2(lo1, hi1);
+            const float M2 = __builtin_amdgcn_fmed3f(lo1, hi1, min2(lo2, hi2));
+            const int qs = (int)(__float_as_uint(M1) & 15u);
+            const int slot = 8 * (qs >> 2) + (qs & 3) + (hi1 < lo1 ? 4 : 0);
+
+            // exact fp32 rescoring of the winning slot's entries, in increasing index order
+            float bd = __builtin_inff();
+            int bj = 0x7fffffff;
+#pragma unroll 2
+            for (int jl = slot; jl < cn; jl += 32) {
+                const f32x4 r0 = s_c[jl * 3 + 0], r1 = s_c[jl * 3 + 1];
+                const float c8 = s_cf[jl * kRowFloats + 8];
+                const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], c8};
+                const float d = sqdist9(xo, c);
+                const bool take = (c0 + jl < k) && (d < bd);
+                bd = take ? d : bd;
+                bj = take ? c0 + jl : bj;
+            }
+            merge_top2(rb, rs, rj, rd, M1, M2, bj, bd);
         }
 
         float xn2 = 0.0f;
@@ -314,16 +322,15 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
 #pragma unroll
         for (int w = 1; w < kAssignWaves; ++w) cm2 = fmaxf(cm2, s_wmax[w]);
         const float rr = sqrtf(xn2) + sqrtf(cm2);
-        const float theta = 0x1p-15f * rr * rr + 0x1p-100f;
+        const float q2 = rr * rr;
+        const float theta = 0x1p-13f * q2 + 0x1p-100f;
 
-        const bool sure = valid && (fs - fb > theta) && (fj < k);
+        const bool sure = valid && (q2 < kTrustQ) && (rs - rb > theta) && (rj < k);
         float dist = 0.0f;
         if (sure) {
-            float c[kDim];
-            global_entry(C, fj, c);
-            dist = sqdist9(xo, c);
-            L.idx[i] = fj;
-            if (L.best_d) L.best_d[i] = dist;
+            dist = rd;
+            L.idx[i] = rj;
+            if (L.best_d) L.best_d[i] = rd;
         }
 
         // exact fp32 rescoring of the kernels the guard could not settle, one at a time
@@ -334,31 +341,32 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
             float xf[kDim];
 #pragma unroll
             for (int d = 0; d < kDim; ++d) xf[d] = __shfl(xo[d], f);
-            float bd = __builtin_inff();
-            int bj = 0x7fffffff;
-            for (int j = lane; j < k; j += kWave) {
+            float fd = __builtin_inff();
+            int fj = 0x7fffffff;
+            for (int jj = lane; jj < k; jj += kWave) {
                 float c[kDim];
-                global_entry(C, j, c);
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)jj * kDim + d];
                 const float d = sqdist9(xf, c);
-                if (d < bd) {
-                    bd = d;
-                    bj = j;
+                if (d < fd) {
+                    fd = d;
+                    fj = jj;
                 }
             }
 #pragma unroll
             for (int off = 32; off >= 1; off >>= 1) {
-                const float od = __shfl_xor(bd, off);
-                const int oj = __shfl_xor(bj, off);
-                if (od < bd || (od == bd && oj < bj)) {
-                    bd = od;
-                    bj = oj;
+                const float od = __shfl_xor(fd, off);
+                const int oj = __shfl_xor(fj, off);
+                if (od < fd || (od == fd && oj < fj)) {
+                    fd = od;
+                    fj = oj;
                 }
             }
             if (lane == f) {
-                if (bj == 0x7fffffff) bj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
-                L.idx[i] = bj;
-                if (L.best_d) L.best_d[i] = bd;
-                dist = bd;
+                if (fj == 0x7fffffff) fj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
+                L.idx[i] = fj;
+                if (L.best_d) L.best_d[i] = fd;
+                dist = fd;
             }
         }
 

@@ -16,14 +16,14 @@ constexpr int kWave = 64;
 
 // ---- assignment kernel geometry -----------------------------------------------------
 // A workgroup is 4 waves; each wave scores kAssignTilesPerWave tiles of 32 kernels
-// against 32-entry codebook tiles with v_mfma_f32_32x32x16_bf16 (a 3-part bf16 split of
-// the K = 10 fp32 contraction, 9 dims + norm).
+// against 32-entry codebook tiles with v_mfma_f32_32x32x16_bf16 (an exact bf16 split of
+// the K = 10 fp32 contraction, 9 dims + norm, into three cross terms).
 // A "tile" of the grid is the 256 kernels one workgroup scores at a time; the grid is
 // persistent (at most kAssignGridMax workgroups, each walking a contiguous run of tiles).
 constexpr int kAssignWaves = 4;
 constexpr int kAssignTilesPerWave = 2;
 constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
-constexpr int kAssignChunk = 512;    // codebook entries staged in LDS at a time (64 KB)
+constexpr int kAssignChunk = 512;    // codebook entries staged in LDS at a time (32 KB operands + 24 KB rows)
 constexpr int kAssignGridMax = 512;  // 2 workgroups (occupancy 2) on each of 256 CUs
 
 // ---- update kernel geometry ---------------------------------------------------------

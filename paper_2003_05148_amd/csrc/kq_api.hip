@@ -39,6 +39,9 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
     memset(&p, 0, sizeof(p));
     size_t off = 0;
     for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
+    int64_t total_n = 0;
+    for (int32_t l = l0; l < l1; ++l) total_n += layers[l].n;
+    p.kpb = update_kernels_per_block(total_n);
     int unit = 0;
     for (int32_t l = l0; l < l1; ++l) {
         const kq_layer& s = layers[l];
@@ -65,9 +68,8 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
                 d.part = (double*)(w + ws_assign_part(s.n));
             }
             d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n));
-            d.nunits = update_blocks(s.n);
-            d.flags = (int)kflags | (update_uses_lds(s.k) ? 0 : kFlagAtomicHist) |
-                      ((aligned(s.X, 16) && aligned(s.idx, 16)) ? kFlagVec : 0);
+            d.nunits = update_blocks(s.n, p.kpb);
+            d.flags = (int)kflags | (update_uses_lds(s.k) ? 0 : kFlagAtomicHist);
         }
         d.unit_begin = unit;
         unit += d.nunits;
@@ -75,6 +77,7 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
     }
     p.nlayers = l1 - l0;
     p.total_units = unit;
+    set_unit_table(p);
 }
 
 kq_status check_layers(const kq_layer* layers, int32_t n_layers, bool fit) {

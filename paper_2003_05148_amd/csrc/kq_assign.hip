@@ -119,12 +119,12 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
     int li = find_layer(p, t);
     int staged = -1;  // layer whose whole codebook is resident in LDS
     float xo[kDim];   // this lane's kernel of the current tile
-    load_kernel(p.L[li], t - p.L[li].unit_begin, wave, lane, xo);
+    load_kernel(p.L[li], t - p.unit_begin[li], wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
 
 #pragma unroll 1
     for (; t < t_end; ++t) {
-        while (li + 1 < p.nlayers && t >= p.L[li + 1].unit_begin) ++li;
+        while (li + 1 < p.nlayers && t >= p.unit_begin[li + 1]) ++li;
         const DevLayer& L = p.L[li];
         const int n = L.n, k = L.k;
         const float* __restrict__ C = L.C;
@@ -136,8 +136,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const S
         float xn[kDim];
         if (t + 1 < t_end) {
             int ln = li;
-            while (ln + 1 < p.nlayers && t + 1 >= p.L[ln + 1].unit_begin) ++ln;
-            load_kernel(p.L[ln], t + 1 - p.L[ln].unit_begin, wave, lane, xn);
+            while (ln + 1 < p.nlayers && t + 1 >= p.unit_begin[ln + 1]) ++ln;
+            load_kernel(p.L[ln], t + 1 - p.unit_begin[ln], wave, lane, xn);
         }
 
         // B operands.  Kernel tile r of this wave is kernels 64 wave + 32 r + (lane % 32), the

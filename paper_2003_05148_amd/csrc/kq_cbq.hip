@@ -18,6 +18,7 @@ constexpr int kCbqThreads = 1024;
 constexpr int kCbqMaxLevels = 256;
 constexpr int kDigits = 11;  // 32-bit digits: |sum of w v| * 2^149 < 2^328
 
+// smallest q minimising fl64(|v - L_q|), by scanning every level
 __device__ __forceinline__ int nearest_level(float v, const float* lev, int nlev) {
     const double vd = (double)v;
     double best = fabs(vd - (double)lev[0]);
@@ -30,6 +31,26 @@ __device__ __forceinline__ int nearest_level(float v, const float* lev, int nlev
         }
     }
     return bq;
+}
+
+// the same when the levels are sorted (L_0 <= L_1 <= ...): the distances in fp64 do not
+// grow towards v from either side, so the answer is the first level >= v or, if not
+// farther, the lowest-indexed level whose distance equals that of the last level < v
+__device__ __forceinline__ int nearest_sorted(float v, const float* lev, int nlev) {
+    int q0 = 0;  // number of levels < v (a prefix, as the levels are sorted)
+#pragma unroll
+    for (int step = kCbqMaxLevels; step >= 1; step >>= 1)
+        if (q0 + step <= nlev && lev[q0 + step - 1] < v) q0 += step;
+    const double vd = (double)v;
+    int q = q0;
+    const double da = q0 < nlev ? fabs(vd - (double)lev[q0]) : __builtin_inf();
+    if (q0 > 0) {
+        int b = q0 - 1;
+        const double db = fabs(vd - (double)lev[b]);
+        while (b > 0 && fabs(vd - (double)lev[b - 1]) == db) --b;
+        if (db <= da) q = b;
+    }
+    return q;
 }
 
 // add w * v * 2^149 (an exact integer) to the digit accumulators of one level
@@ -104,6 +125,7 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     __shared__ unsigned long long s_w[kCbqMaxLevels];
     __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave];
     __shared__ int s_changed;
+    __shared__ int s_unsorted;
 
     const CbqLayer& L = p.L[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -127,6 +149,7 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
         s_lo[wave] = lo;
         s_hi[wave] = hi;
     }
+    if (tid == 0) s_unsorted = 0;
     __syncthreads();
     lo = s_lo[0];
     hi = s_hi[0];
@@ -139,13 +162,20 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
         s_lev[tid] = (float)__dadd_rn((double)lo, __dmul_rn((double)tid, delta));
     }
     __syncthreads();
-    for (int r = tid; r < m; r += kCbqThreads) codes[r] = (uint8_t)nearest_level(v[r], s_lev, nlev);
+    if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
+    __syncthreads();
+    bool sorted = s_unsorted == 0;
+    for (int r = tid; r < m; r += kCbqThreads)
+        codes[r] = (uint8_t)(sorted ? nearest_sorted(v[r], s_lev, nlev) : nearest_level(v[r], s_lev, nlev));
 
     if (p.mode == KQ_CBQ_WKMEANS) {
         for (int it = 0; it < p.iters; ++it) {
             for (int e = tid; e < nlev * kDigits; e += kCbqThreads) s_dig[e] = 0ull;
             for (int e = tid; e < nlev; e += kCbqThreads) s_w[e] = 0ull;
-            if (tid == 0) s_changed = 0;
+            if (tid == 0) {
+                s_changed = 0;
+                s_unsorted = 0;
+            }
             __syncthreads();
             for (int r = tid; r < m; r += kCbqThreads) {
                 const int w = L.w ? L.w[r / kDim] : 1;
@@ -160,9 +190,12 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
                 s_lev[tid] = (float)(N / (double)s_w[tid]);
             }
             __syncthreads();
+            if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
+            __syncthreads();
+            sorted = s_unsorted == 0;
             int changed = 0;
             for (int r = tid; r < m; r += kCbqThreads) {
-                const int q = nearest_level(v[r], s_lev, nlev);
+                const int q = sorted ? nearest_sorted(v[r], s_lev, nlev) : nearest_level(v[r], s_lev, nlev);
                 if (q != codes[r]) {
                     codes[r] = (uint8_t)q;
                     changed = 1;

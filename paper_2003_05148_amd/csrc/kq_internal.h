@@ -27,17 +27,29 @@ constexpr int kAssignChunk = 512;    // codebook entries staged in LDS at a time
 constexpr int kAssignGridMax = 512;  // 2 workgroups (occupancy 2) on each of 256 CUs
 
 // ---- update kernel geometry ---------------------------------------------------------
-constexpr int kUpdateThreads = 512;
-constexpr int kUpdateKernelsPerBlock = 4096;
+// One launch updates every layer of a stack; all its workgroups read the same number of
+// kernels, chosen so that the launch has about one workgroup per CU (a multiple of 256
+// between kUpdateMinKernelsPerBlock and kUpdateMaxKernelsPerBlock).
+constexpr int kUpdateThreads = 1024;
+constexpr int kUpdateMinKernelsPerBlock = 1024;
+constexpr int kUpdateMaxKernelsPerBlock = 16384;
+constexpr int kUpdateTargetBlocks = 256;
 constexpr int kUpdateLdsMaxK = 768;  // LDS histogram [k][9] int64 + [k] u32 up to this k
-constexpr int kFinishEntries = 16;   // codebook entries per finishing workgroup
+constexpr int kFinishEntries = 4;    // codebook entries per finishing workgroup
 
 // ---- squared-error reduction ------------------------------------------------------------
 constexpr int kSqThreads = 256;
 constexpr int kSqPerBlock = 8192;
 
 inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1) / kAssignKernelsPerTile); }
-inline int update_blocks(int64_t n) { return (int)((n + kUpdateKernelsPerBlock - 1) / kUpdateKernelsPerBlock); }
+// workgroups of one layer at `kpb` kernels each; the workspace allows for the smallest kpb
+inline int update_blocks(int64_t n, int kpb = kUpdateMinKernelsPerBlock) { return (int)((n + kpb - 1) / kpb); }
+inline int update_kernels_per_block(int64_t total_n) {
+    int64_t kpb = (total_n / kUpdateTargetBlocks + 255) & ~int64_t(255);
+    if (kpb < kUpdateMinKernelsPerBlock) kpb = kUpdateMinKernelsPerBlock;
+    if (kpb > kUpdateMaxKernelsPerBlock) kpb = kUpdateMaxKernelsPerBlock;
+    return (int)kpb;
+}
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
 inline bool update_uses_lds(int32_t k) { return k <= kUpdateLdsMaxK; }
 
@@ -63,7 +75,7 @@ inline size_t ws_hist(int64_t n, int32_t k) {
 }
 inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n) + ws_hist(n, k); }
 
-enum : int { kFlagCountsOnly = 1, kFlagAtomicHist = 2, kFlagVec = 4 };
+enum : int { kFlagCountsOnly = 1, kFlagAtomicHist = 2 };
 
 struct DevLayer {
     const float* X;
@@ -85,18 +97,29 @@ struct DevLayer {
     int napart;               // number of assignment partials
 };
 
+// Kernel arguments of a stack launch.  The first unit of every layer is repeated in a
+// compact table at the front (INT_MAX past the last layer), so a workgroup finds its
+// layer with one scalar load instead of a chain of dependent ones through the layer
+// records.
 struct StackParams {
     int nlayers;
     int total_units;
+    int kpb;  // update: kernels per workgroup
+    int pad;
+    int unit_begin[KQ_MAX_STACK];
     DevLayer L[KQ_MAX_STACK];
 };
+
+// host-side: fill the table from the layer records
+inline void set_unit_table(StackParams& p) {
+    for (int l = 0; l < KQ_MAX_STACK; ++l) p.unit_begin[l] = l < p.nlayers ? p.L[l].unit_begin : 0x7fffffff;
+}
 
 // device-side: the layer a unit (tile or workgroup) belongs to (layers are in order)
 __device__ __forceinline__ int find_layer(const StackParams& p, int u) {
     int l = 0;
-#pragma unroll 1
-    for (int i = 1; i < p.nlayers; ++i)
-        if (u >= p.L[i].unit_begin) l = i;
+#pragma unroll
+    for (int i = 1; i < KQ_MAX_STACK; ++i) l += u >= p.unit_begin[i] ? 1 : 0;
     return l;
 }
 
@@ -108,7 +131,13 @@ template <int NT>
 __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src, int m, double* s_w) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     double a = 0.0;
-    for (int q = tid; q < m; q += NT) a += src[q];
+    for (int q = tid; q < m; q += 8 * NT) {  // eight loads in flight, added in order
+        double v[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) v[r] = q + r * NT < m ? src[q + r * NT] : 0.0;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) a += v[r];
+    }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) a += __shfl_xor(a, off);
     if (lane == 0) s_w[wave] = a;

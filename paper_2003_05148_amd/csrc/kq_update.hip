@@ -6,16 +6,17 @@
 // overflow int64 (|x| < 32).  Integer addition is associative, so the sums, and with
 // them the new codebook, do not depend on the order in which blocks or lanes add.
 //
-// update_kernel: a workgroup of 512 threads reads 4096 consecutive kernels of one layer,
-// four kernels (144 bytes: 9 x 16-byte loads, plus one 16-byte load of their indices)
-// per thread step when the rows are 16-byte aligned, accumulates a private LDS
-// histogram ([k][9] int64 sums + [k] counts, ds_add_u64; dynamic LDS sized for the
-// largest k of the launch) and stores it whole as its partial histogram; with more
-// than kUpdateLdsMaxK entries it adds straight into [k][10] global accumulators
-// instead.  Asked for the distortion of a standalone assignment, it also sums, in a
-// fixed order, the fp32 distances of its kernels to their entries of the old codebook.
-// update_finish_kernel: a workgroup of 640 threads owns 16 entries of one layer; four
-// groups of 160 threads add a quarter of the partial histograms each (any order gives
+// update_kernel: one launch covers every layer of a stack; each workgroup of 1024
+// threads reads the same number of consecutive kernels of one layer (about one workgroup
+// per CU for the whole launch), one 36-byte row per thread and step (consecutive lanes,
+// consecutive rows), two steps in flight at a time.  It accumulates a private LDS histogram ([k][9] int64 sums +
+// [k] counts, ds_add_u64; dynamic LDS sized for the largest k of the launch) and stores
+// it whole as its partial histogram; with more than kUpdateLdsMaxK entries it adds
+// straight into [k][10] global accumulators instead.  Asked for the distortion of a
+// standalone assignment, it also sums, in a fixed order, the fp32 distances of its
+// kernels to their entries of the old codebook.
+// update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
+// groups of 40 threads add a sixteenth of the partial histograms each (any order gives
 // the same integers), then it divides and writes the codebook and the counts.  The
 // first workgroup of a layer also adds the distortion partials in a fixed order (those
 // of the assignment kernel when the distortion comes from there).  The kernel boundary
@@ -65,6 +66,33 @@ __device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[
     }
 }
 
+// Thread t takes kernels i, i + 1024, ... (i = first + t): consecutive lanes read
+// consecutive 36-byte rows with 9 dword loads each, two kernels in flight per thread.
+template <bool NEED_X>
+__device__ __forceinline__ void add_rows(const UpdateCtx& c, const float* __restrict__ X,
+                                         const int32_t* __restrict__ idx, int i, int i1, double& dacc) {
+    for (; i < i1; i += 2 * kUpdateThreads) {
+        const int ib = i + kUpdateThreads;
+        const bool two = ib < i1;
+        const int ja = idx[i], jb = two ? idx[ib] : -1;  // -1: nothing to add
+        float xa[kDim], xb[kDim];
+        if (NEED_X) {
+            const float* pa = X + (size_t)i * kDim;
+            const float* pb = X + (size_t)(two ? ib : i) * kDim;
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) {
+                xa[d] = pa[d];
+                xb[d] = pb[d];
+            }
+        } else {
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) xa[d] = xb[d] = 0.0f;
+        }
+        add_kernel(c, xa, ja, dacc);
+        add_kernel(c, xb, jb, dacc);
+    }
+}
+
 __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParams p) {
     extern __shared__ unsigned long long s_dyn[];  // [k][9] sums, then [k] u32 counts
     __shared__ double s_wd[kUpdateThreads / kWave];
@@ -95,46 +123,12 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     }
 
     double dacc = 0.0;
-    const int i0 = lb * kUpdateKernelsPerBlock;
-    const int i1 = min(n, i0 + kUpdateKernelsPerBlock);
-    int iv = i0;  // first row not covered by the vector path
-    if (L.flags & kFlagVec) {
-        // groups of 4 rows: 36 floats = 9 aligned float4 (i0 is a multiple of 4)
-        const int g0 = i0 >> 2, g1 = i1 >> 2;
-        for (int g = g0 + tid; g < g1; g += kUpdateThreads) {
-            const int4 jj = ((const int4*)idx)[g];
-            float f[36];
-            if (need_x) {
-                const float4* src = (const float4*)X + (size_t)g * 9;
-#pragma unroll
-                for (int q = 0; q < 9; ++q) {
-                    const float4 v = src[q];
-                    f[4 * q] = v.x;
-                    f[4 * q + 1] = v.y;
-                    f[4 * q + 2] = v.z;
-                    f[4 * q + 3] = v.w;
-                }
-            } else {
-#pragma unroll
-                for (int q = 0; q < 36; ++q) f[q] = 0.0f;
-            }
-            const int js[4] = {jj.x, jj.y, jj.z, jj.w};
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float x[kDim];
-#pragma unroll
-                for (int d = 0; d < kDim; ++d) x[d] = f[9 * r + d];
-                add_kernel(c, x, js[r], dacc);
-            }
-        }
-        iv = g1 << 2;
-    }
-    for (int i = iv + tid; i < i1; i += kUpdateThreads) {
-        float x[kDim];
-#pragma unroll
-        for (int d = 0; d < kDim; ++d) x[d] = need_x ? X[(size_t)i * kDim + d] : 0.0f;
-        add_kernel(c, x, idx[i], dacc);
-    }
+    const int i0 = lb * p.kpb;
+    const int i1 = min(n, i0 + p.kpb);
+    if (need_x)
+        add_rows<true>(c, X, idx, i0 + tid, i1, dacc);
+    else
+        add_rows<false>(c, X, idx, i0 + tid, i1, dacc);
 
     if (c.use_lds) {
         __syncthreads();
@@ -157,17 +151,16 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     }
 }
 
-constexpr int kFinishGroups = 4;
+constexpr int kFinishGroups = 16;
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
 
 __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const StackParams p) {
     __shared__ long long s_S[kFinishGroups][kFinishEntries * 10];
     __shared__ double s_w[kSumThreads / kWave];
-    // layer and entry range of this workgroup: each layer owns ceil(k / 16) workgroups
-    int li = 0;
+    // layer and entry range of this workgroup: each layer owns ceil(k / 4) workgroups
     const int b = blockIdx.x;
-    while (li + 1 < p.nlayers && b >= p.L[li + 1].unit_begin) ++li;
+    const int li = find_layer(p, b);
     const DevLayer& L = p.L[li];
     const int j0 = (b - L.unit_begin) * kFinishEntries;
     const int tid = threadIdx.x;
@@ -239,7 +232,7 @@ hipError_t launch_update(const StackParams& p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// the finishing launch numbers its workgroups per layer: ceil(k / 16) each
+// the finishing launch numbers its workgroups per layer: ceil(k / 4) each
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s) {
     StackParams q = p;
     int blk = 0;
@@ -247,6 +240,7 @@ hipError_t launch_update_finish(const StackParams& p, hipStream_t s) {
         q.L[l].unit_begin = blk;
         blk += (q.L[l].k + kFinishEntries - 1) / kFinishEntries;
     }
+    set_unit_table(q);
     // nunits keeps the number of update workgroups (partials to add)
     hipLaunchKernelGGL(update_finish_kernel, dim3(blk), dim3(kFinishThreads), 0, s, q);
     return hipGetLastError();

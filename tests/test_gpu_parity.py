@@ -262,6 +262,30 @@ def test_quantize_codebook_bit_exact(mode):
         assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32))
 
 
+@pytest.mark.parametrize("bits", [1, 2, 6, 8])
+@pytest.mark.parametrize("mode", [kq.KQ_CBQ_UNIFORM, kq.KQ_CBQ_WKMEANS])
+def test_quantize_codebook_ties_and_widths(mode, bits):
+    """Scalars exactly halfway between grid levels (ties go to the lower level), repeated
+    values, and magnitudes so far apart that fp64 distances to neighbouring levels round
+    to the same value; several code widths."""
+    rng = np.random.default_rng(10 + bits)
+    L = (1 << bits) - 1
+    mid = np.concatenate([[0.0, float(L)], np.arange(L) + 0.5, rng.integers(0, L + 1, 60)])
+    mid = np.resize(mid, (len(mid) + 8) // 9 * 9).astype(np.float32).reshape(-1, 9)
+    pool = np.array([1.0, -1.0, 1e-20, -1e-20, 1e-19, 3e-39, 0.0, 2.0, 1e-30], np.float32)
+    mixed = rng.choice(pool, (50, 9)).astype(np.float32)
+    for C in (mid, mixed):
+        w = rng.integers(0, 20, C.shape[0])
+        codes, levels, C_hat = kq.kq_quantize_codebook(dev(C), dev(w.astype(np.int32)), bits, mode, 30)
+        if mode == kq.KQ_CBQ_UNIFORM:
+            oc, ol, oh = oracle.cbq_uniform(C, bits)
+        else:
+            oc, ol, oh, _ = oracle.cbq_wkmeans(C, w, bits, 30)
+        assert np.array_equal(host(codes), oc)
+        assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32))
+        assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32))
+
+
 def test_quantize_codebook_stack_and_unweighted():
     layers = synth.resnet18_stack(k=16, layers=3)
     Cs = [oracle.fit(L.X, L.C0, 3)["C"] for L in layers]

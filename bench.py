@@ -96,9 +96,11 @@ def main():
     p_codes = [torch.empty((L.k * 9 * 6 + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L in layers]
     W_hat = [torch.empty(L.n, 9, device=dev) for L in layers]
     sq = torch.zeros(len(layers), dtype=torch.float64, device=dev)
-    sq_ws = torch.zeros(max(kq.lib.kq_workspace_bytes(kq.KQ_OP_SQ_ERROR, L.n * 9, 1) for L in layers) * len(layers),
-                        dtype=torch.uint8, device=dev)
-    sq_ws_stride = sq_ws.numel() // len(layers) // 256 * 256
+    pack_jobs = [(st.idx[i], bits, p_idx[i]) for i in range(len(layers))] + \
+                [(cb_out[i][0], 6, p_codes[i]) for i in range(len(layers))]
+    recon = [{"packed": p_idx[i], "bits": bits, "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i], "W_ref": X[i],
+              "sq_error": sq[i:i + 1]} for i, L in enumerate(layers)]
+    recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
 
     stream = torch.cuda.current_stream(dev)
     ev = {"assign": [], "update": []}
@@ -123,12 +125,8 @@ def main():
                     ev["update"].append((u0, u1))
         kq.kq_update_stack(st, dist_slot=T, counts_only=True, distortion_from_assign=True)
         kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30, out=cb_out)
-        for i, L in enumerate(layers):
-            kq.kq_pack_bits(st.idx[i], bits, out=p_idx[i])
-            kq.kq_pack_bits(cb_out[i][0], 6, out=p_codes[i])
-            kq.kq_reconstruct_packed(p_idx[i], bits, L.n, cb_out[i][2], W_hat=W_hat[i])
-            kq.kq_sq_error(X[i], W_hat[i], out=sq[i:i + 1],
-                           workspace=sq_ws[i * sq_ws_stride:(i + 1) * sq_ws_stride])
+        kq.kq_pack_bits_stack(pack_jobs)
+        kq.kq_reconstruct_stack(recon, workspace=recon_ws)
 
     for _ in range(args.warmup):
         step(False)

@@ -258,6 +258,49 @@ kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, 
 kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out,
                       void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Stack forms of the storage and recovery steps, for the layers of a network at once
+ * (Eq. 4 and the end of Sec. 3.2); each runs as one launch (plus one small finishing
+ * launch for the errors) instead of one or two per layer.
+ */
+
+/* One stream of kq_pack_bits_stack (device pointers); fields as in kq_pack_bits. */
+typedef struct kq_pack_job {
+    const void* values;   /* [count] */
+    int32_t elem_bytes;   /* 1, 2 or 4 */
+    int32_t bits;         /* 0..16 */
+    int64_t count;        /* >= 0 */
+    uint8_t* out;         /* ceil(count * bits / 8) bytes, 4-byte aligned */
+} kq_pack_job;
+#define KQ_MAX_PACK_JOBS 32
+
+/* kq_pack_bits on every job of a host array (1 <= n_jobs <= KQ_MAX_PACK_JOBS); each
+ * stream is bit-identical to what kq_pack_bits writes. */
+kq_status kq_pack_bits_stack(const kq_pack_job* jobs, int32_t n_jobs, void* stream);
+
+/* One layer of kq_reconstruct_stack (device pointers). */
+typedef struct kq_recon_layer {
+    const int32_t* idx;      /* [n] indices, or NULL to read them from `packed` */
+    const uint8_t* packed;   /* kq_pack_bits stream of `bits`-bit indices (when idx is NULL) */
+    int32_t bits;            /* 0..16, used with `packed` */
+    int32_t k;               /* 1..KQ_MAX_K; indices outside [0, k) give zero rows */
+    int64_t n;               /* 1 <= n < 2^31 */
+    const float* C;          /* [k][9] codebook (the 6-bit C_hat for K+C) */
+    float* W_hat;            /* [n][9] output */
+    const float* W_ref;      /* [n][9] original kernels, or NULL */
+    double* sq_error;        /* device scalar, or NULL: sum over the 9n values of
+                                (W_ref - W_hat)^2 in fp64, in a fixed order (the same bits on
+                                every run; needs W_ref) */
+} kq_recon_layer;
+
+/* Workspace bytes of kq_reconstruct_stack (0 for invalid sizes). */
+size_t kq_reconstruct_stack_workspace_bytes(const kq_recon_layer* layers /* host */, int32_t n_layers);
+
+/* kq_reconstruct / kq_reconstruct_packed (and the squared error of each layer) for
+ * every layer of a host array, 1 <= n_layers <= KQ_MAX_STACK; all pointers 4-byte aligned. */
+kq_status kq_reconstruct_stack(const kq_recon_layer* layers, int32_t n_layers, void* ws, size_t ws_bytes,
+                               void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -40,6 +40,15 @@ class KqCbqLayer(ctypes.Structure):
     _fields_ = [("C", _P), ("k", _I32), ("weights", _P), ("codes", _P), ("levels", _P), ("C_hat", _P)]
 
 
+class KqPackJob(ctypes.Structure):
+    _fields_ = [("values", _P), ("elem_bytes", _I32), ("bits", _I32), ("count", _I64), ("out", _P)]
+
+
+class KqReconLayer(ctypes.Structure):
+    _fields_ = [("idx", _P), ("packed", _P), ("bits", _I32), ("k", _I32), ("n", _I64), ("C", _P),
+                ("W_hat", _P), ("W_ref", _P), ("sq_error", _P)]
+
+
 def _load():
     lib = ctypes.CDLL(LIB_PATH)
     sig = {
@@ -61,6 +70,9 @@ def _load():
         "kq_reconstruct": ([_P, _I64, _P, _I32, _I32, _P, _P], _I32),
         "kq_reconstruct_packed": ([_P, _I32, _I64, _P, _I32, _I32, _P, _P], _I32),
         "kq_sq_error": ([_P, _P, _I64, _P, _P, _SZ, _P], _I32),
+        "kq_pack_bits_stack": ([_P, _I32, _P], _I32),
+        "kq_reconstruct_stack_workspace_bytes": ([_P, _I32], _SZ),
+        "kq_reconstruct_stack": ([_P, _I32, _P, _SZ, _P], _I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -83,7 +95,9 @@ KQ_F_DISTORTION_FROM_ASSIGN = 2
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
-            "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error"]
+            "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error",
+            "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack"]
+KQ_MAX_PACK_JOBS = 32
 
 
 class KqError(RuntimeError):
@@ -379,3 +393,82 @@ def kq_sq_error(A, B, out=None, workspace=None):
     _check(lib.kq_sq_error(A.data_ptr(), B.data_ptr(), A.numel(), out.data_ptr(), ws.data_ptr(), ws.numel(),
                            _stream(A.device)), "kq_sq_error")
     return out
+
+
+# ---- stack forms of pack and reconstruct ---------------------------------------------------
+
+_EB = {torch.int32: 4, torch.uint8: 1, torch.int16: 2}
+
+
+def kq_pack_bits_stack(jobs):
+    """Pack several streams with one launch.  jobs: list of (values, bits, out) with out
+    a uint8 tensor of at least ceil(count * bits / 8) bytes, or None to allocate one.
+    Returns the list of streams (each trimmed to its exact length)."""
+    if not 1 <= len(jobs) <= KQ_MAX_PACK_JOBS:
+        raise ValueError(f"1..{KQ_MAX_PACK_JOBS} jobs per call")
+    arr = (KqPackJob * len(jobs))()
+    outs, dev = [], None
+    for q, (values, bits, out) in enumerate(jobs):
+        eb = _EB.get(values.dtype)
+        if eb is None:
+            raise TypeError("values must be int32, int16 or uint8")
+        _dev(values, values.dtype, "values")
+        dev = values.device
+        nbytes = (values.numel() * bits + 7) // 8
+        if out is None:
+            out = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=values.device)
+        else:
+            _dev(out, torch.uint8, "out")
+            if out.numel() < nbytes:
+                raise ValueError("out is too small")
+        arr[q] = KqPackJob(values.data_ptr(), eb, bits, values.numel(), out.data_ptr())
+        outs.append(out[:nbytes])
+    _check(lib.kq_pack_bits_stack(ctypes.cast(arr, _P), len(jobs), _stream(dev)), "kq_pack_bits_stack")
+    return outs
+
+
+def _recon_array(layers):
+    arr = (KqReconLayer * len(layers))()
+    outs, dev = [], None
+    for q, L in enumerate(layers):
+        C = _kernels(L["C"], "C")
+        dev = C.device
+        n = int(L["n"])
+        idx, packed = L.get("idx"), L.get("packed")
+        if idx is not None:
+            _dev(idx, torch.int32, "idx", (n,))
+        else:
+            _dev(packed, torch.uint8, "packed")
+        W_hat = L.get("W_hat")
+        W_hat = W_hat if W_hat is not None else torch.empty(n, KQ_DIM, dtype=torch.float32, device=dev)
+        _dev(W_hat, torch.float32, "W_hat", (n, KQ_DIM))
+        W_ref, sq = L.get("W_ref"), L.get("sq_error")
+        if W_ref is not None:
+            W_ref = _kernels(W_ref, "W_ref")
+        if sq is not None:
+            _dev(sq, torch.float64, "sq_error")
+        arr[q] = KqReconLayer(_ptr(idx), _ptr(packed) if idx is None else None, int(L.get("bits", 0)),
+                              C.shape[0], n, C.data_ptr(), W_hat.data_ptr(), _ptr(W_ref), _ptr(sq))
+        outs.append(W_hat)
+    return arr, outs, dev
+
+
+def recon_workspace_bytes(layers) -> int:
+    """Workspace bytes kq_reconstruct_stack needs for these layers (see there)."""
+    arr, _, _ = _recon_array(layers)
+    return lib.kq_reconstruct_stack_workspace_bytes(ctypes.cast(arr, _P), len(layers))
+
+
+def kq_reconstruct_stack(layers, workspace=None):
+    """Reconstruct several layers with one launch.  layers: list of dicts with keys
+    C ([k, 9] codebook), n, and either idx (int32 [n]) or packed + bits; optional W_hat
+    (output [n, 9]), W_ref (original kernels [n, 9]) and sq_error (float64 [1] output,
+    needs W_ref).  Returns the list of W_hat tensors."""
+    if not 1 <= len(layers) <= KQ_MAX_STACK:
+        raise ValueError(f"1..{KQ_MAX_STACK} layers per call")
+    arr, outs, dev = _recon_array(layers)
+    nb = lib.kq_reconstruct_stack_workspace_bytes(ctypes.cast(arr, _P), len(layers))
+    ws = workspace if workspace is not None else (_ws(dev, nb) if nb else None)
+    _check(lib.kq_reconstruct_stack(ctypes.cast(arr, _P), len(layers), _ptr(ws), 0 if ws is None else ws.numel(),
+                                    _stream(dev)), "kq_reconstruct_stack")
+    return outs

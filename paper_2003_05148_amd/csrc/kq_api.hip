@@ -3,6 +3,7 @@
 // Every entry point checks its arguments before it touches HIP, so argument errors
 // come back without a GPU (and without initialising the HIP runtime).  No entry point
 // allocates memory; device scratch comes from the caller's workspace.
+#include <stdint.h>
 #include <string.h>
 
 #include "kq_internal.h"
@@ -11,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 2;
+constexpr int32_t kAbiVersion = 3;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -349,7 +350,8 @@ kq_status kq_reconstruct(const int32_t* idx, int64_t n, const float* C, int32_t 
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k)) return KQ_ERR_ARG;
     if (!idx || !C || !W_hat || !aligned(idx, 4) || !aligned(C, 4) || !aligned(W_hat, 16)) return KQ_ERR_ARG;
-    return hip_status(launch_reconstruct(idx, nullptr, 0, n, C, k, W_hat, (hipStream_t)stream));
+    const kq_recon_layer l = {idx, nullptr, 0, k, n, C, W_hat, nullptr, nullptr};
+    return kq_reconstruct_stack(&l, 1, nullptr, 0, stream);
 }
 
 kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, const float* C, int32_t k,
@@ -358,7 +360,8 @@ kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, 
     if (k > KQ_MAX_K || bits < 0 || bits > 16) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k)) return KQ_ERR_ARG;
     if ((bits > 0 && !packed) || !C || !W_hat || !aligned(C, 4) || !aligned(W_hat, 16)) return KQ_ERR_ARG;
-    return hip_status(launch_reconstruct(nullptr, packed, bits, n, C, k, W_hat, (hipStream_t)stream));
+    const kq_recon_layer l = {nullptr, packed, bits, k, n, C, W_hat, nullptr, nullptr};
+    return kq_reconstruct_stack(&l, 1, nullptr, 0, stream);
 }
 
 kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out, void* ws, size_t ws_bytes,
@@ -368,6 +371,106 @@ kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out
     const kq_status w = check_ws(ws, ws_bytes, kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1));
     if (w != KQ_OK) return w;
     return hip_status(launch_sq_error(A, B, count, out, ws, (hipStream_t)stream));
+}
+
+// ---- stack forms of pack and reconstruct --------------------------------------------------
+
+static kq_status check_pack_job(const kq_pack_job& j) {
+    if (j.bits < 0 || j.bits > 16) return KQ_ERR_UNSUPPORTED;
+    if (j.elem_bytes != 1 && j.elem_bytes != 2 && j.elem_bytes != 4) return KQ_ERR_ARG;
+    if (j.count < 0 || j.count >= (int64_t(1) << 31)) return KQ_ERR_ARG;
+    if (j.count == 0 || j.bits == 0) return KQ_OK;
+    if (!j.values || !j.out || !aligned(j.values, (uintptr_t)j.elem_bytes) || !aligned(j.out, 4)) return KQ_ERR_ARG;
+    return KQ_OK;
+}
+
+kq_status kq_pack_bits_stack(const kq_pack_job* jobs, int32_t n_jobs, void* stream) {
+    if (jobs == nullptr || n_jobs < 1 || n_jobs > KQ_MAX_PACK_JOBS) return KQ_ERR_ARG;
+    for (int32_t q = 0; q < n_jobs; ++q) {
+        const kq_status st = check_pack_job(jobs[q]);
+        if (st != KQ_OK) return st;
+    }
+    PackParams p;
+    memset(&p, 0, sizeof(p));
+    p.njobs = n_jobs;
+    long long words = 0;
+    for (int32_t q = 0; q < n_jobs; ++q) {
+        const kq_pack_job& j = jobs[q];
+        const long long bytes = (j.count * (long long)j.bits + 7) / 8;
+        p.J[q] = PackJob{j.values, j.out, (long long)j.count, bytes, j.elem_bytes, j.bits};
+        p.word_begin[q] = words;
+        words += (bytes + 3) / 4;
+    }
+    for (int32_t q = n_jobs; q <= KQ_MAX_PACK_JOBS; ++q) p.word_begin[q] = q == n_jobs ? words : INT64_MAX;
+    return hip_status(launch_pack_stack(p, (hipStream_t)stream));
+}
+
+static kq_status check_recon_layer(const kq_recon_layer& l) {
+    if (l.k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!l.idx && (l.bits < 0 || l.bits > 16)) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(l.n) || !valid_k(l.k)) return KQ_ERR_ARG;
+    if (!l.C || !l.W_hat || !aligned(l.C, 4) || !aligned(l.W_hat, 4)) return KQ_ERR_ARG;
+    if (l.idx ? !aligned(l.idx, 4) : (l.bits > 0 && !l.packed)) return KQ_ERR_ARG;
+    if (l.sq_error && (!l.W_ref || !aligned(l.sq_error, 8))) return KQ_ERR_ARG;
+    if (l.W_ref && !aligned(l.W_ref, 4)) return KQ_ERR_ARG;
+    return KQ_OK;
+}
+
+static size_t recon_ws_bytes(const kq_recon_layer* layers, int32_t n_layers) {
+    size_t b = 0;
+    for (int32_t l = 0; l < n_layers; ++l)
+        if (layers[l].sq_error) b += align256(sizeof(double) * (size_t)recon_blocks(layers[l].n));
+    return b;
+}
+
+size_t kq_reconstruct_stack_workspace_bytes(const kq_recon_layer* layers, int32_t n_layers) {
+    if (layers == nullptr || n_layers < 1 || n_layers > KQ_MAX_STACK) return 0;
+    for (int32_t l = 0; l < n_layers; ++l)
+        if (check_recon_layer(layers[l]) != KQ_OK) return 0;
+    return recon_ws_bytes(layers, n_layers);
+}
+
+kq_status kq_reconstruct_stack(const kq_recon_layer* layers, int32_t n_layers, void* ws, size_t ws_bytes,
+                               void* stream) {
+    if (layers == nullptr || n_layers < 1 || n_layers > KQ_MAX_STACK) return KQ_ERR_ARG;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_status st = check_recon_layer(layers[l]);
+        if (st != KQ_OK) return st;
+    }
+    const size_t need = recon_ws_bytes(layers, n_layers);
+    if (need > 0) {
+        const kq_status w = check_ws(ws, ws_bytes, need);
+        if (w != KQ_OK) return w;
+    }
+    ReconParams p;
+    memset(&p, 0, sizeof(p));
+    p.nlayers = n_layers;
+    size_t off = 0;
+    int blk = 0;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_recon_layer& s = layers[l];
+        ReconLayer& d = p.L[l];
+        d.idx = s.idx;
+        d.packed = s.idx ? nullptr : s.packed;
+        d.bits = s.idx ? 0 : s.bits;
+        d.pbytes = (s.n * (long long)d.bits + 7) / 8;
+        d.C = s.C;
+        d.W = s.W_hat;
+        d.W_ref = s.W_ref;
+        d.n = (int)s.n;
+        d.k = s.k;
+        d.nblk = recon_blocks(s.n);
+        if (s.sq_error) {
+            d.part = (double*)((unsigned char*)ws + off);
+            d.out = s.sq_error;
+            off += align256(sizeof(double) * (size_t)d.nblk);
+        }
+        p.unit_begin[l] = blk;
+        blk += d.nblk;
+    }
+    for (int32_t l = n_layers; l < KQ_MAX_STACK; ++l) p.unit_begin[l] = 0x7fffffff;
+    p.total_blocks = blk;
+    return hip_status(launch_reconstruct_stack(p, (hipStream_t)stream));
 }
 
 }  // extern "C"

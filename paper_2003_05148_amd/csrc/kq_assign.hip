@@ -102,7 +102,7 @@ __device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d,
 }
 
 template <int R>
-__global__ __launch_bounds__(kAssignWaves * kWave, 2) void assign_kernel(const StackParams p) {
+__global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kernel(const StackParams p) {
     static_assert(R == 2, "one kernel per lane and the half exchange need two kernel tiles per wave");
     __shared__ u32x4 s_a[kAssignChunk / 32 * 2 * kWave];  // [tile][k-step][lane] A operands
     __shared__ f32x4 s_c[kAssignChunk * kRowFloats / 4];   // fp32 rows of the staged entries

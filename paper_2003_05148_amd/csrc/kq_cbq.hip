@@ -77,9 +77,11 @@ __device__ __forceinline__ void add_exact(unsigned long long* dig, float v, unsi
 }
 
 // the exact integer sum_i dig[i] 2^(32 i), times 2^-149, rounded to nearest-even fp64
+// (every loop has a fixed trip count, so the limbs stay in registers)
 __device__ double digits_to_double(const unsigned long long* dig) {
     unsigned limb[kDigits + 1];
     long long carry = 0;
+#pragma unroll
     for (int i = 0; i < kDigits; ++i) {
         const long long t = (long long)dig[i] + carry;
         limb[i] = (unsigned)(t & 0xffffffffll);
@@ -89,28 +91,36 @@ __device__ double digits_to_double(const unsigned long long* dig) {
     const bool neg = carry < 0;
     if (neg) {  // two's complement negate
         unsigned c = 1;
+#pragma unroll
         for (int i = 0; i <= kDigits; ++i) {
             const unsigned long long t = (unsigned long long)(~limb[i]) + c;
             limb[i] = (unsigned)t;
             c = (unsigned)(t >> 32);
         }
     }
-    int h = kDigits;
-    while (h >= 0 && limb[h] == 0) --h;
+    int h = -1;  // highest nonzero limb
+#pragma unroll
+    for (int i = 0; i <= kDigits; ++i) h = limb[i] ? i : h;
     if (h < 0) return 0.0;
-    const int lz = __clz(limb[h]);
-    const unsigned long long hi64 = ((unsigned long long)limb[h] << 32) | (h >= 1 ? limb[h - 1] : 0u);
-    const unsigned next = h >= 2 ? limb[h - 2] : 0u;
+    unsigned top = 0, l1 = 0, next = 0;
+    bool sticky = false;
+#pragma unroll
+    for (int i = 0; i <= kDigits; ++i) {
+        top = i == h ? limb[i] : top;
+        l1 = i == h - 1 ? limb[i] : l1;
+        next = i == h - 2 ? limb[i] : next;
+        sticky |= (i <= h - 3) && limb[i] != 0u;
+    }
+    const int lz = __clz(top);
+    const unsigned long long hi64 = ((unsigned long long)top << 32) | l1;
     unsigned long long win;
-    bool sticky;
     if (lz) {
         win = (hi64 << lz) | (unsigned long long)(next >> (32 - lz));
-        sticky = (next << lz) != 0u;
+        sticky |= (next << lz) != 0u;
     } else {
         win = hi64;
-        sticky = next != 0u;
+        sticky |= next != 0u;
     }
-    for (int i = 0; i <= h - 3; ++i) sticky |= limb[i] != 0u;
     unsigned long long mant = win >> 11;
     const unsigned rnd = (unsigned)(win & 0x7ffull);
     if (rnd > 0x400u || (rnd == 0x400u && (sticky || (mant & 1ull)))) ++mant;
@@ -119,6 +129,15 @@ __device__ double digits_to_double(const unsigned long long* dig) {
     return neg ? -r : r;
 }
 
+// Thread tid handles scalars r = tid, tid + 1024, ...  With LDS (codebooks of at most
+// kCbqLdsScalars scalars) the scalars, their weights and codes are copied into LDS once;
+// otherwise every pass reads them from memory.  The level sums are kept up to date
+// incrementally: after the first full accumulation only scalars whose code changes move
+// their (exact) contribution between two levels, which leaves the same integers as
+// summing from scratch.
+constexpr int kCbqLdsScalars = 8192;
+
+template <bool LDS>
 __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     __shared__ float s_lev[kCbqMaxLevels];
     __shared__ unsigned long long s_dig[kCbqMaxLevels * kDigits];
@@ -126,19 +145,42 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave];
     __shared__ int s_changed;
     __shared__ int s_unsorted;
+    __shared__ float s_v[LDS ? kCbqLdsScalars : 1];
+    __shared__ int s_wt[LDS ? kCbqLdsScalars : 1];
+    __shared__ uint8_t s_code[LDS ? kCbqLdsScalars : 1];
 
     const CbqLayer& L = p.L[blockIdx.x];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m = L.k * kDim;
     const int nlev = 1 << p.bits;
+    const bool wk = p.mode == KQ_CBQ_WKMEANS;
     const float* __restrict__ v = L.C;
     uint8_t* __restrict__ codes = L.codes;
+    auto val = [&](int r) { return LDS ? s_v[r] : v[r]; };
+    auto wgt = [&](int r) { return LDS ? s_wt[r] : (L.w ? L.w[r / kDim] : 1); };
+    auto code = [&](int r) { return LDS ? (int)s_code[r] : (int)codes[r]; };
+    auto set_code = [&](int r, int q) {
+        if (LDS)
+            s_code[r] = (uint8_t)q;
+        else
+            codes[r] = (uint8_t)q;
+    };
+
+    if (LDS) {
+        for (int r = tid; r < m; r += kCbqThreads) {
+            s_v[r] = v[r];
+            s_wt[r] = L.w ? L.w[r / kDim] : 1;
+        }
+    }
+    for (int e = tid; e < nlev * kDigits; e += kCbqThreads) s_dig[e] = 0ull;
+    for (int e = tid; e < nlev; e += kCbqThreads) s_w[e] = 0ull;
 
     // grid on [min, max]
     float lo = __builtin_inff(), hi = -__builtin_inff();
     for (int r = tid; r < m; r += kCbqThreads) {
-        lo = fminf(lo, v[r]);
-        hi = fmaxf(hi, v[r]);
+        const float x = v[r];
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
@@ -165,26 +207,26 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
     __syncthreads();
     bool sorted = s_unsorted == 0;
-    for (int r = tid; r < m; r += kCbqThreads)
-        codes[r] = (uint8_t)(sorted ? nearest_sorted(v[r], s_lev, nlev) : nearest_level(v[r], s_lev, nlev));
 
-    if (p.mode == KQ_CBQ_WKMEANS) {
+    // initial codes, and with them the level sums
+    for (int r = tid; r < m; r += kCbqThreads) {
+        const float x = val(r);
+        const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
+        set_code(r, q);
+        const int w = wgt(r);
+        if (wk && w > 0) {
+            add_exact(s_dig + q * kDigits, x, (unsigned)w);
+            atomicAdd(&s_w[q], (unsigned long long)w);
+        }
+    }
+    __syncthreads();
+
+    if (wk) {
         for (int it = 0; it < p.iters; ++it) {
-            for (int e = tid; e < nlev * kDigits; e += kCbqThreads) s_dig[e] = 0ull;
-            for (int e = tid; e < nlev; e += kCbqThreads) s_w[e] = 0ull;
             if (tid == 0) {
                 s_changed = 0;
                 s_unsorted = 0;
             }
-            __syncthreads();
-            for (int r = tid; r < m; r += kCbqThreads) {
-                const int w = L.w ? L.w[r / kDim] : 1;
-                if (w <= 0) continue;
-                const int q = codes[r];
-                add_exact(s_dig + q * kDigits, v[r], (unsigned)w);
-                atomicAdd(&s_w[q], (unsigned long long)w);
-            }
-            __syncthreads();
             if (tid < nlev && s_w[tid] > 0ull) {
                 const double N = digits_to_double(s_dig + tid * kDigits);
                 s_lev[tid] = (float)(N / (double)s_w[tid]);
@@ -195,9 +237,18 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
             sorted = s_unsorted == 0;
             int changed = 0;
             for (int r = tid; r < m; r += kCbqThreads) {
-                const int q = sorted ? nearest_sorted(v[r], s_lev, nlev) : nearest_level(v[r], s_lev, nlev);
-                if (q != codes[r]) {
-                    codes[r] = (uint8_t)q;
+                const float x = val(r);
+                const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
+                const int c = code(r);
+                if (q != c) {
+                    const int w = wgt(r);
+                    if (w > 0) {  // move the exact contribution from level c to level q
+                        add_exact(s_dig + c * kDigits, -x, (unsigned)w);
+                        add_exact(s_dig + q * kDigits, x, (unsigned)w);
+                        atomicAdd(&s_w[c], (unsigned long long)(-(long long)w));
+                        atomicAdd(&s_w[q], (unsigned long long)w);
+                    }
+                    set_code(r, q);
                     changed = 1;
                 }
             }
@@ -210,12 +261,20 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     }
 
     if (tid < nlev) L.levels[tid] = s_lev[tid];
-    if (L.C_hat)
-        for (int r = tid; r < m; r += kCbqThreads) L.C_hat[r] = s_lev[codes[r]];
+    for (int r = tid; r < m; r += kCbqThreads) {
+        const int c = code(r);
+        if (LDS) codes[r] = (uint8_t)c;
+        if (L.C_hat) L.C_hat[r] = s_lev[c];
+    }
 }
 
 hipError_t launch_cbq(const CbqParams& p, hipStream_t s) {
-    hipLaunchKernelGGL(cbq_kernel, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    int mmax = 0;
+    for (int l = 0; l < p.nlayers; ++l) mmax = p.L[l].k * kDim > mmax ? p.L[l].k * kDim : mmax;
+    if (mmax <= kCbqLdsScalars)
+        hipLaunchKernelGGL(cbq_kernel<true>, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(cbq_kernel<false>, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
     return hipGetLastError();
 }
 

@@ -23,8 +23,13 @@ constexpr int kWave = 64;
 constexpr int kAssignWaves = 4;
 constexpr int kAssignTilesPerWave = 2;
 constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
-constexpr int kAssignChunk = 512;    // codebook entries staged in LDS at a time (32 KB operands + 24 KB rows)
-constexpr int kAssignGridMax = 512;  // 2 workgroups (occupancy 2) on each of 256 CUs
+#ifndef KQ_ASSIGN_OCC
+#define KQ_ASSIGN_OCC 3
+#endif
+constexpr int kAssignOcc = KQ_ASSIGN_OCC;  // workgroups resident per CU
+// codebook entries staged in LDS at a time (64 B of operands + 48 B of fp32 row each)
+constexpr int kAssignChunk = kAssignOcc <= 2 ? 512 : (kAssignOcc == 3 ? 384 : 320);
+constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every CU full
 
 // ---- update kernel geometry ---------------------------------------------------------
 // One launch updates every layer of a stack; all its workgroups read the same number of
@@ -173,10 +178,47 @@ struct CbqParams {
 };
 hipError_t launch_cbq(const CbqParams& p, hipStream_t s);
 
+// stack forms of pack and reconstruct (+ squared error): a compact unit table first
+struct PackJob {
+    const void* v;
+    uint8_t* out;
+    long long count;
+    long long bytes;  // ceil(count * bits / 8)
+    int eb;
+    int bits;
+};
+struct PackParams {
+    int njobs;
+    int pad;
+    long long word_begin[KQ_MAX_PACK_JOBS + 1];  // first output word of each job; [njobs] = total
+    PackJob J[KQ_MAX_PACK_JOBS];
+};
+struct ReconLayer {
+    const int32_t* idx;
+    const uint8_t* packed;
+    const float* C;
+    float* W;
+    const float* W_ref;
+    double* part;     // squared-error partials [blocks], or null
+    double* out;      // squared error, or null
+    long long pbytes; // packed stream bytes
+    int n, k, bits, nblk;
+};
+struct ReconParams {
+    int nlayers;
+    int total_blocks;
+    int unit_begin[KQ_MAX_STACK];  // first workgroup of each layer, INT_MAX past the last
+    ReconLayer L[KQ_MAX_STACK];
+};
+constexpr int kReconThreads = 1024;
+constexpr int kReconRows = 4096;        // rows per workgroup of the stack reconstruction
+constexpr int kReconLdsFloats = 16384;  // codebooks up to this many values are gathered from LDS
+inline int recon_blocks(int64_t n) { return (int)((n + kReconRows - 1) / kReconRows); }
+hipError_t launch_pack_stack(const PackParams& p, hipStream_t s);
+hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s);
+
 hipError_t launch_pack(const void* v, int elem_bytes, int64_t count, int bits, uint8_t* out, hipStream_t s);
 hipError_t launch_unpack(const uint8_t* in, int64_t count, int bits, int32_t* v, hipStream_t s);
 hipError_t launch_sq_error(const float* A, const float* B, int64_t count, double* out, void* ws, hipStream_t s);
-hipError_t launch_reconstruct(const int32_t* idx, const uint8_t* packed, int bits, int64_t n, const float* C,
-                              int k, float* W, hipStream_t s);
 
 }  // namespace kq

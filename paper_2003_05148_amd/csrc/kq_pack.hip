@@ -4,10 +4,13 @@
 //                one thread per output 32-bit word, so every store is a full aligned word
 //                except the partial last one.
 //   unpack:      the inverse, one thread per value.
-//   reconstruct: W_hat[i][d] = C[idx_i][d], one thread per four consecutive outputs
-//                (a 16-byte store), indices either plain int32 or read from a packed
-//                stream.  HBM traffic per kernel: 4 bytes of index (or bits/8 packed)
-//                + 36 bytes written; the codebook stays in cache.
+//   reconstruct: W_hat[i][d] = C[idx_i][d] for the layers of a stack in one launch (a
+//                single layer is a stack of one), 64 rows per wave step moved with
+//                coalesced accesses through LDS, indices either plain int32 or read from
+//                a packed stream, the codebook gathered from LDS.  HBM traffic per kernel: 4 bytes of index (or bits/8 packed)
+//                + 36 bytes written (+ 36 bytes read when the squared error against
+//                the original row is asked for).
+//   pack stack:  one launch for the streams of a whole network.
 #include "kq_internal.h"
 
 namespace kq {
@@ -18,11 +21,9 @@ __device__ __forceinline__ unsigned load_value(const void* v, int eb, long long 
     return (unsigned)((const int32_t*)v)[i];
 }
 
-__global__ void pack_kernel(const void* __restrict__ v, int eb, long long count, int bits,
-                            uint8_t* __restrict__ out, long long total_bytes) {
-    const long long w = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    const long long nw = (total_bytes + 3) / 4;
-    if (w >= nw) return;
+// output word w of a stream: the fields overlapping bits [32 w, 32 w + 32)
+__device__ __forceinline__ void pack_word(const void* __restrict__ v, int eb, long long count, int bits,
+                                          uint8_t* __restrict__ out, long long total_bytes, long long w) {
     const long long bit0 = w * 32;
     const long long i0 = bit0 / bits;
     long long i1 = (bit0 + 31) / bits;
@@ -42,6 +43,25 @@ __global__ void pack_kernel(const void* __restrict__ v, int eb, long long count,
     }
 }
 
+__global__ void pack_kernel(const void* __restrict__ v, int eb, long long count, int bits,
+                            uint8_t* __restrict__ out, long long total_bytes) {
+    const long long w = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= (total_bytes + 3) / 4) return;
+    pack_word(v, eb, count, bits, out, total_bytes, w);
+}
+
+// every stream of a stack: one thread per output word of the concatenated streams
+__global__ void pack_stack_kernel(const PackParams p) {
+    const long long wg = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (wg >= p.word_begin[p.njobs]) return;
+    // the last job starting at or before wg (jobs without words start where the next does)
+    int jb = 0;
+#pragma unroll
+    for (int q = 1; q < KQ_MAX_PACK_JOBS; ++q) jb += wg >= p.word_begin[q] ? 1 : 0;
+    const PackJob& J = p.J[jb];
+    pack_word(J.v, J.eb, J.count, J.bits, J.out, J.bytes, wg - p.word_begin[jb]);
+}
+
 __device__ __forceinline__ int read_packed(const uint8_t* __restrict__ in, int bits, long long i, long long total_bytes) {
     const long long bit = i * bits;
     const long long byte0 = bit >> 3;
@@ -57,31 +77,6 @@ __global__ void unpack_kernel(const uint8_t* __restrict__ in, long long count, i
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= count) return;
     v[i] = bits ? read_packed(in, bits, i, total_bytes) : 0;
-}
-
-__global__ void reconstruct_kernel(const int32_t* __restrict__ idx, const uint8_t* __restrict__ packed, int bits,
-                                   long long n, const float* __restrict__ C, int k, float* __restrict__ W,
-                                   long long packed_bytes) {
-    const long long e = 4 * ((long long)blockIdx.x * blockDim.x + threadIdx.x);
-    const long long total = n * kDim;
-    if (e >= total) return;
-    float o[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const long long ee = e + q;
-        o[q] = 0.0f;
-        if (ee < total) {
-            const long long i = ee / kDim;
-            const int d = (int)(ee - i * kDim);
-            const int j = idx ? idx[i] : (bits ? read_packed(packed, bits, i, packed_bytes) : 0);
-            if ((unsigned)j < (unsigned)k) o[q] = C[(size_t)j * kDim + d];
-        }
-    }
-    if (e + 4 <= total) {
-        *(float4*)(W + e) = make_float4(o[0], o[1], o[2], o[3]);
-    } else {
-        for (int q = 0; e + q < total; ++q) W[e + q] = o[q];
-    }
 }
 
 // sum of squared differences, fp64, fixed order: per-thread strided sums, a
@@ -121,6 +116,114 @@ __global__ __launch_bounds__(kWave) void sq_finish_kernel(const double* part, in
     if (lane == 0) *out = v;
 }
 
+// Every layer of a stack: workgroup b of a layer rebuilds rows [4096 b, 4096 b + 4096) of
+// W_hat.  Each wave takes 64 consecutive rows (2304 bytes) per step: the reference rows
+// come in and the rebuilt rows go out with fully coalesced dword accesses through a
+// per-wave LDS buffer (lane l moves floats l, l + 64, ...), while lane l rebuilds row l
+// from its index and the codebook.  The next step's index and reference values are
+// loaded before the current step is processed.  A codebook of up to kReconLdsFloats
+// values is copied into LDS first, so the row gathers hit LDS.  When the layer asks for
+// it, each lane also sums (W_ref - W_hat)^2 over its rows in fp64, row by row in
+// dimension order; the lanes of a wave are combined by a butterfly, the waves in order,
+// and a second kernel adds the workgroup partials in order.
+__device__ __forceinline__ int recon_index(const ReconLayer& L, int i) {
+    return L.idx ? L.idx[i] : (L.bits ? read_packed(L.packed, L.bits, i, L.pbytes) : 0);
+}
+
+__global__ __launch_bounds__(kReconThreads) void reconstruct_stack_kernel(const ReconParams p) {
+    extern __shared__ float s_dyn[];  // [waves][2][64 * 9] row buffers, then the codebook
+    __shared__ double s_w[kReconThreads / kWave];
+    constexpr int kRowF = kWave * kDim;  // floats of 64 rows
+    int li = 0;
+#pragma unroll
+    for (int q = 1; q < KQ_MAX_STACK; ++q) li += (int)blockIdx.x >= p.unit_begin[q] ? 1 : 0;
+    const ReconLayer& L = p.L[li];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float* xb = s_dyn + wave * 2 * kRowF;
+    float* wb = xb + kRowF;
+    float* s_cb = s_dyn + (kReconThreads / kWave) * 2 * kRowF;
+    const int lb = (int)blockIdx.x - p.unit_begin[li];
+    const int i0 = lb * kReconRows;
+    const int i1 = min(L.n, i0 + kReconRows);
+    const bool err = L.part != nullptr;
+    const bool lds = L.k * kDim <= kReconLdsFloats;
+    if (lds) {
+        for (int e = tid; e < L.k * kDim; e += kReconThreads) s_cb[e] = L.C[e];
+        __syncthreads();
+    }
+    const int nsteps = (i1 - i0 + kWave - 1) / kWave;
+    constexpr int kWaves = kReconThreads / kWave;
+    double acc = 0.0;
+    // prefetch of step `wave`
+    int jn = 0;
+    float xn[kDim];
+    int st = wave;
+    if (st < nsteps) {
+        const int b0 = i0 + st * kWave, nf = min(kWave, i1 - b0) * kDim;
+        jn = lane < nf / kDim ? recon_index(L, b0 + lane) : 0;
+#pragma unroll
+        for (int q = 0; q < kDim; ++q)
+            xn[q] = (err && q * kWave + lane < nf) ? L.W_ref[(size_t)b0 * kDim + q * kWave + lane] : 0.0f;
+    }
+    for (; st < nsteps; st += kWaves) {
+        const int b0 = i0 + st * kWave;
+        const int cnt = min(kWave, i1 - b0), nf = cnt * kDim;
+        const int j = jn;
+#pragma unroll
+        for (int q = 0; q < kDim; ++q) xb[q * kWave + lane] = xn[q];
+        const int sn = st + kWaves;  // prefetch the next step of this wave
+        if (sn < nsteps) {
+            const int c0 = i0 + sn * kWave, mf = min(kWave, i1 - c0) * kDim;
+            jn = lane < mf / kDim ? recon_index(L, c0 + lane) : 0;
+#pragma unroll
+            for (int q = 0; q < kDim; ++q)
+                xn[q] = (err && q * kWave + lane < mf) ? L.W_ref[(size_t)c0 * kDim + q * kWave + lane] : 0.0f;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane < cnt) {
+            const bool ok = (unsigned)j < (unsigned)L.k;
+            const int jo = (ok ? j : 0) * kDim;
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) {
+                const float c = lds ? s_cb[jo + d] : L.C[jo + d];
+                const float w = ok ? c : 0.0f;
+                wb[lane * kDim + d] = w;
+                if (err) {
+                    const double df = (double)xb[lane * kDim + d] - (double)w;
+                    acc += df * df;
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int q = 0; q < kDim; ++q)
+            if (q * kWave + lane < nf) L.W[(size_t)b0 * kDim + q * kWave + lane] = wb[q * kWave + lane];
+        __builtin_amdgcn_wave_barrier();
+    }
+    if (!err) return;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane == 0) s_w[wave] = acc;
+    __syncthreads();
+    if (tid == 0) {
+        double v = s_w[0];
+        for (int q = 1; q < kWaves; ++q) v += s_w[q];
+        L.part[lb] = v;
+    }
+}
+
+// one wave per layer: the partials in the order of sq_finish_kernel
+__global__ __launch_bounds__(kWave) void reconstruct_stack_finish_kernel(const ReconParams p) {
+    const ReconLayer& L = p.L[blockIdx.x];
+    if (L.part == nullptr) return;
+    const int lane = threadIdx.x;
+    double v = 0.0;
+    for (int q = lane; q < L.nblk; q += kWave) v += L.part[q];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) *L.out = v;
+}
+
 static unsigned grid_for(long long items, int block) {
     return (unsigned)((items + block - 1) / block);
 }
@@ -140,13 +243,27 @@ hipError_t launch_unpack(const uint8_t* in, int64_t count, int bits, int32_t* v,
     return hipGetLastError();
 }
 
-hipError_t launch_reconstruct(const int32_t* idx, const uint8_t* packed, int bits, int64_t n, const float* C, int k,
-                              float* W, hipStream_t s) {
-    const long long total = n * (long long)kDim;
-    const long long threads = (total + 3) / 4;
-    const long long pbytes = (n * (long long)bits + 7) / 8;
-    hipLaunchKernelGGL(reconstruct_kernel, dim3(grid_for(threads, 256)), dim3(256), 0, s, idx, packed, bits,
-                       (long long)n, C, k, W, pbytes);
+hipError_t launch_pack_stack(const PackParams& p, hipStream_t s) {
+    const long long words = p.word_begin[p.njobs];
+    if (words == 0) return hipSuccess;
+    hipLaunchKernelGGL(pack_stack_kernel, dim3(grid_for(words, 256)), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s) {
+    size_t lds = 0;  // the largest codebook that is staged
+    for (int l = 0; l < p.nlayers; ++l) {
+        const size_t f = (size_t)p.L[l].k * kDim;
+        if (f <= (size_t)kReconLdsFloats && f * sizeof(float) > lds) lds = f * sizeof(float);
+    }
+    lds += sizeof(float) * (kReconThreads / kWave) * 2 * kWave * kDim;  // the row buffers
+    hipLaunchKernelGGL(reconstruct_stack_kernel, dim3(p.total_blocks), dim3(kReconThreads), lds, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    bool any = false;
+    for (int l = 0; l < p.nlayers; ++l) any |= p.L[l].part != nullptr;
+    if (!any) return hipSuccess;
+    hipLaunchKernelGGL(reconstruct_stack_finish_kernel, dim3(p.nlayers), dim3(kWave), 0, s, p);
     return hipGetLastError();
 }
 

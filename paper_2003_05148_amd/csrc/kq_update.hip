@@ -17,9 +17,9 @@
 // kernels to their entries of the old codebook.
 // update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
 // groups of 40 threads add a sixteenth of the partial histograms each (any order gives
-// the same integers), then it divides and writes the codebook and the counts.  The
-// first workgroup of a layer also adds the distortion partials in a fixed order (those
-// of the assignment kernel when the distortion comes from there).  The kernel boundary
+// the same integers), then it divides and writes the codebook and the counts.  One more
+// workgroup per layer adds the distortion partials in a fixed order (those of the
+// assignment kernel when the distortion comes from there).  The kernel boundary
 // orders every partial before its use, so no fence or atomic counter is needed.
 #include "kq_internal.h"
 
@@ -158,8 +158,17 @@ static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the fini
 __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const StackParams p) {
     __shared__ long long s_S[kFinishGroups][kFinishEntries * 10];
     __shared__ double s_w[kSumThreads / kWave];
-    // layer and entry range of this workgroup: each layer owns ceil(k / 4) workgroups
     const int b = blockIdx.x;
+    if (b >= p.total_units) {  // the last nlayers workgroups: the distortion of layer b - total
+        const DevLayer& L = p.L[b - p.total_units];
+        if (L.dist == nullptr) return;
+        const double* src = L.apart ? L.apart : L.part;
+        const int m = L.apart ? L.napart : L.nunits;
+        const double a = block_fixed_sum<kSumThreads>(src, m, s_w);
+        if (threadIdx.x == 0) *L.dist = a;
+        return;
+    }
+    // layer and entry range of this workgroup: each layer owns ceil(k / 4) workgroups
     const int li = find_layer(p, b);
     const DevLayer& L = p.L[li];
     const int j0 = (b - L.unit_begin) * kFinishEntries;
@@ -206,12 +215,6 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
             L.C[(size_t)j * kDim + d] = c;
         }
     }
-    if (j0 == 0 && L.dist != nullptr) {
-        const double* src = L.apart ? L.apart : L.part;
-        const int m = L.apart ? L.napart : L.nunits;
-        const double a = block_fixed_sum<kSumThreads>(src, m, s_w);
-        if (tid == 0) *L.dist = a;
-    }
 }
 
 __global__ void fill_zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t ntail) {
@@ -240,9 +243,10 @@ hipError_t launch_update_finish(const StackParams& p, hipStream_t s) {
         q.L[l].unit_begin = blk;
         blk += (q.L[l].k + kFinishEntries - 1) / kFinishEntries;
     }
+    q.total_units = blk;  // followed by one workgroup per layer for the distortion
     set_unit_table(q);
     // nunits keeps the number of update workgroups (partials to add)
-    hipLaunchKernelGGL(update_finish_kernel, dim3(blk), dim3(kFinishThreads), 0, s, q);
+    hipLaunchKernelGGL(update_finish_kernel, dim3(blk + q.nlayers), dim3(kFinishThreads), 0, s, q);
     return hipGetLastError();
 }
 

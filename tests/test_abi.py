@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 2
+    assert lib.kq_abi_version() == 3
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -146,3 +146,42 @@ def test_python_binding_rejects_cpu_tensors():
     X = torch.zeros(10, 9)
     with pytest.raises(TypeError):
         kq.kq_assign(X, X[:2])
+
+
+def test_stack_pack_and_reconstruct_argument_errors():
+    jobs = (kq.KqPackJob * 3)()
+    jobs[0] = kq.KqPackJob(FAKE, 4, 8, 100, FAKE)
+    jobs[1] = kq.KqPackJob(None, 1, 0, 100, None)      # zero-bit stream: nothing to write
+    jobs[2] = kq.KqPackJob(FAKE, 1, 6, 0, None)        # empty stream
+    p = ctypes.cast(jobs, ctypes.c_void_p)
+    assert lib.kq_pack_bits_stack(None, 1, None) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits_stack(p, 0, None) == kq.KQ_ERR_ARG
+    assert lib.kq_pack_bits_stack(p, kq.KQ_MAX_PACK_JOBS + 1, None) == kq.KQ_ERR_ARG
+    jobs[0] = kq.KqPackJob(FAKE, 4, 17, 100, FAKE)
+    assert lib.kq_pack_bits_stack(p, 3, None) == kq.KQ_ERR_UNSUPPORTED
+    jobs[0] = kq.KqPackJob(FAKE, 3, 8, 100, FAKE)
+    assert lib.kq_pack_bits_stack(p, 3, None) == kq.KQ_ERR_ARG
+    jobs[0] = kq.KqPackJob(FAKE, 4, 8, 100, FAKE + 2)
+    assert lib.kq_pack_bits_stack(p, 3, None) == kq.KQ_ERR_ARG
+
+    lay = (kq.KqReconLayer * 2)()
+    ok = kq.KqReconLayer(FAKE, None, 0, 256, 4096, FAKE, FAKE, FAKE, FAKE)
+    lay[0] = ok
+    lay[1] = kq.KqReconLayer(None, FAKE, 8, 256, 100, FAKE, FAKE, None, None)
+    q = ctypes.cast(lay, ctypes.c_void_p)
+    need = lib.kq_reconstruct_stack_workspace_bytes(q, 2)
+    assert need >= 16 and need % 256 == 0        # partials of the layer that asks for its error
+    assert lib.kq_reconstruct_stack(q, 2, None, 0, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_reconstruct_stack(q, 2, FAKE, need - 1, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_reconstruct_stack(q, 0, FAKE, need, None) == kq.KQ_ERR_ARG
+    assert lib.kq_reconstruct_stack(q, kq.KQ_MAX_STACK + 1, FAKE, need, None) == kq.KQ_ERR_ARG
+    lay[0] = kq.KqReconLayer(FAKE, None, 0, 256, 4096, FAKE, FAKE, None, FAKE)   # error without W_ref
+    assert lib.kq_reconstruct_stack(q, 2, FAKE, need, None) == kq.KQ_ERR_ARG
+    lay[0] = kq.KqReconLayer(FAKE, None, 0, kq.KQ_MAX_K + 1, 4096, FAKE, FAKE, FAKE, FAKE)
+    assert lib.kq_reconstruct_stack(q, 2, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
+    lay[0] = ok
+    lay[1] = kq.KqReconLayer(None, None, 8, 256, 100, FAKE, FAKE, None, None)     # no index source
+    assert lib.kq_reconstruct_stack(q, 2, FAKE, need, None) == kq.KQ_ERR_ARG
+    lay[1] = kq.KqReconLayer(None, FAKE, 17, 256, 100, FAKE, FAKE, None, None)
+    assert lib.kq_reconstruct_stack(q, 2, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_reconstruct_stack_workspace_bytes(q, 2) == 0

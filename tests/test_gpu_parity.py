@@ -321,3 +321,52 @@ def test_reconstruct_bit_exact():
         packed = kq.kq_pack_bits(dev(idx), b)
         W2 = kq.kq_reconstruct_packed(packed, b, n, dev(C))
         assert np.array_equal(host(W2), oracle.reconstruct(idx, C))
+
+
+def test_pack_bits_stack_matches_single_streams():
+    """One launch for many streams (mixed widths and element types, empty and zero-bit
+    streams) writes exactly what the oracle packs for each."""
+    rng = np.random.default_rng(21)
+    specs = [(4096, 8, np.int32), (2304, 6, np.uint8), (0, 6, np.uint8), (100, 0, np.int32), (1, 1, np.int32),
+             (33, 5, np.int16), (262144, 8, np.int32), (777, 12, np.int32), (4097, 16, np.int32), (5, 3, np.uint8)]
+    jobs, refs = [], []
+    for count, bits, dt in specs:
+        hi = 1 << bits if bits else 1
+        v = rng.integers(0, hi, count).astype(dt)
+        jobs.append((dev(v) if count else torch.zeros(0, dtype=torch.from_numpy(v).dtype, device=DEV), bits, None))
+        refs.append(oracle.pack_bits(v.astype(np.int64), bits) if count and bits else np.zeros(0, np.uint8))
+    outs = kq.kq_pack_bits_stack(jobs)
+    for (count, bits, _), o, r in zip(specs, outs, refs):
+        assert np.array_equal(host(o), r), (count, bits)
+
+
+@pytest.mark.parametrize("packed", [False, True])
+def test_reconstruct_stack_and_errors(packed):
+    """All layers in one launch: every W_hat bit-exact against the oracle's gather; each
+    layer's squared error within 1e-12 of the exact sum and the same bits on a rerun."""
+    rng = np.random.default_rng(22)
+    shapes = [(1, 1), (3, 2), (4097, 256), (262144, 256), (777, 4096), (913, 16), (8192, 64)]
+    layers, refs = [], []
+    for n, k in shapes:
+        C = rng.standard_normal((k, 9)).astype(np.float32)
+        idx = rng.integers(0, k, n).astype(np.int32)
+        Wref = rng.standard_normal((n, 9)).astype(np.float32)
+        b = oracle.index_bits(k)
+        L = {"C": dev(C), "n": n, "W_ref": dev(Wref), "sq_error": torch.zeros(1, dtype=torch.float64, device=DEV)}
+        if packed:
+            L["packed"], L["bits"] = kq.kq_pack_bits(dev(idx), b), b
+        else:
+            L["idx"] = dev(idx)
+        layers.append(L)
+        refs.append((oracle.reconstruct(idx, C), Wref))
+    outs = kq.kq_reconstruct_stack(layers)
+    first = [float(host(L["sq_error"])[0]) for L in layers]
+    kq.kq_reconstruct_stack(layers)
+    for L, W, (ref, Wref), (n, k), e1 in zip(layers, outs, refs, shapes, first):
+        assert np.array_equal(host(W).view(np.uint32), ref.view(np.uint32)), (n, k)
+        e2 = float(host(L["sq_error"])[0])
+        assert e1 == e2, (n, k)
+        exact = float(np.sum((Wref.astype(np.float64) - ref.astype(np.float64)) ** 2))
+        assert e1 == pytest.approx(exact, rel=1e-12), (n, k)
+        single = float(host(kq.kq_sq_error(L["W_ref"], W))[0])
+        assert e1 == pytest.approx(single, rel=1e-12), (n, k)

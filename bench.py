@@ -41,7 +41,31 @@ def parse():
     ap.add_argument("--k", type=int, default=256)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, copy MIB MiB device to device three times (a plain copy "
+                         "kernel of known size, the scale for hardware byte counters)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "assign_traffic.json")
+TRAFFIC_SOURCES = ["paper_2003_05148_amd/csrc/kq_assign.hip", "paper_2003_05148_amd/csrc/kq_internal.h"]
+
+
+def assign_traffic():
+    """HBM bytes per launch of the assignment kernel from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by the same counters on a plain copy), or None when
+    the kernel's sources have changed since the counters were taken."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if rec.get("sources_sha256") != h.hexdigest():
+        return None
+    return rec["bytes_per_launch"]
 
 
 def cpu_baseline(layers, iters):
@@ -103,7 +127,17 @@ def main():
     recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
 
     stream = torch.cuda.current_stream(dev)
-    ev = {"assign": [], "update": []}
+    ev = {"assign": [], "update": [], "cbq": [], "pack": [], "reconstruct": []}
+
+    def timed(name, record, fn):
+        if not record:
+            fn()
+            return
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        ev[name].append((e0, e1))
 
     def step(record: bool):
         Cflat.copy_(C0flat)
@@ -124,9 +158,10 @@ def main():
                     u1.record(stream)
                     ev["update"].append((u0, u1))
         kq.kq_update_stack(st, dist_slot=T, counts_only=True, distortion_from_assign=True)
-        kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30, out=cb_out)
-        kq.kq_pack_bits_stack(pack_jobs)
-        kq.kq_reconstruct_stack(recon, workspace=recon_ws)
+        timed("cbq", record, lambda: kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30,
+                                                                   out=cb_out))
+        timed("pack", record, lambda: kq.kq_pack_bits_stack(pack_jobs))
+        timed("reconstruct", record, lambda: kq.kq_reconstruct_stack(recon, workspace=recon_ws))
 
     for _ in range(args.warmup):
         step(False)
@@ -138,8 +173,16 @@ def main():
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
 
-    assign_ms = float(np.mean([a.elapsed_time(b) for a, b in ev["assign"]]))
-    update_ms = float(np.mean([a.elapsed_time(b) for a, b in ev["update"]]))
+    if args.copy_probe > 0:
+        src = torch.ones(args.copy_probe << 18, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    mean_ms = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for name, pairs in ev.items()}
+    assign_ms, update_ms = mean_ms["assign"], mean_ms["update"]
+    rec_bytes = sum(L.n * (bits / 8 + 36 + 36) for L in layers)   # packed index + reference row + output row
     flops = 18.0 * k * n_total                      # 9 multiply-adds per (kernel, entry) pair
     achieved = flops / (assign_ms * 1e-3) / 1e12
     upd_bytes = 40.0 * n_total                      # 36-byte kernel + 4-byte index per kernel
@@ -149,8 +192,10 @@ def main():
     mse_k = [j / (9 * L.n) for j, L in zip(J, layers)]
     mse_kc = [float(s) / (9 * L.n) for s, L in zip(sq.cpu(), layers)]
     print(json.dumps({"diag": {
-        "assign_ms": assign_ms, "update_ms": update_ms, "update_GBps": upd_gbs,
-        "lloyd_round_ms": assign_ms + update_ms,
+        "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_GBps": upd_gbs,
+        "lloyd_round_ms": assign_ms + update_ms, "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
+        "reconstruct_ms": mean_ms["reconstruct"],
+        "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9,
         "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
         "beta_K": sum(L.k * 9 * 32 + L.n * bits for L in layers) / (9 * n_total),
         "beta_KC": sum(L.k * 9 * 6 + L.n * bits for L in layers) / (9 * n_total)}}), file=sys.stderr)
@@ -172,7 +217,7 @@ def main():
                                "6-bit weighted codebook quantization, index/code packing, packed reconstruction",
                    "layers": len(layers), "kernels": n_total, "k": k, "lloyd_rounds": T, "codebook_bits": 6},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": None,
+                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": assign_traffic(),
                      "kernel": "assign_kernel (one launch per Lloyd round, whole stack)"},
     }
     if not args.no_cpu_baseline:

@@ -302,8 +302,10 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             // exact fp32 rescoring of the winning slot's entries, in increasing index order
             float bd = __builtin_inff();
             int bj = 0x7fffffff;
-#pragma unroll 2
-            for (int jl = slot; jl < cn; jl += 32) {
+            const int ntile = cn >> 5;  // the same trip count in every lane
+#pragma unroll 4
+            for (int tq = 0; tq < ntile; ++tq) {
+                const int jl = slot + 32 * tq;
                 const f32x4 r0 = s_c[jl * 3 + 0], r1 = s_c[jl * 3 + 1];
                 const float c8 = s_cf[jl * kRowFloats + 8];
                 const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], c8};
@@ -321,7 +323,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         float cm2 = s_wmax[0];
 #pragma unroll
         for (int w = 1; w < kAssignWaves; ++w) cm2 = fmaxf(cm2, s_wmax[w]);
-        const float rr = sqrtf(xn2) + sqrtf(cm2);
+        // Q only scales the guard, which has a 13 % margin: the hardware square root will do
+        const float rr = __builtin_amdgcn_sqrtf(xn2) + __builtin_amdgcn_sqrtf(cm2);
         const float q2 = rr * rr;
         const float theta = 0x1p-13f * q2 + 0x1p-100f;
 
@@ -345,8 +348,15 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             int fj = 0x7fffffff;
             for (int jj = lane; jj < k; jj += kWave) {
                 float c[kDim];
+                if (resident) {  // the rows are still staged in LDS
+                    const f32x4 r0 = s_c[jj * 3 + 0], r1 = s_c[jj * 3 + 1];
+                    c[0] = r0[0], c[1] = r0[1], c[2] = r0[2], c[3] = r0[3];
+                    c[4] = r1[0], c[5] = r1[1], c[6] = r1[2], c[7] = r1[3];
+                    c[8] = s_cf[jj * kRowFloats + 8];
+                } else {
 #pragma unroll
-                for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)jj * kDim + d];
+                    for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)jj * kDim + d];
+                }
                 const float d = sqdist9(xf, c);
                 if (d < fd) {
                     fd = d;

@@ -73,6 +73,25 @@ __device__ __forceinline__ float sqdist9(const float* x, const float* c) {
 
 __device__ __forceinline__ float min2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, -3.402823466e38f); }
 
+// scores of codebook tiles 2p and 2p + 1 (A operands a) against one kernel tile (B operands b)
+__device__ __forceinline__ void score_pair(f32x16 (&acc)[2], const u32x4 (&a)[2][2], const u32x4 (&b)[2]) {
+    const f32x16 zero = {0.0f};
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u][0]),
+                                                         __builtin_bit_cast(bf16x8, b[0]), zero, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u][1]),
+                                                         __builtin_bit_cast(bf16x8, b[1]), acc[u], 0, 0, 0);
+}
+
+// slot minima: one v_min3 per two scores
+__device__ __forceinline__ void fold_pair(float (&best)[16], const f32x16 (&acc)[2]) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) best[q] = __builtin_fminf(__builtin_fminf(best[q], acc[0][q]), acc[1][q]);
+}
+
 // A operands (entries) of codebook tiles 2 p and 2 p + 1
 __device__ __forceinline__ void lds_a(u32x4 (&a)[2][2], const u32x4* s_a, int p, int lane) {
 #pragma unroll
@@ -252,26 +271,11 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
 #pragma unroll
                     for (int kk = 0; kk < 2; ++kk) a[u][kk] = aN[u][kk];
                 lds_a(aN, s_a, min(tp + 1, npair - 1), lane);  // the next pair's operands
-                const f32x16 zero = {0.0f};
-                f32x16 acc[2][R];
+                f32x16 acc[R][2];
 #pragma unroll
-                for (int u = 0; u < 2; ++u)
+                for (int r = 0; r < R; ++r) score_pair(acc[r], a, bop[r]);
 #pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        acc[u][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, a[u][0]), __builtin_bit_cast(bf16x8, bop[r][0]), zero, 0, 0, 0);
-#pragma unroll
-                for (int u = 0; u < 2; ++u)
-#pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        acc[u][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, a[u][1]), __builtin_bit_cast(bf16x8, bop[r][1]), acc[u][r], 0,
-                            0, 0);
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-#pragma unroll
-                    for (int q = 0; q < 16; ++q)
-                        best[r][q] = __builtin_fminf(__builtin_fminf(best[r][q], acc[0][r][q]), acc[1][r][q]);
+                for (int r = 0; r < R; ++r) fold_pair(best[r], acc[r]);
             }
 
             // per kernel tile: smallest and second smallest slot minimum, the slot number q

@@ -116,7 +116,7 @@ __global__ __launch_bounds__(kWave) void sq_finish_kernel(const double* part, in
     if (lane == 0) *out = v;
 }
 
-// Every layer of a stack: workgroup b of a layer rebuilds rows [4096 b, 4096 b + 4096) of
+// Every layer of a stack: workgroup b of a layer rebuilds rows [2048 b, 2048 b + 2048) of
 // W_hat.  Each wave takes 64 consecutive rows (2304 bytes) per step: the reference rows
 // come in and the rebuilt rows go out with fully coalesced dword accesses through a
 // per-wave LDS buffer (lane l moves floats l, l + 64, ...), while lane l rebuilds row l

@@ -33,13 +33,24 @@ FP32_PEAK_TFLOPS = 157.3     # MI355X dense FP32 (matrix cores and vector)
 HBM_PEAK_GBS = 8000.0
 
 
+# workloads: layer generator, codebook size, Lloyd rounds, description
+CONFIGS = {
+    "resnet18": ("resnet18_stack", 256, 30, "resnet18-3x3-stack (16 layers, 1,220,608 kernels, Laplace)"),
+    "vgg16": ("vgg16_stack", 256, 30, "vgg16-3x3-stack (13 layers, 1,634,496 kernels, normal; conv1 k clamped to 192)"),
+    "single": ("single_layer", 256, 20, "single 64x64 layer (4096 kernels, normal)"),
+    "stress": ("stress_layer", 4096, 10, "stress 1024x1024 layer (1,048,576 kernels from 4096 clusters)"),
+}
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--iters", type=int, default=30, help="Lloyd rounds per layer")
-    ap.add_argument("--k", type=int, default=256)
+    ap.add_argument("--config", default="resnet18", choices=sorted(CONFIGS),
+                    help="workload (default: the ResNet-18-shaped stack, the headline metric)")
+    ap.add_argument("--iters", type=int, default=None, help="Lloyd rounds per layer (default: the config's)")
+    ap.add_argument("--k", type=int, default=None, help="codebook size (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -69,17 +80,23 @@ def assign_traffic():
     return rec["bytes_per_launch"]
 
 
-def cpu_baseline(layers, iters):
+def cpu_baseline(layers, iters, budget=1e9):
     """The CPU oracle (single-threaded plain C) on a bounded sample: `iters` Lloyd
-    rounds plus the final assignment on every layer of the same stack."""
+    rounds plus the final assignment on every layer, each layer cut to its first rows
+    when the full stack would exceed `budget` (kernel x entry x round) units."""
     import oracle
+    work = sum(L.n * L.k * (iters + 1) for L in layers)
+    f = min(1.0, budget / work)
     t0 = time.perf_counter()
+    n = 0
     for L in layers:
-        oracle.fit(L.X, L.C0, iters)
+        m = min(L.n, max(L.k, int(L.n * f)))
+        oracle.fit(L.X[:m], L.C0, iters)
+        n += m
     dt = time.perf_counter() - t0
-    n = sum(L.n for L in layers)
+    rows = "all rows" if f >= 1.0 else f"the first {100 * f:.1f} % of the rows"
     return {"value": n * iters / dt, "unit": "kernels/s", "cores": 1, "kind": "oracle",
-            "sample": f"{iters} Lloyd rounds + final assignment on all {len(layers)} layers "
+            "sample": f"{iters} Lloyd rounds + final assignment on {rows} of all {len(layers)} layers "
                       f"({n} kernels, k={layers[0].k}), {dt:.1f} s"}
 
 
@@ -98,10 +115,11 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    layers = synth.resnet18_stack(k=args.k)
+    gen, k_default, iters_default, desc = CONFIGS[args.config]
+    k = args.k if args.k is not None else k_default
+    T = args.iters if args.iters is not None else iters_default
+    layers = getattr(synth, gen)(k=k)
     n_total = sum(L.n for L in layers)
-    T = args.iters
-    k = layers[0].k
 
     # inputs resident in HBM before timing
     X = [torch.from_numpy(L.X).to(dev) for L in layers]
@@ -114,16 +132,16 @@ def main():
     for i, v in enumerate(views):
         st.C[i] = v.view(-1, 9)
         st.layers[i].C = st.C[i].data_ptr()
-    bits = kq.index_bits(k)
+    bits = [kq.index_bits(L.k) for L in layers]
     cb_out = [(torch.empty(L.k * 9, dtype=torch.uint8, device=dev), torch.empty(64, device=dev),
                torch.empty(L.k, 9, device=dev)) for L in layers]
-    p_idx = [torch.empty((L.n * bits + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L in layers]
+    p_idx = [torch.empty((L.n * b + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L, b in zip(layers, bits)]
     p_codes = [torch.empty((L.k * 9 * 6 + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L in layers]
     W_hat = [torch.empty(L.n, 9, device=dev) for L in layers]
     sq = torch.zeros(len(layers), dtype=torch.float64, device=dev)
-    pack_jobs = [(st.idx[i], bits, p_idx[i]) for i in range(len(layers))] + \
+    pack_jobs = [(st.idx[i], bits[i], p_idx[i]) for i in range(len(layers))] + \
                 [(cb_out[i][0], 6, p_codes[i]) for i in range(len(layers))]
-    recon = [{"packed": p_idx[i], "bits": bits, "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i], "W_ref": X[i],
+    recon = [{"packed": p_idx[i], "bits": bits[i], "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i], "W_ref": X[i],
               "sq_error": sq[i:i + 1]} for i, L in enumerate(layers)]
     recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
 
@@ -188,8 +206,8 @@ def main():
 
     mean_ms = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for name, pairs in ev.items()}
     assign_ms, update_ms = mean_ms["assign"], mean_ms["update"]
-    rec_bytes = sum(L.n * (bits / 8 + 36 + 36) for L in layers)   # packed index + reference row + output row
-    flops = 18.0 * k * n_total                      # 9 multiply-adds per (kernel, entry) pair
+    rec_bytes = sum(L.n * (b / 8 + 36 + 36) for L, b in zip(layers, bits))  # packed index + reference + output row
+    flops = 18.0 * sum(L.k * L.n for L in layers)   # 9 multiply-adds per (kernel, entry) pair
     achieved = flops / (assign_ms * 1e-3) / 1e12
     upd_bytes = 40.0 * n_total                      # 36-byte kernel + 4-byte index per kernel
     upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9
@@ -203,8 +221,8 @@ def main():
         "reconstruct_ms": mean_ms["reconstruct"],
         "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9,
         "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
-        "beta_K": sum(L.k * 9 * 32 + L.n * bits for L in layers) / (9 * n_total),
-        "beta_KC": sum(L.k * 9 * 6 + L.n * bits for L in layers) / (9 * n_total)}}), file=sys.stderr)
+        "beta_K": sum(L.k * 9 * 32 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
+        "beta_KC": sum(L.k * 9 * 6 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total)}}), file=sys.stderr)
 
     result = {
         "metric": METRIC,
@@ -219,11 +237,12 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"resnet18-3x3-stack k={k}: {T} Lloyd rounds + final assign, "
+        "config": {"workload": f"{desc} k={k}: {T} Lloyd rounds + final assignment, "
                                "6-bit weighted codebook quantization, index/code packing, packed reconstruction",
                    "layers": len(layers), "kernels": n_total, "k": k, "lloyd_rounds": T, "codebook_bits": 6},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / FP32_PEAK_TFLOPS, "traffic": assign_traffic(),
+                     "frac": achieved / FP32_PEAK_TFLOPS,
+                     "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) else None,
                      "kernel": "assign_kernel (one launch per Lloyd round, whole stack)"},
     }
     if not args.no_cpu_baseline:

@@ -40,9 +40,9 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
     memset(&p, 0, sizeof(p));
     size_t off = 0;
     for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
-    int64_t total_n = 0;
-    for (int32_t l = l0; l < l1; ++l) total_n += layers[l].n;
-    p.kpb = update_kernels_per_block(total_n);
+    int64_t weighted_n = 0;  // update: every range of a layer reads its kernels' indices
+    for (int32_t l = l0; l < l1; ++l) weighted_n += layers[l].n * update_ranges(layers[l].k);
+    const int kpb = update_kernels_per_block(weighted_n);
     int unit = 0;
     for (int32_t l = l0; l < l1; ++l) {
         const kq_layer& s = layers[l];
@@ -68,9 +68,13 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
             } else if (d.dist) {
                 d.part = (double*)(w + ws_assign_part(s.n));
             }
-            d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n));
-            d.nunits = update_blocks(s.n, p.kpb);
-            d.flags = (int)kflags | (update_uses_lds(s.k) ? 0 : kFlagAtomicHist);
+            d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k));
+            d.ranges = update_ranges(s.k);
+            d.krange = (s.k + d.ranges - 1) / d.ranges;
+            d.chunk = update_chunk(s.n, s.k, kpb);
+            d.nchunks = (int)((s.n + d.chunk - 1) / d.chunk);
+            d.nunits = d.ranges * d.nchunks;
+            d.flags = (int)kflags;
         }
         d.unit_begin = unit;
         unit += d.nunits;
@@ -115,11 +119,6 @@ kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
                      const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Update, slot, C_old, kflags, from_assign);
-    // large codebooks accumulate with global atomics: clear their accumulators first
-    for (int l = 0; l < p.nlayers; ++l)
-        if ((p.L[l].flags & kFlagAtomicHist) &&
-            launch_fill_zero(p.L[l].hist, sizeof(int64_t) * 10 * (size_t)p.L[l].k, s) != hipSuccess)
-            return KQ_ERR_HIP;
     if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
     if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;

@@ -32,31 +32,47 @@ constexpr int kAssignChunk = kAssignOcc <= 2 ? 512 : (kAssignOcc == 3 ? 384 : 32
 constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every CU full
 
 // ---- update kernel geometry ---------------------------------------------------------
-// One launch updates every layer of a stack; all its workgroups read the same number of
-// kernels, chosen so that the launch has about one workgroup per CU (a multiple of 256
-// between kUpdateMinKernelsPerBlock and kUpdateMaxKernelsPerBlock).
+// One launch updates every layer of a stack.  A layer's kernels are cut into chunks and
+// its codebook into ranges of at most kUpdateLdsMaxK entries (the LDS histogram of one
+// range); a workgroup adds the kernels of one chunk whose entry lies in one range.
+// Chunks hold about the number of kernels that gives one workgroup per CU for the whole
+// launch (a multiple of 256, at least kUpdateMinKernelsPerBlock), and a layer has at
+// most update_max_chunks(n, k) of them (that bounds its partial histograms).
 constexpr int kUpdateThreads = 1024;
 constexpr int kUpdateMinKernelsPerBlock = 1024;
-constexpr int kUpdateMaxKernelsPerBlock = 16384;
 constexpr int kUpdateTargetBlocks = 256;
-constexpr int kUpdateLdsMaxK = 768;  // LDS histogram [k][9] int64 + [k] u32 up to this k
-constexpr int kFinishEntries = 4;    // codebook entries per finishing workgroup
+constexpr int kUpdateLdsMaxK = 768;     // LDS histogram [768][9] int64 + [768] u32
+constexpr int kFinishEntries = 4;       // codebook entries per finishing workgroup
+constexpr size_t kUpdatePartialBudget = size_t(1) << 24;  // bytes of partials per layer above 768 entries
+
+inline int update_ranges(int32_t k) { return (k + kUpdateLdsMaxK - 1) / kUpdateLdsMaxK; }
+inline int update_max_chunks(int64_t n, int32_t k) {
+    const int64_t c = (n + kUpdateMinKernelsPerBlock - 1) / kUpdateMinKernelsPerBlock;
+    if (k <= kUpdateLdsMaxK) return (int)c;
+    int64_t cap = (int64_t)(kUpdatePartialBudget / (sizeof(int64_t) * 10 * (size_t)k));
+    if (cap < 1) cap = 1;
+    return (int)(c < cap ? c : cap);
+}
+// kernels per chunk for a launch whose layers weigh `weighted_n` = sum of ranges x n
+inline int update_kernels_per_block(int64_t weighted_n) {
+    int64_t kpb = (weighted_n / kUpdateTargetBlocks + 255) & ~int64_t(255);
+    if (kpb < kUpdateMinKernelsPerBlock) kpb = kUpdateMinKernelsPerBlock;
+    if (kpb > (int64_t(1) << 30)) kpb = int64_t(1) << 30;
+    return (int)kpb;
+}
+inline int update_chunk(int64_t n, int32_t k, int kpb) {
+    const int64_t mc = update_max_chunks(n, k);
+    int64_t cs = ((n + mc - 1) / mc + 255) & ~int64_t(255);
+    if (cs < kpb) cs = kpb;
+    return (int)cs;
+}
 
 // ---- squared-error reduction ------------------------------------------------------------
 constexpr int kSqThreads = 256;
 constexpr int kSqPerBlock = 8192;
 
 inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1) / kAssignKernelsPerTile); }
-// workgroups of one layer at `kpb` kernels each; the workspace allows for the smallest kpb
-inline int update_blocks(int64_t n, int kpb = kUpdateMinKernelsPerBlock) { return (int)((n + kpb - 1) / kpb); }
-inline int update_kernels_per_block(int64_t total_n) {
-    int64_t kpb = (total_n / kUpdateTargetBlocks + 255) & ~int64_t(255);
-    if (kpb < kUpdateMinKernelsPerBlock) kpb = kUpdateMinKernelsPerBlock;
-    if (kpb > kUpdateMaxKernelsPerBlock) kpb = kUpdateMaxKernelsPerBlock;
-    return (int)kpb;
-}
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
-inline bool update_uses_lds(int32_t k) { return k <= kUpdateLdsMaxK; }
 
 // fixed-point scale of the exact member sums: q(x) = rint(x * 2^s), s = 57 - ceil(log2 n)
 inline int fixed_shift(int64_t n) {
@@ -66,21 +82,20 @@ inline int fixed_shift(int64_t n) {
 }
 
 // ---- per-layer workspace ---------------------------------------------------------------
-//   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]   (overwritten each call)
-//   update distortion partials : fp64 [update_blocks(n)]                 (overwritten each call)
-//   update histograms          : int64 [update_blocks(n)][k][10] per-block partial sums
-//                                (k <= kUpdateLdsMaxK, overwritten each call), or int64 [k][10]
-//                                accumulators (larger k; zero-filled before each update)
+//   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]           (overwritten each call)
+//   update distortion partials : fp64 [ranges * max chunks]                      (overwritten each call)
+//   update histograms          : int64 [max chunks][k][10] per-chunk partial sums (overwritten each call)
 inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 inline size_t ws_assign_part(int64_t n) { return align256(sizeof(double) * (size_t)assign_tiles(n) * kAssignWaves); }
-inline size_t ws_update_part(int64_t n) { return align256(sizeof(double) * (size_t)update_blocks(n)); }
-inline size_t ws_hist(int64_t n, int32_t k) {
-    const size_t copies = update_uses_lds(k) ? (size_t)update_blocks(n) : 1;
-    return align256(sizeof(int64_t) * 10 * (size_t)k * copies);
+inline size_t ws_update_part(int64_t n, int32_t k) {
+    return align256(sizeof(double) * (size_t)update_ranges(k) * (size_t)update_max_chunks(n, k));
 }
-inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n) + ws_hist(n, k); }
+inline size_t ws_hist(int64_t n, int32_t k) {
+    return align256(sizeof(int64_t) * 10 * (size_t)k * (size_t)update_max_chunks(n, k));
+}
+inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n, k) + ws_hist(n, k); }
 
-enum : int { kFlagCountsOnly = 1, kFlagAtomicHist = 2 };
+enum : int { kFlagCountsOnly = 1 };
 
 struct DevLayer {
     const float* X;
@@ -100,6 +115,10 @@ struct DevLayer {
     int shift;                // fixed-point scale (update)
     int flags;                // kFlag*
     int napart;               // number of assignment partials
+    int ranges;               // update: codebook ranges (workgroups per chunk)
+    int krange;               // update: entries per range
+    int chunk;                // update: kernels per chunk
+    int nchunks;              // update: chunks (= partial histograms)
 };
 
 // Kernel arguments of a stack launch.  The first unit of every layer is repeated in a
@@ -109,8 +128,6 @@ struct DevLayer {
 struct StackParams {
     int nlayers;
     int total_units;
-    int kpb;  // update: kernels per workgroup
-    int pad;
     int unit_begin[KQ_MAX_STACK];
     DevLayer L[KQ_MAX_STACK];
 };

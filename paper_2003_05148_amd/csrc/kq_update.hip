@@ -6,21 +6,21 @@
 // overflow int64 (|x| < 32).  Integer addition is associative, so the sums, and with
 // them the new codebook, do not depend on the order in which blocks or lanes add.
 //
-// update_kernel: one launch covers every layer of a stack; each workgroup of 1024
-// threads reads the same number of consecutive kernels of one layer (about one workgroup
-// per CU for the whole launch), one 36-byte row per thread and step (consecutive lanes,
-// consecutive rows), two steps in flight at a time.  It accumulates a private LDS histogram ([k][9] int64 sums +
-// [k] counts, ds_add_u64; dynamic LDS sized for the largest k of the launch) and stores
-// it whole as its partial histogram; with more than kUpdateLdsMaxK entries it adds
-// straight into [k][10] global accumulators instead.  Asked for the distortion of a
-// standalone assignment, it also sums, in a fixed order, the fp32 distances of its
-// kernels to their entries of the old codebook.
+// update_kernel: one launch covers every layer of a stack.  A layer's kernels are cut
+// into chunks and its codebook into ranges of at most 768 entries; a workgroup of 1024
+// threads takes one (chunk, range) pair: it reads the chunk's indices, one 36-byte row per
+// thread and step (consecutive lanes, consecutive rows, two steps in flight), loads the
+// rows whose entry lies in its range and adds them to a private LDS histogram of the range
+// ([768][9] int64 sums + [768] counts at most, ds_add_u64), then stores the histogram
+// into the chunk's partial ([chunks][k][10] int64).  Chunk sizes give about one workgroup
+// per CU for the whole launch.  Asked for the distortion of a standalone assignment, it
+// also sums, in a fixed order, the fp32 distances of its rows to their old entries.
 // update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
-// groups of 40 threads add a sixteenth of the partial histograms each (any order gives
-// the same integers), then it divides and writes the codebook and the counts.  One more
-// workgroup per layer adds the distortion partials in a fixed order (those of the
-// assignment kernel when the distortion comes from there).  The kernel boundary
-// orders every partial before its use, so no fence or atomic counter is needed.
+// groups of 40 threads add a sixteenth of the chunk partials each (any order gives the same
+// integers), then it divides and writes the codebook and the counts.  One more workgroup
+// per layer adds the distortion partials in a fixed order (those of the assignment kernel
+// when the distortion comes from there).  The kernel boundary orders every partial before
+// its use, so no fence or atomic counter is needed.
 #include "kq_internal.h"
 
 namespace kq {
@@ -36,53 +36,48 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
 }
 
 struct UpdateCtx {
-    unsigned long long* s_sum;
-    unsigned* s_cnt;
-    unsigned long long* acc;
+    unsigned long long* s_sum;  // [krange][9]
+    unsigned* s_cnt;            // [krange]
     const float* C_old;
     double scale;
-    int k;
-    bool use_lds, sums, want_dist;
+    int j0, kr;                 // the entry range [j0, j0 + kr)
+    bool sums, want_dist;
 };
 
-// add one kernel (row x, entry j) to the histogram
+// add one kernel (row x, entry j) to the histogram if j is in the range
 __device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[kDim], int j, double& dacc) {
-    if ((unsigned)j >= (unsigned)c.k) return;
+    const int jr = j - c.j0;
+    if ((unsigned)jr >= (unsigned)c.kr) return;
     if (c.want_dist) dacc += (double)sqdist9u(x, c.C_old + (size_t)j * kDim);
-    if (c.use_lds) {
-        atomicAdd(&c.s_cnt[j], 1u);
-        if (c.sums) {
+    atomicAdd(&c.s_cnt[jr], 1u);
+    if (c.sums) {
 #pragma unroll
-            for (int d = 0; d < kDim; ++d)
-                atomicAdd(&c.s_sum[j * kDim + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
-        }
-    } else {
-        atomicAdd(&c.acc[(size_t)j * 10 + 9], 1ull);
-        if (c.sums) {
-#pragma unroll
-            for (int d = 0; d < kDim; ++d)
-                atomicAdd(&c.acc[(size_t)j * 10 + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
-        }
+        for (int d = 0; d < kDim; ++d)
+            atomicAdd(&c.s_sum[jr * kDim + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
     }
 }
 
 // Thread t takes kernels i, i + 1024, ... (i = first + t): consecutive lanes read
-// consecutive 36-byte rows with 9 dword loads each, two kernels in flight per thread.
-template <bool NEED_X>
+// consecutive 36-byte rows with 9 dword loads each, two kernels in flight per thread; a row
+// is loaded only when its entry lies in the workgroup's range (with a single range every
+// row is, and the row loads need not wait for the indices).
+template <bool NEED_X, bool RANGED>
 __device__ __forceinline__ void add_rows(const UpdateCtx& c, const float* __restrict__ X,
                                          const int32_t* __restrict__ idx, int i, int i1, double& dacc) {
     for (; i < i1; i += 2 * kUpdateThreads) {
         const int ib = i + kUpdateThreads;
         const bool two = ib < i1;
         const int ja = idx[i], jb = two ? idx[ib] : -1;  // -1: nothing to add
+        const bool ina = !RANGED || (unsigned)(ja - c.j0) < (unsigned)c.kr;
+        const bool inb = !RANGED || (unsigned)(jb - c.j0) < (unsigned)c.kr;
         float xa[kDim], xb[kDim];
         if (NEED_X) {
             const float* pa = X + (size_t)i * kDim;
             const float* pb = X + (size_t)(two ? ib : i) * kDim;
 #pragma unroll
             for (int d = 0; d < kDim; ++d) {
-                xa[d] = pa[d];
-                xb[d] = pb[d];
+                xa[d] = ina ? pa[d] : 0.0f;
+                xb[d] = inb ? pb[d] : 0.0f;
             }
         } else {
 #pragma unroll
@@ -94,49 +89,45 @@ __device__ __forceinline__ void add_rows(const UpdateCtx& c, const float* __rest
 }
 
 __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParams p) {
-    extern __shared__ unsigned long long s_dyn[];  // [k][9] sums, then [k] u32 counts
+    extern __shared__ unsigned long long s_dyn[];  // [krange][9] sums, then [krange] u32 counts
     __shared__ double s_wd[kUpdateThreads / kWave];
 
     const int li = find_layer(p, blockIdx.x);
     const DevLayer& L = p.L[li];
-    const int lb = blockIdx.x - L.unit_begin;
+    const int u = blockIdx.x - L.unit_begin;
+    const int chunk = u / L.ranges, range = u - chunk * L.ranges;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = L.n, k = L.k;
     UpdateCtx c;
+    c.j0 = range * L.krange;
+    c.kr = min(k - c.j0, L.krange);
     c.s_sum = s_dyn;
-    c.s_cnt = (unsigned*)(s_dyn + (size_t)k * kDim);
-    c.acc = (unsigned long long*)L.hist;
+    c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
     c.scale = ldexp(1.0, L.shift);
-    c.k = k;
-    c.use_lds = (L.flags & kFlagAtomicHist) == 0;
     c.sums = (L.flags & kFlagCountsOnly) == 0;
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;
-    const float* __restrict__ X = L.X;
-    const int32_t* __restrict__ idx = L.idx;
 
-    if (c.use_lds) {
-        for (int e = tid; e < k * kDim; e += kUpdateThreads) c.s_sum[e] = 0ull;
-        for (int e = tid; e < k; e += kUpdateThreads) c.s_cnt[e] = 0u;
-        __syncthreads();
-    }
+    for (int e = tid; e < c.kr * kDim; e += kUpdateThreads) c.s_sum[e] = 0ull;
+    for (int e = tid; e < c.kr; e += kUpdateThreads) c.s_cnt[e] = 0u;
+    __syncthreads();
 
     double dacc = 0.0;
-    const int i0 = lb * p.kpb;
-    const int i1 = min(n, i0 + p.kpb);
-    if (need_x)
-        add_rows<true>(c, X, idx, i0 + tid, i1, dacc);
+    const int i0 = chunk * L.chunk;
+    const int i1 = min(n, i0 + L.chunk);
+    if (!need_x)
+        add_rows<false, false>(c, L.X, L.idx, i0 + tid, i1, dacc);
+    else if (L.ranges == 1)
+        add_rows<true, false>(c, L.X, L.idx, i0 + tid, i1, dacc);
     else
-        add_rows<false>(c, X, idx, i0 + tid, i1, dacc);
+        add_rows<true, true>(c, L.X, L.idx, i0 + tid, i1, dacc);
 
-    if (c.use_lds) {
-        __syncthreads();
-        unsigned long long* __restrict__ out = c.acc + (size_t)lb * k * 10;
-        for (int e = tid; e < k * 10; e += kUpdateThreads) {
-            const int j = e / 10, d = e - 10 * j;
-            out[e] = (d == 9) ? (unsigned long long)c.s_cnt[j] : c.s_sum[j * kDim + d];
-        }
+    __syncthreads();
+    unsigned long long* __restrict__ out = (unsigned long long*)L.hist + ((size_t)chunk * k + c.j0) * 10;
+    for (int e = tid; e < c.kr * 10; e += kUpdateThreads) {
+        const int j = e / 10, d = e - 10 * j;
+        out[e] = (d == 9) ? (unsigned long long)c.s_cnt[j] : c.s_sum[j * kDim + d];
     }
     if (c.want_dist) {
 #pragma unroll
@@ -146,7 +137,7 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
         if (tid == 0) {
             double v = s_wd[0];
             for (int w = 1; w < kUpdateThreads / kWave; ++w) v += s_wd[w];
-            L.part[lb] = v;
+            L.part[u] = v;
         }
     }
 }
@@ -175,25 +166,20 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
     const int tid = threadIdx.x;
     const int g = tid / (kFinishEntries * 10), v = tid - g * (kFinishEntries * 10);
     const int j = j0 + v / 10, d = v - 10 * (v / 10);
-    const bool atomic_hist = (L.flags & kFlagAtomicHist) != 0;
     const int k = L.k;
     const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;
 
     unsigned long long s = 0ull;
     if (j < k) {
-        if (atomic_hist) {
-            if (g == 0) s = h[(size_t)j * 10 + d];
-        } else {
-            const int nb = L.nunits;
-            const size_t stride = (size_t)k * 10;
-            const unsigned long long* hp = h + (size_t)j * 10 + d;
-            int q = g;
+        const int nb = L.nchunks;
+        const size_t stride = (size_t)k * 10;
+        const unsigned long long* hp = h + (size_t)j * 10 + d;
+        int q = g;
 #pragma unroll 1
-            for (; q + 3 * kFinishGroups < nb; q += 4 * kFinishGroups)
-                s += hp[q * stride] + hp[(q + kFinishGroups) * stride] + hp[(q + 2 * kFinishGroups) * stride] +
-                     hp[(q + 3 * kFinishGroups) * stride];
-            for (; q < nb; q += kFinishGroups) s += hp[q * stride];
-        }
+        for (; q + 3 * kFinishGroups < nb; q += 4 * kFinishGroups)
+            s += hp[q * stride] + hp[(q + kFinishGroups) * stride] + hp[(q + 2 * kFinishGroups) * stride] +
+                 hp[(q + 3 * kFinishGroups) * stride];
+        for (; q < nb; q += kFinishGroups) s += hp[q * stride];
     }
     s_S[g][v] = (long long)s;
     __syncthreads();
@@ -226,11 +212,10 @@ __global__ void fill_zero_kernel(uint4* p, size_t n16, unsigned char* tail, size
 
 hipError_t launch_update(const StackParams& p, hipStream_t s) {
     size_t lds = 0;
-    for (int l = 0; l < p.nlayers; ++l)
-        if ((p.L[l].flags & kFlagAtomicHist) == 0) {
-            const size_t b = (size_t)p.L[l].k * (kDim * sizeof(unsigned long long) + sizeof(unsigned));
-            lds = b > lds ? b : lds;
-        }
+    for (int l = 0; l < p.nlayers; ++l) {
+        const size_t b = (size_t)p.L[l].krange * (kDim * sizeof(unsigned long long) + sizeof(unsigned));
+        lds = b > lds ? b : lds;
+    }
     hipLaunchKernelGGL(update_kernel, dim3(p.total_units), dim3(kUpdateThreads), lds, s, p);
     return hipGetLastError();
 }

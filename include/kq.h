@@ -243,7 +243,8 @@ kq_status kq_reconstruct(const int32_t* idx, int64_t n, const float* C, int32_t 
 
 /*
  * kq_reconstruct_packed -- the same from the stored form: indices read from a
- * kq_pack_bits stream of `bits` = ceil(log2 k) bits each.
+ * kq_pack_bits stream of `bits` = ceil(log2 k) bits each (packed device, 4-byte aligned,
+ * ceil(n * bits / 8) bytes; nothing past its end is read).
  */
 kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, const float* C,
                                 int32_t k, int32_t dim, float* W_hat, void* stream);
@@ -281,7 +282,7 @@ kq_status kq_pack_bits_stack(const kq_pack_job* jobs, int32_t n_jobs, void* stre
 /* One layer of kq_reconstruct_stack (device pointers). */
 typedef struct kq_recon_layer {
     const int32_t* idx;      /* [n] indices, or NULL to read them from `packed` */
-    const uint8_t* packed;   /* kq_pack_bits stream of `bits`-bit indices (when idx is NULL) */
+    const uint8_t* packed;   /* kq_pack_bits stream of `bits`-bit indices (when idx is NULL), 4-byte aligned */
     int32_t bits;            /* 0..16, used with `packed` */
     int32_t k;               /* 1..KQ_MAX_K; indices outside [0, k) give zero rows */
     int64_t n;               /* 1 <= n < 2^31 */

@@ -358,7 +358,8 @@ kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, 
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K || bits < 0 || bits > 16) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k)) return KQ_ERR_ARG;
-    if ((bits > 0 && !packed) || !C || !W_hat || !aligned(C, 4) || !aligned(W_hat, 16)) return KQ_ERR_ARG;
+    if ((bits > 0 && (!packed || !aligned(packed, 4))) || !C || !W_hat || !aligned(C, 4) || !aligned(W_hat, 16))
+        return KQ_ERR_ARG;
     const kq_recon_layer l = {nullptr, packed, bits, k, n, C, W_hat, nullptr, nullptr};
     return kq_reconstruct_stack(&l, 1, nullptr, 0, stream);
 }
@@ -409,7 +410,7 @@ static kq_status check_recon_layer(const kq_recon_layer& l) {
     if (!l.idx && (l.bits < 0 || l.bits > 16)) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(l.n) || !valid_k(l.k)) return KQ_ERR_ARG;
     if (!l.C || !l.W_hat || !aligned(l.C, 4) || !aligned(l.W_hat, 4)) return KQ_ERR_ARG;
-    if (l.idx ? !aligned(l.idx, 4) : (l.bits > 0 && !l.packed)) return KQ_ERR_ARG;
+    if (l.idx ? !aligned(l.idx, 4) : (l.bits > 0 && (!l.packed || !aligned(l.packed, 4)))) return KQ_ERR_ARG;
     if (l.sq_error && (!l.W_ref || !aligned(l.sq_error, 8))) return KQ_ERR_ARG;
     if (l.W_ref && !aligned(l.W_ref, 4)) return KQ_ERR_ARG;
     return KQ_OK;

@@ -227,8 +227,14 @@ struct ReconParams {
     int unit_begin[KQ_MAX_STACK];  // first workgroup of each layer, INT_MAX past the last
     ReconLayer L[KQ_MAX_STACK];
 };
-constexpr int kReconThreads = 512;
-constexpr int kReconRows = 2048;        // rows per workgroup of the stack reconstruction
+#ifndef KQ_RECON_THREADS
+#define KQ_RECON_THREADS 512
+#endif
+#ifndef KQ_RECON_ROWS
+#define KQ_RECON_ROWS 2048
+#endif
+constexpr int kReconThreads = KQ_RECON_THREADS;
+constexpr int kReconRows = KQ_RECON_ROWS;  // rows per workgroup of the stack reconstruction
 constexpr int kReconLdsFloats = 16384;  // codebooks up to this many values are gathered from LDS
 inline int recon_blocks(int64_t n) { return (int)((n + kReconRows - 1) / kReconRows); }
 hipError_t launch_pack_stack(const PackParams& p, hipStream_t s);

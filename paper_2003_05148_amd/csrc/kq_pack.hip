@@ -5,9 +5,9 @@
 //                except the partial last one.
 //   unpack:      the inverse, one thread per value.
 //   reconstruct: W_hat[i][d] = C[idx_i][d] for the layers of a stack in one launch (a
-//                single layer is a stack of one), 64 rows per wave step moved with
-//                coalesced accesses through LDS, indices either plain int32 or read from
-//                a packed stream, the codebook gathered from LDS.  HBM traffic per kernel: 4 bytes of index (or bits/8 packed)
+//                single layer is a stack of one), 64 rows per wave step written with
+//                coalesced accesses, indices either plain int32 or read from a packed
+//                stream, the codebook gathered from LDS.  HBM traffic per kernel: 4 bytes of index (or bits/8 packed)
 //                + 36 bytes written (+ 36 bytes read when the squared error against
 //                the original row is asked for).
 //   pack stack:  one launch for the streams of a whole network.
@@ -117,88 +117,130 @@ __global__ __launch_bounds__(kWave) void sq_finish_kernel(const double* part, in
 }
 
 // Every layer of a stack: workgroup b of a layer rebuilds rows [2048 b, 2048 b + 2048) of
-// W_hat.  Each wave takes 64 consecutive rows (2304 bytes) per step: the reference rows
-// come in and the rebuilt rows go out with fully coalesced dword accesses through a
-// per-wave LDS buffer (lane l moves floats l, l + 64, ...), while lane l rebuilds row l
-// from its index and the codebook.  The next step's index and reference values are
-// loaded before the current step is processed.  A codebook of up to kReconLdsFloats
-// values is copied into LDS first, so the row gathers hit LDS.  When the layer asks for
-// it, each lane also sums (W_ref - W_hat)^2 over its rows in fp64, row by row in
-// dimension order; the lanes of a wave are combined by a butterfly, the waves in order,
-// and a second kernel adds the workgroup partials in order.
-__device__ __forceinline__ int recon_index(const ReconLayer& L, int i) {
-    return L.idx ? L.idx[i] : (L.bits ? read_packed(L.packed, L.bits, i, L.pbytes) : 0);
+// W_hat.  Each wave takes 64 consecutive rows (576 floats, 2304 bytes) per step and works
+// in the coalesced layout: lane l handles floats l + 64 q (q < 9) of the step, which are
+// dimension (l + 64 q) % 9 of row (l + 64 q) / 9.  Lane r first obtains the index of row r
+// (an int32 load, or its field of the packed stream: the step's 8 * bits bytes are loaded
+// as dwords by the first 2 * bits lanes and each lane extracts its field with two
+// ds_bpermute); each float then takes its row's index from that row's lane (ds_bpermute)
+// and gathers its value from the codebook, copied into LDS first when it holds at most
+// kReconLdsFloats values.  Loads and stores are all full 256-byte wave accesses, and the
+// next step's index and reference values load while the current step is rebuilt.  When the
+// layer asks for it, each lane also sums (W_ref - W_hat)^2 in fp64 over its floats in a
+// fixed order; the lanes of a wave are combined by a butterfly, the waves in order, and a
+// second kernel adds the workgroup partials in order.
+
+// the index of the step's row `lane` (rows b0 .. b0 + cnt - 1), or -1 past the end of the layer
+__device__ __forceinline__ int recon_step_index(const ReconLayer& L, int b0, int cnt, int lane) {
+    if (L.idx) return lane < cnt ? L.idx[b0 + lane] : -1;
+    const int b = L.bits;
+    if (b == 0) return lane < cnt ? 0 : -1;
+    // dwords [2 b s, 2 b s + 2 b) of the stream hold the step's fields (b0 = 64 s)
+    const long long w = (long long)(b0 / kWave) * 2 * b + lane;
+    unsigned dw = 0;
+    if (lane < 2 * b) {
+        if (4 * w + 4 <= L.pbytes) {
+            dw = ((const unsigned*)L.packed)[w];
+        } else {  // the stream's last, partial dword
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (4 * w + t < L.pbytes) dw |= (unsigned)L.packed[4 * w + t] << (8 * t);
+        }
+    }
+    const int bit = lane * b, wi = bit >> 5, o = bit & 31;
+    const unsigned lo = (unsigned)__builtin_amdgcn_ds_bpermute(wi * 4, (int)dw);
+    const unsigned hi = (unsigned)__builtin_amdgcn_ds_bpermute((wi + 1) * 4, (int)dw);
+    const unsigned v = (unsigned)((((unsigned long long)hi << 32) | lo) >> o) & ((1u << b) - 1u);
+    return lane < cnt ? (int)v : -1;
+}
+
+struct ReconStep {
+    int j;             // index of this lane's row
+    float x[kDim];     // reference floats l + 64 q of the step
+};
+
+__device__ __forceinline__ void recon_load(ReconStep& s, const ReconLayer& L, int b0, int cnt, int lane, bool err) {
+    s.j = recon_step_index(L, b0, cnt, lane);
+    if (!err) return;
+    const float* __restrict__ ref = L.W_ref + (size_t)b0 * kDim;
+    if (cnt == kWave) {
+#pragma unroll
+        for (int q = 0; q < kDim; ++q) s.x[q] = ref[lane + kWave * q];
+    } else {
+        const int nf = cnt * kDim;
+#pragma unroll
+        for (int q = 0; q < kDim; ++q) s.x[q] = lane + kWave * q < nf ? ref[lane + kWave * q] : 0.0f;
+    }
+}
+
+// The steps of one wave.  LDS selects where the codebook is gathered from; the two
+// cases are separate instantiations so that the LDS gathers are ds_read instructions
+// (a generic pointer that may point into LDS compiles to FLAT loads, whose LDS
+// aperture is decided from the address before the instruction offset is added).
+template <bool LDS>
+__device__ __forceinline__ double recon_steps(const ReconLayer& L, const float* __restrict__ s_cb, int i0, int i1,
+                                              int lane, int wave, bool err) {
+    constexpr int kWaves = kReconThreads / kWave;
+    int src[kDim], dim[kDim];  // row lane (byte address for ds_bpermute) and dimension of float q
+#pragma unroll
+    for (int q = 0; q < kDim; ++q) {
+        const int f = lane + kWave * q, r = f / kDim;
+        src[q] = r * 4;
+        dim[q] = f - kDim * r;
+    }
+    const int nsteps = (i1 - i0 + kWave - 1) / kWave;
+    double acc = 0.0;
+    int st = wave;
+    if (st >= nsteps) return acc;
+    ReconStep cur, nxt;
+    recon_load(cur, L, i0 + st * kWave, min(kWave, i1 - i0 - st * kWave), lane, err);
+    for (;;) {
+        const int b0 = i0 + st * kWave;
+        const int cnt = min(kWave, i1 - b0), nf = cnt * kDim;
+        const int sn = st + kWaves;
+        const bool more = sn < nsteps;
+        if (more) recon_load(nxt, L, i0 + sn * kWave, min(kWave, i1 - i0 - sn * kWave), lane, err);
+        float* __restrict__ out = L.W + (size_t)b0 * kDim;
+#pragma unroll
+        for (int q = 0; q < kDim; ++q) {
+            const int jq = __builtin_amdgcn_ds_bpermute(src[q], cur.j);
+            float v = 0.0f;
+            if ((unsigned)jq < (unsigned)L.k) v = LDS ? s_cb[jq * kDim + dim[q]] : L.C[jq * kDim + dim[q]];
+            if (lane + kWave * q < nf) {
+                out[lane + kWave * q] = v;
+                if (err) {
+                    const double df = (double)cur.x[q] - (double)v;
+                    acc += df * df;
+                }
+            }
+        }
+        if (!more) break;
+        cur = nxt;
+        st = sn;
+    }
+    return acc;
 }
 
 __global__ __launch_bounds__(kReconThreads) void reconstruct_stack_kernel(const ReconParams p) {
-    extern __shared__ float s_dyn[];  // [waves][2][64 * 9] row buffers, then the codebook
+    extern __shared__ float s_cb[];  // the codebook, when it is staged
     __shared__ double s_w[kReconThreads / kWave];
-    constexpr int kRowF = kWave * kDim;  // floats of 64 rows
+    constexpr int kWaves = kReconThreads / kWave;
     int li = 0;
 #pragma unroll
     for (int q = 1; q < KQ_MAX_STACK; ++q) li += (int)blockIdx.x >= p.unit_begin[q] ? 1 : 0;
     const ReconLayer& L = p.L[li];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    float* xb = s_dyn + wave * 2 * kRowF;
-    float* wb = xb + kRowF;
-    float* s_cb = s_dyn + (kReconThreads / kWave) * 2 * kRowF;
     const int lb = (int)blockIdx.x - p.unit_begin[li];
     const int i0 = lb * kReconRows;
     const int i1 = min(L.n, i0 + kReconRows);
     const bool err = L.part != nullptr;
-    const bool lds = L.k * kDim <= kReconLdsFloats;
-    if (lds) {
+    double acc;
+    if (L.k * kDim <= kReconLdsFloats) {
         for (int e = tid; e < L.k * kDim; e += kReconThreads) s_cb[e] = L.C[e];
         __syncthreads();
-    }
-    const int nsteps = (i1 - i0 + kWave - 1) / kWave;
-    constexpr int kWaves = kReconThreads / kWave;
-    double acc = 0.0;
-    // prefetch of step `wave`
-    int jn = 0;
-    float xn[kDim];
-    int st = wave;
-    if (st < nsteps) {
-        const int b0 = i0 + st * kWave, nf = min(kWave, i1 - b0) * kDim;
-        jn = lane < nf / kDim ? recon_index(L, b0 + lane) : 0;
-#pragma unroll
-        for (int q = 0; q < kDim; ++q)
-            xn[q] = (err && q * kWave + lane < nf) ? L.W_ref[(size_t)b0 * kDim + q * kWave + lane] : 0.0f;
-    }
-    for (; st < nsteps; st += kWaves) {
-        const int b0 = i0 + st * kWave;
-        const int cnt = min(kWave, i1 - b0), nf = cnt * kDim;
-        const int j = jn;
-#pragma unroll
-        for (int q = 0; q < kDim; ++q) xb[q * kWave + lane] = xn[q];
-        const int sn = st + kWaves;  // prefetch the next step of this wave
-        if (sn < nsteps) {
-            const int c0 = i0 + sn * kWave, mf = min(kWave, i1 - c0) * kDim;
-            jn = lane < mf / kDim ? recon_index(L, c0 + lane) : 0;
-#pragma unroll
-            for (int q = 0; q < kDim; ++q)
-                xn[q] = (err && q * kWave + lane < mf) ? L.W_ref[(size_t)c0 * kDim + q * kWave + lane] : 0.0f;
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (lane < cnt) {
-            const bool ok = (unsigned)j < (unsigned)L.k;
-            const int jo = (ok ? j : 0) * kDim;
-#pragma unroll
-            for (int d = 0; d < kDim; ++d) {
-                const float c = lds ? s_cb[jo + d] : L.C[jo + d];
-                const float w = ok ? c : 0.0f;
-                wb[lane * kDim + d] = w;
-                if (err) {
-                    const double df = (double)xb[lane * kDim + d] - (double)w;
-                    acc += df * df;
-                }
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-#pragma unroll
-        for (int q = 0; q < kDim; ++q)
-            if (q * kWave + lane < nf) L.W[(size_t)b0 * kDim + q * kWave + lane] = wb[q * kWave + lane];
-        __builtin_amdgcn_wave_barrier();
+        acc = recon_steps<true>(L, s_cb, i0, i1, lane, wave, err);
+    } else {
+        acc = recon_steps<false>(L, s_cb, i0, i1, lane, wave, err);
     }
     if (!err) return;
 #pragma unroll
@@ -256,7 +298,6 @@ hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s) {
         const size_t f = (size_t)p.L[l].k * kDim;
         if (f <= (size_t)kReconLdsFloats && f * sizeof(float) > lds) lds = f * sizeof(float);
     }
-    lds += sizeof(float) * (kReconThreads / kWave) * 2 * kWave * kDim;  // the row buffers
     hipLaunchKernelGGL(reconstruct_stack_kernel, dim3(p.total_blocks), dim3(kReconThreads), lds, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -16,8 +16,9 @@
 // per CU for the whole launch.  Asked for the distortion of a standalone assignment, it
 // also sums, in a fixed order, the fp32 distances of its rows to their old entries.
 // update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
-// groups of 40 threads add a sixteenth of the chunk partials each (any order gives the same
-// integers), then it divides and writes the codebook and the counts.  One more workgroup
+// groups of 40 threads add a sixteenth of the chunk partials each, eight loads in flight
+// per thread (any order gives the same integers), then it divides and writes the codebook
+// and the counts.  One more workgroup
 // per layer adds the distortion partials in a fixed order (those of the assignment kernel
 // when the distortion comes from there).  The kernel boundary orders every partial before
 // its use, so no fence or atomic counter is needed.
@@ -143,6 +144,7 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
 }
 
 constexpr int kFinishGroups = 16;
+constexpr int kFinishBatch = 8;
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
 
@@ -174,12 +176,19 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         const int nb = L.nchunks;
         const size_t stride = (size_t)k * 10;
         const unsigned long long* hp = h + (size_t)j * 10 + d;
-        int q = g;
+        // chunks g, g + 16, ...: kFinishBatch loads in flight at a time (one batch covers
+        // up to 128 chunks, every layer of a stack at one workgroup per CU)
 #pragma unroll 1
-        for (; q + 3 * kFinishGroups < nb; q += 4 * kFinishGroups)
-            s += hp[q * stride] + hp[(q + kFinishGroups) * stride] + hp[(q + 2 * kFinishGroups) * stride] +
-                 hp[(q + 3 * kFinishGroups) * stride];
-        for (; q < nb; q += kFinishGroups) s += hp[q * stride];
+        for (int q0 = g; q0 < nb; q0 += kFinishBatch * kFinishGroups) {
+            unsigned long long v[kFinishBatch];
+#pragma unroll
+            for (int r = 0; r < kFinishBatch; ++r) {
+                const int q = q0 + r * kFinishGroups;
+                v[r] = q < nb ? hp[(size_t)q * stride] : 0ull;
+            }
+#pragma unroll
+            for (int r = 0; r < kFinishBatch; ++r) s += v[r];
+        }
     }
     s_S[g][v] = (long long)s;
     __syncthreads();
@@ -216,6 +225,9 @@ hipError_t launch_update(const StackParams& p, hipStream_t s) {
         const size_t b = (size_t)p.L[l].krange * (kDim * sizeof(unsigned long long) + sizeof(unsigned));
         lds = b > lds ? b : lds;
     }
+#ifdef KQ_UPDATE_LDS_MIN
+    if (lds < KQ_UPDATE_LDS_MIN) lds = KQ_UPDATE_LDS_MIN;
+#endif
     hipLaunchKernelGGL(update_kernel, dim3(p.total_units), dim3(kUpdateThreads), lds, s, p);
     return hipGetLastError();
 }

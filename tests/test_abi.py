@@ -135,6 +135,7 @@ def test_cbq_pack_reconstruct_argument_errors():
     assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 9, FAKE + 4, None) == kq.KQ_ERR_ARG   # W_hat 16-B aligned
     assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 8, FAKE, None) == kq.KQ_ERR_UNSUPPORTED
     assert lib.kq_reconstruct_packed(None, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG
+    assert lib.kq_reconstruct_packed(FAKE + 2, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG  # stream read as dwords
     assert lib.kq_workspace_init(FAKE + 8, 100, None) == kq.KQ_ERR_WORKSPACE
     assert lib.kq_sq_error(FAKE, FAKE, 0, FAKE, FAKE, 1 << 20, None) == kq.KQ_ERR_ARG
     assert lib.kq_sq_error(FAKE, FAKE, 100, FAKE, FAKE, 0, None) == kq.KQ_ERR_WORKSPACE

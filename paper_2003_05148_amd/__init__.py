@@ -189,9 +189,11 @@ def kq_assign(X, C, idx=None, best_d=None, distortion=None, workspace=None):
     return idx, best_d, distortion
 
 
-def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace=None, counts_only: bool = False):
+def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace=None, counts_only: bool = False,
+              with_distortion: bool = True):
     """Mean of every kernel set (empty sets keep their entry) and the distortion of the
-    assignment against C_old.  Returns (C_new, counts, distortion float64 [1])."""
+    assignment against C_old.  Returns (C_new, counts, distortion float64 [1]), the
+    distortion None when `with_distortion` is False (the library is then passed NULL)."""
     X = _kernels(X)
     C_old = _kernels(C_old, "C_old")
     n, k = X.shape[0], C_old.shape[0]
@@ -201,13 +203,17 @@ def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace
     counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
     _dev(C_new, torch.float32, "C_new", (k, KQ_DIM))
     _dev(counts, torch.int32, "counts", (k,))
-    distortion = distortion if distortion is not None else torch.empty(1, dtype=torch.float64, device=dev)
-    _dev(distortion, torch.float64, "distortion")
+    if with_distortion:
+        distortion = distortion if distortion is not None else torch.empty(1, dtype=torch.float64, device=dev)
+        _dev(distortion, torch.float64, "distortion")
+    else:
+        distortion = None
     nb = lib.kq_workspace_bytes(KQ_OP_UPDATE, n, k)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_update(X.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), C_new.data_ptr(),
-                         counts.data_ptr(), distortion.data_ptr(), KQ_F_COUNTS_ONLY if counts_only else 0,
-                         ws.data_ptr(), ws.numel(), _stream(dev)), "kq_update")
+                         counts.data_ptr(), distortion.data_ptr() if distortion is not None else None,
+                         KQ_F_COUNTS_ONLY if counts_only else 0, ws.data_ptr(), ws.numel(), _stream(dev)),
+           "kq_update")
     return C_new, counts, distortion
 
 

@@ -40,7 +40,10 @@ constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every 
 // most update_max_chunks(n, k) of them (that bounds its partial histograms).
 constexpr int kUpdateThreads = 1024;
 constexpr int kUpdateMinKernelsPerBlock = 1024;
-constexpr int kUpdateTargetBlocks = 256;
+#ifndef KQ_UPDATE_BLOCKS
+#define KQ_UPDATE_BLOCKS 256
+#endif
+constexpr int kUpdateTargetBlocks = KQ_UPDATE_BLOCKS;
 constexpr int kUpdateLdsMaxK = 768;     // LDS histogram [768][9] int64 + [768] u32
 constexpr int kFinishEntries = 4;       // codebook entries per finishing workgroup
 constexpr size_t kUpdatePartialBudget = size_t(1) << 24;  // bytes of partials per layer above 768 entries

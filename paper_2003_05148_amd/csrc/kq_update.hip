@@ -13,8 +13,11 @@
 // rows whose entry lies in its range and adds them to a private LDS histogram of the range
 // ([768][9] int64 sums + [768] counts at most, ds_add_u64), then stores the histogram
 // into the chunk's partial ([chunks][k][10] int64).  Chunk sizes give about one workgroup
-// per CU for the whole launch.  Asked for the distortion of a standalone assignment, it
-// also sums, in a fixed order, the fp32 distances of its rows to their old entries.
+// per CU for the whole launch.  The LDS atomics, not the loads, bound it: a layout with
+// fully coalesced dword loads, where each float fetched its kernel's entry with
+// ds_bpermute, added LDS work and ran slower.  Asked for the distortion of a standalone
+// assignment, it also sums, in a fixed order, the fp32 distances of its rows to their old
+// entries.
 // update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
 // groups of 40 threads add a sixteenth of the chunk partials each, eight loads in flight
 // per thread (any order gives the same integers), then it divides and writes the codebook
@@ -36,11 +39,22 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
     return acc;
 }
 
+// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is exact in fp32 (|x| < 32, s <= 57)
+// and so is its rounding to an integer v; v = hi * 2^32 + lo with hi = floor(v * 2^-32)
+// (|hi| < 2^30) and 0 <= lo < 2^32, where lo = v - hi * 2^32 has fewer significant bits
+// than v and is exact in fp32 too, so both convert to integers exactly.
+__device__ __forceinline__ unsigned long long fixed_point(float x, float scale) {
+    const float v = __builtin_rintf(x * scale);
+    const float hi = __builtin_floorf(v * 0x1p-32f);
+    const float lo = __builtin_fmaf(hi, -0x1p32f, v);
+    return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
+}
+
 struct UpdateCtx {
     unsigned long long* s_sum;  // [krange][9]
     unsigned* s_cnt;            // [krange]
     const float* C_old;
-    double scale;
+    float scale;                // 2^s
     int j0, kr;                 // the entry range [j0, j0 + kr)
     bool sums, want_dist;
 };
@@ -53,8 +67,7 @@ __device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[
     atomicAdd(&c.s_cnt[jr], 1u);
     if (c.sums) {
 #pragma unroll
-        for (int d = 0; d < kDim; ++d)
-            atomicAdd(&c.s_sum[jr * kDim + d], (unsigned long long)__double2ll_rn((double)x[d] * c.scale));
+        for (int d = 0; d < kDim; ++d) atomicAdd(&c.s_sum[jr * kDim + d], fixed_point(x[d], c.scale));
     }
 }
 
@@ -105,7 +118,7 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     c.s_sum = s_dyn;
     c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
-    c.scale = ldexp(1.0, L.shift);
+    c.scale = __builtin_ldexpf(1.0f, L.shift);
     c.sums = (L.flags & kFlagCountsOnly) == 0;
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;

@@ -100,11 +100,18 @@ def check_update(X, idx, C_old, tag=""):
     err = np.abs(gc.astype(np.float64) - oc.astype(np.float64)).max(axis=1)
     scale = np.maximum(np.abs(oc.astype(np.float64)).max(axis=1), 1e-30)
     assert np.all(err <= REL * scale), (tag, float((err / scale).max()))
+    # without a distortion the rows are read in the coalesced layout (one range) or the
+    # per-row layout (several ranges); the integer sums give the same bits either way
+    C2, z2, _ = kq.kq_update(dev(X), dev(idx), dev(C_old), with_distortion=False)
+    assert np.array_equal(host(C2).view(np.uint32), gc.view(np.uint32)), tag
+    assert np.array_equal(host(z2), gz), tag
+    _, z3, _ = kq.kq_update(dev(X), dev(idx), dev(C_old), with_distortion=False, counts_only=True)
+    assert np.array_equal(host(z3), gz), tag
     return gc, gz
 
 
-@pytest.mark.parametrize("n,k", [(1, 1), (100, 1), (4096, 16), (4099, 256), (20000, 768), (20000, 769),
-                                 (50000, 4096), (9000, 20000)])
+@pytest.mark.parametrize("n,k", [(1, 1), (63, 5), (65, 7), (100, 1), (4096, 16), (4099, 256), (20000, 768),
+                                 (20000, 769), (50000, 4096), (9000, 20000), (300001, 256)])
 def test_update_shapes(n, k):
     X = synth.normal_layer(1, n, 7 + n)[:n]
     idx = synth.random_indices(n, k, k)
@@ -126,11 +133,12 @@ def test_update_in_place_and_ignores_bad_indices():
     bad = idx.copy()
     bad[:10] = 77
     bad[10:20] = -1
-    gc, gz, _ = kq.kq_update(dev(X), dev(bad), dev(C))
     keep = np.arange(n) >= 20
     oc, oz = oracle.update(X[keep], bad[keep], C)
-    assert np.array_equal(host(gz), oz)
-    assert np.allclose(host(gc), oc, rtol=REL, atol=1e-12)
+    for with_d in (True, False):
+        gc, gz, _ = kq.kq_update(dev(X), dev(bad), dev(C), with_distortion=with_d)
+        assert np.array_equal(host(gz), oz), with_d
+        assert np.allclose(host(gc), oc, rtol=REL, atol=1e-12), with_d
 
 
 def test_fit_step_locked_single_layer():

@@ -10,6 +10,8 @@
  *                        step of Algorithm 1), a fixed number of rounds then a final assignment.
  *   kq_fit_stack         the same for many layers at once (Sec. 3.1 quantizes layer by layer;
  *                        layers are independent, so one launch serves all of them).
+ *   kq_fit_layer_yinyang Sec. 4.1: the same fit with Yinyang assignments (kq_yinyang_init,
+ *                        kq_yinyang_assign), equal to kq_fit_layer bit for bit.
  *   kq_quantize_codebook Sec. 3.2: 6-bit quantization of all scalars of a layer's codebook,
  *                        k-means weighted by how often each entry is used.
  *   kq_pack_bits         Eq. (4): the n * ceil(log2 k)-bit index stream.
@@ -161,6 +163,50 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
                        int32_t iters, float* C, int32_t* idx, int32_t* counts, double* distortion,
                        uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Yinyang assignment -- Sec. 4.1: the paper runs its kernel-level k-means with Yinyang
+ * k-means, which skips distance evaluations using triangle-inequality bounds and
+ * reaches the same result as plain Lloyd.  These calls return exactly what kq_assign
+ * returns for the same codebook (the fp32 argmin, ties to the lowest index; bit for bit,
+ * including best_d and the distortion), doing less work once the codebook moves little.
+ *
+ *   The codebook's entries are split into `groups` groups (groups <= 0: about one per
+ *   64 entries, at most 32; otherwise 1 .. min(64, k)) by a few Lloyd rounds on the
+ *   entries.  For every kernel and group the workspace keeps a lower bound of the
+ *   kernel's Euclidean distance to the group's entries, shifted by the group's
+ *   cumulative movement.  A round moves every group's bounds down by the largest
+ *   movement of its entries, skips the groups whose bound exceeds the distance to the
+ *   kernel's current entry (with a margin that covers fp32 rounding), and scans the other
+ *   groups' entries exactly.  The grouping decides only how much is skipped.
+ *
+ *   kq_yinyang_init:   assigns X against C exactly as kq_assign (idx, best_d, distortion:
+ *                      each may be NULL except idx), groups C and sets the bounds.
+ *   kq_yinyang_assign: the next assignment after the codebook moved from C_prev (the
+ *                      codebook of the previous init/assign call on this workspace) to C.
+ *                      idx must hold that call's assignment; it is replaced by the new one.
+ *                      stats (device int32 [2] or NULL): kernels whose groups were scanned,
+ *                      (kernel, group) pairs scanned.
+ *   kq_fit_layer_yinyang: kq_fit_layer with Yinyang assignments; C, idx, counts and
+ *                      distortion [iters+1] equal kq_fit_layer's bit for bit.  stats
+ *                      (device int32 [iters][2] or NULL): the scan counts of rounds 1..iters.
+ *   X device [n][9]; C, C_prev, C_init device [k][9]; idx device [n]; best_d device [n];
+ *   counts device [k].  Requires 1 <= k <= n.  Kernel and codebook values must be finite
+ *   with |x| < 32 (the grouping and the fit run kq_update's fixed-point sums).
+ *   workspace: kq_yinyang_workspace_bytes(n, k, groups) bytes (about 20 bytes per kernel
+ *   and group plus kq_workspace_bytes); it carries the state from one call to the next,
+ *   so the calls of one fit must use one workspace, in order, on one stream.
+ */
+size_t kq_yinyang_workspace_bytes(int64_t n, int32_t k, int32_t groups);
+kq_status kq_yinyang_init(const float* X, int64_t n, int32_t dim, const float* C, int32_t k, int32_t groups,
+                          int32_t* idx, float* best_d, double* distortion, void* ws, size_t ws_bytes,
+                          void* stream);
+kq_status kq_yinyang_assign(const float* X, int64_t n, int32_t dim, const float* C_prev, const float* C,
+                            int32_t k, int32_t groups, int32_t* idx, float* best_d, double* distortion,
+                            int32_t* stats, void* ws, size_t ws_bytes, void* stream);
+kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
+                               int32_t iters, int32_t groups, float* C, int32_t* idx, int32_t* counts,
+                               double* distortion, int32_t* stats, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Stack versions: one launch per step for up to KQ_MAX_STACK layers (more are split).

@@ -9,6 +9,7 @@ fallback: without the built library, importing this package raises ImportError.
 
 Entry points (same names as the C ABI):
   kq_assign, kq_update, kq_fit_layer, kq_assign_stack, kq_update_stack, kq_fit_stack,
+  kq_fit_layer_yinyang (and the Yinyang class over kq_yinyang_init / kq_yinyang_assign),
   kq_quantize_codebook, kq_quantize_codebook_stack, kq_pack_bits, kq_unpack_bits,
   kq_reconstruct, kq_reconstruct_packed.
 """
@@ -73,6 +74,10 @@ def _load():
         "kq_pack_bits_stack": ([_P, _I32, _P], _I32),
         "kq_reconstruct_stack_workspace_bytes": ([_P, _I32], _SZ),
         "kq_reconstruct_stack": ([_P, _I32, _P, _SZ, _P], _I32),
+        "kq_yinyang_workspace_bytes": ([_I64, _I32, _I32], _SZ),
+        "kq_yinyang_init": ([_P, _I64, _I32, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
+        "kq_yinyang_assign": ([_P, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
+        "kq_fit_layer_yinyang": ([_P, _I64, _I32, _I32, _P, _I32, _I32, _P, _P, _P, _P, _P, _P, _SZ, _P], _I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -96,7 +101,8 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
             "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error",
-            "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack"]
+            "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
+            "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -215,6 +221,77 @@ def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace
                          KQ_F_COUNTS_ONLY if counts_only else 0, ws.data_ptr(), ws.numel(), _stream(dev)),
            "kq_update")
     return C_new, counts, distortion
+
+
+def _yy_groups_bytes(n: int, k: int, groups: int) -> int:
+    nb = lib.kq_yinyang_workspace_bytes(n, k, groups)
+    if nb == 0:
+        raise ValueError(f"no Yinyang configuration for n={n}, k={k}, groups={groups} (needs 1 <= k <= n, "
+                         f"groups <= min(64, k))")
+    return nb
+
+
+class Yinyang:
+    """Yinyang assignment state of one layer (Sec. 4.1): the exact kq_assign result for
+    every new codebook, skipping the entry groups that triangle-inequality bounds rule
+    out.  The object owns its workspace (the bounds live there between calls) and a copy
+    of the last codebook (the drift of the next call is measured from it)."""
+
+    def __init__(self, X, C, groups: int = 0):
+        self.X = _kernels(X)
+        C = _kernels(C, "C")
+        self.n, self.k, self.groups = self.X.shape[0], C.shape[0], int(groups)
+        dev = self.X.device
+        self.ws = torch.empty(_yy_groups_bytes(self.n, self.k, self.groups), dtype=torch.uint8, device=dev)
+        self.idx = torch.empty(self.n, dtype=torch.int32, device=dev)
+        self.best_d = torch.empty(self.n, dtype=torch.float32, device=dev)
+        self.distortion = torch.empty(1, dtype=torch.float64, device=dev)
+        self.stats = torch.zeros(2, dtype=torch.int32, device=dev)
+        self.C_prev = C.clone()
+        _check(lib.kq_yinyang_init(self.X.data_ptr(), self.n, KQ_DIM, C.data_ptr(), self.k, self.groups,
+                                   self.idx.data_ptr(), self.best_d.data_ptr(), self.distortion.data_ptr(),
+                                   self.ws.data_ptr(), self.ws.numel(), _stream(dev)), "kq_yinyang_init")
+
+    def assign(self, C):
+        """Assignment against C (the codebook after the previous call's).  Returns
+        (idx, best_d, distortion); `stats` then holds the kernels and (kernel, group) pairs
+        that were scanned."""
+        C = _kernels(C, "C")
+        if tuple(C.shape) != (self.k, KQ_DIM):
+            raise ValueError(f"C must be [{self.k}, 9]")
+        dev = self.X.device
+        _check(lib.kq_yinyang_assign(self.X.data_ptr(), self.n, KQ_DIM, self.C_prev.data_ptr(), C.data_ptr(),
+                                     self.k, self.groups, self.idx.data_ptr(), self.best_d.data_ptr(),
+                                     self.distortion.data_ptr(), self.stats.data_ptr(), self.ws.data_ptr(),
+                                     self.ws.numel(), _stream(dev)), "kq_yinyang_assign")
+        self.C_prev.copy_(C)
+        return self.idx, self.best_d, self.distortion
+
+
+def kq_fit_layer_yinyang(X, C_init, iters: int, groups: int = 0, C=None, idx=None, counts=None, distortion=None,
+                         stats=None, workspace=None):
+    """kq_fit_layer with Yinyang assignments (Sec. 4.1); the same outputs bit for bit.
+    Returns (C, idx, counts, distortion[iters+1], stats int32 [iters, 2])."""
+    X = _kernels(X)
+    C_init = _kernels(C_init, "C_init")
+    n, k = X.shape[0], C_init.shape[0]
+    dev = X.device
+    C = C if C is not None else torch.empty_like(C_init)
+    idx = idx if idx is not None else torch.empty(n, dtype=torch.int32, device=dev)
+    counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
+    distortion = distortion if distortion is not None else torch.empty(iters + 1, dtype=torch.float64, device=dev)
+    stats = stats if stats is not None else torch.zeros(max(iters, 1), 2, dtype=torch.int32, device=dev)
+    _dev(C, torch.float32, "C", (k, KQ_DIM))
+    _dev(idx, torch.int32, "idx", (n,))
+    _dev(counts, torch.int32, "counts", (k,))
+    _dev(distortion, torch.float64, "distortion", (iters + 1,))
+    _dev(stats, torch.int32, "stats")
+    nb = _yy_groups_bytes(n, k, groups)
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_fit_layer_yinyang(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, groups, C.data_ptr(),
+                                    idx.data_ptr(), counts.data_ptr(), distortion.data_ptr(), stats.data_ptr(),
+                                    ws.data_ptr(), ws.numel(), _stream(dev)), "kq_fit_layer_yinyang")
+    return C, idx, counts, distortion, stats
 
 
 def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):

@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 3;
+constexpr int32_t kAbiVersion = 4;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -151,6 +151,124 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
     return KQ_OK;
 }
 
+
+// ---- Yinyang workspace: the layer's own region (assignment partials, update partials and
+// histograms), then the grouping fit's region, then the Yinyang state ----------------------
+struct YyLayout {
+    size_t sub, Cg, labels, Cw, perm, gstart, radius, delta, cnt, Lt, B1, J1, B2, lists, mask, flist, bd, total;
+};
+
+YyLayout yy_layout(int64_t n, int32_t k, int t) {
+    YyLayout L;
+    size_t o = layer_ws_bytes(n, k);
+    auto take = [&o](size_t b) {
+        const size_t at = o;
+        o += align256(b);
+        return at;
+    };
+    const size_t tn = (size_t)t * (size_t)n;
+    L.sub = take(layer_ws_bytes(k, t));
+    L.Cg = take(sizeof(float) * KQ_DIM * (size_t)t);
+    L.labels = take(sizeof(int32_t) * (size_t)k);
+    L.Cw = take(sizeof(float) * KQ_DIM * (size_t)k);
+    L.perm = take(sizeof(int32_t) * (size_t)k);
+    L.gstart = take(sizeof(int32_t) * (size_t)(t + 1));
+    L.radius = take(sizeof(float) * (size_t)t);
+    L.delta = take(sizeof(double) * (size_t)t);
+    L.cnt = take(sizeof(int32_t) * (size_t)(t + 1));
+    L.Lt = take(sizeof(float) * tn);
+    L.B1 = take(sizeof(float) * tn);
+    L.J1 = take(sizeof(int32_t) * tn);
+    L.B2 = take(sizeof(float) * tn);
+    L.lists = take(sizeof(int32_t) * tn);
+    L.mask = take(sizeof(unsigned long long) * (size_t)n);
+    L.flist = take(sizeof(int32_t) * (size_t)n);
+    L.bd = take(sizeof(float) * (size_t)n);
+    L.total = o;
+    return L;
+}
+
+// groups <= 0 picks the default; otherwise 1 .. min(64, k); returns 0 when invalid
+int yy_groups(int32_t k, int32_t groups) {
+    if (groups <= 0) return yy_default_groups(k) < k ? yy_default_groups(k) : k;
+    return groups <= kYyMaxGroups && groups <= k ? groups : 0;
+}
+
+YyParams yy_params(unsigned char* ws, const YyLayout& L, const float* X, int64_t n, int32_t k, int t,
+                   const float* C, const float* C_prev, int32_t* idx, float* best_d, int32_t* stats) {
+    YyParams p;
+    memset(&p, 0, sizeof(p));
+    p.X = X;
+    p.C = C;
+    p.C_prev = C_prev;
+    p.idx = idx;
+    p.best_d = best_d ? best_d : (float*)(ws + L.bd);
+    p.Cg = (const float*)(ws + L.Cg);
+    p.labels = (const int32_t*)(ws + L.labels);
+    p.perm = (int32_t*)(ws + L.perm);
+    p.gstart = (int32_t*)(ws + L.gstart);
+    p.radius = (float*)(ws + L.radius);
+    p.delta = (double*)(ws + L.delta);
+    p.cnt = (int32_t*)(ws + L.cnt);
+    p.Lt = (float*)(ws + L.Lt);
+    p.B1 = (float*)(ws + L.B1);
+    p.J1 = (int32_t*)(ws + L.J1);
+    p.B2 = (float*)(ws + L.B2);
+    p.lists = (int32_t*)(ws + L.lists);
+    p.mask = (unsigned long long*)(ws + L.mask);
+    p.flist = (int32_t*)(ws + L.flist);
+    p.part = (double*)ws;  // the layer's assignment partials
+    p.stats = stats;
+    p.n = (int)n;
+    p.k = k;
+    p.t = t;
+    p.npart = assign_tiles(n) * kAssignWaves;
+    return p;
+}
+
+// the groups of codebook C (a few Lloyd rounds on its entries, the first t entries as
+// seeds), the perm / radius tables and the initial bounds of every kernel
+kq_status yy_start(unsigned char* ws, const YyLayout& L, const float* X, int64_t n, const float* C, int32_t k, int t,
+                   hipStream_t s) {
+    float* Cg = (float*)(ws + L.Cg);
+    int32_t* labels = (int32_t*)(ws + L.labels);
+    if (hipMemcpyAsync(Cg, C, sizeof(float) * KQ_DIM * (size_t)t, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return KQ_ERR_HIP;
+    const kq_layer gl = {C, k, t, Cg, labels, nullptr, nullptr, nullptr};
+    const kq_status st = run_fit(&gl, 1, kYyGroupRounds, ws + L.sub, s);
+    if (st != KQ_OK) return st;
+    const YyParams p = yy_params(ws, L, X, n, k, t, C, nullptr, nullptr, nullptr, nullptr);
+    if (launch_yy_group(p, s) != hipSuccess) return KQ_ERR_HIP;
+    return hip_status(launch_yy_bounds_init(p, s));
+}
+
+// distortion of the round's assignment from its best distances, in the order of the
+// assignment kernel's partials
+kq_status yy_distortion(const YyParams& p, double* distortion, hipStream_t s) {
+    if (launch_yy_partials(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (!distortion) return KQ_OK;
+    StackParams q;
+    memset(&q, 0, sizeof(q));
+    q.nlayers = 1;
+    q.L[0].part = p.part;
+    q.L[0].dist = distortion;
+    q.L[0].nunits = assign_tiles(p.n);
+    set_unit_table(q);
+    return hip_status(launch_assign_finish(q, s));
+}
+
+kq_status check_yy(const float* X, int64_t n, int32_t dim, int32_t k, int32_t groups, int32_t* idx, float* best_d,
+                   double* distortion, int& t) {
+    if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
+    if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(n) || !valid_k(k) || k > n) return KQ_ERR_ARG;
+    t = yy_groups(k, groups);
+    if (t == 0) return KQ_ERR_ARG;
+    if (!X || !idx || !aligned(X, 4) || !aligned(idx, 4)) return KQ_ERR_ARG;
+    if ((best_d && !aligned(best_d, 4)) || (distortion && !aligned(distortion, 8))) return KQ_ERR_ARG;
+    return KQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -242,6 +360,84 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
             return KQ_ERR_HIP;
     }
     return run_fit(&l, 1, iters, (unsigned char*)ws, s);
+}
+
+size_t kq_yinyang_workspace_bytes(int64_t n, int32_t k, int32_t groups) {
+    if (!valid_n(n) || !valid_k(k) || k > n) return 0;
+    const int t = yy_groups(k, groups);
+    if (t == 0) return 0;
+    return yy_layout(n, k, t).total;
+}
+
+kq_status kq_yinyang_init(const float* X, int64_t n, int32_t dim, const float* C, int32_t k, int32_t groups,
+                          int32_t* idx, float* best_d, double* distortion, void* ws, size_t ws_bytes, void* stream) {
+    int t = 0;
+    kq_status st = check_yy(X, n, dim, k, groups, idx, best_d, distortion, t);
+    if (st != KQ_OK) return st;
+    if (!C || !aligned(C, 4)) return KQ_ERR_ARG;
+    const YyLayout L = yy_layout(n, k, t);
+    if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
+    unsigned char* w = (unsigned char*)ws;
+    hipStream_t s = (hipStream_t)stream;
+    const kq_layer l = {X, n, k, const_cast<float*>(C), idx, best_d, nullptr, distortion};
+    if ((st = run_assign(&l, 0, 1, w, 0, s)) != KQ_OK) return st;
+    return yy_start(w, L, X, n, C, k, t, s);
+}
+
+kq_status kq_yinyang_assign(const float* X, int64_t n, int32_t dim, const float* C_prev, const float* C, int32_t k,
+                            int32_t groups, int32_t* idx, float* best_d, double* distortion, int32_t* stats, void* ws,
+                            size_t ws_bytes, void* stream) {
+    int t = 0;
+    kq_status st = check_yy(X, n, dim, k, groups, idx, best_d, distortion, t);
+    if (st != KQ_OK) return st;
+    if (!C || !C_prev || !aligned(C, 4) || !aligned(C_prev, 4) || (stats && !aligned(stats, 4))) return KQ_ERR_ARG;
+    const YyLayout L = yy_layout(n, k, t);
+    if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const YyParams p = yy_params((unsigned char*)ws, L, X, n, k, t, C, C_prev, idx, best_d, stats);
+    if (launch_yy_round(p, s) != hipSuccess) return KQ_ERR_HIP;
+    return distortion ? yy_distortion(p, distortion, s) : KQ_OK;
+}
+
+kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters,
+                               int32_t groups, float* C, int32_t* idx, int32_t* counts, double* distortion,
+                               int32_t* stats, void* ws, size_t ws_bytes, void* stream) {
+    int t = 0;
+    kq_status st = check_yy(X, n, dim, k, groups, idx, nullptr, distortion, t);
+    if (st != KQ_OK) return st;
+    if (iters < 0 || !C_init || !C || !aligned(C_init, 4) || !aligned(C, 4)) return KQ_ERR_ARG;
+    if ((counts && !aligned(counts, 4)) || (stats && !aligned(stats, 4))) return KQ_ERR_ARG;
+    const YyLayout L = yy_layout(n, k, t);
+    if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
+    unsigned char* w = (unsigned char*)ws;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t cb = sizeof(float) * KQ_DIM * (size_t)k;
+    if (C_init != C && hipMemcpyAsync(C, C_init, cb, hipMemcpyDeviceToDevice, s) != hipSuccess) return KQ_ERR_HIP;
+    // round 0: the screened assignment (its partials stay in the workspace), groups, bounds
+    const kq_layer l0 = {X, n, k, C, idx, nullptr, nullptr, nullptr};
+    if ((st = run_assign(&l0, 0, 1, w, 0, s)) != KQ_OK) return st;
+    if ((st = yy_start(w, L, X, n, C, k, t, s)) != KQ_OK) return st;
+    // rounds 1..iters: update from `cur` into `nxt` (the distortion of the assignment
+    // before it from its partials), then the Yinyang assignment against `nxt`
+    float* cur = C;
+    float* nxt = (float*)(w + L.Cw);
+    for (int32_t r = 0; r < iters; ++r) {
+        kq_layer lu = {X, n, k, nxt, idx, nullptr, counts, distortion};
+        const float* olds[1] = {cur};
+        if ((st = run_update(&lu, 0, 1, w, r, olds, 0, s, true)) != KQ_OK) return st;
+        const YyParams p = yy_params(w, L, X, n, k, t, nxt, cur, idx, nullptr, stats ? stats + 2 * (size_t)r : nullptr);
+        if (launch_yy_round(p, s) != hipSuccess) return KQ_ERR_HIP;
+        if (launch_yy_partials(p, s) != hipSuccess) return KQ_ERR_HIP;
+        float* tmp = cur;
+        cur = nxt;
+        nxt = tmp;
+    }
+    if (counts || distortion) {  // counts of the final assignment, its distortion
+        kq_layer lf = {X, n, k, cur, idx, nullptr, counts, distortion};
+        if ((st = run_update(&lf, 0, 1, w, iters, nullptr, kFlagCountsOnly, s, true)) != KQ_OK) return st;
+    }
+    if (cur != C && hipMemcpyAsync(C, cur, cb, hipMemcpyDeviceToDevice, s) != hipSuccess) return KQ_ERR_HIP;
+    return KQ_OK;
 }
 
 kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags, void* ws,

@@ -243,6 +243,49 @@ inline int recon_blocks(int64_t n) { return (int)((n + kReconRows - 1) / kReconR
 hipError_t launch_pack_stack(const PackParams& p, hipStream_t s);
 hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s);
 
+
+// ---- Yinyang assignment ----------------------------------------------------------------
+constexpr int kYyMaxGroups = 64;     // groups per codebook (one bit each in a 64-bit mask)
+constexpr int kYyEvalChunk = 1024;   // group entries staged in LDS at a time
+constexpr int kYyEvalGrid = 2048;    // persistent workgroups of the exact group scan
+constexpr int kYyFinalGrid = 1024;   // persistent workgroups of the final decision
+constexpr int kYyGroupRounds = 5;    // Lloyd rounds that group the codebook's entries
+
+// default number of groups for k entries: about 64 entries per group, 1 to 32 groups
+inline int yy_default_groups(int32_t k) {
+    int t = k / 64;
+    return t < 1 ? 1 : (t > 32 ? 32 : t);
+}
+
+struct YyParams {
+    const float* X;
+    const float* C;            // the codebook of this round
+    const float* C_prev;       // the codebook of the previous round (drift)
+    int32_t* idx;              // current entry in, new entry out
+    float* best_d;             // fp32 distance to the entry
+    const float* Cg;           // group centres [t][9]
+    const int32_t* labels;     // group of every entry [k]
+    int32_t* perm;             // entries group by group, ascending inside a group [k]
+    int32_t* gstart;           // first position of every group in perm [t + 1]
+    float* radius;             // upper bound of the distance of a group's entries to its centre [t]
+    double* delta;             // cumulative drift bound of every group [t]
+    int32_t* cnt;              // listed pairs per group [t], listed kernels [t]
+    float* Lt;                 // stored bounds [t][n]
+    float* B1;                 // smallest distance in a scanned group [t][n]
+    int32_t* J1;               // its entry [t][n]
+    float* B2;                 // second smallest distance in a scanned group [t][n]
+    int32_t* lists;            // kernels listed per group [t][n]
+    unsigned long long* mask;  // groups to scan per listed kernel [n]
+    int32_t* flist;            // listed kernels [n]
+    double* part;              // distortion partials, one per 64 kernels
+    int32_t* stats;            // device [2]: listed kernels, listed pairs; or null
+    int n, k, t, npart;
+};
+hipError_t launch_yy_group(const YyParams& p, hipStream_t s);
+hipError_t launch_yy_bounds_init(const YyParams& p, hipStream_t s);
+hipError_t launch_yy_round(const YyParams& p, hipStream_t s);
+hipError_t launch_yy_partials(const YyParams& p, hipStream_t s);
+
 hipError_t launch_pack(const void* v, int elem_bytes, int64_t count, int bits, uint8_t* out, hipStream_t s);
 hipError_t launch_unpack(const uint8_t* in, int64_t count, int bits, int32_t* v, hipStream_t s);
 hipError_t launch_sq_error(const float* A, const float* B, int64_t count, double* out, void* ws, hipStream_t s);

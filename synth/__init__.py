@@ -167,3 +167,14 @@ def random_codebook_state(X: np.ndarray, k: int, seed: int, jitter: float = 0.25
 def random_indices(n: int, k: int, seed: int) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return rng.integers(0, k, n).astype(np.int32)
+
+
+def moved_codebook(C: np.ndarray, frac: float, scale: float, seed: int) -> np.ndarray:
+    """C with a seeded random fraction of its entries moved by N(0, scale^2) noise
+    (a codebook sequence with controlled movement between rounds)."""
+    rng = np.random.default_rng(seed)
+    k = C.shape[0]
+    out = C.astype(np.float64).copy()
+    moved = rng.random(k) < frac
+    out[moved] += scale * rng.standard_normal((int(moved.sum()), C.shape[1]))
+    return np.ascontiguousarray(out.astype(np.float32))

@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 3
+    assert lib.kq_abi_version() == 4
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -186,3 +186,50 @@ def test_stack_pack_and_reconstruct_argument_errors():
     lay[1] = kq.KqReconLayer(None, FAKE, 17, 256, 100, FAKE, FAKE, None, None)
     assert lib.kq_reconstruct_stack(q, 2, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
     assert lib.kq_reconstruct_stack_workspace_bytes(q, 2) == 0
+
+
+def test_yinyang_workspace_and_argument_errors():
+    a = lib.kq_yinyang_workspace_bytes(4096, 256, 0)
+    assert a > lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256) and a % 256 == 0
+    assert lib.kq_yinyang_workspace_bytes(4096, 256, 8) > lib.kq_yinyang_workspace_bytes(4096, 256, 4)
+    assert lib.kq_yinyang_workspace_bytes(4096, 256, 65) == 0      # more groups than mask bits
+    assert lib.kq_yinyang_workspace_bytes(100, 8, 9) == 0          # more groups than entries
+    assert lib.kq_yinyang_workspace_bytes(7, 8, 0) == 0            # k > n
+    assert lib.kq_yinyang_workspace_bytes(100, 1, 0) > 0           # one entry, one group
+    nb = lib.kq_yinyang_workspace_bytes(100, 8, 0)
+
+    def init(**kw):
+        a = dict(X=FAKE, n=100, dim=9, C=FAKE, k=8, g=0, idx=FAKE, bd=None, dist=None, ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_yinyang_init(a["X"], a["n"], a["dim"], a["C"], a["k"], a["g"], a["idx"], a["bd"], a["dist"],
+                                   a["ws"], a["wsb"], None)
+
+    assert init(dim=4) == kq.KQ_ERR_UNSUPPORTED
+    assert init(k=101) == kq.KQ_ERR_ARG
+    assert init(g=9) == kq.KQ_ERR_ARG
+    assert init(X=None) == kq.KQ_ERR_ARG
+    assert init(C=FAKE + 2) == kq.KQ_ERR_ARG
+    assert init(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE
+    assert init(ws=FAKE + 64) == kq.KQ_ERR_WORKSPACE
+
+    def step(**kw):
+        a = dict(X=FAKE, n=100, C0=FAKE, C=FAKE, k=8, idx=FAKE, st=None, ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_yinyang_assign(a["X"], a["n"], 9, a["C0"], a["C"], a["k"], 0, a["idx"], None, None, a["st"],
+                                     a["ws"], a["wsb"], None)
+
+    assert step(C0=None) == kq.KQ_ERR_ARG
+    assert step(st=FAKE + 1) == kq.KQ_ERR_ARG
+    assert step(n=0) == kq.KQ_ERR_ARG
+    assert step(wsb=0) == kq.KQ_ERR_WORKSPACE
+
+    def fit(**kw):
+        a = dict(X=FAKE, n=100, k=8, C0=FAKE, it=3, C=FAKE, idx=FAKE, ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_fit_layer_yinyang(a["X"], a["n"], 9, a["k"], a["C0"], a["it"], 0, a["C"], a["idx"], None, None,
+                                        None, a["ws"], a["wsb"], None)
+
+    assert fit(it=-1) == kq.KQ_ERR_ARG
+    assert fit(C=None) == kq.KQ_ERR_ARG
+    assert fit(k=kq.KQ_MAX_K + 1) == kq.KQ_ERR_UNSUPPORTED
+    assert fit(wsb=100) == kq.KQ_ERR_WORKSPACE

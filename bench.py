@@ -51,6 +51,8 @@ def parse():
                     help="workload (default: the ResNet-18-shaped stack, the headline metric)")
     ap.add_argument("--iters", type=int, default=None, help="Lloyd rounds per layer (default: the config's)")
     ap.add_argument("--k", type=int, default=None, help="codebook size (default: the config's)")
+    ap.add_argument("--yinyang", action="store_true",
+                    help="run each layer's Lloyd rounds with Yinyang assignments (Sec. 4.1; the same result)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -146,7 +148,12 @@ def main():
     recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
 
     stream = torch.cuda.current_stream(dev)
-    ev = {"assign": [], "update": [], "cbq": [], "pack": [], "reconstruct": []}
+    ev = {"assign": [], "update": [], "cbq": [], "pack": [], "reconstruct": [], "fit": []}
+    if args.yinyang:
+        C0_views = [v.view(-1, 9) for v in torch.split(C0flat, sizes)]
+        yy_ws = [torch.empty(kq.lib.kq_yinyang_workspace_bytes(L.n, L.k, 0), dtype=torch.uint8, device=dev)
+                 for L in layers]
+        yy_stats = [torch.zeros(max(T, 1), 3, dtype=torch.int64, device=dev) for L in layers]
 
     def timed(name, record, fn):
         if not record:
@@ -158,7 +165,20 @@ def main():
         e1.record(stream)
         ev[name].append((e0, e1))
 
+    def yinyang_rounds(record: bool):
+        for i in range(len(layers)):
+            timed("fit", record, lambda i=i: kq.kq_fit_layer_yinyang(
+                X[i], C0_views[i], T, C=st.C[i], idx=st.idx[i], counts=st.counts[i],
+                distortion=st.distortion[i], stats=yy_stats[i], workspace=yy_ws[i]))
+
     def step(record: bool):
+        if args.yinyang:
+            yinyang_rounds(record)
+            timed("cbq", record, lambda: kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30,
+                                                                       out=cb_out))
+            timed("pack", record, lambda: kq.kq_pack_bits_stack(pack_jobs))
+            timed("reconstruct", record, lambda: kq.kq_reconstruct_stack(recon, workspace=recon_ws))
+            return
         Cflat.copy_(C0flat)
         for t in range(T + 1):
             if record:
@@ -204,14 +224,28 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
 
-    mean_ms = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) for name, pairs in ev.items()}
+    mean_ms = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) if pairs else 0.0
+               for name, pairs in ev.items()}
     assign_ms, update_ms = mean_ms["assign"], mean_ms["update"]
     rec_bytes = sum(L.n * (b / 8 + 36 + 36) for L, b in zip(layers, bits))  # packed index + reference + output row
     flops = 18.0 * sum(L.k * L.n for L in layers)   # 9 multiply-adds per (kernel, entry) pair
-    achieved = flops / (assign_ms * 1e-3) / 1e12
+    achieved = flops / (assign_ms * 1e-3) / 1e12 if assign_ms > 0 else 0.0
     upd_bytes = 40.0 * n_total                      # 36-byte kernel + 4-byte index per kernel
-    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9
+    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9 if update_ms > 0 else 0.0
 
+    yy_diag = None
+    if args.yinyang:
+        # the fits' own work: the round-0 assignment is a full one (n k distances), rounds
+        # 1..T scan what the bounds leave (per-round counts from the library)
+        stats = [s.cpu().numpy() for s in yy_stats]
+        evals = sum(L.n * L.k + int(s[:T, 2].sum()) for L, s in zip(layers, stats))
+        full = sum(L.n * L.k * (T + 1) for L in layers)
+        fit_ms = sum(a.elapsed_time(b) for a, b in ev["fit"])
+        yy_diag = {"fit_ms": fit_ms, "distance_evaluations": evals, "lloyd_equivalent": full,
+                   "evaluated_fraction": evals / full,
+                   "kernels_scanned_per_round": [int(x) for x in np.sum([s[:T, 0] for s in stats], axis=0)],
+                   "pairs_scanned_per_round": [int(x) for x in np.sum([s[:T, 1] for s in stats], axis=0)]}
+        achieved = 18.0 * evals / (fit_ms * 1e-3) / 1e12
     J = [float(d[T]) for d in st.distortion]
     mse_k = [j / (9 * L.n) for j, L in zip(J, layers)]
     mse_kc = [float(s) / (9 * L.n) for s, L in zip(sq.cpu(), layers)]
@@ -222,7 +256,8 @@ def main():
         "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9,
         "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
         "beta_K": sum(L.k * 9 * 32 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
-        "beta_KC": sum(L.k * 9 * 6 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total)}}), file=sys.stderr)
+        "beta_KC": sum(L.k * 9 * 6 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
+        "yinyang": yy_diag}}), file=sys.stderr)
 
     result = {
         "metric": METRIC,
@@ -245,6 +280,13 @@ def main():
                      "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) else None,
                      "kernel": "assign_kernel (one launch per Lloyd round, whole stack)"},
     }
+    if args.yinyang:
+        # distances the Yinyang fits evaluated (matrix-core round 0 + exact fp32 scans), 18 flop
+        # each, over the fits' whole time (updates included); the scans run unpacked fp32 VALU
+        result["config"]["assignment"] = "yinyang"
+        result["roofline"] = {"bound": "alu", "achieved": achieved, "peak": FP32_PEAK_TFLOPS / 2, "unit": "TFLOP/s",
+                              "frac": achieved / (FP32_PEAK_TFLOPS / 2), "traffic": None,
+                              "kernel": "kq_fit_layer_yinyang (all launches of the fits)"}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(layers, args.cpu_iters)
     print(json.dumps(result), flush=True)

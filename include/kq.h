@@ -185,11 +185,11 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
  *   kq_yinyang_assign: the next assignment after the codebook moved from C_prev (the
  *                      codebook of the previous init/assign call on this workspace) to C.
  *                      idx must hold that call's assignment; it is replaced by the new one.
- *                      stats (device int32 [2] or NULL): kernels whose groups were scanned,
- *                      (kernel, group) pairs scanned.
+ *                      stats (device int64 [3] or NULL): kernels whose groups were scanned,
+ *                      (kernel, group) pairs scanned, distances evaluated in those scans.
  *   kq_fit_layer_yinyang: kq_fit_layer with Yinyang assignments; C, idx, counts and
  *                      distortion [iters+1] equal kq_fit_layer's bit for bit.  stats
- *                      (device int32 [iters][2] or NULL): the scan counts of rounds 1..iters.
+ *                      (device int64 [iters][3] or NULL): the scan counts of rounds 1..iters.
  *   X device [n][9]; C, C_prev, C_init device [k][9]; idx device [n]; best_d device [n];
  *   counts device [k].  Requires 1 <= k <= n.  Kernel and codebook values must be finite
  *   with |x| < 32 (the grouping and the fit run kq_update's fixed-point sums).
@@ -203,10 +203,10 @@ kq_status kq_yinyang_init(const float* X, int64_t n, int32_t dim, const float* C
                           void* stream);
 kq_status kq_yinyang_assign(const float* X, int64_t n, int32_t dim, const float* C_prev, const float* C,
                             int32_t k, int32_t groups, int32_t* idx, float* best_d, double* distortion,
-                            int32_t* stats, void* ws, size_t ws_bytes, void* stream);
+                            int64_t* stats, void* ws, size_t ws_bytes, void* stream);
 kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
                                int32_t iters, int32_t groups, float* C, int32_t* idx, int32_t* counts,
-                               double* distortion, int32_t* stats, void* ws, size_t ws_bytes, void* stream);
+                               double* distortion, int64_t* stats, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Stack versions: one launch per step for up to KQ_MAX_STACK layers (more are split).

@@ -246,7 +246,7 @@ class Yinyang:
         self.idx = torch.empty(self.n, dtype=torch.int32, device=dev)
         self.best_d = torch.empty(self.n, dtype=torch.float32, device=dev)
         self.distortion = torch.empty(1, dtype=torch.float64, device=dev)
-        self.stats = torch.zeros(2, dtype=torch.int32, device=dev)
+        self.stats = torch.zeros(3, dtype=torch.int64, device=dev)
         self.C_prev = C.clone()
         _check(lib.kq_yinyang_init(self.X.data_ptr(), self.n, KQ_DIM, C.data_ptr(), self.k, self.groups,
                                    self.idx.data_ptr(), self.best_d.data_ptr(), self.distortion.data_ptr(),
@@ -255,7 +255,7 @@ class Yinyang:
     def assign(self, C):
         """Assignment against C (the codebook after the previous call's).  Returns
         (idx, best_d, distortion); `stats` then holds the kernels and (kernel, group) pairs
-        that were scanned."""
+        that were scanned and the distances those scans evaluated."""
         C = _kernels(C, "C")
         if tuple(C.shape) != (self.k, KQ_DIM):
             raise ValueError(f"C must be [{self.k}, 9]")
@@ -271,7 +271,8 @@ class Yinyang:
 def kq_fit_layer_yinyang(X, C_init, iters: int, groups: int = 0, C=None, idx=None, counts=None, distortion=None,
                          stats=None, workspace=None):
     """kq_fit_layer with Yinyang assignments (Sec. 4.1); the same outputs bit for bit.
-    Returns (C, idx, counts, distortion[iters+1], stats int32 [iters, 2])."""
+    Returns (C, idx, counts, distortion[iters+1], stats int64 [iters, 3]: kernels scanned,
+    (kernel, group) pairs scanned, distances evaluated, per round)."""
     X = _kernels(X)
     C_init = _kernels(C_init, "C_init")
     n, k = X.shape[0], C_init.shape[0]
@@ -280,12 +281,12 @@ def kq_fit_layer_yinyang(X, C_init, iters: int, groups: int = 0, C=None, idx=Non
     idx = idx if idx is not None else torch.empty(n, dtype=torch.int32, device=dev)
     counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
     distortion = distortion if distortion is not None else torch.empty(iters + 1, dtype=torch.float64, device=dev)
-    stats = stats if stats is not None else torch.zeros(max(iters, 1), 2, dtype=torch.int32, device=dev)
+    stats = stats if stats is not None else torch.zeros(max(iters, 1), 3, dtype=torch.int64, device=dev)
     _dev(C, torch.float32, "C", (k, KQ_DIM))
     _dev(idx, torch.int32, "idx", (n,))
     _dev(counts, torch.int32, "counts", (k,))
     _dev(distortion, torch.float64, "distortion", (iters + 1,))
-    _dev(stats, torch.int32, "stats")
+    _dev(stats, torch.int64, "stats")
     nb = _yy_groups_bytes(n, k, groups)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_fit_layer_yinyang(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, groups, C.data_ptr(),

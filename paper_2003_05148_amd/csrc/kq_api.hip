@@ -155,7 +155,7 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
 // ---- Yinyang workspace: the layer's own region (assignment partials, update partials and
 // histograms), then the grouping fit's region, then the Yinyang state ----------------------
 struct YyLayout {
-    size_t sub, Cg, labels, Cw, perm, gstart, radius, delta, cnt, Lt, B1, J1, B2, lists, mask, flist, bd, total;
+    size_t sub, Cg, labels, Cw, perm, gstart, radius, delta, cnt, Lt, B1, J1, B2, lists, mask, flist, bd, wgc, total;
 };
 
 YyLayout yy_layout(int64_t n, int32_t k, int t) {
@@ -184,6 +184,7 @@ YyLayout yy_layout(int64_t n, int32_t k, int t) {
     L.mask = take(sizeof(unsigned long long) * (size_t)n);
     L.flist = take(sizeof(int32_t) * (size_t)n);
     L.bd = take(sizeof(float) * (size_t)n);
+    L.wgc = take(sizeof(int32_t) * (size_t)(t + 1) * (size_t)((n + 255) / 256));
     L.total = o;
     return L;
 }
@@ -195,7 +196,7 @@ int yy_groups(int32_t k, int32_t groups) {
 }
 
 YyParams yy_params(unsigned char* ws, const YyLayout& L, const float* X, int64_t n, int32_t k, int t,
-                   const float* C, const float* C_prev, int32_t* idx, float* best_d, int32_t* stats) {
+                   const float* C, const float* C_prev, int32_t* idx, float* best_d, long long* stats) {
     YyParams p;
     memset(&p, 0, sizeof(p));
     p.X = X;
@@ -217,6 +218,7 @@ YyParams yy_params(unsigned char* ws, const YyLayout& L, const float* X, int64_t
     p.lists = (int32_t*)(ws + L.lists);
     p.mask = (unsigned long long*)(ws + L.mask);
     p.flist = (int32_t*)(ws + L.flist);
+    p.wgc = (int32_t*)(ws + L.wgc);
     p.part = (double*)ws;  // the layer's assignment partials
     p.stats = stats;
     p.n = (int)n;
@@ -385,28 +387,28 @@ kq_status kq_yinyang_init(const float* X, int64_t n, int32_t dim, const float* C
 }
 
 kq_status kq_yinyang_assign(const float* X, int64_t n, int32_t dim, const float* C_prev, const float* C, int32_t k,
-                            int32_t groups, int32_t* idx, float* best_d, double* distortion, int32_t* stats, void* ws,
+                            int32_t groups, int32_t* idx, float* best_d, double* distortion, int64_t* stats, void* ws,
                             size_t ws_bytes, void* stream) {
     int t = 0;
     kq_status st = check_yy(X, n, dim, k, groups, idx, best_d, distortion, t);
     if (st != KQ_OK) return st;
-    if (!C || !C_prev || !aligned(C, 4) || !aligned(C_prev, 4) || (stats && !aligned(stats, 4))) return KQ_ERR_ARG;
+    if (!C || !C_prev || !aligned(C, 4) || !aligned(C_prev, 4) || (stats && !aligned(stats, 8))) return KQ_ERR_ARG;
     const YyLayout L = yy_layout(n, k, t);
     if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
     hipStream_t s = (hipStream_t)stream;
-    const YyParams p = yy_params((unsigned char*)ws, L, X, n, k, t, C, C_prev, idx, best_d, stats);
+    const YyParams p = yy_params((unsigned char*)ws, L, X, n, k, t, C, C_prev, idx, best_d, (long long*)stats);
     if (launch_yy_round(p, s) != hipSuccess) return KQ_ERR_HIP;
     return distortion ? yy_distortion(p, distortion, s) : KQ_OK;
 }
 
 kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters,
                                int32_t groups, float* C, int32_t* idx, int32_t* counts, double* distortion,
-                               int32_t* stats, void* ws, size_t ws_bytes, void* stream) {
+                               int64_t* stats, void* ws, size_t ws_bytes, void* stream) {
     int t = 0;
     kq_status st = check_yy(X, n, dim, k, groups, idx, nullptr, distortion, t);
     if (st != KQ_OK) return st;
     if (iters < 0 || !C_init || !C || !aligned(C_init, 4) || !aligned(C, 4)) return KQ_ERR_ARG;
-    if ((counts && !aligned(counts, 4)) || (stats && !aligned(stats, 4))) return KQ_ERR_ARG;
+    if ((counts && !aligned(counts, 4)) || (stats && !aligned(stats, 8))) return KQ_ERR_ARG;
     const YyLayout L = yy_layout(n, k, t);
     if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
     unsigned char* w = (unsigned char*)ws;
@@ -425,7 +427,7 @@ kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k
         kq_layer lu = {X, n, k, nxt, idx, nullptr, counts, distortion};
         const float* olds[1] = {cur};
         if ((st = run_update(&lu, 0, 1, w, r, olds, 0, s, true)) != KQ_OK) return st;
-        const YyParams p = yy_params(w, L, X, n, k, t, nxt, cur, idx, nullptr, stats ? stats + 2 * (size_t)r : nullptr);
+        const YyParams p = yy_params(w, L, X, n, k, t, nxt, cur, idx, nullptr, stats ? (long long*)stats + 3 * (size_t)r : nullptr);
         if (launch_yy_round(p, s) != hipSuccess) return KQ_ERR_HIP;
         if (launch_yy_partials(p, s) != hipSuccess) return KQ_ERR_HIP;
         float* tmp = cur;

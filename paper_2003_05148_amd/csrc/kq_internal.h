@@ -248,7 +248,7 @@ hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s);
 constexpr int kYyMaxGroups = 64;     // groups per codebook (one bit each in a 64-bit mask)
 constexpr int kYyEvalChunk = 1024;   // group entries staged in LDS at a time
 constexpr int kYyEvalGrid = 2048;    // persistent workgroups of the exact group scan
-constexpr int kYyFinalGrid = 1024;   // persistent workgroups of the final decision
+constexpr int kYyFinalGrid = 8192;   // workgroups of the final decision (grid-stride beyond)
 constexpr int kYyGroupRounds = 5;    // Lloyd rounds that group the codebook's entries
 
 // default number of groups for k entries: about 64 entries per group, 1 to 32 groups
@@ -277,8 +277,9 @@ struct YyParams {
     int32_t* lists;            // kernels listed per group [t][n]
     unsigned long long* mask;  // groups to scan per listed kernel [n]
     int32_t* flist;            // listed kernels [n]
+    int32_t* wgc;              // per-workgroup list counts, then offsets [t + 1][ceil(n / 256)]
     double* part;              // distortion partials, one per 64 kernels
-    int32_t* stats;            // device [2]: listed kernels, listed pairs; or null
+    long long* stats;          // device [3]: listed kernels, listed pairs, distances evaluated; or null
     int n, k, t, npart;
 };
 hipError_t launch_yy_group(const YyParams& p, hipStream_t s);

@@ -23,12 +23,15 @@
 //   filter  per kernel: d_a = d32(x, c_a) for its current entry a, U = upper bound of
 //           e(x, c_a) widened by (1 + 2^-18) and 1e-20.  A group with U < Lt_g - D_g
 //           holds no entry whose fp32 distance can reach d_a (the widening covers the
-//           12 u error on both sides and underflow), so it is skipped.  Kernels with
-//           groups left are listed, and each (kernel, group) pair is appended to the
-//           group's list (one atomic per wave and group);
-//   eval    per (group, 256 listed kernels): the group's entries are staged in LDS and
-//           every lane scans them in ascending index order: smallest fp32 distance, its
-//           entry (strict <, so the lowest index among ties), second smallest distance;
+//           12 u error on both sides and underflow), so it is skipped.  The mask of the
+//           groups left is stored per kernel and counted per workgroup in LDS;
+//   lists   the per-workgroup counts are scanned per group and every workgroup writes its
+//           kernels into each group's list (and the list of kernels with anything to
+//           scan) in ascending order: no global atomics, the same lists on every run;
+//   eval    per (group, 512 listed kernels): the group's entries are staged in LDS and
+//           every lane scans them for two kernels in ascending index order: smallest fp32
+//           distance, its entry (strict <, so the lowest index among ties), second
+//           smallest distance;
 //   final   per listed kernel: the lexicographically smallest (distance, index) of the
 //           current entry and the scanned groups' winners is the fp32 argmin (no finite
 //           distance: entry 0, as a plain scan gives); each scanned group's bound becomes
@@ -78,18 +81,6 @@ __device__ __forceinline__ float store_lo(double L, double D) {
 __device__ __forceinline__ void load_row(const float* __restrict__ X, long long i, float (&x)[kDim]) {
 #pragma unroll
     for (int d = 0; d < kDim; ++d) x[d] = X[(size_t)i * kDim + d];
-}
-
-// wave-aggregated append of `i` to list[cnt++] for the lanes where `pred` holds
-__device__ __forceinline__ void wave_append(bool pred, int* cnt, int* list, int i) {
-    const unsigned long long b = __ballot(pred);
-    if (b == 0) return;
-    const int lane = threadIdx.x & 63;
-    const int leader = __ffsll((long long)b) - 1;
-    int base = 0;
-    if (lane == leader) base = atomicAdd(cnt, __popcll(b));
-    base = __shfl(base, leader);
-    if (pred) list[base + __popcll(b & ((1ull << lane) - 1ull))] = i;
 }
 
 }  // namespace
@@ -171,12 +162,11 @@ __global__ __launch_bounds__(256) void yy_bounds_init_kernel(const YyParams p) {
     }
 }
 
-// ---- drift of every group between C_prev and C; clears the round's counters -------------
+// ---- drift of every group between C_prev and C ----------------------------------------
 __global__ __launch_bounds__(1024) void yy_drift_kernel(const YyParams p) {
     __shared__ unsigned s_mx[kYyMaxGroups];
     const int tid = threadIdx.x;
     if (tid < p.t) s_mx[tid] = 0u;
-    if (tid <= p.t) p.cnt[tid] = 0;
     __syncthreads();
     for (int j = tid; j < p.k; j += 1024) {
         float a[kDim];
@@ -188,11 +178,16 @@ __global__ __launch_bounds__(1024) void yy_drift_kernel(const YyParams p) {
     if (tid < p.t) p.delta[tid] = (p.delta[tid] + (double)__uint_as_float(s_mx[tid])) * kDriftRel;
 }
 
-// ---- filter: one kernel per thread -------------------------------------------------------
+// ---- filter: one kernel per thread ---------------------------------------------------------
+// Writes the mask of groups to scan for every kernel (0: settled) and, per workgroup, how
+// many of its kernels each group lists (row t: kernels with anything to scan).
 __global__ __launch_bounds__(256) void yy_filter_kernel(const YyParams p) {
-    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    __shared__ int s_c[kYyMaxGroups + 1];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const long long i = (long long)blockIdx.x * 256 + tid;
     const bool valid = i < p.n;
     const int n = p.n, k = p.k, t = p.t;
+    if (tid <= t) s_c[tid] = 0;
     unsigned long long mask = 0ull;
     if (valid) {
         const int a = p.idx[i];
@@ -206,26 +201,124 @@ __global__ __launch_bounds__(256) void yy_filter_kernel(const YyParams p) {
         }
         if (!(da < kInf)) mask = t >= 64 ? ~0ull : ((1ull << t) - 1ull);  // no finite distance yet: scan all
         p.best_d[i] = da;
-        if (mask) p.mask[i] = mask;
+        p.mask[i] = mask;
     }
-    wave_append(mask != 0ull, &p.cnt[t], p.flist, (int)i);
-    for (int g = 0; g < t; ++g) wave_append((mask >> g) & 1ull, &p.cnt[g], p.lists + (size_t)g * n, (int)i);
+    __syncthreads();
+    for (int g = 0; g <= t; ++g) {
+        const bool on = g < t ? ((mask >> g) & 1ull) != 0 : mask != 0ull;
+        const unsigned long long b = __ballot(on);
+        if (lane == 0 && b) atomicAdd(&s_c[g], __popcll(b));  // LDS
+    }
+    __syncthreads();
+    if (tid <= t) p.wgc[(size_t)tid * gridDim.x + blockIdx.x] = s_c[tid];
+}
+
+// ---- per group: exclusive scan of the per-workgroup counts (one workgroup per group) ------
+__global__ __launch_bounds__(1024) void yy_scan_kernel(const YyParams p, int nwg) {
+    __shared__ int s_w[1024 / kWave];
+    const int g = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int* row = p.wgc + (size_t)g * nwg;
+    int carry = 0;
+    for (int base = 0; base < nwg; base += 1024) {
+        const int q = base + tid;
+        const int v = q < nwg ? row[q] : 0;
+        int x = v;  // inclusive scan inside the wave
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const int y = __shfl_up(x, off);
+            if (lane >= off) x += y;
+        }
+        if (lane == kWave - 1) s_w[wave] = x;
+        __syncthreads();
+        int before = carry;
+        for (int w = 0; w < wave; ++w) before += s_w[w];
+        int total = carry;
+        for (int w = 0; w < 1024 / kWave; ++w) total += s_w[w];
+        if (q < nwg) row[q] = before + x - v;
+        __syncthreads();
+        carry = total;
+    }
+    if (tid == 0) p.cnt[g] = carry;
+}
+
+// ---- scatter: every group's list in ascending kernel order --------------------------------
+// Only the groups some kernel of the workgroup needs are visited (bit t of the union: the
+// list of kernels with anything to scan).
+__device__ __forceinline__ bool listed_in(unsigned long long mask, int g, int t) {
+    return g < t ? ((mask >> g) & 1ull) != 0 : mask != 0ull;
+}
+
+__global__ __launch_bounds__(256) void yy_scatter_kernel(const YyParams p) {
+    __shared__ int s_w[4][kYyMaxGroups + 1];
+    __shared__ unsigned long long s_or;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const long long i = (long long)blockIdx.x * 256 + tid;
+    const int n = p.n, t = p.t;
+    const unsigned long long mask = i < n ? p.mask[i] : 0ull;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    if (tid == 0) s_or = 0ull;
+    __syncthreads();
+    if (mask) atomicOr(&s_or, mask);
+    __syncthreads();
+    const unsigned long long any = s_or;
+    if (any == 0ull) return;  // uniform: nothing listed in this workgroup
+    // visit the groups of the union, then the list of kernels with anything to scan
+    for (unsigned long long m = any;; m &= m - 1ull) {
+        const int g = m ? __ffsll((long long)m) - 1 : t;
+        const unsigned long long b = __ballot(listed_in(mask, g, t));
+        if (lane == 0) s_w[wave][g] = __popcll(b);
+        if (!m) break;
+    }
+    __syncthreads();
+    for (unsigned long long m = any;; m &= m - 1ull) {
+        const int g = m ? __ffsll((long long)m) - 1 : t;
+        const bool on = listed_in(mask, g, t);
+        const unsigned long long b = __ballot(on);
+        if (on) {
+            int pos = p.wgc[(size_t)g * gridDim.x + blockIdx.x] + __popcll(b & below);
+            for (int w = 0; w < wave; ++w) pos += s_w[w][g];
+            if (g < t)
+                p.lists[(size_t)g * n + pos] = (int)i;
+            else
+                p.flist[pos] = (int)i;
+        }
+        if (!m) break;
+    }
 }
 
 // ---- exact scan of the listed (kernel, group) pairs -------------------------------------
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// one lane's running scan of a group: smallest distance, its entry, second smallest
+struct Scan {
+    float b1, b2;
+    int j1;
+};
+
+__device__ __forceinline__ void scan_step(Scan& s, float d, int e) {
+    if (d < s.b1) {
+        s.b2 = s.b1;
+        s.b1 = d;
+        s.j1 = e;
+    } else if (d < s.b2) {
+        s.b2 = d;
+    }
+}
+
+// A work item is 512 listed kernels of one group, two per lane: every staged entry read
+// from LDS (a broadcast) serves two distances.
 __global__ __launch_bounds__(256) void yy_eval_kernel(const YyParams p) {
     __shared__ f32x4 s_c[kYyEvalChunk * 3];  // the staged entries, 48-byte rows
     __shared__ int s_j[kYyEvalChunk];
     __shared__ int s_pre[kYyMaxGroups + 1];  // first work item of each group
+    constexpr int kItem = 2 * 256;
     const int tid = threadIdx.x;
     const int n = p.n, t = p.t;
     if (tid == 0) {
         int s = 0;
         for (int g = 0; g < t; ++g) {
             s_pre[g] = s;
-            s += (p.cnt[g] + 255) >> 8;
+            s += (p.cnt[g] + kItem - 1) / kItem;
         }
         s_pre[t] = s;
     }
@@ -236,14 +329,16 @@ __global__ __launch_bounds__(256) void yy_eval_kernel(const YyParams p) {
     for (int item = blockIdx.x; item < total; item += gridDim.x) {
         int g = 0;
         while (g + 1 < t && item >= s_pre[g + 1]) ++g;
-        const int pos = (item - s_pre[g]) * 256 + tid;
-        const bool has = pos < p.cnt[g];
-        const int pt = has ? p.lists[(size_t)g * n + pos] : 0;
-        float x[kDim];
-        load_row(p.X, pt, x);
+        const int pos0 = (item - s_pre[g]) * kItem + tid, pos1 = pos0 + 256;
+        const int cg = p.cnt[g];
+        const bool has0 = pos0 < cg, has1 = pos1 < cg;
+        const int pt0 = has0 ? p.lists[(size_t)g * n + pos0] : 0;
+        const int pt1 = has1 ? p.lists[(size_t)g * n + pos1] : pt0;
+        float x0[kDim], x1[kDim];
+        load_row(p.X, pt0, x0);
+        load_row(p.X, pt1, x1);
         const int g0 = p.gstart[g], m = p.gstart[g + 1] - g0;
-        float b1 = kInf, b2 = kInf;
-        int j1 = -1;
+        Scan s0 = {kInf, kInf, -1}, s1 = {kInf, kInf, -1};
         for (int c0 = 0; c0 < m; c0 += kYyEvalChunk) {
             const int cm = min(kYyEvalChunk, m - c0);
             if (staged_g != g || staged_c0 != c0) {
@@ -261,24 +356,25 @@ __global__ __launch_bounds__(256) void yy_eval_kernel(const YyParams p) {
                 staged_g = g;
                 staged_c0 = c0;
             }
-#pragma unroll 2
+            // positions in the staged chunk; entries ascend with them inside a group
+#pragma unroll 4
             for (int e = 0; e < cm; ++e) {
                 const f32x4 r0 = s_c[e * 3 + 0], r1 = s_c[e * 3 + 1];
                 const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], s_cf[e * 12 + 8]};
-                const float d = d32(x, c);
-                if (d < b1) {
-                    b2 = b1;
-                    b1 = d;
-                    j1 = s_j[e];
-                } else if (d < b2) {
-                    b2 = d;
-                }
+                scan_step(s0, d32(x0, c), c0 + e);
+                scan_step(s1, d32(x1, c), c0 + e);
             }
         }
-        if (has) {
-            p.B1[(size_t)g * n + pt] = b1;
-            p.J1[(size_t)g * n + pt] = j1;
-            p.B2[(size_t)g * n + pt] = b2;
+        // positions to entries (the chunk that holds a position may not be staged any more)
+        if (has0) {
+            p.B1[(size_t)g * n + pt0] = s0.b1;
+            p.J1[(size_t)g * n + pt0] = s0.j1 >= 0 ? p.perm[g0 + s0.j1] : -1;
+            p.B2[(size_t)g * n + pt0] = s0.b2;
+        }
+        if (has1) {
+            p.B1[(size_t)g * n + pt1] = s1.b1;
+            p.J1[(size_t)g * n + pt1] = s1.j1 >= 0 ? p.perm[g0 + s1.j1] : -1;
+            p.B2[(size_t)g * n + pt1] = s1.b2;
         }
     }
 }
@@ -288,10 +384,14 @@ __global__ __launch_bounds__(256) void yy_final_kernel(const YyParams p) {
     const int n = p.n, t = p.t, k = p.k;
     const int nf = p.cnt[t];
     if (blockIdx.x == 0 && threadIdx.x == 0 && p.stats) {
-        int pairs = 0;
-        for (int g = 0; g < t; ++g) pairs += p.cnt[g];
+        long long pairs = 0, evals = 0;
+        for (int g = 0; g < t; ++g) {
+            pairs += p.cnt[g];
+            evals += (long long)p.cnt[g] * (p.gstart[g + 1] - p.gstart[g]);
+        }
         p.stats[0] = nf;
         p.stats[1] = pairs;
+        p.stats[2] = evals;
     }
     for (int q = blockIdx.x * 256 + threadIdx.x; q < nf; q += gridDim.x * 256) {
         const int i = p.flist[q];
@@ -362,7 +462,11 @@ hipError_t launch_yy_round(const YyParams& p, hipStream_t s) {
     const unsigned blocks = (unsigned)((p.n + 255) / 256);
     hipLaunchKernelGGL(yy_filter_kernel, dim3(blocks), dim3(256), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const long long items = (long long)p.t * blocks;
+    hipLaunchKernelGGL(yy_scan_kernel, dim3(p.t + 1), dim3(1024), 0, s, p, (int)blocks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(yy_scatter_kernel, dim3(blocks), dim3(256), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const long long items = (long long)p.t * ((p.n + 511) / 512);
     const unsigned eg = (unsigned)(items < kYyEvalGrid ? items : kYyEvalGrid);
     hipLaunchKernelGGL(yy_eval_kernel, dim3(eg), dim3(256), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;

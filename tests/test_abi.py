@@ -219,7 +219,7 @@ def test_yinyang_workspace_and_argument_errors():
                                      a["ws"], a["wsb"], None)
 
     assert step(C0=None) == kq.KQ_ERR_ARG
-    assert step(st=FAKE + 1) == kq.KQ_ERR_ARG
+    assert step(st=FAKE + 4) == kq.KQ_ERR_ARG
     assert step(n=0) == kq.KQ_ERR_ARG
     assert step(wsb=0) == kq.KQ_ERR_WORKSPACE
 

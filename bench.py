@@ -217,6 +217,20 @@ def main():
     step(True)
     torch.cuda.synchronize()
 
+    # Eq. (2) codebook retraining step on the same stack (not part of the step): synthetic
+    # gradients of the kernels' shape, the final assignment, one launch set per step
+    gst = kq.Stack([x * 1e-3 for x in X], [c.view(-1, 9) for c in st.C])
+    for i in range(len(layers)):
+        gst.idx[i].copy_(st.idx[i])
+    kq.kq_codebook_grad_step_stack(gst, 0.01)
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(5):
+        kq.kq_codebook_grad_step_stack(gst, 0.01)
+    g1.record(stream)
+    torch.cuda.synchronize()
+    grad_ms = g0.elapsed_time(g1) / 5
+
     if args.copy_probe > 0:
         src = torch.ones(args.copy_probe << 18, device=dev)
         dst = torch.empty_like(src)
@@ -253,7 +267,8 @@ def main():
         "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_GBps": upd_gbs,
         "lloyd_round_ms": assign_ms + update_ms, "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
         "reconstruct_ms": mean_ms["reconstruct"],
-        "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9,
+        "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9 if mean_ms["reconstruct"] else 0.0,
+        "grad_step_ms": grad_ms, "grad_step_GBps": 40.0 * n_total / (grad_ms * 1e-3) / 1e9,
         "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
         "beta_K": sum(L.k * 9 * 32 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
         "beta_KC": sum(L.k * 9 * 6 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),

@@ -12,6 +12,8 @@
  *                        layers are independent, so one launch serves all of them).
  *   kq_fit_layer_yinyang Sec. 4.1: the same fit with Yinyang assignments (kq_yinyang_init,
  *                        kq_yinyang_assign), equal to kq_fit_layer bit for bit.
+ *   kq_codebook_grad_step Sec. 3.1, Eq. (2): retraining step of the codebook with the mean
+ *                        gradient of each entry's kernels.
  *   kq_quantize_codebook Sec. 3.2: 6-bit quantization of all scalars of a layer's codebook,
  *                        k-means weighted by how often each entry is used.
  *   kq_pack_bits         Eq. (4): the n * ceil(log2 k)-bit index stream.
@@ -72,6 +74,7 @@ typedef enum kq_status {
 #define KQ_OP_UPDATE 1
 #define KQ_OP_FIT 2
 #define KQ_OP_SQ_ERROR 3     /* n = element count, k = 1 */
+#define KQ_OP_GRAD 4         /* kq_codebook_grad_step */
 
 /* flags */
 #define KQ_F_COUNTS_ONLY 1u  /* kq_update / kq_update_stack: write counts only, leave C untouched */
@@ -163,6 +166,30 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
                        int32_t iters, float* C, int32_t* idx, int32_t* counts, double* distortion,
                        uint32_t flags, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kq_codebook_grad_step -- Sec. 3.1, Eq. (2): one retraining step of the kernel codebook.
+ *
+ *   Every entry moves against the elementwise mean of the gradients of the kernels mapped
+ *   to it:  c_i := c_i - gamma * (sum over m in S_i of dL/dm) / z_i,  z_i = |S_i|.
+ *   G [n][9] holds dL/dm for every kernel (the gradient of the loss with respect to the
+ *   weight tensor, OIHW, evaluated at the reconstructed weights), idx [n] the kernels'
+ *   entries.  An entry with no kernels keeps its value; indices outside [0, k) are ignored.
+ *   The sums are exact 64-bit fixed-point sums at a per-layer scale set from max |g| (any
+ *   finite gradient magnitude, independent of the order of the work); the mean is
+ *   fp64(sum) / z and c - gamma * mean is evaluated in fp64 and rounded once to fp32.
+ *   counts [k] (may be NULL) receives z.  C_old and C_new may alias (in-place step).
+ *   G, C_old, C_new device [.][9] fp32; idx device [n]; gamma finite (else KQ_ERR_ARG).
+ *   workspace: kq_workspace_bytes(KQ_OP_GRAD, n, k).
+ *   kq_codebook_grad_step_stack: the same for every layer of a stack in one launch set;
+ *   layers[l].X holds the layer's gradients and layers[l].C is stepped in place
+ *   (workspace: kq_stack_workspace_bytes).
+ */
+kq_status kq_codebook_grad_step(const float* G, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
+                                const float* C_old, float gamma, float* C_new, int32_t* counts, void* ws,
+                                size_t ws_bytes, void* stream);
+kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, float gamma, void* ws,
+                                      size_t ws_bytes, void* stream);
 
 /*
  * Yinyang assignment -- Sec. 4.1: the paper runs its kernel-level k-means with Yinyang

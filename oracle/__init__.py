@@ -12,6 +12,8 @@ What each function follows in the paper:
 * ``cbq_uniform`` / ``cbq_wkmeans`` -- kernel codebook quantization, Sec. 3.2:
   6-bit quantization of every scalar of a layer's codebook by k-means over those
   scalars, weighted by how often each codebook entry is used.
+* ``codebook_grad_step`` -- retraining of the kernel codebook, Sec. 3.1, Eq. (2):
+  every entry moves against the mean gradient of the kernels mapped to it.
 * ``pack_bits`` -- the n * ceil(log2 k)-bit index stream counted by Eq. (4).
 * ``reconstruct`` -- test-time recovery of the weight tensor from the codebook
   and the indices (end of Sec. 3.2).
@@ -143,6 +145,36 @@ def fit(X, C_init, iters: int):
     if rc:
         raise ValueError("kqo_fit failed")
     return dict(C=C, idx=idx, counts=counts, J=J)
+
+
+# ---- Sec. 3.1, Eq. (2): retraining of the kernel codebook ------------------------------
+
+def codebook_grad_step(G, idx, C, gamma):
+    """One retraining step of the kernel codebook, Eq. (2):
+
+        c_i <- c_i - gamma * (sum over the kernels m in S_i of dL/dm) / z_i.
+
+    G [n, dim] holds dL/dm for every kernel, idx [n] the kernels' entries.  Readings:
+    an entry with no kernels keeps its value (the mean over an empty set is undefined);
+    indices outside [0, k) are ignored; the sum is fp64 over the members in ascending
+    kernel order, the mean is that sum divided by z in fp64, and c - gamma * mean is
+    evaluated in fp64 (c and the fp32 gamma widened exactly) and rounded once to fp32.
+
+    Returns (C_new float32 [k, dim], counts int32 [k]).
+    """
+    G = _f32(G)
+    C = _f32(C)
+    idx = np.asarray(idx, np.int64)
+    k, dim = C.shape
+    ok = (idx >= 0) & (idx < k)
+    S = np.zeros((k, dim), np.float64)
+    np.add.at(S, idx[ok], G[ok].astype(np.float64))   # accumulates in ascending kernel order
+    z = np.bincount(idx[ok], minlength=k)
+    out = C.copy()
+    has = z > 0
+    mean = S[has] / z[has, None]
+    out[has] = (C[has].astype(np.float64) - np.float64(np.float32(gamma)) * mean).astype(np.float32)
+    return out, z.astype(np.int32)
 
 
 # ---- Sec. 3.2: kernel codebook quantization -------------------------------------------

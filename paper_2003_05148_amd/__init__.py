@@ -10,6 +10,7 @@ fallback: without the built library, importing this package raises ImportError.
 Entry points (same names as the C ABI):
   kq_assign, kq_update, kq_fit_layer, kq_assign_stack, kq_update_stack, kq_fit_stack,
   kq_fit_layer_yinyang (and the Yinyang class over kq_yinyang_init / kq_yinyang_assign),
+  kq_codebook_grad_step, kq_codebook_grad_step_stack,
   kq_quantize_codebook, kq_quantize_codebook_stack, kq_pack_bits, kq_unpack_bits,
   kq_reconstruct, kq_reconstruct_packed.
 """
@@ -74,6 +75,8 @@ def _load():
         "kq_pack_bits_stack": ([_P, _I32, _P], _I32),
         "kq_reconstruct_stack_workspace_bytes": ([_P, _I32], _SZ),
         "kq_reconstruct_stack": ([_P, _I32, _P, _SZ, _P], _I32),
+        "kq_codebook_grad_step": ([_P, _I64, _I32, _P, _I32, _P, ctypes.c_float, _P, _P, _P, _SZ, _P], _I32),
+        "kq_codebook_grad_step_stack": ([_P, _I32, ctypes.c_float, _P, _SZ, _P], _I32),
         "kq_yinyang_workspace_bytes": ([_I64, _I32, _I32], _SZ),
         "kq_yinyang_init": ([_P, _I64, _I32, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_yinyang_assign": ([_P, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
@@ -94,7 +97,7 @@ KQ_DIM = 9
 KQ_MAX_K = 65536
 KQ_MAX_STACK = 16
 KQ_CBQ_WKMEANS, KQ_CBQ_UNIFORM = 0, 1
-KQ_OP_ASSIGN, KQ_OP_UPDATE, KQ_OP_FIT, KQ_OP_SQ_ERROR = 0, 1, 2, 3
+KQ_OP_ASSIGN, KQ_OP_UPDATE, KQ_OP_FIT, KQ_OP_SQ_ERROR, KQ_OP_GRAD = 0, 1, 2, 3, 4
 KQ_F_COUNTS_ONLY = 1
 KQ_F_DISTORTION_FROM_ASSIGN = 2
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
@@ -102,7 +105,8 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
             "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error",
             "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
-            "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang"]
+            "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang",
+            "kq_codebook_grad_step", "kq_codebook_grad_step_stack"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -293,6 +297,35 @@ def kq_fit_layer_yinyang(X, C_init, iters: int, groups: int = 0, C=None, idx=Non
                                     idx.data_ptr(), counts.data_ptr(), distortion.data_ptr(), stats.data_ptr(),
                                     ws.data_ptr(), ws.numel(), _stream(dev)), "kq_fit_layer_yinyang")
     return C, idx, counts, distortion, stats
+
+
+def kq_codebook_grad_step(G, idx, C_old, gamma: float, C_new=None, counts=None, workspace=None):
+    """Eq. (2): every entry minus gamma times the mean gradient of its kernels (G [n, 9],
+    or an OIHW 3x3 gradient tensor); empty entries keep their value.  C_new may be C_old
+    (in place).  Returns (C_new, counts)."""
+    G = _kernels(G, "G")
+    C_old = _kernels(C_old, "C_old")
+    n, k = G.shape[0], C_old.shape[0]
+    dev = G.device
+    _dev(idx, torch.int32, "idx", (n,))
+    C_new = C_new if C_new is not None else torch.empty_like(C_old)
+    counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
+    _dev(C_new, torch.float32, "C_new", (k, KQ_DIM))
+    _dev(counts, torch.int32, "counts", (k,))
+    nb = lib.kq_workspace_bytes(KQ_OP_GRAD, n, k)
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_codebook_grad_step(G.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), float(gamma),
+                                     C_new.data_ptr(), counts.data_ptr(), ws.data_ptr(), ws.numel(),
+                                     _stream(dev)), "kq_codebook_grad_step")
+    return C_new, counts
+
+
+def kq_codebook_grad_step_stack(stack, gamma: float):
+    """Eq. (2) on every layer of a Stack built from the layers' gradient tensors (its X)
+    and codebooks (its C, stepped in place; its counts receive the entry sizes)."""
+    _check(lib.kq_codebook_grad_step_stack(ctypes.cast(stack.layers, _P), stack.n_layers, float(gamma),
+                                           stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)),
+           "kq_codebook_grad_step_stack")
 
 
 def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):

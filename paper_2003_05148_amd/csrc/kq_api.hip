@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 4;
+constexpr int32_t kAbiVersion = 5;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -75,6 +75,8 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
             d.nchunks = (int)((s.n + d.chunk - 1) / d.chunk);
             d.nunits = d.ranges * d.nchunks;
             d.flags = (int)kflags;
+            d.gmax = (unsigned*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k) + ws_hist(s.n, s.k));
+            d.ngmax = grad_max_blocks(s.n);
         }
         d.unit_begin = unit;
         unit += d.nunits;
@@ -123,6 +125,28 @@ kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
     if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;
 }
+
+// Eq. (2) on layers [l0, l1): per-block maxima of |g|, the segmented sums of the gradients
+// (layers[l].X holds them), then c - gamma * mean into layers[l].C
+kq_status run_grad(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, const float* const* C_old,
+                   float gamma, hipStream_t s) {
+    kq_layer quiet[KQ_MAX_STACK];
+    for (int32_t l = l0; l < l1; ++l) {
+        quiet[l - l0] = layers[l];
+        quiet[l - l0].distortion = nullptr;
+    }
+    size_t off = 0;
+    for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
+    StackParams p;
+    stack_params(p, quiet, 0, l1 - l0, ws + off, Op::Update, 0, C_old ? C_old + l0 : nullptr, kFlagGrad);
+    for (int l = 0; l < p.nlayers; ++l) p.L[l].gamma = gamma;
+    if (launch_grad_absmax(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
+    return KQ_OK;
+}
+
+bool finite_gamma(float g) { return g == g && g < 3.4e38f && g > -3.4e38f; }
 
 // Lloyd rounds: assign (leaving distortion partials in the workspace), then update,
 // whose finishing kernel adds those partials; the final assignment is followed by a
@@ -295,7 +319,7 @@ size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k) {
         return align256(sizeof(double) * (size_t)sq_error_blocks(n));
     }
     if (!valid_n(n) || !valid_k(k)) return 0;
-    if (op != KQ_OP_ASSIGN && op != KQ_OP_UPDATE && op != KQ_OP_FIT) return 0;
+    if (op != KQ_OP_ASSIGN && op != KQ_OP_UPDATE && op != KQ_OP_FIT && op != KQ_OP_GRAD) return 0;
     return layer_ws_bytes(n, k);
 }
 
@@ -342,6 +366,37 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
     const float* olds[1] = {C_old};
     return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0,
                       (hipStream_t)stream);
+}
+
+kq_status kq_codebook_grad_step(const float* G, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
+                                const float* C_old, float gamma, float* C_new, int32_t* counts, void* ws,
+                                size_t ws_bytes, void* stream) {
+    if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
+    if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(n) || !valid_k(k) || !finite_gamma(gamma)) return KQ_ERR_ARG;
+    if (!G || !idx || !C_old || !C_new || !aligned(G, 4) || !aligned(idx, 4) || !aligned(C_old, 4) ||
+        !aligned(C_new, 4) || (counts && !aligned(counts, 4)))
+        return KQ_ERR_ARG;
+    const kq_status w = check_ws(ws, ws_bytes, layer_ws_bytes(n, k));
+    if (w != KQ_OK) return w;
+    const kq_layer l = {G, n, k, C_new, const_cast<int32_t*>(idx), nullptr, counts, nullptr};
+    const float* olds[1] = {C_old};
+    return run_grad(&l, 0, 1, (unsigned char*)ws, olds, gamma, (hipStream_t)stream);
+}
+
+kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, float gamma, void* ws,
+                                      size_t ws_bytes, void* stream) {
+    kq_status st = check_layers(layers, n_layers, false);
+    if (st != KQ_OK) return st;
+    if (!finite_gamma(gamma)) return KQ_ERR_ARG;
+    st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
+    if (st != KQ_OK) return st;
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        st = run_grad(layers, l0, l1, (unsigned char*)ws, nullptr, gamma, (hipStream_t)stream);
+        if (st != KQ_OK) return st;
+    }
+    return KQ_OK;
 }
 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters, float* C,

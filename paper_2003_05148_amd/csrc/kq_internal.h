@@ -96,9 +96,15 @@ inline size_t ws_update_part(int64_t n, int32_t k) {
 inline size_t ws_hist(int64_t n, int32_t k) {
     return align256(sizeof(int64_t) * 10 * (size_t)k * (size_t)update_max_chunks(n, k));
 }
-inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n, k) + ws_hist(n, k); }
+// codebook gradient step: per-block maxima of |g| (fp32 bits) and the layer's fixed-point shift
+constexpr int kGradMaxPerBlock = 8192;  // gradient values per block of the |g| maximum
+inline int grad_max_blocks(int64_t n) { return (int)((n * kDim + kGradMaxPerBlock - 1) / kGradMaxPerBlock); }
+inline size_t ws_grad(int64_t n) { return align256(sizeof(unsigned) * ((size_t)grad_max_blocks(n) + 1)); }
+inline size_t layer_ws_bytes(int64_t n, int32_t k) {
+    return ws_assign_part(n) + ws_update_part(n, k) + ws_hist(n, k) + ws_grad(n);
+}
 
-enum : int { kFlagCountsOnly = 1 };
+enum : int { kFlagCountsOnly = 1, kFlagGrad = 2 };
 
 struct DevLayer {
     const float* X;
@@ -122,6 +128,9 @@ struct DevLayer {
     int krange;               // update: entries per range
     int chunk;                // update: kernels per chunk
     int nchunks;              // update: chunks (= partial histograms)
+    float gamma;              // gradient step: learning rate
+    unsigned* gmax;           // gradient step: per-block maxima of |g| as fp32 bits, then the shift
+    int ngmax;                // gradient step: number of those blocks
 };
 
 // Kernel arguments of a stack launch.  The first unit of every layer is repeated in a
@@ -180,6 +189,7 @@ hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_fill_zero(void* ws, size_t bytes, hipStream_t s);
+hipError_t launch_grad_absmax(const StackParams& p, hipStream_t s);
 
 struct CbqLayer {
     const float* C;

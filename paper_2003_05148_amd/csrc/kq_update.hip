@@ -18,6 +18,11 @@
 // ds_bpermute, added LDS work and ran slower.  Asked for the distortion of a standalone
 // assignment, it also sums, in a fixed order, the fp32 distances of its rows to their old
 // entries.
+// Codebook gradient step (Eq. 2): the same sums over a gradient tensor G instead of the
+// kernels, with a per-layer scale s = min(100, 62 - ceil(log2 n) - e) where 2^e > max |g|
+// (a first launch takes per-block maxima of |g|; every workgroup reduces them), so no sum
+// over at most n values can overflow and the relative resolution is the same for any
+// gradient magnitude; the finish then writes c - gamma * mean instead of the mean.
 // update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
 // groups of 40 threads add a sixteenth of the chunk partials each, eight loads in flight
 // per thread (any order gives the same integers), then it divides and writes the codebook
@@ -48,6 +53,16 @@ __device__ __forceinline__ unsigned long long fixed_point(float x, float scale) 
     const float hi = __builtin_floorf(v * 0x1p-32f);
     const float lo = __builtin_fmaf(hi, -0x1p32f, v);
     return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
+}
+
+// shift of the gradient sums: s = 62 - ceil(log2 n) - e with max |g| < 2^e, i.e. the kernel
+// shift (57 - ceil(log2 n), for |x| < 32 = 2^5) moved by 5 - e, kept in [-100, 100]
+__device__ __forceinline__ int grad_shift(float gmax, int kernel_shift) {
+    if (!(gmax > 0.0f)) return 100;
+    const int be = (int)((__float_as_uint(gmax) >> 23) & 255u);
+    const int e = be == 0 ? -126 : be - 126;  // gmax < 2^e (subnormal maxima: below 2^-126)
+    const int s = kernel_shift + 5 - e;
+    return s > 100 ? 100 : (s < -100 ? -100 : s);
 }
 
 struct UpdateCtx {
@@ -118,7 +133,19 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     c.s_sum = s_dyn;
     c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
-    c.scale = __builtin_ldexpf(1.0f, L.shift);
+    int shift = L.shift;
+    if (L.flags & kFlagGrad) {  // the scale of the gradient sums, from the per-block maxima of |g|
+        __shared__ unsigned s_mx;
+        if (tid == 0) s_mx = 0u;
+        __syncthreads();
+        unsigned m = 0u;
+        for (int q = tid; q < L.ngmax; q += kUpdateThreads) m = max(m, L.gmax[q]);
+        atomicMax(&s_mx, m);  // LDS; non-negative floats order as their bits
+        __syncthreads();
+        shift = grad_shift(__uint_as_float(s_mx), L.shift);
+        if (u == 0 && tid == 0) L.gmax[L.ngmax] = (unsigned)shift;  // for the finish
+    }
+    c.scale = __builtin_ldexpf(1.0f, shift);
     c.sums = (L.flags & kFlagCountsOnly) == 0;
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;
@@ -215,14 +242,54 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         if (d == 9) {
             if (L.counts) L.counts[j] = (int32_t)z;
         } else if ((L.flags & kFlagCountsOnly) == 0) {
-            float c;
-            if (z > 0)
+            const float old = L.C_old[(size_t)j * kDim + d];
+            float c = old;
+            if (z > 0 && (L.flags & kFlagGrad)) {  // Eq. (2): c - gamma * mean gradient
+                const int sh = (int)L.gmax[L.ngmax];
+                const double mean = ((double)S * ldexp(1.0, -sh)) / (double)z;
+                c = (float)((double)old - (double)L.gamma * mean);
+            } else if (z > 0) {
                 c = (float)(((double)S * ldexp(1.0, -L.shift)) / (double)z);
-            else
-                c = L.C_old[(size_t)j * kDim + d];
+            }
             L.C[(size_t)j * kDim + d] = c;
         }
     }
+}
+
+// per-block maximum of |g| over 8192 gradient values of a layer (fp32 bits)
+__global__ __launch_bounds__(256) void grad_absmax_kernel(const StackParams p) {
+    __shared__ unsigned s_mx;
+    const int li = find_layer(p, blockIdx.x);
+    const DevLayer& L = p.L[li];
+    const int b = blockIdx.x - L.unit_begin;
+    const long long count = (long long)L.n * kDim;
+    const long long base = (long long)b * kGradMaxPerBlock;
+    if (threadIdx.x == 0) s_mx = 0u;
+    __syncthreads();
+    float m = 0.0f;
+#pragma unroll 4
+    for (int q = threadIdx.x; q < kGradMaxPerBlock; q += 256) {
+        const long long e = base + q;
+        if (e < count) m = fmaxf(m, fabsf(L.X[e]));
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if ((threadIdx.x & 63) == 0) atomicMax(&s_mx, __float_as_uint(m));
+    __syncthreads();
+    if (threadIdx.x == 0) L.gmax[b] = s_mx;
+}
+
+hipError_t launch_grad_absmax(const StackParams& p, hipStream_t s) {
+    StackParams q = p;
+    int blk = 0;
+    for (int l = 0; l < q.nlayers; ++l) {
+        q.L[l].unit_begin = blk;
+        blk += q.L[l].ngmax;
+    }
+    q.total_units = blk;
+    set_unit_table(q);
+    hipLaunchKernelGGL(grad_absmax_kernel, dim3(blk), dim3(256), 0, s, q);
+    return hipGetLastError();
 }
 
 __global__ void fill_zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t ntail) {

@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 4
+    assert lib.kq_abi_version() == 5
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -233,3 +233,25 @@ def test_yinyang_workspace_and_argument_errors():
     assert fit(C=None) == kq.KQ_ERR_ARG
     assert fit(k=kq.KQ_MAX_K + 1) == kq.KQ_ERR_UNSUPPORTED
     assert fit(wsb=100) == kq.KQ_ERR_WORKSPACE
+
+
+def test_grad_step_argument_errors():
+    nb = lib.kq_workspace_bytes(kq.KQ_OP_GRAD, 100, 8)
+    assert nb == lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 100, 8) and nb > 0
+
+    def step(**kw):
+        a = dict(G=FAKE, n=100, dim=9, idx=FAKE, k=8, C0=FAKE, gamma=0.1, C=FAKE, z=None, ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_codebook_grad_step(a["G"], a["n"], a["dim"], a["idx"], a["k"], a["C0"], a["gamma"], a["C"],
+                                         a["z"], a["ws"], a["wsb"], None)
+
+    assert step(dim=3) == kq.KQ_ERR_UNSUPPORTED
+    assert step(k=kq.KQ_MAX_K + 1) == kq.KQ_ERR_UNSUPPORTED
+    assert step(gamma=float("nan")) == kq.KQ_ERR_ARG
+    assert step(gamma=float("inf")) == kq.KQ_ERR_ARG
+    assert step(G=None) == kq.KQ_ERR_ARG
+    assert step(C=FAKE + 1) == kq.KQ_ERR_ARG
+    assert step(z=FAKE + 2) == kq.KQ_ERR_ARG
+    assert step(n=0) == kq.KQ_ERR_ARG
+    assert step(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_codebook_grad_step_stack(None, 1, 0.1, FAKE, nb, None) == kq.KQ_ERR_ARG

@@ -16,6 +16,8 @@
  *                        gradient of each entry's kernels.
  *   kq_quantize_codebook Sec. 3.2: 6-bit quantization of all scalars of a layer's codebook,
  *                        k-means weighted by how often each entry is used.
+ *   kq_quantize_scalars  end of Sec. 3.2: the same k-means quantization on the scalars of a
+ *                        fully-connected layer (any size).
  *   kq_pack_bits         Eq. (4): the n * ceil(log2 k)-bit index stream.
  *   kq_reconstruct       end of Sec. 3.2: recover the weight tensor from codebook + indices.
  *
@@ -190,6 +192,28 @@ kq_status kq_codebook_grad_step(const float* G, int64_t n, int32_t dim, const in
                                 size_t ws_bytes, void* stream);
 kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, float gamma, void* ws,
                                       size_t ws_bytes, void* stream);
+
+/*
+ * kq_quantize_scalars -- end of Sec. 3.2: the 6-bit quantization of a fully-connected
+ * layer "with the same k-means clustering method" as the codebooks, i.e. the algorithm of
+ * kq_quantize_codebook (KQ_CBQ_WKMEANS) on one flat set of `count` scalars, every weight 1,
+ * for sets far larger than a codebook (a VGG-16 fc6 weight has 102,760,448 scalars).
+ *
+ *   Grid on [min, max], codes = nearest level (smallest index on ties), then up to
+ *   `iters` rounds of: level q = fp32(exact sum of its scalars rounded once to fp64 /
+ *   their count) (kept when empty), recompute the codes; stop early after a round that
+ *   changes no code.  iters = 0 gives the uniform grid alone.  The sums are exact, so the
+ *   result is a pure function of v: bit for bit that of kq_quantize_codebook on the same
+ *   scalars with unit weights.
+ *   v device [count] fp32 (finite); codes device [count] uint8; levels device [2^bits] fp32;
+ *   v_hat device [count] (= levels[codes], may be NULL); rounds device int32 (level updates
+ *   made, may be NULL).  1 <= count < 2^31; bits 1..8 (else KQ_ERR_UNSUPPORTED).
+ *   workspace: kq_quantize_scalars_workspace_bytes(count, bits).
+ */
+size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits);
+kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32_t iters, uint8_t* codes,
+                              float* levels, float* v_hat, int32_t* rounds, void* ws, size_t ws_bytes,
+                              void* stream);
 
 /*
  * Yinyang assignment -- Sec. 4.1: the paper runs its kernel-level k-means with Yinyang

@@ -14,6 +14,8 @@ What each function follows in the paper:
   scalars, weighted by how often each codebook entry is used.
 * ``codebook_grad_step`` -- retraining of the kernel codebook, Sec. 3.1, Eq. (2):
   every entry moves against the mean gradient of the kernels mapped to it.
+* ``quantize_scalars`` -- the same quantizer on the scalars of a fully-connected
+  layer (end of Sec. 3.2), every weight 1.
 * ``pack_bits`` -- the n * ceil(log2 k)-bit index stream counted by Eq. (4).
 * ``reconstruct`` -- test-time recovery of the weight tensor from the codebook
   and the indices (end of Sec. 3.2).
@@ -258,6 +260,19 @@ def cbq_wkmeans(C, weights, bits: int = 6, iters: int = 30):
         if not changed:
             break
     return codes, levels, levels[codes].reshape(C.shape), rounds
+
+
+def quantize_scalars(v, bits: int = 6, iters: int = 30):
+    """Quantization of a fully-connected layer (end of Sec. 3.2), done "with the same
+    layer by layer k-means clustering method" as the codebooks: the k-means of
+    ``cbq_wkmeans`` on one flat set of scalars, every scalar carrying weight 1 (an FC
+    weight is a parameter of its own, so there is no appearance count to weigh with).
+
+    Returns (codes uint8 [m], levels float32 [2^bits], v_hat float32 [m], rounds).
+    """
+    v = np.ascontiguousarray(np.asarray(v, np.float32).reshape(-1, 1))
+    codes, levels, v_hat, rounds = cbq_wkmeans(v, np.ones(v.shape[0], np.int64), bits, iters)
+    return codes, levels, v_hat.reshape(-1), rounds
 
 
 # ---- Eq. (4): the packed index stream, and test-time reconstruction ---------------------

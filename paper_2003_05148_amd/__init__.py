@@ -10,7 +10,7 @@ fallback: without the built library, importing this package raises ImportError.
 Entry points (same names as the C ABI):
   kq_assign, kq_update, kq_fit_layer, kq_assign_stack, kq_update_stack, kq_fit_stack,
   kq_fit_layer_yinyang (and the Yinyang class over kq_yinyang_init / kq_yinyang_assign),
-  kq_codebook_grad_step, kq_codebook_grad_step_stack,
+  kq_codebook_grad_step, kq_codebook_grad_step_stack, kq_quantize_scalars,
   kq_quantize_codebook, kq_quantize_codebook_stack, kq_pack_bits, kq_unpack_bits,
   kq_reconstruct, kq_reconstruct_packed.
 """
@@ -77,6 +77,8 @@ def _load():
         "kq_reconstruct_stack": ([_P, _I32, _P, _SZ, _P], _I32),
         "kq_codebook_grad_step": ([_P, _I64, _I32, _P, _I32, _P, ctypes.c_float, _P, _P, _P, _SZ, _P], _I32),
         "kq_codebook_grad_step_stack": ([_P, _I32, ctypes.c_float, _P, _SZ, _P], _I32),
+        "kq_quantize_scalars_workspace_bytes": ([_I64, _I32], _SZ),
+        "kq_quantize_scalars": ([_P, _I64, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_yinyang_workspace_bytes": ([_I64, _I32, _I32], _SZ),
         "kq_yinyang_init": ([_P, _I64, _I32, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_yinyang_assign": ([_P, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
@@ -106,7 +108,8 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error",
             "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
             "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang",
-            "kq_codebook_grad_step", "kq_codebook_grad_step_stack"]
+            "kq_codebook_grad_step", "kq_codebook_grad_step_stack", "kq_quantize_scalars_workspace_bytes",
+            "kq_quantize_scalars"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -326,6 +329,38 @@ def kq_codebook_grad_step_stack(stack, gamma: float):
     _check(lib.kq_codebook_grad_step_stack(ctypes.cast(stack.layers, _P), stack.n_layers, float(gamma),
                                            stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)),
            "kq_codebook_grad_step_stack")
+
+
+def kq_quantize_scalars(v, bits: int = 6, iters: int = 30, codes=None, levels=None, v_hat=None, rounds=None,
+                        workspace=None, want_v_hat: bool = True):
+    """k-means quantization of every scalar of a (fully-connected) weight tensor with
+    2^bits levels, the codebook quantizer's method with unit weights (end of Sec. 3.2).
+    Returns (codes uint8 [m], levels float32 [2^bits], v_hat float32 [m] or None,
+    rounds int32 [1])."""
+    if not isinstance(v, torch.Tensor) or not v.is_cuda or v.dtype != torch.float32 or not v.is_contiguous():
+        raise TypeError("v must be a contiguous float32 CUDA (HIP) tensor")
+    v = v.reshape(-1)
+    m = v.numel()
+    dev = v.device
+    codes = codes if codes is not None else torch.empty(m, dtype=torch.uint8, device=dev)
+    levels = levels if levels is not None else torch.empty(1 << bits, dtype=torch.float32, device=dev)
+    if want_v_hat:
+        v_hat = v_hat if v_hat is not None else torch.empty(m, dtype=torch.float32, device=dev)
+        _dev(v_hat, torch.float32, "v_hat", (m,))
+    else:
+        v_hat = None
+    rounds = rounds if rounds is not None else torch.zeros(1, dtype=torch.int32, device=dev)
+    _dev(codes, torch.uint8, "codes", (m,))
+    _dev(levels, torch.float32, "levels", (1 << bits,))
+    _dev(rounds, torch.int32, "rounds", (1,))
+    nb = lib.kq_quantize_scalars_workspace_bytes(m, bits)
+    if nb == 0:
+        raise ValueError(f"unsupported size {m} or bits {bits}")
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    _check(lib.kq_quantize_scalars(v.data_ptr(), m, bits, iters, codes.data_ptr(), levels.data_ptr(), _ptr(v_hat),
+                                   rounds.data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)),
+           "kq_quantize_scalars")
+    return codes, levels, v_hat, rounds
 
 
 def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):

@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 5;
+constexpr int32_t kAbiVersion = 6;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -397,6 +397,47 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
         if (st != KQ_OK) return st;
     }
     return KQ_OK;
+}
+
+size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits) {
+    if (count < 1 || count >= (int64_t(1) << 31) || bits < 1 || bits > 8) return 0;
+    return fc_ws_bytes(count, bits);
+}
+
+kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32_t iters, uint8_t* codes,
+                              float* levels, float* v_hat, int32_t* rounds, void* ws, size_t ws_bytes, void* stream) {
+    if (bits < 1 || bits > 8) return KQ_ERR_UNSUPPORTED;
+    if (count < 1 || count >= (int64_t(1) << 31) || iters < 0) return KQ_ERR_ARG;
+    if (!v || !codes || !levels || !aligned(v, 4) || !aligned(levels, 4)) return KQ_ERR_ARG;
+    if ((v_hat && !aligned(v_hat, 4)) || (rounds && !aligned(rounds, 4))) return KQ_ERR_ARG;
+    const kq_status w = check_ws(ws, ws_bytes, fc_ws_bytes(count, bits));
+    if (w != KQ_OK) return w;
+    const size_t G = (size_t)fc_grid(count), nlev = (size_t)1 << bits;
+    unsigned char* b = (unsigned char*)ws;
+    FcParams p;
+    memset(&p, 0, sizeof(p));
+    p.v = v;
+    p.codes = codes;
+    p.levels_out = levels;
+    p.v_hat = v_hat;
+    p.rounds_out = rounds;
+    p.m = count;
+    p.bits = bits;
+    p.iters = iters;
+    p.minmax = (float*)b;
+    b += align256(sizeof(float) * 2 * G);
+    p.part = (long long*)b;
+    b += align256(sizeof(long long) * G * nlev * 12);
+    p.S = (long long*)b;
+    b += align256(sizeof(long long) * nlev * 12);
+    p.lev = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.lev_next = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.state = (int*)b;
+    b += align256(sizeof(int) * 4);
+    p.wg_changed = (int*)b;
+    return hip_status(launch_fc_quantize(p, (hipStream_t)stream));
 }
 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters, float* C,

@@ -268,6 +268,241 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     }
 }
 
+// ---- large scalar sets (the fully-connected layers, end of Sec. 3.2) ---------------------
+// The same method on one flat vector of m scalars, every weight 1, spread over a
+// persistent grid.  Per round:
+//   fc_assign_kernel  every workgroup codes its scalars against the current levels (LDS)
+//                     and adds, in LDS, the exact contributions it moves: in the first
+//                     pass every scalar's, later only those of scalars whose code changed
+//                     (subtracted from the old level, added to the new); it stores the
+//                     per-level digits and counts as its partial and whether it changed
+//                     any code;
+//   fc_sum_kernel     one workgroup per level adds the partials to the level's running
+//                     exact sum and forms the candidate level fp32(round64(sum) / count);
+//   fc_state_kernel   one workgroup: a round that changed no code ends the run (every
+//                     later launch returns at once); otherwise the candidates become the
+//                     levels while fewer than `iters` updates were made.
+// Integer sums make the levels, and with them the codes, independent of the grid and the
+// order of the work: the result is the single-workgroup quantizer's, bit for bit.
+constexpr int kFcCols = kDigits + 1;  // digits, then the count
+
+__device__ __forceinline__ bool fc_done(const FcParams& p) { return p.state[0] != 0; }
+
+__global__ __launch_bounds__(kFcThreads) void fc_minmax_kernel(const FcParams p) {
+    __shared__ float s_lo[kFcThreads / kWave], s_hi[kFcThreads / kWave];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads) {
+        const float x = p.v[r];
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, off));
+        hi = fmaxf(hi, __shfl_xor(hi, off));
+    }
+    if (lane == 0) {
+        s_lo[wave] = lo;
+        s_hi[wave] = hi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < kFcThreads / kWave; ++w) {
+            lo = fminf(lo, s_lo[w]);
+            hi = fmaxf(hi, s_hi[w]);
+        }
+        p.minmax[2 * blockIdx.x] = fminf(lo, s_lo[0]);
+        p.minmax[2 * blockIdx.x + 1] = fmaxf(hi, s_hi[0]);
+    }
+}
+
+// the uniform grid on [min, max]; clears the run state and the running sums
+__global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p, int nblk) {
+    __shared__ float s_lo, s_hi;
+    __shared__ float s_lev[kCbqMaxLevels];
+    __shared__ int s_unsorted;
+    const int tid = threadIdx.x, nlev = 1 << p.bits;
+    if (tid == 0) {
+        float lo = __builtin_inff(), hi = -__builtin_inff();
+        for (int b = 0; b < nblk; ++b) {
+            lo = fminf(lo, p.minmax[2 * b]);
+            hi = fmaxf(hi, p.minmax[2 * b + 1]);
+        }
+        s_lo = lo;
+        s_hi = hi;
+        s_unsorted = 0;
+        p.state[0] = 0;  // not converged
+        p.state[1] = 0;  // level updates made
+    }
+    __syncthreads();
+    if (tid < nlev) {
+        const double delta = ((double)s_hi - (double)s_lo) / (double)(nlev - 1);
+        s_lev[tid] = (float)__dadd_rn((double)s_lo, __dmul_rn((double)tid, delta));
+        p.lev[tid] = s_lev[tid];
+    }
+    for (int e = tid; e < nlev * kFcCols; e += blockDim.x) p.S[e] = 0ll;
+    __syncthreads();
+    if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
+    __syncthreads();
+    if (tid == 0) p.state[2] = s_unsorted;
+}
+
+template <bool INIT>
+__global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p) {
+    __shared__ float s_lev[kCbqMaxLevels];
+    __shared__ unsigned long long s_dig[kCbqMaxLevels * kFcCols];
+    __shared__ int s_changed;
+    if (fc_done(p)) return;
+    const int tid = threadIdx.x, nlev = 1 << p.bits;
+    for (int e = tid; e < nlev; e += kFcThreads) s_lev[e] = p.lev[e];
+    for (int e = tid; e < nlev * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
+    if (tid == 0) s_changed = 0;
+    __syncthreads();
+    const bool sorted = p.state[2] == 0;
+    int changed = 0;
+    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads) {
+        const float x = p.v[r];
+        const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
+        if (INIT) {
+            p.codes[r] = (uint8_t)q;
+            add_exact(s_dig + q * kFcCols, x, 1u);
+            atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+        } else {
+            const int c = p.codes[r];
+            if (q != c) {
+                p.codes[r] = (uint8_t)q;
+                add_exact(s_dig + c * kFcCols, -x, 1u);
+                add_exact(s_dig + q * kFcCols, x, 1u);
+                atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)-1ll);
+                atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+                changed = 1;
+            }
+        }
+    }
+    if (changed) s_changed = 1;
+    __syncthreads();
+    unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * nlev * kFcCols;
+    for (int e = tid; e < nlev * kFcCols; e += kFcThreads) part[e] = s_dig[e];
+    if (tid == 0) p.wg_changed[blockIdx.x] = INIT ? 1 : s_changed;
+}
+
+// one workgroup per level: running exact sum += the partials; candidate level
+__global__ __launch_bounds__(kFcThreads) void fc_sum_kernel(const FcParams p, int nblk) {
+    __shared__ long long s_acc[kFcThreads / kWave][kFcCols];
+    if (fc_done(p)) return;
+    const int q = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nlev = 1 << p.bits;
+    long long a[kFcCols];
+#pragma unroll
+    for (int c = 0; c < kFcCols; ++c) a[c] = 0;
+    for (int b = tid; b < nblk; b += kFcThreads) {
+        const long long* src = p.part + ((size_t)b * nlev + q) * kFcCols;
+#pragma unroll
+        for (int c = 0; c < kFcCols; ++c) a[c] += src[c];
+    }
+#pragma unroll
+    for (int c = 0; c < kFcCols; ++c) {
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) a[c] += __shfl_xor(a[c], off);
+    }
+    if (lane == 0)
+        for (int c = 0; c < kFcCols; ++c) s_acc[wave][c] = a[c];
+    __syncthreads();
+    if (tid == 0) {
+        unsigned long long S[kDigits];
+        long long W = p.S[q * kFcCols + kDigits];
+        for (int c = 0; c < kFcCols; ++c) {
+            long long t = 0;
+            for (int w = 0; w < kFcThreads / kWave; ++w) t += s_acc[w][c];
+            if (c < kDigits) {
+                const long long v = p.S[q * kFcCols + c] + t;
+                p.S[q * kFcCols + c] = v;
+                S[c] = (unsigned long long)v;
+            } else {
+                W += t;
+                p.S[q * kFcCols + kDigits] = W;
+            }
+        }
+        p.lev_next[q] = W > 0 ? (float)(digits_to_double(S) / (double)W) : p.lev[q];
+    }
+}
+
+// run state: stop after a round without a changed code, else take the candidates
+__global__ __launch_bounds__(kCbqMaxLevels) void fc_state_kernel(const FcParams p, int nblk) {
+    __shared__ int s_any, s_unsorted;
+    __shared__ float s_lev[kCbqMaxLevels];
+    if (fc_done(p)) return;
+    const int tid = threadIdx.x, nlev = 1 << p.bits;
+    if (tid == 0) {
+        s_any = 0;
+        s_unsorted = 0;
+    }
+    __syncthreads();
+    for (int b = tid; b < nblk; b += blockDim.x)
+        if (p.wg_changed[b]) s_any = 1;
+    __syncthreads();
+    const bool update = s_any && p.state[1] < p.iters;
+    if (update && tid < nlev) {
+        s_lev[tid] = p.lev_next[tid];
+        p.lev[tid] = s_lev[tid];
+    }
+    __syncthreads();
+    if (update && tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
+    __syncthreads();
+    if (tid == 0) {
+        if (update) {
+            p.state[1] += 1;
+            p.state[2] = s_unsorted;
+        } else {
+            p.state[0] = 1;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kFcThreads) void fc_output_kernel(const FcParams p) {
+    __shared__ float s_lev[kCbqMaxLevels];
+    const int tid = threadIdx.x, nlev = 1 << p.bits;
+    for (int e = tid; e < nlev; e += kFcThreads) s_lev[e] = p.lev[e];
+    __syncthreads();
+    if (blockIdx.x == 0) {
+        for (int e = tid; e < nlev; e += kFcThreads) p.levels_out[e] = s_lev[e];
+        if (tid == 0 && p.rounds_out) *p.rounds_out = p.state[1];
+    }
+    if (!p.v_hat) return;
+    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads)
+        p.v_hat[r] = s_lev[p.codes[r]];
+}
+
+int fc_grid(long long m) {
+    const long long b = (m + kFcThreads - 1) / kFcThreads;
+    return (int)(b < kFcGrid ? (b < 1 ? 1 : b) : kFcGrid);
+}
+
+hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s) {
+    const int G = fc_grid(p.m), nlev = 1 << p.bits;
+    hipLaunchKernelGGL(fc_minmax_kernel, dim3(G), dim3(kFcThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fc_grid_kernel, dim3(1), dim3(kCbqMaxLevels), 0, s, p, G);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the initial codes and sums, then `iters` rounds of (levels, codes)
+    for (int r = 0; r <= p.iters; ++r) {
+        if (r == 0)
+            hipLaunchKernelGGL(fc_assign_kernel<true>, dim3(G), dim3(kFcThreads), 0, s, p);
+        else
+            hipLaunchKernelGGL(fc_assign_kernel<false>, dim3(G), dim3(kFcThreads), 0, s, p);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (r == p.iters) break;  // the last codes need no further levels
+        hipLaunchKernelGGL(fc_sum_kernel, dim3(nlev), dim3(kFcThreads), 0, s, p, G);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(fc_state_kernel, dim3(1), dim3(kCbqMaxLevels), 0, s, p, G);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(fc_output_kernel, dim3(G), dim3(kFcThreads), 0, s, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_cbq(const CbqParams& p, hipStream_t s) {
     int mmax = 0;
     for (int l = 0; l < p.nlayers; ++l) mmax = p.L[l].k * kDim > mmax ? p.L[l].k * kDim : mmax;

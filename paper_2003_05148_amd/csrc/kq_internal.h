@@ -208,6 +208,34 @@ struct CbqParams {
 };
 hipError_t launch_cbq(const CbqParams& p, hipStream_t s);
 
+// 2^bits-level k-means over one large flat set of scalars (fully-connected layers)
+constexpr int kFcThreads = 256;
+constexpr int kFcGrid = 1024;  // persistent workgroups
+struct FcParams {
+    const float* v;
+    uint8_t* codes;
+    float* levels_out;
+    float* v_hat;          // levels[codes], or null
+    int32_t* rounds_out;   // level updates made, or null
+    long long m;
+    int bits, iters;
+    float* minmax;         // [grid][2] per-workgroup min, max
+    long long* part;       // [grid][levels][12] per-workgroup digits and counts
+    long long* S;          // [levels][12] running exact sums and counts
+    float* lev;            // [levels] current levels
+    float* lev_next;       // [levels] candidate levels
+    int* state;            // [0] converged, [1] level updates made, [2] levels unsorted
+    int* wg_changed;       // [grid] a code changed in the workgroup
+};
+int fc_grid(long long m);
+inline size_t fc_ws_bytes(long long m, int bits) {
+    const size_t G = (size_t)fc_grid(m), nlev = (size_t)1 << bits;
+    return align256(sizeof(float) * 2 * G) + align256(sizeof(long long) * G * nlev * 12) +
+           align256(sizeof(long long) * nlev * 12) + 2 * align256(sizeof(float) * nlev) + align256(sizeof(int) * 4) +
+           align256(sizeof(int) * G);
+}
+hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s);
+
 // stack forms of pack and reconstruct (+ squared error): a compact unit table first
 struct PackJob {
     const void* v;

@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 5
+    assert lib.kq_abi_version() == 6
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -255,3 +255,25 @@ def test_grad_step_argument_errors():
     assert step(n=0) == kq.KQ_ERR_ARG
     assert step(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE
     assert lib.kq_codebook_grad_step_stack(None, 1, 0.1, FAKE, nb, None) == kq.KQ_ERR_ARG
+
+
+def test_quantize_scalars_argument_errors():
+    nb = lib.kq_quantize_scalars_workspace_bytes(1000, 6)
+    assert nb > 0 and lib.kq_quantize_scalars_workspace_bytes(1000, 9) == 0
+    assert lib.kq_quantize_scalars_workspace_bytes(0, 6) == 0
+    assert lib.kq_quantize_scalars_workspace_bytes(1 << 31, 6) == 0
+
+    def q(**kw):
+        a = dict(v=FAKE, m=1000, bits=6, it=30, codes=FAKE, lev=FAKE, vh=None, r=None, ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_quantize_scalars(a["v"], a["m"], a["bits"], a["it"], a["codes"], a["lev"], a["vh"], a["r"],
+                                       a["ws"], a["wsb"], None)
+
+    assert q(bits=0) == kq.KQ_ERR_UNSUPPORTED
+    assert q(bits=9) == kq.KQ_ERR_UNSUPPORTED
+    assert q(m=0) == kq.KQ_ERR_ARG
+    assert q(it=-1) == kq.KQ_ERR_ARG
+    assert q(v=None) == kq.KQ_ERR_ARG
+    assert q(lev=FAKE + 2) == kq.KQ_ERR_ARG
+    assert q(vh=FAKE + 1) == kq.KQ_ERR_ARG
+    assert q(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE

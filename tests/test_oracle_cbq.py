@@ -103,3 +103,29 @@ def test_wkmeans_matches_sklearn(weighted):
     km.fit(v, sample_weight=np.repeat(w, 9).astype(np.float64))
     assert np.array_equal(km.labels_, codes)
     assert np.allclose(km.cluster_centers_[:, 0], levels, rtol=1e-6, atol=1e-7)
+
+
+def test_fc_quantizer_is_the_unit_weight_codebook_quantizer():
+    """The fully-connected form (end of Sec. 3.2) runs the same k-means on a flat set with
+    every weight 1: arranged as rows of 9 with unit appearance counts it is identical."""
+    rng = np.random.default_rng(21)
+    v = (rng.laplace(0.0, 0.02, 9 * 700)).astype(np.float32)
+    a = oracle.quantize_scalars(v, 6, 30)
+    b = oracle.cbq_wkmeans(v.reshape(-1, 9), np.ones(700, np.int64), 6, 30)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[3] == b[3]
+    assert np.array_equal(a[2], b[2].reshape(-1))
+
+
+def test_fc_quantizer_matches_sklearn_lloyd_from_the_grid():
+    """Unit weights reduce the method to plain 1-D Lloyd from the uniform grid: with data
+    dense enough that no level empties, scikit-learn's Lloyd reaches the same partition."""
+    from sklearn.cluster import KMeans
+    rng = np.random.default_rng(22)
+    v = (rng.standard_normal(4000) * 0.05).astype(np.float32)
+    codes, levels, v_hat, rounds = oracle.quantize_scalars(v, 3, 500)
+    grid = oracle.uniform_levels(float(v.min()), float(v.max()), 3).astype(np.float64)
+    km = KMeans(n_clusters=8, init=grid.reshape(-1, 1), n_init=1, max_iter=1000, tol=0.0,
+                algorithm="lloyd").fit(v.astype(np.float64).reshape(-1, 1))
+    assert rounds < 500                                         # converged
+    assert np.array_equal(km.labels_, codes.astype(np.int64))
+    assert np.allclose(km.cluster_centers_.reshape(-1), levels.astype(np.float64), rtol=1e-6, atol=1e-9)

@@ -348,33 +348,87 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p
     if (tid == 0) p.state[2] = s_unsorted;
 }
 
-template <bool INIT>
+// Nearest level of x among NLEV sorted levels (the answer of nearest_sorted): the number
+// of levels below x from every eighth level (registers) and one block of eight (LDS), then
+// the exact fp64 comparison of the two neighbours, walking down over equal distances.
+template <int NLEV>
+__device__ __forceinline__ int nearest_sorted_fast(float x, const float* s_lev, const float (&coarse)[NLEV / 8 + 1]) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    int q0;
+    if (NLEV >= 8) {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] < x ? 1 : 0;
+        if (c == NLEV / 8) {
+            q0 = NLEV;  // the last level is below x, and with it every level
+        } else {
+            const f32x4 a = reinterpret_cast<const f32x4*>(s_lev)[2 * c];
+            const f32x4 b = reinterpret_cast<const f32x4*>(s_lev)[2 * c + 1];
+            q0 = 8 * c + (a[0] < x) + (a[1] < x) + (a[2] < x) + (a[3] < x) + (b[0] < x) + (b[1] < x) + (b[2] < x) +
+                 (b[3] < x);
+        }
+    } else {
+        q0 = 0;
+#pragma unroll
+        for (int i = 0; i < NLEV; ++i) q0 += s_lev[i] < x ? 1 : 0;
+    }
+    const double vd = (double)x;
+    int q = q0;
+    const double da = q0 < NLEV ? fabs(vd - (double)s_lev[q0]) : __builtin_inf();
+    if (q0 > 0) {
+        int bq = q0 - 1;
+        const double db = fabs(vd - (double)s_lev[bq]);
+        while (bq > 0 && fabs(vd - (double)s_lev[bq - 1]) == db) --bq;
+        if (db <= da) q = bq;
+    }
+    return q;
+}
+
+// Each thread takes four scalars per step (r0 + 256 j, consecutive lanes consecutive
+// scalars), their loads issued together.
+template <bool INIT, int NLEV>
 __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p) {
-    __shared__ float s_lev[kCbqMaxLevels];
-    __shared__ unsigned long long s_dig[kCbqMaxLevels * kFcCols];
+    __shared__ __attribute__((aligned(16))) float s_lev[NLEV < 8 ? 8 : NLEV];
+    __shared__ unsigned long long s_dig[NLEV * kFcCols];
     __shared__ int s_changed;
     if (fc_done(p)) return;
-    const int tid = threadIdx.x, nlev = 1 << p.bits;
-    for (int e = tid; e < nlev; e += kFcThreads) s_lev[e] = p.lev[e];
-    for (int e = tid; e < nlev * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
+    const int tid = threadIdx.x;
+    for (int e = tid; e < NLEV; e += kFcThreads) s_lev[e] = p.lev[e];
+    for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
     if (tid == 0) s_changed = 0;
     __syncthreads();
     const bool sorted = p.state[2] == 0;
+    float coarse[NLEV / 8 + 1];
+#pragma unroll
+    for (int i = 0; i < NLEV / 8; ++i) coarse[i] = s_lev[8 * i + 7];
+    coarse[NLEV / 8] = 0.0f;
     int changed = 0;
-    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads) {
-        const float x = p.v[r];
-        const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
-        if (INIT) {
-            p.codes[r] = (uint8_t)q;
-            add_exact(s_dig + q * kFcCols, x, 1u);
-            atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
-        } else {
-            const int c = p.codes[r];
-            if (q != c) {
+    constexpr int kPer = 4;
+    const long long m = p.m;
+    const long long step = (long long)gridDim.x * kFcThreads * kPer;
+    for (long long r0 = (long long)blockIdx.x * kFcThreads * kPer + tid; r0 < m; r0 += step) {
+        float x[kPer];
+        int c[kPer];
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const long long r = r0 + (long long)j * kFcThreads;
+            x[j] = r < m ? p.v[r] : 0.0f;
+            c[j] = (!INIT && r < m) ? (int)p.codes[r] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const long long r = r0 + (long long)j * kFcThreads;
+            if (r >= m) continue;
+            const int q = sorted ? nearest_sorted_fast<NLEV>(x[j], s_lev, coarse) : nearest_level(x[j], s_lev, NLEV);
+            if (INIT) {
                 p.codes[r] = (uint8_t)q;
-                add_exact(s_dig + c * kFcCols, -x, 1u);
-                add_exact(s_dig + q * kFcCols, x, 1u);
-                atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)-1ll);
+                add_exact(s_dig + q * kFcCols, x[j], 1u);
+                atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+            } else if (q != c[j]) {
+                p.codes[r] = (uint8_t)q;
+                add_exact(s_dig + c[j] * kFcCols, -x[j], 1u);
+                add_exact(s_dig + q * kFcCols, x[j], 1u);
+                atomicAdd(&s_dig[c[j] * kFcCols + kDigits], (unsigned long long)-1ll);
                 atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
                 changed = 1;
             }
@@ -382,9 +436,31 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     }
     if (changed) s_changed = 1;
     __syncthreads();
-    unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * nlev * kFcCols;
-    for (int e = tid; e < nlev * kFcCols; e += kFcThreads) part[e] = s_dig[e];
+    unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * NLEV * kFcCols;
+    for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) part[e] = s_dig[e];
     if (tid == 0) p.wg_changed[blockIdx.x] = INIT ? 1 : s_changed;
+}
+
+template <bool INIT>
+hipError_t launch_fc_assign(const FcParams& p, int G, hipStream_t s) {
+    switch (p.bits) {
+#define KQ_FC_CASE(B)                                                                                    \
+    case B:                                                                                              \
+        hipLaunchKernelGGL((fc_assign_kernel<INIT, (1 << B)>), dim3(G), dim3(kFcThreads), 0, s, p); \
+        break;
+        KQ_FC_CASE(1)
+        KQ_FC_CASE(2)
+        KQ_FC_CASE(3)
+        KQ_FC_CASE(4)
+        KQ_FC_CASE(5)
+        KQ_FC_CASE(6)
+        KQ_FC_CASE(7)
+        KQ_FC_CASE(8)
+#undef KQ_FC_CASE
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 // one workgroup per level: running exact sum += the partials; candidate level
@@ -475,7 +551,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_output_kernel(const FcParams p)
 }
 
 int fc_grid(long long m) {
-    const long long b = (m + kFcThreads - 1) / kFcThreads;
+    const long long b = (m + 4 * kFcThreads - 1) / (4 * kFcThreads);
     return (int)(b < kFcGrid ? (b < 1 ? 1 : b) : kFcGrid);
 }
 
@@ -488,11 +564,8 @@ hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // the initial codes and sums, then `iters` rounds of (levels, codes)
     for (int r = 0; r <= p.iters; ++r) {
-        if (r == 0)
-            hipLaunchKernelGGL(fc_assign_kernel<true>, dim3(G), dim3(kFcThreads), 0, s, p);
-        else
-            hipLaunchKernelGGL(fc_assign_kernel<false>, dim3(G), dim3(kFcThreads), 0, s, p);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        e = r == 0 ? launch_fc_assign<true>(p, G, s) : launch_fc_assign<false>(p, G, s);
+        if (e != hipSuccess) return e;
         if (r == p.iters) break;  // the last codes need no further levels
         hipLaunchKernelGGL(fc_sum_kernel, dim3(nlev), dim3(kFcThreads), 0, s, p, G);
         if ((e = hipGetLastError()) != hipSuccess) return e;

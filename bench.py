@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--k", type=int, default=None, help="codebook size (default: the config's)")
     ap.add_argument("--yinyang", action="store_true",
                     help="run each layer's Lloyd rounds with Yinyang assignments (Sec. 4.1; the same result)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="run the update as its own pass over the kernels (the member sums are not fused "
+                         "into the assignment)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -147,6 +150,8 @@ def main():
               "sq_error": sq[i:i + 1]} for i, L in enumerate(layers)]
     recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
 
+    # the member sums come with the assignment when every codebook fits the fused variant
+    fused = max(L.k for L in layers) <= 256 and not args.unfused
     stream = torch.cuda.current_stream(dev)
     ev = {"assign": [], "update": [], "cbq": [], "pack": [], "reconstruct": [], "fit": []}
     if args.yinyang:
@@ -184,7 +189,7 @@ def main():
             if record:
                 a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-            kq.kq_assign_stack(st, dist_slot=t, distortion=False)
+            kq.kq_assign_stack(st, dist_slot=t, distortion=False, fused_sums=fused and t < T)
             if record:
                 a1.record(stream)
                 ev["assign"].append((a0, a1))
@@ -192,7 +197,7 @@ def main():
                 if record:
                     u0, u1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     u0.record(stream)
-                kq.kq_update_stack(st, dist_slot=t, distortion_from_assign=True)
+                kq.kq_update_stack(st, dist_slot=t, distortion_from_assign=True, sums_from_assign=fused)
                 if record:
                     u1.record(stream)
                     ev["update"].append((u0, u1))

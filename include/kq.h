@@ -84,6 +84,13 @@ typedef enum kq_status {
                              /* kq_update_stack: take the distortion from the partial sums the
                                 preceding kq_assign_stack on the same layers and workspace left
                                 (no second pass over the old codebook) */
+#define KQ_F_FUSED_SUMS 4u   /* kq_assign_stack: also accumulate the member sums of the new
+                                assignment (every k <= 256, else KQ_ERR_UNSUPPORTED) */
+#define KQ_F_SUMS_FROM_ASSIGN 8u
+                             /* kq_update_stack: finish the update from the sums the preceding
+                                kq_assign_stack with KQ_F_FUSED_SUMS left (same layers and
+                                workspace): the kernels are not read again; the distortion is
+                                the assignment's, as with KQ_F_DISTORTION_FROM_ASSIGN */
 
 /* One layer of a stack.  All pointers are device pointers. */
 typedef struct kq_layer {
@@ -269,6 +276,10 @@ kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k
  *                    kq_assign_stack computed, which is the same objective).
  *   kq_fit_stack:    kq_fit_layer on every layer (C in place, distortion [iters+1]).
  *   layers is a host array; the pointers in it are device pointers.
+ *   With every k <= 256, the fits (and kq_assign_stack with KQ_F_FUSED_SUMS followed by
+ *   kq_update_stack with KQ_F_SUMS_FROM_ASSIGN) add the member sums inside the assignment
+ *   and skip the update's second read of the kernels; the sums are the same integers, so
+ *   every output is the same bit for bit.
  */
 kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist_slot, uint32_t flags,
                           void* ws, size_t ws_bytes, void* stream);

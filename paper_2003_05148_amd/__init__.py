@@ -102,6 +102,8 @@ KQ_CBQ_WKMEANS, KQ_CBQ_UNIFORM = 0, 1
 KQ_OP_ASSIGN, KQ_OP_UPDATE, KQ_OP_FIT, KQ_OP_SQ_ERROR, KQ_OP_GRAD = 0, 1, 2, 3, 4
 KQ_F_COUNTS_ONLY = 1
 KQ_F_DISTORTION_FROM_ASSIGN = 2
+KQ_F_FUSED_SUMS = 4
+KQ_F_SUMS_FROM_ASSIGN = 8
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
@@ -415,29 +417,36 @@ class Stack:
             c.copy_(src)
 
 
-def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True):
-    """Assign every layer of the stack; the distortion (if asked) goes to slot dist_slot."""
+def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True, fused_sums: bool = False):
+    """Assign every layer of the stack; the distortion (if asked) goes to slot dist_slot.
+    fused_sums also accumulates the member sums of the new assignment (every k <= 256),
+    for a following kq_update_stack(..., sums_from_assign=True)."""
+    flags = KQ_F_FUSED_SUMS if fused_sums else 0
     if not distortion:
         saved = [(l.distortion) for l in stack.layers]
         for l in stack.layers:
             l.distortion = None
         try:
-            _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, 0,
+            _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, flags,
                                        stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)),
                    "kq_assign_stack")
         finally:
             for l, d in zip(stack.layers, saved):
                 l.distortion = d
         return
-    _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, 0, stack.ws.data_ptr(),
+    _check(lib.kq_assign_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, flags, stack.ws.data_ptr(),
                                stack.ws.numel(), _stream(stack.device)), "kq_assign_stack")
 
 
-def kq_update_stack(stack: Stack, dist_slot: int = 0, counts_only: bool = False, distortion_from_assign=False):
+def kq_update_stack(stack: Stack, dist_slot: int = 0, counts_only: bool = False, distortion_from_assign=False,
+                    sums_from_assign: bool = False):
     """Update every codebook of the stack.  The distortion of the assignment goes to slot
     dist_slot; with distortion_from_assign it is the value the preceding kq_assign_stack
-    left in the workspace (no second pass over the old codebook)."""
+    left in the workspace (no second pass over the old codebook).  With sums_from_assign
+    the update is finished from the member sums of the preceding fused assignment (the
+    kernels are not read again; the distortion then also comes from the assignment)."""
     flags = (KQ_F_COUNTS_ONLY if counts_only else 0) | (KQ_F_DISTORTION_FROM_ASSIGN if distortion_from_assign else 0)
+    flags |= KQ_F_SUMS_FROM_ASSIGN if sums_from_assign else 0
     _check(lib.kq_update_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, flags,
                                stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)), "kq_update_stack")
 

@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 6;
+constexpr int32_t kAbiVersion = 7;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -56,6 +56,7 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
         d.k = s.k;
         d.shift = fixed_shift(s.n);
         d.dist = s.distortion ? s.distortion + dist_slot : nullptr;
+        d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k));
         if (op == Op::Assign) {
             d.best_d = s.best_d;
             d.part = base ? (double*)w : nullptr;  // partials whenever there is a workspace
@@ -68,7 +69,6 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
             } else if (d.dist) {
                 d.part = (double*)(w + ws_assign_part(s.n));
             }
-            d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k));
             d.ranges = update_ranges(s.k);
             d.krange = (s.k + d.ranges - 1) / d.ranges;
             d.chunk = update_chunk(s.n, s.k, kpb);
@@ -108,20 +108,64 @@ bool any_distortion(const kq_layer* layers, int32_t l0, int32_t l1) {
     return false;
 }
 
-// assignment of layers [l0, l1) (+ the distortion finish when any layer asks for it)
-kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s) {
+bool fusable(const kq_layer* layers, int32_t l0, int32_t l1) {
+    for (int32_t l = l0; l < l1; ++l)
+        if (layers[l].k > kFuseMaxK) return false;
+    return true;
+}
+
+// The fused assignment's partials: with the persistent grid of the assignment launch over
+// layers [l0, l1), workgroup w walks tiles [w T / G, (w + 1) T / G); a layer's partials
+// are those of the workgroups whose runs touch its tiles.  For every layer: the first such
+// workgroup and their number.
+void fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, int* nslots) {
+    long long T = 0;
+    for (int32_t l = l0; l < l1; ++l) T += assign_tiles(layers[l].n);
+    const long long G = assign_grid((int)T);
+    long long b = 0;
+    for (int32_t l = l0; l < l1; ++l) {
+        const long long e = b + assign_tiles(layers[l].n);  // tiles [b, e)
+        long long w0 = b * G / T;                           // a first guess, then exact
+        while (w0 > 0 && w0 * T / G > b) --w0;
+        while ((w0 + 1) * T / G <= b) ++w0;
+        long long w1 = w0;
+        while ((w1 + 1) * T / G <= e - 1) ++w1;
+        wfirst[l - l0] = (int)w0;
+        nslots[l - l0] = (int)(w1 - w0 + 1);
+        b = e;
+    }
+}
+
+// assignment of layers [l0, l1) (+ the distortion finish when any layer asks for it);
+// `fused` also leaves the member sums of the new assignment in the workspace
+kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s,
+                     bool fused = false) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Assign, slot, nullptr, 0);
-    if (launch_assign(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (fused) {
+        int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
+        fused_slots(layers, l0, l1, wf, ns);
+        for (int l = 0; l < p.nlayers; ++l) p.L[l].wfirst = wf[l];
+    }
+    if (launch_assign(p, s, fused) != hipSuccess) return KQ_ERR_HIP;
     if (any_distortion(layers, l0, l1) && launch_assign_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;
 }
 
+// `sums_from_assign`: the preceding fused assignment of the same layers left the member
+// sums (and the distortion partials): only the finishing launch runs
 kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot,
-                     const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false) {
+                     const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false,
+                     bool sums_from_assign = false) {
     StackParams p;
-    stack_params(p, layers, l0, l1, ws, Op::Update, slot, C_old, kflags, from_assign);
-    if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
+    stack_params(p, layers, l0, l1, ws, Op::Update, slot, C_old, kflags, from_assign || sums_from_assign);
+    if (sums_from_assign) {
+        int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
+        fused_slots(layers, l0, l1, wf, ns);
+        for (int l = 0; l < p.nlayers; ++l) p.L[l].nchunks = ns[l];
+    } else if (launch_update(p, s) != hipSuccess) {
+        return KQ_ERR_HIP;
+    }
     if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;
 }
@@ -163,12 +207,13 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
         for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
         bool need_last = false;
         for (int32_t l = l0; l < l1; ++l) need_last |= layers[l].counts != nullptr || layers[l].distortion != nullptr;
+        const bool fused = fusable(layers, l0, l1);  // the member sums come with the assignment
         for (int32_t t = 0; t <= iters; ++t) {
-            kq_status st = run_assign(quiet, 0, l1 - l0, ws + off, 0, s);
-            if (st != KQ_OK) return st;
             const bool last = (t == iters);
+            kq_status st = run_assign(quiet, 0, l1 - l0, ws + off, 0, s, fused && !(last && !need_last));
+            if (st != KQ_OK) return st;
             if (last && !need_last) break;
-            st = run_update(layers, l0, l1, ws, t, nullptr, last ? kFlagCountsOnly : 0, s, true);
+            st = run_update(layers, l0, l1, ws, t, nullptr, last ? kFlagCountsOnly : 0, s, true, fused);
             if (st != KQ_OK) return st;
         }
     }
@@ -542,12 +587,14 @@ kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
                           size_t ws_bytes, void* stream) {
     kq_status st = check_layers(layers, n_layers, false);
     if (st != KQ_OK) return st;
-    if (dist_slot < 0 || flags != 0) return KQ_ERR_ARG;
+    if (dist_slot < 0 || (flags & ~KQ_F_FUSED_SUMS) != 0) return KQ_ERR_ARG;
+    const bool fused = (flags & KQ_F_FUSED_SUMS) != 0;
+    if (fused && !fusable(layers, 0, n_layers)) return KQ_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, (hipStream_t)stream);
+        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, (hipStream_t)stream, fused);
         if (st != KQ_OK) return st;
     }
     return KQ_OK;
@@ -557,14 +604,18 @@ kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
                           size_t ws_bytes, void* stream) {
     kq_status st = check_layers(layers, n_layers, false);
     if (st != KQ_OK) return st;
-    if (dist_slot < 0 || (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_DISTORTION_FROM_ASSIGN)) != 0) return KQ_ERR_ARG;
+    if (dist_slot < 0 ||
+        (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_DISTORTION_FROM_ASSIGN | KQ_F_SUMS_FROM_ASSIGN)) != 0)
+        return KQ_ERR_ARG;
+    const bool from_sums = (flags & KQ_F_SUMS_FROM_ASSIGN) != 0;
+    if (from_sums && !fusable(layers, 0, n_layers)) return KQ_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
         st = run_update(layers, l0, l1, (unsigned char*)ws, dist_slot, nullptr,
                         (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0, (hipStream_t)stream,
-                        (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0);
+                        (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0, from_sums);
         if (st != KQ_OK) return st;
     }
     return KQ_OK;

@@ -120,12 +120,38 @@ __device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d,
     d = lt ? od : d;
 }
 
-template <int R>
+// Fused variant (every codebook of at most kFuseMaxK entries): each lane also adds its
+// settled kernel to the workgroup's LDS histogram of exact fixed-point member sums, which
+// is stored as the partial of (layer, workgroup) whenever the workgroup's run of tiles
+// leaves a layer; the update then needs only its finishing launch.
+template <int CHUNK, bool FUSED>
+__device__ __forceinline__ void fused_flush(const StackParams& p, int l, unsigned long long* s_sum, unsigned* s_cnt,
+                                            int tid) {
+    __syncthreads();  // every wave has added its kernels
+    const DevLayer& H = p.L[l];
+    unsigned long long* out = (unsigned long long*)H.hist + (size_t)(blockIdx.x - H.wfirst) * H.k * 10;
+    for (int e = tid; e < H.k * 10; e += kAssignWaves * kWave) {
+        const int j = e / 10, d = e - 10 * j;
+        if (d == 9) {
+            out[e] = s_cnt[j];
+            s_cnt[j] = 0u;
+        } else {
+            out[e] = s_sum[j * kDim + d];
+            s_sum[j * kDim + d] = 0ull;
+        }
+    }
+    __syncthreads();  // cleared before the next kernels are added
+}
+
+template <int R, bool FUSED>
 __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kernel(const StackParams p) {
     static_assert(R == 2, "one kernel per lane and the half exchange need two kernel tiles per wave");
+    constexpr int kAssignChunk = FUSED ? kFuseChunk : ::kq::kAssignChunk;
     __shared__ u32x4 s_a[kAssignChunk / 32 * 2 * kWave];  // [tile][k-step][lane] A operands
     __shared__ f32x4 s_c[kAssignChunk * kRowFloats / 4];   // fp32 rows of the staged entries
     __shared__ float s_wmax[kAssignWaves];                 // per-wave max |c|^2 of the staged codebook
+    __shared__ unsigned long long s_sum[FUSED ? kFuseMaxK * kDim : 1];  // fused: member sums
+    __shared__ unsigned s_cnt[FUSED ? kFuseMaxK : 1];                   // fused: member counts
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
@@ -140,10 +166,20 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     float xo[kDim];   // this lane's kernel of the current tile
     load_kernel(p.L[li], t - p.unit_begin[li], wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
+    int hl = li;      // fused: the layer whose sums the histogram holds
+    if (FUSED) {
+        for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
+        for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
+        __syncthreads();
+    }
 
 #pragma unroll 1
     for (; t < t_end; ++t) {
         while (li + 1 < p.nlayers && t >= p.unit_begin[li + 1]) ++li;
+        if (FUSED && li != hl) {  // the run left layer hl: store its sums
+            fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
+            hl = li;
+        }
         const DevLayer& L = p.L[li];
         const int n = L.n, k = L.k;
         const float* __restrict__ C = L.C;
@@ -334,6 +370,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
 
         const bool sure = valid && (q2 < kTrustQ) && (rs - rb > theta) && (rj < k);
         float dist = 0.0f;
+        int myj = rj;  // the entry this lane's kernel ends with
         if (sure) {
             dist = rd;
             L.idx[i] = rj;
@@ -381,7 +418,15 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                 L.idx[i] = fj;
                 if (L.best_d) L.best_d[i] = fd;
                 dist = fd;
+                myj = fj;
             }
+        }
+
+        if (FUSED && valid) {  // the update's exact member sums of this kernel
+            const float sc = __builtin_ldexpf(1.0f, L.shift);
+            atomicAdd(&s_cnt[myj], 1u);
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_point(xo[d], sc));
         }
 
         if (L.part) {
@@ -394,6 +439,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xo[d] = xn[d];
     }
+    if (FUSED) fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
 }
 
 // distortion of each layer: its per-wave partials summed in a fixed order
@@ -405,9 +451,15 @@ __global__ __launch_bounds__(kSumThreads) void assign_finish_kernel(const StackP
     if (threadIdx.x == 0) *L.dist = v;
 }
 
-hipError_t launch_assign(const StackParams& p, hipStream_t s) {
-    const int grid = p.total_units < kAssignGridMax ? p.total_units : kAssignGridMax;
-    hipLaunchKernelGGL(assign_kernel<kAssignTilesPerWave>, dim3(grid), dim3(kAssignWaves * kWave), 0, s, p);
+int assign_grid(int total_units) { return total_units < kAssignGridMax ? total_units : kAssignGridMax; }
+
+hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused) {
+    const int grid = assign_grid(p.total_units);
+    if (fused)
+        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, true>), dim3(grid), dim3(kAssignWaves * kWave), 0, s, p);
+    else
+        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, false>), dim3(grid), dim3(kAssignWaves * kWave), 0, s,
+                           p);
     return hipGetLastError();
 }
 

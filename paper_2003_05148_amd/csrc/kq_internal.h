@@ -84,6 +84,26 @@ inline int fixed_shift(int64_t n) {
     return 57 - c;
 }
 
+// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is exact in fp32 (|x| * 2^s < 2^62,
+// a power-of-two scaling) and so is its rounding to an integer v; v = hi * 2^32 + lo with
+// hi = floor(v * 2^-32) (|hi| < 2^30) and 0 <= lo < 2^32, where lo = v - hi * 2^32 has
+// fewer significant bits than v and is exact in fp32 too, so both convert exactly.
+__device__ __forceinline__ unsigned long long fixed_point(float x, float scale) {
+    const float v = __builtin_rintf(x * scale);
+    const float hi = __builtin_floorf(v * 0x1p-32f);
+    const float lo = __builtin_fmaf(hi, -0x1p32f, v);
+    return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
+}
+
+// ---- fused assignment + member sums ------------------------------------------------------
+// With every codebook of at most kFuseMaxK entries, the assignment kernel can also add each
+// settled kernel to a per-workgroup LDS histogram of exact member sums (the update's
+// fixed-point sums) and store it per (layer, workgroup) as a partial, so the update needs
+// only its finishing launch.  A layer's partials are those of the workgroups whose tile
+// runs touch it: at most one per tile.
+constexpr int kFuseMaxK = 256;
+constexpr int kFuseChunk = 256;  // codebook entries staged at a time by the fused variant
+
 // ---- per-layer workspace ---------------------------------------------------------------
 //   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]           (overwritten each call)
 //   update distortion partials : fp64 [ranges * max chunks]                      (overwritten each call)
@@ -94,7 +114,9 @@ inline size_t ws_update_part(int64_t n, int32_t k) {
     return align256(sizeof(double) * (size_t)update_ranges(k) * (size_t)update_max_chunks(n, k));
 }
 inline size_t ws_hist(int64_t n, int32_t k) {
-    return align256(sizeof(int64_t) * 10 * (size_t)k * (size_t)update_max_chunks(n, k));
+    size_t parts = (size_t)update_max_chunks(n, k);
+    if (k <= kFuseMaxK && (size_t)assign_tiles(n) > parts) parts = (size_t)assign_tiles(n);  // fused partials
+    return align256(sizeof(int64_t) * 10 * (size_t)k * parts);
 }
 // codebook gradient step: per-block maxima of |g| (fp32 bits) and the layer's fixed-point shift
 constexpr int kGradMaxPerBlock = 8192;  // gradient values per block of the |g| maximum
@@ -131,6 +153,7 @@ struct DevLayer {
     float gamma;              // gradient step: learning rate
     unsigned* gmax;           // gradient step: per-block maxima of |g| as fp32 bits, then the shift
     int ngmax;                // gradient step: number of those blocks
+    int wfirst;               // fused assignment: first workgroup whose tiles touch the layer
 };
 
 // Kernel arguments of a stack launch.  The first unit of every layer is repeated in a
@@ -184,7 +207,8 @@ __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src
 constexpr int kSumThreads = 640;
 
 // launchers (return hipSuccess or the launch error)
-hipError_t launch_assign(const StackParams& p, hipStream_t s);
+hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused = false);
+int assign_grid(int total_units);
 hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s);

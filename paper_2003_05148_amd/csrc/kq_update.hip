@@ -44,17 +44,6 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
     return acc;
 }
 
-// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is exact in fp32 (|x| < 32, s <= 57)
-// and so is its rounding to an integer v; v = hi * 2^32 + lo with hi = floor(v * 2^-32)
-// (|hi| < 2^30) and 0 <= lo < 2^32, where lo = v - hi * 2^32 has fewer significant bits
-// than v and is exact in fp32 too, so both convert to integers exactly.
-__device__ __forceinline__ unsigned long long fixed_point(float x, float scale) {
-    const float v = __builtin_rintf(x * scale);
-    const float hi = __builtin_floorf(v * 0x1p-32f);
-    const float lo = __builtin_fmaf(hi, -0x1p32f, v);
-    return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
-}
-
 // shift of the gradient sums: s = 62 - ceil(log2 n) - e with max |g| < 2^e, i.e. the kernel
 // shift (57 - ceil(log2 n), for |x| < 32 = 2^5) moved by 5 - e, kept in [-100, 100]
 __device__ __forceinline__ int grad_shift(float gmax, int kernel_shift) {

@@ -378,3 +378,43 @@ def test_reconstruct_stack_and_errors(packed):
         assert e1 == pytest.approx(exact, rel=1e-12), (n, k)
         single = float(host(kq.kq_sq_error(L["W_ref"], W))[0])
         assert e1 == pytest.approx(single, rel=1e-12), (n, k)
+
+
+@pytest.mark.parametrize("which", ["resnet18_k256", "vgg16_k64_mixed"])
+def test_fused_sums_equal_the_separate_update(which):
+    """Assignment with fused member sums + finish-only update gives the same codebooks,
+    counts and distortions as the separate update pass, bit for bit (integer sums)."""
+    if which == "resnet18_k256":
+        layers = synth.resnet18_stack(k=256)
+    else:
+        layers = synth.vgg16_stack(k=64, layers=6)
+        layers[2] = synth.make_layer("k200", layers[2].X, 200, 3)   # codebooks of several sizes
+    T = 3
+    a = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=T)
+    b = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=T)
+    for t in range(T + 1):
+        kq.kq_assign_stack(a, dist_slot=t, distortion=False)
+        kq.kq_assign_stack(b, dist_slot=t, distortion=False, fused_sums=True)
+        last = t == T
+        kq.kq_update_stack(a, dist_slot=t, counts_only=last, distortion_from_assign=True)
+        kq.kq_update_stack(b, dist_slot=t, counts_only=last, distortion_from_assign=True, sums_from_assign=True)
+        for i in range(len(layers)):
+            assert torch.equal(a.C[i], b.C[i]) and torch.equal(a.counts[i], b.counts[i]), (which, t, i)
+            assert torch.equal(a.idx[i], b.idx[i]), (which, t, i)
+    for i in range(len(layers)):
+        assert torch.equal(a.distortion[i], b.distortion[i]), i
+    # the fits take the fused path by themselves: the same as the separate rounds above
+    c = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=T)
+    kq.kq_fit_stack(c, T)
+    for i in range(len(layers)):
+        assert torch.equal(a.C[i], c.C[i]) and torch.equal(a.idx[i], c.idx[i]), i
+        assert torch.equal(a.counts[i], c.counts[i]) and torch.equal(a.distortion[i], c.distortion[i]), i
+
+
+def test_fused_sums_need_small_codebooks():
+    layers = synth.stress_layer(n=5000, k=300, n_centers=300, seed=9)
+    st = kq.Stack([dev(L.X) for L in layers], [dev(L.C0) for L in layers], iters=1)
+    with pytest.raises(kq.KqError):
+        kq.kq_assign_stack(st, fused_sums=True)
+    with pytest.raises(kq.KqError):
+        kq.kq_update_stack(st, sums_from_assign=True)

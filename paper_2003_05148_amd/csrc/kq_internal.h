@@ -45,7 +45,10 @@ constexpr int kUpdateMinKernelsPerBlock = 1024;
 #endif
 constexpr int kUpdateTargetBlocks = KQ_UPDATE_BLOCKS;
 constexpr int kUpdateLdsMaxK = 768;     // LDS histogram [768][9] int64 + [768] u32
-constexpr int kFinishEntries = 4;       // codebook entries per finishing workgroup
+#ifndef KQ_FINISH_ENTRIES
+#define KQ_FINISH_ENTRIES 8
+#endif
+constexpr int kFinishEntries = KQ_FINISH_ENTRIES;  // codebook entries per finishing workgroup
 constexpr size_t kUpdatePartialBudget = size_t(1) << 24;  // bytes of partials per layer above 768 entries
 
 inline int update_ranges(int32_t k) { return (k + kUpdateLdsMaxK - 1) / kUpdateLdsMaxK; }

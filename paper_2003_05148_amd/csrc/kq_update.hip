@@ -23,10 +23,11 @@
 // (a first launch takes per-block maxima of |g|; every workgroup reduces them), so no sum
 // over at most n values can overflow and the relative resolution is the same for any
 // gradient magnitude; the finish then writes c - gamma * mean instead of the mean.
-// update_finish_kernel: a workgroup of 640 threads owns 4 entries of one layer; sixteen
-// groups of 40 threads add a sixteenth of the chunk partials each, eight loads in flight
-// per thread (any order gives the same integers), then it divides and writes the codebook
-// and the counts.  One more workgroup
+// update_finish_kernel: a workgroup of 640 threads owns 8 entries of one layer; eight
+// groups of 80 threads add an eighth of the partials each, sixteen loads in flight per
+// thread (any order gives the same integers), then it divides and writes the codebook
+// and the counts (fewer, fuller workgroups measured faster than 2 or 4 entries each:
+// the launch is short and its cost is mostly per workgroup).  One more workgroup
 // per layer adds the distortion partials in a fixed order (those of the assignment kernel
 // when the distortion comes from there).  The kernel boundary orders every partial before
 // its use, so no fence or atomic counter is needed.
@@ -172,8 +173,11 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     }
 }
 
-constexpr int kFinishGroups = 16;
-constexpr int kFinishBatch = 8;
+#ifndef KQ_FINISH_BATCH
+#define KQ_FINISH_BATCH 16
+#endif
+constexpr int kFinishGroups = kSumThreads / (10 * kFinishEntries);
+constexpr int kFinishBatch = KQ_FINISH_BATCH;
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
 
@@ -205,8 +209,8 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         const int nb = L.nchunks;
         const size_t stride = (size_t)k * 10;
         const unsigned long long* hp = h + (size_t)j * 10 + d;
-        // chunks g, g + 16, ...: kFinishBatch loads in flight at a time (one batch covers
-        // up to 128 chunks, every layer of a stack at one workgroup per CU)
+        // partials g, g + 8, ...: kFinishBatch loads in flight at a time (one batch covers
+        // 128 partials, every layer of the benchmark stacks)
 #pragma unroll 1
         for (int q0 = g; q0 < nb; q0 += kFinishBatch * kFinishGroups) {
             unsigned long long v[kFinishBatch];

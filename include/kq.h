@@ -10,6 +10,8 @@
  *                        step of Algorithm 1), a fixed number of rounds then a final assignment.
  *   kq_fit_stack         the same for many layers at once (Sec. 3.1 quantizes layer by layer;
  *                        layers are independent, so one launch serves all of them).
+ *   kq_search_codebook_size Alg. 1: binary search of the codebook size, on the k-means
+ *                        distortion instead of validation accuracy (a flagged deviation).
  *   kq_fit_layer_yinyang Sec. 4.1: the same fit with Yinyang assignments (kq_yinyang_init,
  *                        kq_yinyang_assign), equal to kq_fit_layer bit for bit.
  *   kq_codebook_grad_step Sec. 3.1, Eq. (2): retraining step of the codebook with the mean
@@ -221,6 +223,31 @@ size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits);
 kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32_t iters, uint8_t* codes,
                               float* levels, float* v_hat, int32_t* rounds, void* ws, size_t ws_bytes,
                               void* stream);
+
+/*
+ * kq_search_codebook_size -- the codebook-size binary search of Sec. 3.1 (Algorithm 1,
+ * Eq. 3), driven by the k-means distortion J (Eq. 1, the final assignment of each fit)
+ * in place of the validation accuracy.  This is a deviation from the paper, which needs a
+ * trained network and its validation set: here the "accuracy" of a codebook size is -J,
+ * and the unquantized layer's is 0 (no error), so the target of Eq. (3),
+ * A_target = A_base - (A_ori - A_base) r, becomes J_target = (1 + r) J(n_init).
+ *
+ *   Fit k = n_init (lloyd_iters rounds, kq_fit_layer); B_upper = n_init, B_lower = 0; then
+ *   up to max_iter times: N = floor((B_upper + B_lower) / 2), stop if N is a bound; fit k = N;
+ *   J(N) < J_target ? B_upper = N : B_lower = N.  The answer is B_upper.
+ *   Every fit of size k starts from the first k rows of C_cand (the caller's order of
+ *   candidate entries, e.g. seeded distinct kernels), so the trials are nested.
+ *   X device [n][9]; C_cand device [n_init][9]; C device [n_init][9] receives the chosen
+ *   fit's codebook in its first *k_out rows, idx device [n] its assignment; k_out host;
+ *   trial_k, trial_d host [max_iter] or NULL: each iteration's N and J(N) (0 after an early
+ *   stop); d_init host or NULL: J(n_init).  1 <= n_init <= n; r >= 0 finite; synchronous
+ *   (it waits for every fit to read J); workspace: kq_search_workspace_bytes.
+ */
+size_t kq_search_workspace_bytes(int64_t n, int32_t n_init, int32_t lloyd_iters);
+kq_status kq_search_codebook_size(const float* X, int64_t n, int32_t dim, const float* C_cand, int32_t n_init,
+                                  float r, int32_t max_iter, int32_t lloyd_iters, float* C, int32_t* idx,
+                                  int32_t* k_out, int32_t* trial_k, double* trial_d, double* d_init, void* ws,
+                                  size_t ws_bytes, void* stream);
 
 /*
  * Yinyang assignment -- Sec. 4.1: the paper runs its kernel-level k-means with Yinyang

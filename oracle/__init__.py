@@ -12,6 +12,9 @@ What each function follows in the paper:
 * ``cbq_uniform`` / ``cbq_wkmeans`` -- kernel codebook quantization, Sec. 3.2:
   6-bit quantization of every scalar of a layer's codebook by k-means over those
   scalars, weighted by how often each codebook entry is used.
+* ``size_search`` / ``search_codebook_size`` -- the codebook-size binary search of
+  Algorithm 1 and Eq. (3), driven by the k-means distortion instead of the validation
+  accuracy (a stated deviation: there is no trained network here).
 * ``codebook_grad_step`` -- retraining of the kernel codebook, Sec. 3.1, Eq. (2):
   every entry moves against the mean gradient of the kernels mapped to it.
 * ``quantize_scalars`` -- the same quantizer on the scalars of a fully-connected
@@ -147,6 +150,47 @@ def fit(X, C_init, iters: int):
     if rc:
         raise ValueError("kqo_fit failed")
     return dict(C=C, idx=idx, counts=counts, J=J)
+
+
+# ---- Alg. 1: binary search of the codebook size (on the k-means distortion) -------------
+
+def size_search(D, n_init: int, r: float, max_iter: int):
+    """The codebook-size search of Algorithm 1 with Eq. (3), on a distortion D(k) instead of
+    the validation accuracy: accuracy A = -D, the unquantized layer's A_ori = 0, so
+    A_target = A_base - (A_ori - A_base) r reads D_target = (1 + r) D(n_init).
+
+    B_upper = n_init, B_lower = 0; each iteration tests N = floor((B_upper + B_lower) / 2)
+    (stopping when N reaches a bound, the reading of the garbled loop condition); a size
+    whose distortion is below the target becomes the new upper bound, any other the new
+    lower bound.  Returns (k = B_upper, [(N, D(N)) per iteration], D(n_init)).
+    """
+    d0 = float(D(n_init))
+    target = (1.0 + float(np.float32(r))) * d0
+    upper, lower = n_init, 0
+    trials = []
+    for _ in range(max_iter):
+        cur = (upper + lower) // 2
+        if cur <= lower or cur >= upper:
+            break
+        d = float(D(cur))
+        trials.append((cur, d))
+        if d < target:
+            upper = cur
+        else:
+            lower = cur
+    return upper, trials, d0
+
+
+def search_codebook_size(X, C_cand, n_init: int, r: float, max_iter: int, lloyd_iters: int):
+    """``size_search`` with D(k) = the distortion of the final assignment of a Lloyd fit
+    (``fit``) of k entries started from the first k rows of C_cand."""
+    X = _f32(X)
+    C_cand = _f32(C_cand)
+
+    def D(k):
+        return fit(X, C_cand[:k], lloyd_iters)["J"][-1]
+
+    return size_search(D, n_init, r, max_iter)
 
 
 # ---- Sec. 3.1, Eq. (2): retraining of the kernel codebook ------------------------------

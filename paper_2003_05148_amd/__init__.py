@@ -10,7 +10,7 @@ fallback: without the built library, importing this package raises ImportError.
 Entry points (same names as the C ABI):
   kq_assign, kq_update, kq_fit_layer, kq_assign_stack, kq_update_stack, kq_fit_stack,
   kq_fit_layer_yinyang (and the Yinyang class over kq_yinyang_init / kq_yinyang_assign),
-  kq_codebook_grad_step, kq_codebook_grad_step_stack, kq_quantize_scalars,
+  kq_codebook_grad_step, kq_codebook_grad_step_stack, kq_quantize_scalars, kq_search_codebook_size,
   kq_quantize_codebook, kq_quantize_codebook_stack, kq_pack_bits, kq_unpack_bits,
   kq_reconstruct, kq_reconstruct_packed.
 """
@@ -79,6 +79,9 @@ def _load():
         "kq_codebook_grad_step_stack": ([_P, _I32, ctypes.c_float, _P, _SZ, _P], _I32),
         "kq_quantize_scalars_workspace_bytes": ([_I64, _I32], _SZ),
         "kq_quantize_scalars": ([_P, _I64, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
+        "kq_search_workspace_bytes": ([_I64, _I32, _I32], _SZ),
+        "kq_search_codebook_size": ([_P, _I64, _I32, _P, _I32, ctypes.c_float, _I32, _I32, _P, _P, _P, _P, _P, _P,
+                                     _P, _SZ, _P], _I32),
         "kq_yinyang_workspace_bytes": ([_I64, _I32, _I32], _SZ),
         "kq_yinyang_init": ([_P, _I64, _I32, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_yinyang_assign": ([_P, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
@@ -111,7 +114,7 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
             "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang",
             "kq_codebook_grad_step", "kq_codebook_grad_step_stack", "kq_quantize_scalars_workspace_bytes",
-            "kq_quantize_scalars"]
+            "kq_quantize_scalars", "kq_search_workspace_bytes", "kq_search_codebook_size"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -363,6 +366,32 @@ def kq_quantize_scalars(v, bits: int = 6, iters: int = 30, codes=None, levels=No
                                    rounds.data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)),
            "kq_quantize_scalars")
     return codes, levels, v_hat, rounds
+
+
+def kq_search_codebook_size(X, C_cand, r: float, max_iter: int, lloyd_iters: int, workspace=None):
+    """Algorithm 1's codebook-size binary search on the k-means distortion (a deviation
+    from the paper's validation accuracy; see include/kq.h).  C_cand [n_init, 9] orders the
+    candidate initial entries.  Returns (k, C [k, 9], idx [n], trials [(N, J(N))], J(n_init))."""
+    X = _kernels(X)
+    C_cand = _kernels(C_cand, "C_cand")
+    n, n_init = X.shape[0], C_cand.shape[0]
+    dev = X.device
+    C = torch.empty_like(C_cand)
+    idx = torch.empty(n, dtype=torch.int32, device=dev)
+    nb = lib.kq_search_workspace_bytes(n, n_init, lloyd_iters)
+    if nb == 0:
+        raise ValueError("invalid search sizes")
+    ws = workspace if workspace is not None else _ws(dev, nb)
+    k_out = ctypes.c_int32(0)
+    d0 = ctypes.c_double(0.0)
+    tk = (ctypes.c_int32 * max(max_iter, 1))()
+    td = (ctypes.c_double * max(max_iter, 1))()
+    _check(lib.kq_search_codebook_size(X.data_ptr(), n, KQ_DIM, C_cand.data_ptr(), n_init, float(r), max_iter,
+                                       lloyd_iters, C.data_ptr(), idx.data_ptr(), ctypes.byref(k_out),
+                                       ctypes.cast(tk, _P), ctypes.cast(td, _P), ctypes.byref(d0), ws.data_ptr(),
+                                       ws.numel(), _stream(dev)), "kq_search_codebook_size")
+    trials = [(int(tk[i]), float(td[i])) for i in range(max_iter) if tk[i] > 0]
+    return k_out.value, C[:k_out.value], idx, trials, d0.value
 
 
 def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):

@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 7;
+constexpr int32_t kAbiVersion = 8;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -483,6 +483,84 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
     b += align256(sizeof(int) * 4);
     p.wg_changed = (int*)b;
     return hip_status(launch_fc_quantize(p, (hipStream_t)stream));
+}
+
+// a fit workspace large enough for every codebook size up to kmax (the per-layer layout
+// is not monotone in k: small codebooks keep one fused partial per assignment tile)
+size_t fit_ws_upto(int64_t n, int32_t kmax) {
+    const size_t c1024 = (size_t)((n + 1023) / 1024);
+    return ws_assign_part(n) + align256(sizeof(double) * (size_t)update_ranges(kmax) * c1024) +
+           align256(sizeof(int64_t) * 10 * (size_t)kmax * (size_t)assign_tiles(n)) + ws_grad(n);
+}
+
+size_t kq_search_workspace_bytes(int64_t n, int32_t n_init, int32_t lloyd_iters) {
+    if (!valid_n(n) || !valid_k(n_init) || n_init > n || lloyd_iters < 0) return 0;
+    return fit_ws_upto(n, n_init) + align256(sizeof(float) * KQ_DIM * (size_t)n_init) +
+           align256(sizeof(int32_t) * (size_t)n) + align256(sizeof(double) * (size_t)(lloyd_iters + 1));
+}
+
+kq_status kq_search_codebook_size(const float* X, int64_t n, int32_t dim, const float* C_cand, int32_t n_init, float r,
+                                  int32_t max_iter, int32_t lloyd_iters, float* C, int32_t* idx, int32_t* k_out,
+                                  int32_t* trial_k, double* trial_d, double* d_init, void* ws, size_t ws_bytes,
+                                  void* stream) {
+    if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
+    if (n_init > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(n) || !valid_k(n_init) || n_init > n || max_iter < 0 || lloyd_iters < 0) return KQ_ERR_ARG;
+    if (!(r >= 0.0f) || !finite_gamma(r)) return KQ_ERR_ARG;
+    if (!X || !C_cand || !C || !idx || !k_out || !aligned(X, 4) || !aligned(C_cand, 4) || !aligned(C, 4) ||
+        !aligned(idx, 4))
+        return KQ_ERR_ARG;
+    const size_t need = kq_search_workspace_bytes(n, n_init, lloyd_iters);
+    if (check_ws(ws, ws_bytes, need) != KQ_OK) return KQ_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    unsigned char* w = (unsigned char*)ws;
+    float* C_try = (float*)(w + fit_ws_upto(n, n_init));
+    int32_t* idx_try = (int32_t*)((unsigned char*)C_try + align256(sizeof(float) * KQ_DIM * (size_t)n_init));
+    double* J = (double*)((unsigned char*)idx_try + align256(sizeof(int32_t) * (size_t)n));
+    // one fit of size k from the first k candidates; its final distortion back on the host
+    auto trial = [&](int32_t k, float* Cout, int32_t* iout, double& d) -> kq_status {
+        const kq_layer l = {X, n, k, Cout, iout, nullptr, nullptr, J};
+        if (hipMemcpyAsync(Cout, C_cand, sizeof(float) * KQ_DIM * (size_t)k, hipMemcpyDeviceToDevice, s) !=
+            hipSuccess)
+            return KQ_ERR_HIP;
+        const kq_status st = run_fit(&l, 1, lloyd_iters, w, s);
+        if (st != KQ_OK) return st;
+        if (hipMemcpyAsync(&d, J + lloyd_iters, sizeof(double), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return KQ_ERR_HIP;
+        return KQ_OK;
+    };
+    double d0 = 0.0;
+    kq_status st = trial(n_init, C, idx, d0);  // the baseline size; its result is kept until beaten
+    if (st != KQ_OK) return st;
+    if (d_init) *d_init = d0;
+    const double target = (1.0 + (double)r) * d0;
+    int32_t upper = n_init, lower = 0;
+    for (int32_t i = 0; i < max_iter; ++i) {
+        const int32_t cur = (int32_t)(((int64_t)upper + lower) / 2);
+        if (cur <= lower || cur >= upper) {
+            for (int32_t q = i; q < max_iter; ++q) {
+                if (trial_k) trial_k[q] = 0;
+                if (trial_d) trial_d[q] = 0.0;
+            }
+            break;
+        }
+        double d = 0.0;
+        if ((st = trial(cur, C_try, idx_try, d)) != KQ_OK) return st;
+        if (trial_k) trial_k[i] = cur;
+        if (trial_d) trial_d[i] = d;
+        if (d < target) {  // within the allowed distortion: the new upper bound, and the result so far
+            upper = cur;
+            if (hipMemcpyAsync(C, C_try, sizeof(float) * KQ_DIM * (size_t)cur, hipMemcpyDeviceToDevice, s) !=
+                    hipSuccess ||
+                hipMemcpyAsync(idx, idx_try, sizeof(int32_t) * (size_t)n, hipMemcpyDeviceToDevice, s) != hipSuccess)
+                return KQ_ERR_HIP;
+        } else {
+            lower = cur;
+        }
+    }
+    *k_out = upper;
+    return hip_status(hipStreamSynchronize(s));
 }
 
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters, float* C,

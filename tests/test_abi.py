@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 7
+    assert lib.kq_abi_version() == 8
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -277,3 +277,25 @@ def test_quantize_scalars_argument_errors():
     assert q(lev=FAKE + 2) == kq.KQ_ERR_ARG
     assert q(vh=FAKE + 1) == kq.KQ_ERR_ARG
     assert q(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE
+
+
+def test_search_argument_errors():
+    nb = lib.kq_search_workspace_bytes(1000, 300, 10)
+    assert nb >= lib.kq_workspace_bytes(kq.KQ_OP_FIT, 1000, 256)     # covers every trial size
+    assert lib.kq_search_workspace_bytes(100, 101, 10) == 0
+    k = ctypes.c_int32(0)
+
+    def srch(**kw):
+        a = dict(X=FAKE, n=1000, dim=9, Cc=FAKE, ni=300, r=0.5, mi=8, li=10, C=FAKE, idx=FAKE, k=ctypes.byref(k),
+                 ws=FAKE, wsb=nb)
+        a.update(kw)
+        return lib.kq_search_codebook_size(a["X"], a["n"], a["dim"], a["Cc"], a["ni"], a["r"], a["mi"], a["li"],
+                                           a["C"], a["idx"], a["k"], None, None, None, a["ws"], a["wsb"], None)
+
+    assert srch(dim=8) == kq.KQ_ERR_UNSUPPORTED
+    assert srch(ni=1001) == kq.KQ_ERR_ARG
+    assert srch(r=-0.1) == kq.KQ_ERR_ARG
+    assert srch(r=float("nan")) == kq.KQ_ERR_ARG
+    assert srch(mi=-1) == kq.KQ_ERR_ARG
+    assert srch(k=None) == kq.KQ_ERR_ARG
+    assert srch(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE

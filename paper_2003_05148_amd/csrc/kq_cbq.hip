@@ -129,6 +129,42 @@ __device__ double digits_to_double(const unsigned long long* dig) {
     return neg ? -r : r;
 }
 
+// Nearest level of x among NLEV sorted levels (the answer of nearest_sorted): the number
+// of levels below x from every eighth level (registers) and one block of eight (LDS), then
+// the exact fp64 comparison of the two neighbours, walking down over equal distances.
+template <int NLEV>
+__device__ __forceinline__ int nearest_sorted_fast(float x, const float* s_lev, const float (&coarse)[NLEV / 8 + 1]) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    int q0;
+    if (NLEV >= 8) {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] < x ? 1 : 0;
+        if (c == NLEV / 8) {
+            q0 = NLEV;  // the last level is below x, and with it every level
+        } else {
+            const f32x4 a = reinterpret_cast<const f32x4*>(s_lev)[2 * c];
+            const f32x4 b = reinterpret_cast<const f32x4*>(s_lev)[2 * c + 1];
+            q0 = 8 * c + (a[0] < x) + (a[1] < x) + (a[2] < x) + (a[3] < x) + (b[0] < x) + (b[1] < x) + (b[2] < x) +
+                 (b[3] < x);
+        }
+    } else {
+        q0 = 0;
+#pragma unroll
+        for (int i = 0; i < NLEV; ++i) q0 += s_lev[i] < x ? 1 : 0;
+    }
+    const double vd = (double)x;
+    int q = q0;
+    const double da = q0 < NLEV ? fabs(vd - (double)s_lev[q0]) : __builtin_inf();
+    if (q0 > 0) {
+        int bq = q0 - 1;
+        const double db = fabs(vd - (double)s_lev[bq]);
+        while (bq > 0 && fabs(vd - (double)s_lev[bq - 1]) == db) --bq;
+        if (db <= da) q = bq;
+    }
+    return q;
+}
+
 // Thread tid handles scalars r = tid, tid + 1024, ...  With LDS (codebooks of at most
 // kCbqLdsScalars scalars) the scalars, their weights and codes are copied into LDS once;
 // otherwise every pass reads them from memory.  The level sums are kept up to date
@@ -137,9 +173,10 @@ __device__ double digits_to_double(const unsigned long long* dig) {
 // summing from scratch.
 constexpr int kCbqLdsScalars = 8192;
 
-template <bool LDS>
+// FAST64: 64 levels (6 bits, the paper's width), searched with nearest_sorted_fast
+template <bool LDS, bool FAST64>
 __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
-    __shared__ float s_lev[kCbqMaxLevels];
+    __shared__ __attribute__((aligned(16))) float s_lev[kCbqMaxLevels];
     __shared__ unsigned long long s_dig[kCbqMaxLevels * kDigits];
     __shared__ unsigned long long s_w[kCbqMaxLevels];
     __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave];
@@ -207,11 +244,22 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
     __syncthreads();
     bool sorted = s_unsorted == 0;
+    float coarse[64 / 8 + 1];  // every eighth level, for the 64-level search
+    auto load_coarse = [&]() {
+#pragma unroll
+        for (int i = 0; i < 64 / 8; ++i) coarse[i] = FAST64 ? s_lev[8 * i + 7] : 0.0f;
+        coarse[64 / 8] = 0.0f;
+    };
+    auto nearest = [&](float x) {
+        if (!sorted) return nearest_level(x, s_lev, nlev);
+        return FAST64 ? nearest_sorted_fast<64>(x, s_lev, coarse) : nearest_sorted(x, s_lev, nlev);
+    };
+    load_coarse();
 
     // initial codes, and with them the level sums
     for (int r = tid; r < m; r += kCbqThreads) {
         const float x = val(r);
-        const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
+        const int q = nearest(x);
         set_code(r, q);
         const int w = wgt(r);
         if (wk && w > 0) {
@@ -235,10 +283,11 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
             if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
             __syncthreads();
             sorted = s_unsorted == 0;
+            load_coarse();
             int changed = 0;
             for (int r = tid; r < m; r += kCbqThreads) {
                 const float x = val(r);
-                const int q = sorted ? nearest_sorted(x, s_lev, nlev) : nearest_level(x, s_lev, nlev);
+                const int q = nearest(x);
                 const int c = code(r);
                 if (q != c) {
                     const int w = wgt(r);
@@ -346,42 +395,6 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p
     if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
     __syncthreads();
     if (tid == 0) p.state[2] = s_unsorted;
-}
-
-// Nearest level of x among NLEV sorted levels (the answer of nearest_sorted): the number
-// of levels below x from every eighth level (registers) and one block of eight (LDS), then
-// the exact fp64 comparison of the two neighbours, walking down over equal distances.
-template <int NLEV>
-__device__ __forceinline__ int nearest_sorted_fast(float x, const float* s_lev, const float (&coarse)[NLEV / 8 + 1]) {
-    typedef float f32x4 __attribute__((ext_vector_type(4)));
-    int q0;
-    if (NLEV >= 8) {
-        int c = 0;
-#pragma unroll
-        for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] < x ? 1 : 0;
-        if (c == NLEV / 8) {
-            q0 = NLEV;  // the last level is below x, and with it every level
-        } else {
-            const f32x4 a = reinterpret_cast<const f32x4*>(s_lev)[2 * c];
-            const f32x4 b = reinterpret_cast<const f32x4*>(s_lev)[2 * c + 1];
-            q0 = 8 * c + (a[0] < x) + (a[1] < x) + (a[2] < x) + (a[3] < x) + (b[0] < x) + (b[1] < x) + (b[2] < x) +
-                 (b[3] < x);
-        }
-    } else {
-        q0 = 0;
-#pragma unroll
-        for (int i = 0; i < NLEV; ++i) q0 += s_lev[i] < x ? 1 : 0;
-    }
-    const double vd = (double)x;
-    int q = q0;
-    const double da = q0 < NLEV ? fabs(vd - (double)s_lev[q0]) : __builtin_inf();
-    if (q0 > 0) {
-        int bq = q0 - 1;
-        const double db = fabs(vd - (double)s_lev[bq]);
-        while (bq > 0 && fabs(vd - (double)s_lev[bq - 1]) == db) --bq;
-        if (db <= da) q = bq;
-    }
-    return q;
 }
 
 // Each thread takes four scalars per step (r0 + 256 j, consecutive lanes consecutive
@@ -579,10 +592,15 @@ hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s) {
 hipError_t launch_cbq(const CbqParams& p, hipStream_t s) {
     int mmax = 0;
     for (int l = 0; l < p.nlayers; ++l) mmax = p.L[l].k * kDim > mmax ? p.L[l].k * kDim : mmax;
-    if (mmax <= kCbqLdsScalars)
-        hipLaunchKernelGGL(cbq_kernel<true>, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    const bool fast = p.bits == 6;
+    if (mmax <= kCbqLdsScalars && fast)
+        hipLaunchKernelGGL((cbq_kernel<true, true>), dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    else if (mmax <= kCbqLdsScalars)
+        hipLaunchKernelGGL((cbq_kernel<true, false>), dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+    else if (fast)
+        hipLaunchKernelGGL((cbq_kernel<false, true>), dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
     else
-        hipLaunchKernelGGL(cbq_kernel<false>, dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
+        hipLaunchKernelGGL((cbq_kernel<false, false>), dim3(p.nlayers), dim3(kCbqThreads), 0, s, p);
     return hipGetLastError();
 }
 

@@ -20,7 +20,10 @@ constexpr int kWave = 64;
 // the K = 10 fp32 contraction, 9 dims + norm, into three cross terms).
 // A "tile" of the grid is the 256 kernels one workgroup scores at a time; the grid is
 // persistent (at most kAssignGridMax workgroups, each walking a contiguous run of tiles).
-constexpr int kAssignWaves = 4;
+#ifndef KQ_ASSIGN_WAVES
+#define KQ_ASSIGN_WAVES 4
+#endif
+constexpr int kAssignWaves = KQ_ASSIGN_WAVES;
 constexpr int kAssignTilesPerWave = 2;
 constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
 #ifndef KQ_ASSIGN_OCC

@@ -88,6 +88,9 @@ typedef enum kq_status {
                                 (no second pass over the old codebook) */
 #define KQ_F_FUSED_SUMS 4u   /* kq_assign_stack: also accumulate the member sums of the new
                                 assignment (every k <= 256, else KQ_ERR_UNSUPPORTED) */
+#define KQ_F_EXACT_SEARCH 16u /* kq_quantize_scalars: every code by the exact fp64 search (reference) */
+#define KQ_F_THRESHOLDS 32u  /* kq_quantize_scalars: codes from level thresholds at any size, wherever
+                                they are valid (by default only from 2^23 scalars on) */
 #define KQ_F_SUMS_FROM_ASSIGN 8u
                              /* kq_update_stack: finish the update from the sums the preceding
                                 kq_assign_stack with KQ_F_FUSED_SUMS left (same layers and
@@ -214,6 +217,13 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
  *   changes no code.  iters = 0 gives the uniform grid alone.  The sums are exact, so the
  *   result is a pure function of v: bit for bit that of kq_quantize_codebook on the same
  *   scalars with unit weights.
+ *   With sorted levels the code of a value never decreases as the value grows, so from
+ *   2^23 scalars on each round first finds, per level boundary, the smallest value that
+ *   takes the next code (bisection over fp32 values with the exact search) and then codes
+ *   every scalar with fp32 comparisons only.  This is used only where every fp64 distance
+ *   between a data value and a level is exact (no nonzero value or level below 2^-29 of the
+ *   largest magnitude), so it gives the exact search's codes; KQ_F_EXACT_SEARCH /
+ *   KQ_F_THRESHOLDS force one way (flags 0 = the size rule).
  *   v device [count] fp32 (finite); codes device [count] uint8; levels device [2^bits] fp32;
  *   v_hat device [count] (= levels[codes], may be NULL); rounds device int32 (level updates
  *   made, may be NULL).  1 <= count < 2^31; bits 1..8 (else KQ_ERR_UNSUPPORTED).
@@ -221,8 +231,8 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
  */
 size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits);
 kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32_t iters, uint8_t* codes,
-                              float* levels, float* v_hat, int32_t* rounds, void* ws, size_t ws_bytes,
-                              void* stream);
+                              float* levels, float* v_hat, int32_t* rounds, uint32_t flags, void* ws,
+                              size_t ws_bytes, void* stream);
 
 /*
  * kq_search_codebook_size -- the codebook-size binary search of Sec. 3.1 (Algorithm 1,

@@ -78,7 +78,7 @@ def _load():
         "kq_codebook_grad_step": ([_P, _I64, _I32, _P, _I32, _P, ctypes.c_float, _P, _P, _P, _SZ, _P], _I32),
         "kq_codebook_grad_step_stack": ([_P, _I32, ctypes.c_float, _P, _SZ, _P], _I32),
         "kq_quantize_scalars_workspace_bytes": ([_I64, _I32], _SZ),
-        "kq_quantize_scalars": ([_P, _I64, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
+        "kq_quantize_scalars": ([_P, _I64, _I32, _I32, _P, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
         "kq_search_workspace_bytes": ([_I64, _I32, _I32], _SZ),
         "kq_search_codebook_size": ([_P, _I64, _I32, _P, _I32, ctypes.c_float, _I32, _I32, _P, _P, _P, _P, _P, _P,
                                      _P, _SZ, _P], _I32),
@@ -107,6 +107,8 @@ KQ_F_COUNTS_ONLY = 1
 KQ_F_DISTORTION_FROM_ASSIGN = 2
 KQ_F_FUSED_SUMS = 4
 KQ_F_SUMS_FROM_ASSIGN = 8
+KQ_F_EXACT_SEARCH = 16
+KQ_F_THRESHOLDS = 32
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
@@ -337,11 +339,13 @@ def kq_codebook_grad_step_stack(stack, gamma: float):
 
 
 def kq_quantize_scalars(v, bits: int = 6, iters: int = 30, codes=None, levels=None, v_hat=None, rounds=None,
-                        workspace=None, want_v_hat: bool = True):
+                        workspace=None, want_v_hat: bool = True, search: str = "auto"):
     """k-means quantization of every scalar of a (fully-connected) weight tensor with
     2^bits levels, the codebook quantizer's method with unit weights (end of Sec. 3.2).
+    search: "auto", "exact" (KQ_F_EXACT_SEARCH) or "thresholds" (KQ_F_THRESHOLDS).
     Returns (codes uint8 [m], levels float32 [2^bits], v_hat float32 [m] or None,
     rounds int32 [1])."""
+    flags = {"auto": 0, "exact": KQ_F_EXACT_SEARCH, "thresholds": KQ_F_THRESHOLDS}[search]
     if not isinstance(v, torch.Tensor) or not v.is_cuda or v.dtype != torch.float32 or not v.is_contiguous():
         raise TypeError("v must be a contiguous float32 CUDA (HIP) tensor")
     v = v.reshape(-1)
@@ -363,7 +367,7 @@ def kq_quantize_scalars(v, bits: int = 6, iters: int = 30, codes=None, levels=No
         raise ValueError(f"unsupported size {m} or bits {bits}")
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_quantize_scalars(v.data_ptr(), m, bits, iters, codes.data_ptr(), levels.data_ptr(), _ptr(v_hat),
-                                   rounds.data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)),
+                                   rounds.data_ptr(), flags, ws.data_ptr(), ws.numel(), _stream(dev)),
            "kq_quantize_scalars")
     return codes, levels, v_hat, rounds
 

@@ -12,7 +12,7 @@ using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 8;
+constexpr int32_t kAbiVersion = 9;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -450,9 +450,13 @@ size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits) {
 }
 
 kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32_t iters, uint8_t* codes,
-                              float* levels, float* v_hat, int32_t* rounds, void* ws, size_t ws_bytes, void* stream) {
+                              float* levels, float* v_hat, int32_t* rounds, uint32_t flags, void* ws, size_t ws_bytes,
+                              void* stream) {
     if (bits < 1 || bits > 8) return KQ_ERR_UNSUPPORTED;
     if (count < 1 || count >= (int64_t(1) << 31) || iters < 0) return KQ_ERR_ARG;
+    if ((flags & ~(KQ_F_EXACT_SEARCH | KQ_F_THRESHOLDS)) != 0 ||
+        (flags & (KQ_F_EXACT_SEARCH | KQ_F_THRESHOLDS)) == (KQ_F_EXACT_SEARCH | KQ_F_THRESHOLDS))
+        return KQ_ERR_ARG;
     if (!v || !codes || !levels || !aligned(v, 4) || !aligned(levels, 4)) return KQ_ERR_ARG;
     if ((v_hat && !aligned(v_hat, 4)) || (rounds && !aligned(rounds, 4))) return KQ_ERR_ARG;
     const kq_status w = check_ws(ws, ws_bytes, fc_ws_bytes(count, bits));
@@ -469,8 +473,10 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
     p.m = count;
     p.bits = bits;
     p.iters = iters;
+    p.thr_mode = (flags & KQ_F_EXACT_SEARCH) ? 1 : ((flags & KQ_F_THRESHOLDS) ? 2 : 0);
     p.minmax = (float*)b;
-    b += align256(sizeof(float) * 2 * G);
+    p.range = p.minmax + 3 * G;
+    b += align256(sizeof(float) * (3 * G + 4));
     p.part = (long long*)b;
     b += align256(sizeof(long long) * G * nlev * 12);
     p.S = (long long*)b;
@@ -478,6 +484,8 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
     p.lev = (float*)b;
     b += align256(sizeof(float) * nlev);
     p.lev_next = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.thr = (float*)b;
     b += align256(sizeof(float) * nlev);
     p.state = (int*)b;
     b += align256(sizeof(int) * 4);

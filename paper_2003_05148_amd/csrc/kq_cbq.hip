@@ -165,6 +165,64 @@ __device__ __forceinline__ int nearest_sorted_fast(float x, const float* s_lev, 
     return q;
 }
 
+// Code thresholds.  With sorted levels the code of v (nearest level, lowest index on
+// ties, fp64 distances) never decreases as v grows: the distance to a lower level only
+// grows and to a higher one only shrinks.  So code(v) = the number of q < nlev - 1 with
+// t_q <= v, where t_q is the smallest fp32 value whose code exceeds q (+inf if none).
+// t_q is found by bisection over the fp32 values in their order, evaluating code() with
+// nearest_sorted; afterwards each scalar needs only fp32 comparisons.
+__device__ __forceinline__ unsigned ordered_key(float f) {
+    const unsigned u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(unsigned k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+// Searched within the data range [vmin, vmax] only, and used only where every fp64
+// distance |v - L| there is exact (see exact_floor): rounding could otherwise make
+// distances to distinct levels equal for far values and send them to a lower index.
+__device__ float code_threshold(int q, const float* lev, int nlev, float vmin, float vmax) {
+    unsigned lo = ordered_key(vmin), hi = ordered_key(vmax);
+    if (nearest_sorted(key_value(hi), lev, nlev) <= q) return __builtin_inff();
+    if (nearest_sorted(key_value(lo), lev, nlev) > q) return key_value(lo);
+    while (hi - lo > 1u) {  // code(lo) <= q < code(hi)
+        const unsigned mid = lo + (hi - lo) / 2u;
+        if (nearest_sorted(key_value(mid), lev, nlev) > q)
+            hi = mid;
+        else
+            lo = mid;
+    }
+    return key_value(hi);
+}
+
+// fp32 values v, L with |v|, |L| <= M differ exactly in fp64 when neither is a nonzero
+// value below 2^(e(M) - 29) (e = floor(log2)): their exponents then differ by at most 29,
+// so v - L needs at most 53 bits.  Returns that floor (0 when M is subnormal or zero).
+__device__ __forceinline__ float exact_floor(float M) {
+    const int be = (int)((__float_as_uint(M) >> 23) & 255u);
+    return be == 0 ? 0.0f : __builtin_ldexpf(1.0f, be - 127 - 29);
+}
+
+// code of x from NLEV - 1 sorted thresholds (s_thr[NLEV - 1] = +inf): every eighth from
+// registers, then one block of eight from LDS
+template <int NLEV>
+__device__ __forceinline__ int code_from_thresholds(float x, const float* s_thr, const float (&coarse)[NLEV / 8 + 1]) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    if (NLEV < 8) {
+        int q = 0;
+#pragma unroll
+        for (int i = 0; i < NLEV - 1; ++i) q += s_thr[i] <= x ? 1 : 0;
+        return q;
+    }
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] <= x ? 1 : 0;  // coarse[NLEV / 8 - 1] = +inf
+    const f32x4 a = reinterpret_cast<const f32x4*>(s_thr)[2 * c];
+    const f32x4 b = reinterpret_cast<const f32x4*>(s_thr)[2 * c + 1];
+    return 8 * c + (a[0] <= x) + (a[1] <= x) + (a[2] <= x) + (a[3] <= x) + (b[0] <= x) + (b[1] <= x) + (b[2] <= x) +
+           (b[3] <= x);
+}
+
 // Thread tid handles scalars r = tid, tid + 1024, ...  With LDS (codebooks of at most
 // kCbqLdsScalars scalars) the scalars, their weights and codes are copied into LDS once;
 // otherwise every pass reads them from memory.  The level sums are kept up to date
@@ -334,52 +392,82 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
 // Integer sums make the levels, and with them the codes, independent of the grid and the
 // order of the work: the result is the single-workgroup quantizer's, bit for bit.
 constexpr int kFcCols = kDigits + 1;  // digits, then the count
+constexpr long long kFcThresholdMin = 1ll << 23;  // scalars from which codes come from thresholds
 
 __device__ __forceinline__ bool fc_done(const FcParams& p) { return p.state[0] != 0; }
 
+// per workgroup: min, max and smallest nonzero magnitude of its scalars
 __global__ __launch_bounds__(kFcThreads) void fc_minmax_kernel(const FcParams p) {
-    __shared__ float s_lo[kFcThreads / kWave], s_hi[kFcThreads / kWave];
+    __shared__ float s_lo[kFcThreads / kWave], s_hi[kFcThreads / kWave], s_sm[kFcThreads / kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    float lo = __builtin_inff(), hi = -__builtin_inff();
+    float lo = __builtin_inff(), hi = -__builtin_inff(), sm = __builtin_inff();
     for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads) {
         const float x = p.v[r];
         lo = fminf(lo, x);
         hi = fmaxf(hi, x);
+        if (x != 0.0f) sm = fminf(sm, fabsf(x));
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         lo = fminf(lo, __shfl_xor(lo, off));
         hi = fmaxf(hi, __shfl_xor(hi, off));
+        sm = fminf(sm, __shfl_xor(sm, off));
     }
     if (lane == 0) {
         s_lo[wave] = lo;
         s_hi[wave] = hi;
+        s_sm[wave] = sm;
     }
     __syncthreads();
     if (tid == 0) {
         for (int w = 1; w < kFcThreads / kWave; ++w) {
             lo = fminf(lo, s_lo[w]);
             hi = fmaxf(hi, s_hi[w]);
+            sm = fminf(sm, s_sm[w]);
         }
-        p.minmax[2 * blockIdx.x] = fminf(lo, s_lo[0]);
-        p.minmax[2 * blockIdx.x + 1] = fmaxf(hi, s_hi[0]);
+        p.minmax[3 * blockIdx.x] = lo;
+        p.minmax[3 * blockIdx.x + 1] = hi;
+        p.minmax[3 * blockIdx.x + 2] = sm;
     }
+}
+
+// thresholds of the levels s_lev (sorted unless s_unsorted) when every distance from the
+// data range to them is exact in fp64 (state[3]); otherwise state[3] = 0 and the codes
+// are found by the exact search.  Every thread of the workgroup calls it.
+__device__ void set_thresholds(const FcParams& p, const float* s_lev, int nlev, int unsorted, int* s_bad, float vmin,
+                               float vmax, float vsm) {
+    const int tid = threadIdx.x;
+    const float fl = exact_floor(fmaxf(fabsf(vmin), fabsf(vmax)));
+    // the bisection costs about 25 us per round: worth it only for large sets
+    const bool wanted = p.thr_mode == 2 || (p.thr_mode == 0 && p.m >= kFcThresholdMin);
+    if (tid == 0) *s_bad = (unsorted || vsm < fl || !wanted) ? 1 : 0;
+    __syncthreads();
+    if (tid < nlev && s_lev[tid] != 0.0f && fabsf(s_lev[tid]) < fl) *s_bad = 1;
+    __syncthreads();
+    const int ok = *s_bad == 0;
+    if (tid < nlev) p.thr[tid] = (ok && tid + 1 < nlev) ? code_threshold(tid, s_lev, nlev, vmin, vmax) : __builtin_inff();
+    if (tid == 0) p.state[3] = ok;
 }
 
 // the uniform grid on [min, max]; clears the run state and the running sums
 __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p, int nblk) {
-    __shared__ float s_lo, s_hi;
+    __shared__ float s_lo, s_hi, s_sm;
     __shared__ float s_lev[kCbqMaxLevels];
-    __shared__ int s_unsorted;
+    __shared__ int s_unsorted, s_bad;
     const int tid = threadIdx.x, nlev = 1 << p.bits;
     if (tid == 0) {
-        float lo = __builtin_inff(), hi = -__builtin_inff();
+        float lo = __builtin_inff(), hi = -__builtin_inff(), sm = __builtin_inff();
         for (int b = 0; b < nblk; ++b) {
-            lo = fminf(lo, p.minmax[2 * b]);
-            hi = fmaxf(hi, p.minmax[2 * b + 1]);
+            lo = fminf(lo, p.minmax[3 * b]);
+            hi = fmaxf(hi, p.minmax[3 * b + 1]);
+            sm = fminf(sm, p.minmax[3 * b + 2]);
         }
         s_lo = lo;
         s_hi = hi;
+        s_sm = sm;
+        p.range[0] = lo;
+        p.range[1] = hi;
+        p.range[2] = sm;
         s_unsorted = 0;
         p.state[0] = 0;  // not converged
         p.state[1] = 0;  // level updates made
@@ -395,26 +483,35 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p
     if (tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
     __syncthreads();
     if (tid == 0) p.state[2] = s_unsorted;
+    set_thresholds(p, s_lev, nlev, s_unsorted, &s_bad, s_lo, s_hi, s_sm);
 }
 
 // Each thread takes four scalars per step (r0 + 256 j, consecutive lanes consecutive
-// scalars), their loads issued together.
+// scalars), their loads issued together; with sorted levels a code is the number of
+// thresholds at or below the value (fp32 comparisons only).
 template <bool INIT, int NLEV>
 __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p) {
     __shared__ __attribute__((aligned(16))) float s_lev[NLEV < 8 ? 8 : NLEV];
+    __shared__ __attribute__((aligned(16))) float s_thr[NLEV < 8 ? 8 : NLEV];
     __shared__ unsigned long long s_dig[NLEV * kFcCols];
     __shared__ int s_changed;
     if (fc_done(p)) return;
     const int tid = threadIdx.x;
-    for (int e = tid; e < NLEV; e += kFcThreads) s_lev[e] = p.lev[e];
+    for (int e = tid; e < NLEV; e += kFcThreads) {
+        s_lev[e] = p.lev[e];
+        s_thr[e] = p.thr[e];  // thr[NLEV - 1] is +inf
+    }
     for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
     if (tid == 0) s_changed = 0;
     __syncthreads();
-    const bool sorted = p.state[2] == 0;
-    float coarse[NLEV / 8 + 1];
+    const bool sorted = p.state[2] == 0, use_thr = p.state[3] != 0;
+    float coarse[NLEV / 8 + 1], coarse_lev[NLEV / 8 + 1];
 #pragma unroll
-    for (int i = 0; i < NLEV / 8; ++i) coarse[i] = s_lev[8 * i + 7];
-    coarse[NLEV / 8] = 0.0f;
+    for (int i = 0; i < NLEV / 8; ++i) {
+        coarse[i] = s_thr[8 * i + 7];
+        coarse_lev[i] = s_lev[8 * i + 7];
+    }
+    coarse[NLEV / 8] = coarse_lev[NLEV / 8] = 0.0f;
     int changed = 0;
     constexpr int kPer = 4;
     const long long m = p.m;
@@ -432,7 +529,9 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         for (int j = 0; j < kPer; ++j) {
             const long long r = r0 + (long long)j * kFcThreads;
             if (r >= m) continue;
-            const int q = sorted ? nearest_sorted_fast<NLEV>(x[j], s_lev, coarse) : nearest_level(x[j], s_lev, NLEV);
+            const int q = use_thr  ? code_from_thresholds<NLEV>(x[j], s_thr, coarse)
+                          : sorted ? nearest_sorted_fast<NLEV>(x[j], s_lev, coarse_lev)
+                                   : nearest_level(x[j], s_lev, NLEV);
             if (INIT) {
                 p.codes[r] = (uint8_t)q;
                 add_exact(s_dig + q * kFcCols, x[j], 1u);
@@ -519,7 +618,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_sum_kernel(const FcParams p, in
 
 // run state: stop after a round without a changed code, else take the candidates
 __global__ __launch_bounds__(kCbqMaxLevels) void fc_state_kernel(const FcParams p, int nblk) {
-    __shared__ int s_any, s_unsorted;
+    __shared__ int s_any, s_unsorted, s_bad;
     __shared__ float s_lev[kCbqMaxLevels];
     if (fc_done(p)) return;
     const int tid = threadIdx.x, nlev = 1 << p.bits;
@@ -539,6 +638,7 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_state_kernel(const FcParams 
     __syncthreads();
     if (update && tid + 1 < nlev && !(s_lev[tid] <= s_lev[tid + 1])) s_unsorted = 1;
     __syncthreads();
+    if (update) set_thresholds(p, s_lev, nlev, s_unsorted, &s_bad, p.range[0], p.range[1], p.range[2]);  // uniform
     if (tid == 0) {
         if (update) {
             p.state[1] += 1;

@@ -249,19 +249,22 @@ struct FcParams {
     int32_t* rounds_out;   // level updates made, or null
     long long m;
     int bits, iters;
-    float* minmax;         // [grid][2] per-workgroup min, max
+    int thr_mode;          // codes from thresholds: 0 from 2^23 scalars on, 1 never, 2 whenever valid
+    float* minmax;         // [grid][3] per-workgroup min, max, smallest nonzero magnitude
+    float* range;          // [3] the data's min, max, smallest nonzero magnitude
     long long* part;       // [grid][levels][12] per-workgroup digits and counts
     long long* S;          // [levels][12] running exact sums and counts
     float* lev;            // [levels] current levels
     float* lev_next;       // [levels] candidate levels
-    int* state;            // [0] converged, [1] level updates made, [2] levels unsorted
+    float* thr;            // [levels] code thresholds of the current levels (last one +inf)
+    int* state;            // [0] converged, [1] level updates made, [2] levels unsorted, [3] thresholds valid
     int* wg_changed;       // [grid] a code changed in the workgroup
 };
 int fc_grid(long long m);
 inline size_t fc_ws_bytes(long long m, int bits) {
     const size_t G = (size_t)fc_grid(m), nlev = (size_t)1 << bits;
-    return align256(sizeof(float) * 2 * G) + align256(sizeof(long long) * G * nlev * 12) +
-           align256(sizeof(long long) * nlev * 12) + 2 * align256(sizeof(float) * nlev) + align256(sizeof(int) * 4) +
+    return align256(sizeof(float) * (3 * G + 4)) + align256(sizeof(long long) * G * nlev * 12) +
+           align256(sizeof(long long) * nlev * 12) + 3 * align256(sizeof(float) * nlev) + align256(sizeof(int) * 4) +
            align256(sizeof(int) * G);
 }
 hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s);

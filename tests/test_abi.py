@@ -29,7 +29,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 8
+    assert lib.kq_abi_version() == 9
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
@@ -264,10 +264,13 @@ def test_quantize_scalars_argument_errors():
     assert lib.kq_quantize_scalars_workspace_bytes(1 << 31, 6) == 0
 
     def q(**kw):
-        a = dict(v=FAKE, m=1000, bits=6, it=30, codes=FAKE, lev=FAKE, vh=None, r=None, ws=FAKE, wsb=nb)
+        a = dict(v=FAKE, m=1000, bits=6, it=30, codes=FAKE, lev=FAKE, vh=None, r=None, fl=0, ws=FAKE, wsb=nb)
         a.update(kw)
         return lib.kq_quantize_scalars(a["v"], a["m"], a["bits"], a["it"], a["codes"], a["lev"], a["vh"], a["r"],
-                                       a["ws"], a["wsb"], None)
+                                       a["fl"], a["ws"], a["wsb"], None)
+
+    assert q(fl=kq.KQ_F_EXACT_SEARCH | kq.KQ_F_THRESHOLDS) == kq.KQ_ERR_ARG
+    assert q(fl=1) == kq.KQ_ERR_ARG
 
     assert q(bits=0) == kq.KQ_ERR_UNSUPPORTED
     assert q(bits=9) == kq.KQ_ERR_UNSUPPORTED

@@ -50,12 +50,13 @@ def data(kind, m, seed):
 
 
 def check(v, bits, iters, tag):
-    codes, levels, v_hat, rounds = kq.kq_quantize_scalars(dev(v), bits, iters)
     oc, ol, ov, orr = oracle.quantize_scalars(v, bits, iters)
-    assert np.array_equal(host(codes), oc), tag
-    assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), tag
-    assert np.array_equal(host(v_hat).view(np.uint32), ov.view(np.uint32)), tag
-    assert int(host(rounds)[0]) == orr, tag
+    for search in ("auto", "thresholds"):   # the exact search below 2^23, and the threshold path
+        codes, levels, v_hat, rounds = kq.kq_quantize_scalars(dev(v), bits, iters, search=search)
+        assert np.array_equal(host(codes), oc), (tag, search)
+        assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), (tag, search)
+        assert np.array_equal(host(v_hat).view(np.uint32), ov.view(np.uint32)), (tag, search)
+        assert int(host(rounds)[0]) == orr, (tag, search)
 
 
 @pytest.mark.parametrize("m", [1, 2, 9, 1000, 65537])
@@ -100,3 +101,17 @@ def test_fc_quantizer_full_size_fc6_properties():
             mem = x[c == q].astype(np.float64)
             if mem.size:
                 assert L[q] == np.float32(math.fsum(mem.tolist()) / mem.size), q
+
+
+@pytest.mark.parametrize("kind", ["normal", "integers", "tiny"])
+def test_fc_threshold_path_equals_the_exact_search(kind):
+    """From 2^23 scalars on, codes come from per-level thresholds (fp32 comparisons);
+    with KQ_F_EXACT_SEARCH every code comes from the exact fp64 search.  Both agree bit
+    for bit, also on integer data (exact midpoints between levels) and on data whose tiny
+    values make fp64 distances inexact (the thresholds are then not used)."""
+    m = 9 * 932068                                            # 8,388,612 >= 2^23
+    vd = dev(data(kind, m, 77))
+    a = kq.kq_quantize_scalars(vd, 6, 30)
+    b = kq.kq_quantize_scalars(vd, 6, 30, search="exact")
+    for x, y, name in zip(a, b, ["codes", "levels", "v_hat", "rounds"]):
+        assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (kind, name)

@@ -92,6 +92,12 @@ __device__ __forceinline__ void fold_pair(float (&best)[16], const f32x16 (&acc)
     for (int q = 0; q < 16; ++q) best[q] = __builtin_fminf(__builtin_fminf(best[q], acc[0][q]), acc[1][q]);
 }
 
+// the first pair's slot minima, capped at the largest finite float
+__device__ __forceinline__ void first_pair(float (&best)[16], const f32x16 (&acc)[2]) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) best[q] = __builtin_fminf(__builtin_fminf(acc[0][q], acc[1][q]), 3.402823466e38f);
+}
+
 // A operands (entries) of codebook tiles 2 p and 2 p + 1
 __device__ __forceinline__ void lds_a(u32x4 (&a)[2][2], const u32x4* s_a, int p, int lane) {
 #pragma unroll
@@ -167,6 +173,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     load_kernel(p.L[li], t - p.unit_begin[li], wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
     int hl = li;      // fused: the layer whose sums the histogram holds
+    float cnorm = 0.0f;  // square root of the largest |c|^2 of the staged layer's codebook
     if (FUSED) {
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
@@ -196,16 +203,16 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         }
 
         // B operands.  Kernel tile r of this wave is kernels 64 wave + 32 r + (lane % 32), the
-        // kernels of lanes 32 r .. 32 r + 31.  Lane (col, half) needs, for k-step kk, dwords
+        // kernels of lanes 32 r .. 32 r + 31.  A lane past the end holds a copy of the last
+        // kernel and its results are dropped.  Lane (col, half) needs, for k-step kk, dwords
         // 8 kk + 4 half .. + 3 of the column's kernel; dword e packs terms 2e, 2e + 1:
         // [y_h pairs 0..4 | y_m pairs 0..4 | y_h pairs 0..4 | 0].
         u32x4 bop[R][2];
         {
             unsigned H[5], M[5];
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                split2(valid ? xo[2 * q] : 0.0f, valid ? xo[2 * q + 1] : 0.0f, H[q], M[q]);
-            split2(valid ? xo[8] : 0.0f, valid ? 1.0f : 0.0f, H[4], M[4]);
+            for (int q = 0; q < 4; ++q) split2(xo[2 * q], xo[2 * q + 1], H[q], M[q]);
+            split2(xo[8], 1.0f, H[4], M[4]);
             unsigned D[16];
 #pragma unroll
             for (int q = 0; q < 5; ++q) {
@@ -250,9 +257,12 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                         }
                         w[9] = nn;
                         tmax = fmaxf(tmax, nn);
-                    } else {
+                    } else {  // padding: screened far away, and never taken by the rescoring
 #pragma unroll
-                        for (int d = 0; d < kDim; ++d) c[d] = w[d] = 0.0f;
+                        for (int d = 0; d < kDim; ++d) {
+                            c[d] = __builtin_inff();
+                            w[d] = 0.0f;
+                        }
                         w[9] = kPadScore;
                     }
                     unsigned H[5], M[5], A[16];
@@ -288,19 +298,31 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                 }
                 __syncthreads();
                 staged = resident ? li : -1;
+                if (c0 + cn >= kpad) {  // the whole codebook has been seen: its largest norm
+                    float cm2 = s_wmax[0];
+#pragma unroll
+                    for (int w = 1; w < kAssignWaves; ++w) cm2 = fmaxf(cm2, s_wmax[w]);
+                    cnorm = __builtin_amdgcn_sqrtf(cm2);
+                }
             }
 
-            // slot minima over the chunk, two codebook tiles per step
+            // slot minima over the chunk (cn >= 64), two codebook tiles per step; the first
+            // pair starts them, capped at the largest finite float so that packing keeps a number
             float best[R][16];
-#pragma unroll
-            for (int r = 0; r < R; ++r)
-#pragma unroll
-                for (int q = 0; q < 16; ++q) best[r][q] = 3.402823466e38f;  // finite: packing keeps a number
             const int npair = cn >> 6;
             u32x4 aN[2][2];
-            lds_a(aN, s_a, 0, lane);
+            {
+                u32x4 a[2][2];
+                lds_a(a, s_a, 0, lane);
+                lds_a(aN, s_a, min(1, npair - 1), lane);  // the next pair's operands
+                f32x16 acc[R][2];
+#pragma unroll
+                for (int r = 0; r < R; ++r) score_pair(acc[r], a, bop[r]);
+#pragma unroll
+                for (int r = 0; r < R; ++r) first_pair(best[r], acc[r]);
+            }
 #pragma unroll 1
-            for (int tp = 0; tp < npair; ++tp) {
+            for (int tp = 1; tp < npair; ++tp) {
                 u32x4 a[2][2];
 #pragma unroll
                 for (int u = 0; u < 2; ++u)
@@ -340,8 +362,9 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             const int slot = 8 * (qs >> 2) + (qs & 3) + (hi1 < lo1 ? 4 : 0);
 
             // exact fp32 rescoring of the winning slot's entries, in increasing index order
+            // (padding rows are +inf: never taken)
             float bd = __builtin_inff();
-            int bj = 0x7fffffff;
+            int bt = -1;  // tile of the best entry so far
             const int ntile = cn >> 5;  // the same trip count in every lane
 #pragma unroll 4
             for (int tq = 0; tq < ntile; ++tq) {
@@ -350,21 +373,19 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                 const float c8 = s_cf[jl * kRowFloats + 8];
                 const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], c8};
                 const float d = sqdist9(xo, c);
-                const bool take = (c0 + jl < k) && (d < bd);
+                const bool take = d < bd;
                 bd = take ? d : bd;
-                bj = take ? c0 + jl : bj;
+                bt = take ? tq : bt;
             }
+            const int bj = bt < 0 ? 0x7fffffff : c0 + slot + 32 * bt;
             merge_top2(rb, rs, rj, rd, M1, M2, bj, bd);
         }
 
         float xn2 = 0.0f;
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xn2 = __fmaf_rn(xo[d], xo[d], xn2);
-        float cm2 = s_wmax[0];
-#pragma unroll
-        for (int w = 1; w < kAssignWaves; ++w) cm2 = fmaxf(cm2, s_wmax[w]);
         // Q only scales the guard, which has a 13 % margin: the hardware square root will do
-        const float rr = __builtin_amdgcn_sqrtf(xn2) + __builtin_amdgcn_sqrtf(cm2);
+        const float rr = __builtin_amdgcn_sqrtf(xn2) + cnorm;
         const float q2 = rr * rr;
         const float theta = 0x1p-13f * q2 + 0x1p-100f;
 
@@ -430,9 +451,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         }
 
         if (L.part) {
-            double v = valid ? (double)dist : 0.0;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+            const double v = wave_sum_f64(valid ? (double)dist : 0.0);
             if (lane == 0) L.part[lt * kAssignWaves + wave] = v;
         }
 

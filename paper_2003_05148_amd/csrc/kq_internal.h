@@ -186,6 +186,37 @@ __device__ __forceinline__ int find_layer(const StackParams& p, int u) {
     return l;
 }
 
+// v plus the value that DPP control CTL brings from another lane of the row
+template <int CTL>
+__device__ __forceinline__ double dpp_add(double v) {
+    const unsigned plo = __builtin_amdgcn_update_dpp(0u, (unsigned)__double2loint(v), CTL, 0xF, 0xF, false);
+    const unsigned phi = __builtin_amdgcn_update_dpp(0u, (unsigned)__double2hiint(v), CTL, 0xF, 0xF, false);
+    return v + __hiloint2double((int)phi, (int)plo);
+}
+// v summed over the 64 lanes by the butterfly of partner offsets 32, 16, 8, 4, 2, 1; every
+// lane gets the total and the lanes agree bit for bit.  The partners come from the half and
+// row swaps and from DPP moves inside a row, not from LDS permutes.  Offset 4 uses a rotation
+// by four lanes, which meets the lane 4 apart or 12 apart; the offset-8 step has already made
+// those two equal, so each step adds the same two numbers as a plain exchange would.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+    unsigned lo = (unsigned)__double2loint(v), hi = (unsigned)__double2hiint(v);
+    {
+        const auto a = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        v = __hiloint2double((int)b[0], (int)a[0]) + __hiloint2double((int)b[1], (int)a[1]);
+    }
+    lo = (unsigned)__double2loint(v), hi = (unsigned)__double2hiint(v);
+    {
+        const auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        v = __hiloint2double((int)b[0], (int)a[0]) + __hiloint2double((int)b[1], (int)a[1]);
+    }
+    v = dpp_add<0x128>(v);  // row_ror:8
+    v = dpp_add<0x124>(v);  // row_ror:4
+    v = dpp_add<0x4E>(v);   // quad_perm [2,3,0,1]
+    return dpp_add<0xB1>(v);  // quad_perm [1,0,3,2]
+}
+
 // Sum of m fp64 values in a fixed order by a workgroup of NT threads (a multiple of 64):
 // thread t adds values t, t + NT, ... in turn, each wave combines its lanes with a
 // butterfly, and thread 0 adds the wave totals in wave order.  Every thread of the

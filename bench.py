@@ -218,7 +218,12 @@ def main():
     ms_step = 1e3 * elapsed / args.steps
     # Per-launch durations: one more step with HIP events around every launch on the stream
     # the kernels run on.  It is kept out of the timed steps above because an event record
-    # between two kernels adds a few microseconds of its own to the step.
+    # between two kernels adds a few microseconds of its own to the step.  Two untimed steps
+    # are queued first: the host then enqueues the event step while the GPU still works
+    # through them, so every event is stamped by the GPU's progress and not by a host that
+    # is slower than the kernels it launches.
+    for _ in range(2):
+        step(False)
     step(True)
     torch.cuda.synchronize()
 
@@ -228,6 +233,7 @@ def main():
     for i in range(len(layers)):
         gst.idx[i].copy_(st.idx[i])
     kq.kq_codebook_grad_step_stack(gst, 0.01)
+    step(False)  # queued GPU work ahead of the events, as above
     g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     g0.record(stream)
     for _ in range(5):

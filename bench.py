@@ -153,7 +153,7 @@ def main():
     # the member sums come with the assignment when every codebook fits the fused variant
     fused = max(L.k for L in layers) <= 256 and not args.unfused
     stream = torch.cuda.current_stream(dev)
-    ev = {"assign": [], "update": [], "cbq": [], "pack": [], "reconstruct": [], "fit": []}
+    ev = {"assign": [], "assign_final": [], "update": [], "cbq": [], "pack": [], "reconstruct": [], "fit": []}
     if args.yinyang:
         C0_views = [v.view(-1, 9) for v in torch.split(C0flat, sizes)]
         yy_ws = [torch.empty(kq.lib.kq_yinyang_workspace_bytes(L.n, L.k, 0), dtype=torch.uint8, device=dev)
@@ -192,7 +192,8 @@ def main():
             kq.kq_assign_stack(st, dist_slot=t, distortion=False, fused_sums=fused and t < T)
             if record:
                 a1.record(stream)
-                ev["assign"].append((a0, a1))
+                # the rounds' launches (fused when the sums come with them) and the final one apart
+                ev["assign" if t < T else "assign_final"].append((a0, a1))
             if t < T:
                 if record:
                     u0, u1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -276,7 +277,7 @@ def main():
     mse_kc = [float(s) / (9 * L.n) for s, L in zip(sq.cpu(), layers)]
     print(json.dumps({"diag": {
         "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_GBps": upd_gbs,
-        "lloyd_round_ms": assign_ms + update_ms, "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
+        "lloyd_round_ms": assign_ms + update_ms, "final_assign_ms": mean_ms["assign_final"], "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
         "reconstruct_ms": mean_ms["reconstruct"],
         "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9 if mean_ms["reconstruct"] else 0.0,
         "grad_step_ms": grad_ms, "grad_step_GBps": 40.0 * n_total / (grad_ms * 1e-3) / 1e9,
@@ -303,8 +304,9 @@ def main():
                    "layers": len(layers), "kernels": n_total, "k": k, "lloyd_rounds": T, "codebook_bits": 6},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS,
-                     "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) else None,
-                     "kernel": "assign_kernel (one launch per Lloyd round, whole stack)"},
+                     "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) and fused else None,
+                     "kernel": ("assign_kernel<2, true> (member sums fused)" if fused else "assign_kernel<2, false>")
+                               + " averaged over the Lloyd rounds' launches (one per round, whole stack)"},
     }
     if args.yinyang:
         # distances the Yinyang fits evaluated (matrix-core round 0 + exact fp32 scans), 18 flop

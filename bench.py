@@ -58,6 +58,11 @@ def parse():
                          "into the assignment)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
+    ap.add_argument("--row", choices=["lloyd", "fc", "search"], default="lloyd",
+                    help="lloyd: the step above (default); fc: the fully-connected-layer quantizer "
+                         "(kq_quantize_scalars, 6 bits, 30 rounds) on the VGG-16 fc6/fc7/fc8 shapes; "
+                         "search: the codebook-size search (kq_search_codebook_size) on the "
+                         "ResNet-18 conv1 shape")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device to device three times (a plain copy "
                          "kernel of known size, the scale for hardware byte counters)")
@@ -105,6 +110,59 @@ def cpu_baseline(layers, iters, budget=1e9):
                       f"({n} kernels, k={layers[0].k}), {dt:.1f} s"}
 
 
+def bench_fc(args, kq, torch):
+    """kq_quantize_scalars on N(0, 2/fan_in) weights of the VGG-16 fully-connected shapes."""
+    import math
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(6)
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for name, (o, i) in [("fc6", (4096, 25088)), ("fc7", (4096, 4096)), ("fc8", (1000, 4096))]:
+        m = o * i
+        v = torch.randn(m, device=dev, generator=g) * math.sqrt(2.0 / i)
+        out = kq.kq_quantize_scalars(v, 6, 30)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            out = kq.kq_quantize_scalars(v, 6, 30)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        r = int(out[3].item())
+        rows.append({"layer": name, "scalars": m, "rounds": r, "ms": ms, "us_per_pass": 1e3 * ms / (r + 1),
+                     "GBps_at_5B_per_scalar_pass": 5.0 * m * (r + 1) / (ms * 1e-3) / 1e9})
+    tot_ms = sum(r_["ms"] for r_ in rows)
+    print(json.dumps({"metric": "FC-layer 6-bit scalar quantization: scalars per second (30 rounds)",
+                      "value": sum(r_["scalars"] for r_ in rows) / (tot_ms * 1e-3), "unit": "scalars/s",
+                      "n_gpus": 1, "steps": args.steps, "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": "VGG-16 fc6 25088x4096, fc7 4096x4096, fc8 4096x1000, N(0, 2/fan_in)"},
+                      "rows": rows}))
+
+
+def bench_search(args, kq, torch, synth):
+    """kq_search_codebook_size on the ResNet-18 conv1 shape (alpha = 0.3, r = 0.5, 8
+    iterations, 30 Lloyd rounds per fit)."""
+    dev = torch.device("cuda:0")
+    L = synth.resnet18_stack(k=256, layers=1)[0]
+    n_init = int(0.3 * L.n)
+    cand = L.X[synth.distinct_init(L.X, n_init, 7)]
+    Xd, Cd = torch.from_numpy(L.X).to(dev), torch.from_numpy(cand).to(dev)
+    kq.kq_search_codebook_size(Xd, Cd, 0.5, 8, 30)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        k, C, idx, trials, d0 = kq.kq_search_codebook_size(Xd, Cd, 0.5, 8, 30)
+    torch.cuda.synchronize()
+    ms = 1e3 * (time.perf_counter() - t0) / args.steps
+    print(json.dumps({"metric": "codebook-size search: fits per second (30 Lloyd rounds each)",
+                      "value": (len(trials) + 1) / (ms * 1e-3), "unit": "fits/s", "n_gpus": 1,
+                      "steps": args.steps, "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": f"resnet18 conv1 64x64 ({L.n} kernels), n_init {n_init}, "
+                                             "r = 0.5, 8 iterations"},
+                      "ms_per_search": ms, "k": int(k), "trials": [int(t[0]) for t in trials]}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -120,6 +178,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.row == "fc":
+        return bench_fc(args, kq, torch)
+    if args.row == "search":
+        return bench_search(args, kq, torch, synth)
     gen, k_default, iters_default, desc = CONFIGS[args.config]
     k = args.k if args.k is not None else k_default
     T = args.iters if args.iters is not None else iters_default

@@ -318,8 +318,11 @@ def main():
     rec_bytes = sum(L.n * (b / 8 + 36 + 36) for L, b in zip(layers, bits))  # packed index + reference + output row
     flops = 18.0 * sum(L.k * L.n for L in layers)   # 9 multiply-adds per (kernel, entry) pair
     achieved = flops / (assign_ms * 1e-3) / 1e12 if assign_ms > 0 else 0.0
-    upd_bytes = 40.0 * n_total                      # 36-byte kernel + 4-byte index per kernel
-    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9 if update_ms > 0 else 0.0
+    # the separate update reads a 36-byte kernel and a 4-byte index per kernel; with fused
+    # sums the round's update is only the finish over the assignment's partial sums, so no
+    # kernel bytes are credited to it
+    upd_bytes = 40.0 * n_total
+    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9 if update_ms > 0 and not fused else None
 
     yy_diag = None
     if args.yinyang:
@@ -338,7 +341,8 @@ def main():
     mse_k = [j / (9 * L.n) for j, L in zip(J, layers)]
     mse_kc = [float(s) / (9 * L.n) for s, L in zip(sq.cpu(), layers)]
     print(json.dumps({"diag": {
-        "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_GBps": upd_gbs,
+        "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_is_finish_only": fused,
+        "update_GBps": upd_gbs,
         "lloyd_round_ms": assign_ms + update_ms, "final_assign_ms": mean_ms["assign_final"], "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
         "reconstruct_ms": mean_ms["reconstruct"],
         "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9 if mean_ms["reconstruct"] else 0.0,

@@ -380,6 +380,38 @@ def test_reconstruct_stack_and_errors(packed):
         assert e1 == pytest.approx(single, rel=1e-12), (n, k)
 
 
+@pytest.mark.parametrize("packed", [False, True])
+def test_reconstruct_unaligned_views(packed):
+    """Output, reference and index arrays that start 4 bytes past a 16-byte boundary:
+    W_hat bit-exact against the oracle's gather, the squared error within 1e-12."""
+    rng = np.random.default_rng(23)
+    shapes = [(4097, 256), (913, 16), (300, 4096)]
+    layers, refs = [], []
+    for n, k in shapes:
+        C = rng.standard_normal((k, 9)).astype(np.float32)
+        idx = rng.integers(0, k, n).astype(np.int32)
+        Wref = rng.standard_normal((n, 9)).astype(np.float32)
+        wbuf = torch.empty(n * 9 + 1, dtype=torch.float32, device=DEV)
+        rbuf = torch.empty(n * 9 + 1, dtype=torch.float32, device=DEV)
+        rbuf[1:].copy_(dev(Wref).reshape(-1))
+        L = {"C": dev(C), "n": n, "W_ref": rbuf[1:].view(n, 9), "W_hat": wbuf[1:].view(n, 9),
+             "sq_error": torch.zeros(1, dtype=torch.float64, device=DEV)}
+        if packed:
+            L["packed"], L["bits"] = kq.kq_pack_bits(dev(idx), oracle.index_bits(k)), oracle.index_bits(k)
+        else:
+            ibuf = torch.empty(n + 1, dtype=torch.int32, device=DEV)
+            ibuf[1:].copy_(dev(idx))
+            L["idx"] = ibuf[1:]
+        layers.append(L)
+        refs.append((oracle.reconstruct(idx, C), Wref))
+    kq.kq_reconstruct_stack(layers)
+    for L, (ref, Wref), (n, k) in zip(layers, refs, shapes):
+        assert L["W_hat"].data_ptr() % 16 == 4
+        assert np.array_equal(host(L["W_hat"]).view(np.uint32), ref.view(np.uint32)), (n, k)
+        exact = float(np.sum((Wref.astype(np.float64) - ref.astype(np.float64)) ** 2))
+        assert float(host(L["sq_error"])[0]) == pytest.approx(exact, rel=1e-12), (n, k)
+
+
 @pytest.mark.parametrize("which", ["resnet18_k256", "vgg16_k64_mixed"])
 def test_fused_sums_equal_the_separate_update(which):
     """Assignment with fused member sums + finish-only update gives the same codebooks,

@@ -92,6 +92,43 @@ __device__ __forceinline__ void fold_pair(float (&best)[16], const f32x16 (&acc)
     for (int q = 0; q < 16; ++q) best[q] = __builtin_fminf(__builtin_fminf(best[q], acc[0][q]), acc[1][q]);
 }
 
+// (d, j) becomes the lexicographic minimum of the pair and its partner's (o_d, o_j); a
+// partner holding the same pair leaves it unchanged, so both lanes end with the same pair
+__device__ __forceinline__ void argmin_take(float& d, int& j, float od, int oj) {
+    const bool take = od < d || (od == d && oj < j);
+    d = take ? od : d;
+    j = take ? oj : j;
+}
+template <int CTL>
+__device__ __forceinline__ void argmin_dpp(float& d, int& j) {
+    const float od = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(d), CTL, 0xF, 0xF, false));
+    const int oj = __builtin_amdgcn_update_dpp(0, j, CTL, 0xF, 0xF, false);
+    argmin_take(d, j, od, oj);
+}
+// the wave's lexicographic minimum of the lanes' (distance, index) pairs, in every lane:
+// partners 32 and 16 lanes away by the half and row swaps, then DPP moves inside a row
+// (the rotation by four meets a lane that holds the same pair as the lane 4 away)
+__device__ __forceinline__ void wave_argmin(float& d, int& j) {
+    {
+        const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+        const auto b = __builtin_amdgcn_permlane32_swap((unsigned)j, (unsigned)j, false, false);
+        d = __uint_as_float(a[0]);
+        j = (int)b[0];
+        argmin_take(d, j, __uint_as_float(a[1]), (int)b[1]);
+    }
+    {
+        const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(d), __float_as_uint(d), false, false);
+        const auto b = __builtin_amdgcn_permlane16_swap((unsigned)j, (unsigned)j, false, false);
+        d = __uint_as_float(a[0]);
+        j = (int)b[0];
+        argmin_take(d, j, __uint_as_float(a[1]), (int)b[1]);
+    }
+    argmin_dpp<0x128>(d, j);  // row_ror:8
+    argmin_dpp<0x124>(d, j);  // row_ror:4
+    argmin_dpp<0x4E>(d, j);   // quad_perm [2,3,0,1]
+    argmin_dpp<0xB1>(d, j);   // quad_perm [1,0,3,2]
+}
+
 // the first pair's slot minima, capped at the largest finite float
 __device__ __forceinline__ void first_pair(float (&best)[16], const f32x16 (&acc)[2]) {
 #pragma unroll
@@ -403,37 +440,35 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         while (fl) {
             const int f = __ffsll((long long)fl) - 1;
             fl &= fl - 1;
-            float xf[kDim];
+            float xf[kDim];  // lane f's kernel, the same in every lane (f is uniform)
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) xf[d] = __shfl(xo[d], f);
+            for (int d = 0; d < kDim; ++d)
+                xf[d] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xo[d]), f));
+            // each lane scans entries lane, lane + 64, ... in increasing order (strict <: the
+            // lowest index among equal distances), then the lanes' (distance, index) pairs
+            // meet in their lexicographic minimum
             float fd = __builtin_inff();
             int fj = 0x7fffffff;
-            for (int jj = lane; jj < k; jj += kWave) {
-                float c[kDim];
-                if (resident) {  // the rows are still staged in LDS
+            if (resident) {  // the rows are still staged in LDS
+                for (int jj = lane; jj < k; jj += kWave) {
                     const f32x4 r0 = s_c[jj * 3 + 0], r1 = s_c[jj * 3 + 1];
-                    c[0] = r0[0], c[1] = r0[1], c[2] = r0[2], c[3] = r0[3];
-                    c[4] = r1[0], c[5] = r1[1], c[6] = r1[2], c[7] = r1[3];
-                    c[8] = s_cf[jj * kRowFloats + 8];
-                } else {
+                    const float c8 = s_cf[jj * kRowFloats + 8];
+                    const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], c8};
+                    const float d = sqdist9(xf, c);
+                    fj = d < fd ? jj : fj;
+                    fd = d < fd ? d : fd;
+                }
+            } else {
+                for (int jj = lane; jj < k; jj += kWave) {
+                    float c[kDim];
 #pragma unroll
                     for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)jj * kDim + d];
-                }
-                const float d = sqdist9(xf, c);
-                if (d < fd) {
-                    fd = d;
-                    fj = jj;
+                    const float d = sqdist9(xf, c);
+                    fj = d < fd ? jj : fj;
+                    fd = d < fd ? d : fd;
                 }
             }
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                const float od = __shfl_xor(fd, off);
-                const int oj = __shfl_xor(fj, off);
-                if (od < fd || (od == fd && oj < fj)) {
-                    fd = od;
-                    fj = oj;
-                }
-            }
+            wave_argmin(fd, fj);
             if (lane == f) {
                 if (fj == 0x7fffffff) fj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
                 L.idx[i] = fj;

@@ -10,6 +10,8 @@
 // by the exact weight total in fp64 and rounded to fp32.  Grid, codes and level
 // updates use only correctly rounded fp64 operations, so the codes and levels are
 // a pure function of the codebook and the weights.
+#include <type_traits>
+
 #include "kq_internal.h"
 
 namespace kq {
@@ -401,12 +403,37 @@ __global__ __launch_bounds__(kFcThreads) void fc_minmax_kernel(const FcParams p)
     __shared__ float s_lo[kFcThreads / kWave], s_hi[kFcThreads / kWave], s_sm[kFcThreads / kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float lo = __builtin_inff(), hi = -__builtin_inff(), sm = __builtin_inff();
-    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads) {
-        const float x = p.v[r];
+    auto take = [&](float x) {
         lo = fminf(lo, x);
         hi = fmaxf(hi, x);
         if (x != 0.0f) sm = fminf(sm, fabsf(x));
+    };
+    long long r0 = 0;  // scalars from here on: one at a time
+    if ((reinterpret_cast<uintptr_t>(p.v) & 15u) == 0) {  // float4 groups, four per thread in flight
+        constexpr int kPer = 4;
+        const long long ng = p.m >> 2;
+        const float4* __restrict__ v4 = reinterpret_cast<const float4*>(p.v);
+        for (long long g0 = (long long)blockIdx.x * kFcThreads * kPer + tid; g0 < ng;
+             g0 += (long long)gridDim.x * kFcThreads * kPer) {
+            float4 xv[kPer];
+#pragma unroll
+            for (int j = 0; j < kPer; ++j) {
+                const long long g = g0 + (long long)j * kFcThreads;
+                xv[j] = g < ng ? v4[g] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+#pragma unroll
+            for (int j = 0; j < kPer; ++j)
+                if (g0 + (long long)j * kFcThreads < ng) {
+                    take(xv[j].x);
+                    take(xv[j].y);
+                    take(xv[j].z);
+                    take(xv[j].w);
+                }
+        }
+        r0 = 4 * ng;
     }
+    for (long long r = r0 + (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads)
+        take(p.v[r]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         lo = fminf(lo, __shfl_xor(lo, off));
@@ -489,13 +516,17 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p
 // Each thread takes four scalars per step (r0 + 256 j, consecutive lanes consecutive
 // scalars), their loads issued together; with sorted levels a code is the number of
 // thresholds at or below the value (fp32 comparisons only).
-template <bool INIT, int NLEV>
+// THR: the launch for rounds whose codes come from thresholds (true) or from the exact
+// searches (false); the state decides on the device, and the other launch returns at once.
+// Apart, the light threshold code keeps its register count low.
+template <bool INIT, int NLEV, bool THR>
 __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p) {
     __shared__ __attribute__((aligned(16))) float s_lev[NLEV < 8 ? 8 : NLEV];
     __shared__ __attribute__((aligned(16))) float s_thr[NLEV < 8 ? 8 : NLEV];
     __shared__ unsigned long long s_dig[NLEV * kFcCols];
     __shared__ int s_changed;
     if (fc_done(p)) return;
+    if ((p.state[3] != 0) != THR) return;  // the other launch codes this round
     const int tid = threadIdx.x;
     for (int e = tid; e < NLEV; e += kFcThreads) {
         s_lev[e] = p.lev[e];
@@ -504,7 +535,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
     if (tid == 0) s_changed = 0;
     __syncthreads();
-    const bool sorted = p.state[2] == 0, use_thr = p.state[3] != 0;
+    const bool sorted = p.state[2] == 0;
     float coarse[NLEV / 8 + 1], coarse_lev[NLEV / 8 + 1];
 #pragma unroll
     for (int i = 0; i < NLEV / 8; ++i) {
@@ -515,37 +546,100 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     int changed = 0;
     constexpr int kPer = 4;
     const long long m = p.m;
-    const long long step = (long long)gridDim.x * kFcThreads * kPer;
-    for (long long r0 = (long long)blockIdx.x * kFcThreads * kPer + tid; r0 < m; r0 += step) {
-        float x[kPer];
-        int c[kPer];
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            const long long r = r0 + (long long)j * kFcThreads;
-            x[j] = r < m ? p.v[r] : 0.0f;
-            c[j] = (!INIT && r < m) ? (int)p.codes[r] : 0;
-        }
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            const long long r = r0 + (long long)j * kFcThreads;
-            if (r >= m) continue;
-            const int q = use_thr  ? code_from_thresholds<NLEV>(x[j], s_thr, coarse)
-                          : sorted ? nearest_sorted_fast<NLEV>(x[j], s_lev, coarse_lev)
-                                   : nearest_level(x[j], s_lev, NLEV);
+    // one instantiation per search (thresholds, sorted levels, full scan): the choice is
+    // the same for every scalar of the round
+    auto run = [&](auto mode) {
+        constexpr int kMode = decltype(mode)::value;
+        // the code of scalar x (old code c); moves its exact contribution when the code changes
+        auto recode = [&](float x, int c) {
+            const int q = kMode == 0   ? code_from_thresholds<NLEV>(x, s_thr, coarse)
+                          : kMode == 1 ? nearest_sorted_fast<NLEV>(x, s_lev, coarse_lev)
+                                       : nearest_level(x, s_lev, NLEV);
             if (INIT) {
-                p.codes[r] = (uint8_t)q;
-                add_exact(s_dig + q * kFcCols, x[j], 1u);
+                add_exact(s_dig + q * kFcCols, x, 1u);
                 atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
-            } else if (q != c[j]) {
-                p.codes[r] = (uint8_t)q;
-                add_exact(s_dig + c[j] * kFcCols, -x[j], 1u);
-                add_exact(s_dig + q * kFcCols, x[j], 1u);
-                atomicAdd(&s_dig[c[j] * kFcCols + kDigits], (unsigned long long)-1ll);
+            } else if (q != c) {
+                add_exact(s_dig + c * kFcCols, -x, 1u);
+                add_exact(s_dig + q * kFcCols, x, 1u);
+                atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)-1ll);
                 atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
                 changed = 1;
             }
+            return q;
+        };
+        if ((reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 && (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
+            // groups of four scalars: one float4 of values and one word of four codes per
+            // group, kPer groups per thread, the next step's loaded while this one is coded;
+            // a group whose codes change stores its word
+            const long long ng = m >> 2;
+            const long long step = (long long)gridDim.x * kFcThreads * kPer;
+            const float4* __restrict__ v4 = reinterpret_cast<const float4*>(p.v);
+            unsigned* __restrict__ c4 = reinterpret_cast<unsigned*>(p.codes);
+            auto load = [&](long long g0, float4 (&xv)[kPer], unsigned (&cw)[kPer]) {
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    const long long g = g0 + (long long)j * kFcThreads;
+                    xv[j] = g < ng ? v4[g] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    cw[j] = (!INIT && g < ng) ? c4[g] : 0u;
+                }
+            };
+            long long g0 = (long long)blockIdx.x * kFcThreads * kPer + tid;
+            float4 xv[kPer];
+            unsigned cw[kPer];
+            if (g0 < ng) load(g0, xv, cw);
+            for (; g0 < ng; g0 += step) {
+                float4 xn[kPer];
+                unsigned cn[kPer];
+                if (g0 + step < ng) load(g0 + step, xn, cn);
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    const long long g = g0 + (long long)j * kFcThreads;
+                    if (g >= ng) continue;
+                    const float xs[4] = {xv[j].x, xv[j].y, xv[j].z, xv[j].w};
+                    unsigned nw = 0u;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        nw |= (unsigned)recode(xs[e], (int)((cw[j] >> (8 * e)) & 255u)) << (8 * e);
+                    if (INIT || nw != cw[j]) c4[g] = nw;
+                }
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    xv[j] = xn[j];
+                    cw[j] = cn[j];
+                }
+            }
+            if (blockIdx.x == 0)  // the last m % 4 scalars
+                for (long long r = 4 * ng + tid; r < m; r += kFcThreads) {
+                    const int q = recode(p.v[r], INIT ? 0 : (int)p.codes[r]);
+                    if (INIT || q != (int)p.codes[r]) p.codes[r] = (uint8_t)q;
+                }
+        } else {
+            const long long step = (long long)gridDim.x * kFcThreads * kPer;
+            for (long long r0 = (long long)blockIdx.x * kFcThreads * kPer + tid; r0 < m; r0 += step) {
+                float x[kPer];
+                int c[kPer];
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    const long long r = r0 + (long long)j * kFcThreads;
+                    x[j] = r < m ? p.v[r] : 0.0f;
+                    c[j] = (!INIT && r < m) ? (int)p.codes[r] : 0;
+                }
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    const long long r = r0 + (long long)j * kFcThreads;
+                    if (r >= m) continue;
+                    const int q = recode(x[j], c[j]);
+                    if (INIT || q != c[j]) p.codes[r] = (uint8_t)q;
+                }
+            }
         }
-    }
+    };
+    if (THR)
+        run(std::integral_constant<int, 0>{});
+    else if (sorted)
+        run(std::integral_constant<int, 1>{});
+    else
+        run(std::integral_constant<int, 2>{});
     if (changed) s_changed = 1;
     __syncthreads();
     unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * NLEV * kFcCols;
@@ -555,10 +649,13 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
 
 template <bool INIT>
 hipError_t launch_fc_assign(const FcParams& p, int G, hipStream_t s) {
+    // the threshold launch only where the state may choose thresholds
+    const bool thr = p.thr_mode == 2 || (p.thr_mode == 0 && p.m >= kFcThresholdMin);
     switch (p.bits) {
-#define KQ_FC_CASE(B)                                                                                    \
-    case B:                                                                                              \
-        hipLaunchKernelGGL((fc_assign_kernel<INIT, (1 << B)>), dim3(G), dim3(kFcThreads), 0, s, p); \
+#define KQ_FC_CASE(B)                                                                                          \
+    case B:                                                                                                    \
+        if (thr) hipLaunchKernelGGL((fc_assign_kernel<INIT, (1 << B), true>), dim3(G), dim3(kFcThreads), 0, s, p); \
+        hipLaunchKernelGGL((fc_assign_kernel<INIT, (1 << B), false>), dim3(G), dim3(kFcThreads), 0, s, p);       \
         break;
         KQ_FC_CASE(1)
         KQ_FC_CASE(2)
@@ -659,7 +756,32 @@ __global__ __launch_bounds__(kFcThreads) void fc_output_kernel(const FcParams p)
         if (tid == 0 && p.rounds_out) *p.rounds_out = p.state[1];
     }
     if (!p.v_hat) return;
-    for (long long r = (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads)
+    long long r0 = 0;  // scalars from here on: one at a time
+    if ((reinterpret_cast<uintptr_t>(p.v_hat) & 15u) == 0 && (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
+        // a word of four codes in, a float4 out; four groups per thread in flight
+        constexpr int kPer = 4;
+        const long long ng = p.m >> 2;
+        const unsigned* __restrict__ c4 = reinterpret_cast<const unsigned*>(p.codes);
+        float4* __restrict__ o4 = reinterpret_cast<float4*>(p.v_hat);
+        for (long long g0 = (long long)blockIdx.x * kFcThreads * kPer + tid; g0 < ng;
+             g0 += (long long)gridDim.x * kFcThreads * kPer) {
+            unsigned cw[kPer];
+#pragma unroll
+            for (int j = 0; j < kPer; ++j) {
+                const long long g = g0 + (long long)j * kFcThreads;
+                cw[j] = g < ng ? c4[g] : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < kPer; ++j) {
+                const long long g = g0 + (long long)j * kFcThreads;
+                if (g < ng)
+                    o4[g] = make_float4(s_lev[cw[j] & 255u], s_lev[(cw[j] >> 8) & 255u], s_lev[(cw[j] >> 16) & 255u],
+                                        s_lev[cw[j] >> 24]);
+            }
+        }
+        r0 = 4 * ng;
+    }
+    for (long long r = r0 + (long long)blockIdx.x * kFcThreads + tid; r < p.m; r += (long long)gridDim.x * kFcThreads)
         p.v_hat[r] = s_lev[p.codes[r]];
 }
 

@@ -183,13 +183,43 @@ __device__ __forceinline__ float key_value(unsigned k) {
 // Searched within the data range [vmin, vmax] only, and used only where every fp64
 // distance |v - L| there is exact (see exact_floor): rounding could otherwise make
 // distances to distinct levels equal for far values and send them to a lower index.
+// The boundary lies next to the midpoint of levels q and q + 1, so the search starts there:
+// it steps away from the midpoint by 1, 2, 4, ... keys until the code crosses q, then
+// bisects the last step.  Every probe keeps code(lo) <= q < code(hi), and the code does not
+// decrease with the value, so the answer is the same as bisecting [vmin, vmax] from the
+// start; the midpoint only saves probes (about 5 instead of 32).
 __device__ float code_threshold(int q, const float* lev, int nlev, float vmin, float vmax) {
     unsigned lo = ordered_key(vmin), hi = ordered_key(vmax);
-    if (nearest_sorted(key_value(hi), lev, nlev) <= q) return __builtin_inff();
-    if (nearest_sorted(key_value(lo), lev, nlev) > q) return key_value(lo);
+    auto above = [&](unsigned key) { return nearest_sorted(key_value(key), lev, nlev) > q; };
+    if (!above(hi)) return __builtin_inff();
+    if (above(lo)) return key_value(lo);
+    if (q + 1 < nlev) {
+        const unsigned g = ordered_key((float)(0.5 * ((double)lev[q] + (double)lev[q + 1])));
+        if (g > lo && g < hi) {
+            if (above(g)) {  // the boundary is at g or below: step down from g
+                hi = g;
+                for (unsigned st = 1u; hi - lo > st; st *= 2u) {
+                    if (!above(hi - st)) {
+                        lo = hi - st;
+                        break;
+                    }
+                    hi -= st;
+                }
+            } else {  // above g: step up from g
+                lo = g;
+                for (unsigned st = 1u; hi - lo > st; st *= 2u) {
+                    if (above(lo + st)) {
+                        hi = lo + st;
+                        break;
+                    }
+                    lo += st;
+                }
+            }
+        }
+    }
     while (hi - lo > 1u) {  // code(lo) <= q < code(hi)
         const unsigned mid = lo + (hi - lo) / 2u;
-        if (nearest_sorted(key_value(mid), lev, nlev) > q)
+        if (above(mid))
             hi = mid;
         else
             lo = mid;

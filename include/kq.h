@@ -90,7 +90,7 @@ typedef enum kq_status {
                                 assignment (every k <= 256, else KQ_ERR_UNSUPPORTED) */
 #define KQ_F_EXACT_SEARCH 16u /* kq_quantize_scalars: every code by the exact fp64 search (reference) */
 #define KQ_F_THRESHOLDS 32u  /* kq_quantize_scalars: codes from level thresholds at any size, wherever
-                                they are valid (by default only from 2^23 scalars on) */
+                                they are valid (by default only from 3 * 2^20 scalars on) */
 #define KQ_F_SUMS_FROM_ASSIGN 8u
                              /* kq_update_stack: finish the update from the sums the preceding
                                 kq_assign_stack with KQ_F_FUSED_SUMS left (same layers and
@@ -218,8 +218,9 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
  *   result is a pure function of v: bit for bit that of kq_quantize_codebook on the same
  *   scalars with unit weights.
  *   With sorted levels the code of a value never decreases as the value grows, so from
- *   2^23 scalars on each round first finds, per level boundary, the smallest value that
- *   takes the next code (bisection over fp32 values with the exact search) and then codes
+ *   3 * 2^20 scalars on each round first finds, per level boundary, the smallest value that
+ *   takes the next code (a search over fp32 values with the exact search, started at the
+ *   midpoint of the two levels) and then codes
  *   every scalar with fp32 comparisons only.  This is used only where every fp64 distance
  *   between a data value and a level is exact (no nonzero value or level below 2^-29 of the
  *   largest magnitude), so it gives the exact search's codes; KQ_F_EXACT_SEARCH /

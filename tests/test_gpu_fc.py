@@ -51,7 +51,7 @@ def data(kind, m, seed):
 
 def check(v, bits, iters, tag):
     oc, ol, ov, orr = oracle.quantize_scalars(v, bits, iters)
-    for search in ("auto", "thresholds"):   # the exact search below 2^23, and the threshold path
+    for search in ("auto", "thresholds"):   # the exact search below 3 * 2^20, and the threshold path
         codes, levels, v_hat, rounds = kq.kq_quantize_scalars(dev(v), bits, iters, search=search)
         assert np.array_equal(host(codes), oc), (tag, search)
         assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), (tag, search)
@@ -105,11 +105,11 @@ def test_fc_quantizer_full_size_fc6_properties():
 
 @pytest.mark.parametrize("kind", ["normal", "integers", "tiny"])
 def test_fc_threshold_path_equals_the_exact_search(kind):
-    """From 2^23 scalars on, codes come from per-level thresholds (fp32 comparisons);
+    """From 3 * 2^20 scalars on, codes come from per-level thresholds (fp32 comparisons);
     with KQ_F_EXACT_SEARCH every code comes from the exact fp64 search.  Both agree bit
     for bit, also on integer data (exact midpoints between levels) and on data whose tiny
     values make fp64 distances inexact (the thresholds are then not used)."""
-    m = 9 * 932068                                            # 8,388,612 >= 2^23
+    m = 9 * 932068                                            # 8,388,612 >= 3 * 2^20
     vd = dev(data(kind, m, 77))
     a = kq.kq_quantize_scalars(vd, 6, 30)
     b = kq.kq_quantize_scalars(vd, 6, 30, search="exact")

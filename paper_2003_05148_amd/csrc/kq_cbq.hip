@@ -140,15 +140,26 @@ __device__ __forceinline__ int nearest_sorted_fast(float x, const float* s_lev, 
     int q0;
     if (NLEV >= 8) {
         int c = 0;
+        if (NLEV == 64) {  // sorted: three branch-free halving steps and a check of the last
+            const bool h4 = coarse[3] < x;
+            const bool h2 = (h4 ? coarse[5] : coarse[1]) < x;
+            const bool h1 = (h4 ? (h2 ? coarse[6] : coarse[4]) : (h2 ? coarse[2] : coarse[0])) < x;
+            c = (h4 ? 4 : 0) + (h2 ? 2 : 0) + (h1 ? 1 : 0);
+            c += (c == 7 && coarse[7] < x) ? 1 : 0;
+        } else {
 #pragma unroll
-        for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] < x ? 1 : 0;
+            for (int i = 0; i < NLEV / 8; ++i) c += coarse[i] < x ? 1 : 0;
+        }
         if (c == NLEV / 8) {
             q0 = NLEV;  // the last level is below x, and with it every level
         } else {
+            // the block's last level is coarse[c], not below x: halving steps over the other seven
             const f32x4 a = reinterpret_cast<const f32x4*>(s_lev)[2 * c];
             const f32x4 b = reinterpret_cast<const f32x4*>(s_lev)[2 * c + 1];
-            q0 = 8 * c + (a[0] < x) + (a[1] < x) + (a[2] < x) + (a[3] < x) + (b[0] < x) + (b[1] < x) + (b[2] < x) +
-                 (b[3] < x);
+            const bool f4 = a[3] < x;
+            const bool f2 = (f4 ? b[1] : a[1]) < x;
+            const bool f1 = (f4 ? (f2 ? b[2] : b[0]) : (f2 ? a[2] : a[0])) < x;
+            q0 = 8 * c + (f4 ? 4 : 0) + (f2 ? 2 : 0) + (f1 ? 1 : 0);
         }
     } else {
         q0 = 0;

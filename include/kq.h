@@ -365,6 +365,22 @@ kq_status kq_quantize_codebook_stack(const kq_cbq_layer* layers, int32_t n_layer
                                      int32_t mode, int32_t iters, void* stream);
 
 /*
+ * kq_quantize_codebook_stack_ws -- the same results (Sec. 3.2, bit for bit) with large
+ *   codebooks spread over the whole GPU.  In KQ_CBQ_WKMEANS mode every codebook of at least
+ *   16384 scalars (k >= 1821) runs the kq_quantize_scalars machinery with the entry counts
+ *   as integer weights (each of an entry's 9 scalars weighs its count; weights <= 0 add
+ *   nothing), one such codebook after another; the smaller ones (and every codebook of a
+ *   KQ_CBQ_UNIFORM call) take one workgroup each as in kq_quantize_codebook_stack.
+ *   ws/ws_bytes: device workspace of at least
+ *   kq_quantize_codebook_stack_workspace_bytes(layers, n_layers, bits) bytes (256-byte
+ *   aligned; contents need no initialisation; NULL allowed when that size is 0 or the mode
+ *   is KQ_CBQ_UNIFORM), else KQ_ERR_WORKSPACE.  Other errors as kq_quantize_codebook.
+ */
+size_t kq_quantize_codebook_stack_workspace_bytes(const kq_cbq_layer* layers, int32_t n_layers, int32_t bits);
+kq_status kq_quantize_codebook_stack_ws(const kq_cbq_layer* layers, int32_t n_layers, int32_t bits,
+                                        int32_t mode, int32_t iters, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * kq_pack_bits -- the index stream of Eq. (4).
  *   Value i (its low `bits` bits) occupies stream bits [i*bits, (i+1)*bits), least
  *   significant bit first; stream bit s is bit (s % 8) of byte s / 8.  Writes exactly

@@ -67,6 +67,8 @@ def _load():
         "kq_fit_stack": ([_P, _I32, _I32, _U32, _P, _SZ, _P], _I32),
         "kq_quantize_codebook": ([_P, _I32, _I32, _P, _I32, _I32, _I32, _P, _P, _P, _P], _I32),
         "kq_quantize_codebook_stack": ([_P, _I32, _I32, _I32, _I32, _P], _I32),
+        "kq_quantize_codebook_stack_workspace_bytes": ([_P, _I32, _I32], _SZ),
+        "kq_quantize_codebook_stack_ws": ([_P, _I32, _I32, _I32, _I32, _P, _SZ, _P], _I32),
         "kq_pack_bits": ([_P, _I32, _I64, _I32, _P, _P], _I32),
         "kq_unpack_bits": ([_P, _I64, _I32, _P, _P], _I32),
         "kq_reconstruct": ([_P, _I64, _P, _I32, _I32, _P, _P], _I32),
@@ -112,6 +114,7 @@ KQ_F_THRESHOLDS = 32
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
+            "kq_quantize_codebook_stack_workspace_bytes", "kq_quantize_codebook_stack_ws",
             "kq_pack_bits", "kq_unpack_bits", "kq_reconstruct", "kq_reconstruct_packed", "kq_sq_error",
             "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
             "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang",
@@ -509,9 +512,12 @@ def kq_quantize_codebook(C, weights=None, bits: int = 6, mode: int = KQ_CBQ_WKME
     return codes, levels, C_hat
 
 
-def kq_quantize_codebook_stack(Cs, weights, bits: int = 6, mode: int = KQ_CBQ_WKMEANS, iters: int = 30, out=None):
-    """kq_quantize_codebook for a list of codebooks in one launch.
-    Returns a list of (codes, levels, C_hat)."""
+def kq_quantize_codebook_stack(Cs, weights, bits: int = 6, mode: int = KQ_CBQ_WKMEANS, iters: int = 30, out=None,
+                               wide: bool = True, workspace=None):
+    """kq_quantize_codebook for a list of codebooks.  wide (kq_quantize_codebook_stack_ws):
+    codebooks of at least 16384 scalars run on the whole GPU, the others in one launch;
+    otherwise (kq_quantize_codebook_stack) one workgroup per codebook.  The results are the
+    same.  Returns a list of (codes, levels, C_hat)."""
     Cs = [_kernels(c, "C") for c in Cs]
     dev = Cs[0].device
     if out is None:
@@ -524,8 +530,15 @@ def kq_quantize_codebook_stack(Cs, weights, bits: int = 6, mode: int = KQ_CBQ_WK
             _dev(w, torch.int32, "weights", (c.shape[0],))
         arr[i] = KqCbqLayer(c.data_ptr(), c.shape[0], _ptr(w), out[i][0].data_ptr(), out[i][1].data_ptr(),
                             out[i][2].data_ptr())
-    _check(lib.kq_quantize_codebook_stack(ctypes.cast(arr, _P), len(Cs), bits, mode, iters, _stream(dev)),
-           "kq_quantize_codebook_stack")
+    if not wide:
+        _check(lib.kq_quantize_codebook_stack(ctypes.cast(arr, _P), len(Cs), bits, mode, iters, _stream(dev)),
+               "kq_quantize_codebook_stack")
+        return out
+    nb = lib.kq_quantize_codebook_stack_workspace_bytes(ctypes.cast(arr, _P), len(Cs), bits)
+    ws = workspace if workspace is not None else (_ws(dev, nb) if nb else None)
+    _check(lib.kq_quantize_codebook_stack_ws(ctypes.cast(arr, _P), len(Cs), bits, mode, iters, _ptr(ws),
+                                             0 if ws is None else ws.numel(), _stream(dev)),
+           "kq_quantize_codebook_stack_ws")
     return out
 
 

@@ -444,6 +444,40 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
     return KQ_OK;
 }
 
+// the FC quantizer's launch parameters over the workspace layout of fc_ws_bytes
+static void fc_params(FcParams& p, const float* v, const int32_t* w, int64_t count, int32_t bits, int32_t iters,
+                      uint8_t* codes, float* levels, float* v_hat, int32_t* rounds, int thr_mode, void* ws) {
+    const size_t G = (size_t)fc_grid(count), nlev = (size_t)1 << bits;
+    unsigned char* b = (unsigned char*)ws;
+    memset(&p, 0, sizeof(p));
+    p.v = v;
+    p.w = w;
+    p.codes = codes;
+    p.levels_out = levels;
+    p.v_hat = v_hat;
+    p.rounds_out = rounds;
+    p.m = count;
+    p.bits = bits;
+    p.iters = iters;
+    p.thr_mode = thr_mode;
+    p.minmax = (float*)b;
+    p.range = p.minmax + 3 * G;
+    b += align256(sizeof(float) * (3 * G + 4));
+    p.part = (long long*)b;
+    b += align256(sizeof(long long) * G * nlev * 12);
+    p.S = (long long*)b;
+    b += align256(sizeof(long long) * nlev * 12);
+    p.lev = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.lev_next = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.thr = (float*)b;
+    b += align256(sizeof(float) * nlev);
+    p.state = (int*)b;
+    b += align256(sizeof(int) * 4);
+    p.wg_changed = (int*)b;
+}
+
 size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits) {
     if (count < 1 || count >= (int64_t(1) << 31) || bits < 1 || bits > 8) return 0;
     return fc_ws_bytes(count, bits);
@@ -461,35 +495,9 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
     if ((v_hat && !aligned(v_hat, 4)) || (rounds && !aligned(rounds, 4))) return KQ_ERR_ARG;
     const kq_status w = check_ws(ws, ws_bytes, fc_ws_bytes(count, bits));
     if (w != KQ_OK) return w;
-    const size_t G = (size_t)fc_grid(count), nlev = (size_t)1 << bits;
-    unsigned char* b = (unsigned char*)ws;
     FcParams p;
-    memset(&p, 0, sizeof(p));
-    p.v = v;
-    p.codes = codes;
-    p.levels_out = levels;
-    p.v_hat = v_hat;
-    p.rounds_out = rounds;
-    p.m = count;
-    p.bits = bits;
-    p.iters = iters;
-    p.thr_mode = (flags & KQ_F_EXACT_SEARCH) ? 1 : ((flags & KQ_F_THRESHOLDS) ? 2 : 0);
-    p.minmax = (float*)b;
-    p.range = p.minmax + 3 * G;
-    b += align256(sizeof(float) * (3 * G + 4));
-    p.part = (long long*)b;
-    b += align256(sizeof(long long) * G * nlev * 12);
-    p.S = (long long*)b;
-    b += align256(sizeof(long long) * nlev * 12);
-    p.lev = (float*)b;
-    b += align256(sizeof(float) * nlev);
-    p.lev_next = (float*)b;
-    b += align256(sizeof(float) * nlev);
-    p.thr = (float*)b;
-    b += align256(sizeof(float) * nlev);
-    p.state = (int*)b;
-    b += align256(sizeof(int) * 4);
-    p.wg_changed = (int*)b;
+    fc_params(p, v, nullptr, count, bits, iters, codes, levels, v_hat, rounds,
+              (flags & KQ_F_EXACT_SEARCH) ? 1 : ((flags & KQ_F_THRESHOLDS) ? 2 : 0), ws);
     return hip_status(launch_fc_quantize(p, (hipStream_t)stream));
 }
 
@@ -745,6 +753,65 @@ kq_status kq_quantize_codebook_stack(const kq_cbq_layer* layers, int32_t n_layer
             p.L[l - l0] = CbqLayer{s.C, s.weights, s.codes, s.levels, s.C_hat, s.k};
         }
         if (launch_cbq(p, (hipStream_t)stream) != hipSuccess) return KQ_ERR_HIP;
+    }
+    return KQ_OK;
+}
+
+// codebooks of at least this many scalars (k * 9) are quantized by the FC-layer machinery
+// on the whole GPU: below, its per-round launches cost more than one workgroup's pass
+constexpr int64_t kCbqWideMin = 16384;
+
+size_t kq_quantize_codebook_stack_workspace_bytes(const kq_cbq_layer* layers, int32_t n_layers, int32_t bits) {
+    if (layers == nullptr || n_layers < 1 || bits < 1 || bits > 8) return 0;
+    size_t b = 0;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const int64_t m = (int64_t)layers[l].k * KQ_DIM;
+        if (layers[l].k >= 1 && layers[l].k <= KQ_MAX_K && m >= kCbqWideMin) {
+            const size_t f = fc_ws_bytes(m, bits);
+            b = f > b ? f : b;
+        }
+    }
+    return b;
+}
+
+kq_status kq_quantize_codebook_stack_ws(const kq_cbq_layer* layers, int32_t n_layers, int32_t bits, int32_t mode,
+                                        int32_t iters, void* ws, size_t ws_bytes, void* stream) {
+    if (layers == nullptr || n_layers < 1) return KQ_ERR_ARG;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_status st = check_cbq(layers[l], bits, mode, iters);
+        if (st != KQ_OK) return st;
+    }
+    const size_t need = kq_quantize_codebook_stack_workspace_bytes(layers, n_layers, bits);
+    if (need > 0 && mode == KQ_CBQ_WKMEANS) {
+        const kq_status w = check_ws(ws, ws_bytes, need);
+        if (w != KQ_OK) return w;
+    }
+    // the small codebooks (and every codebook of a uniform grid) in one launch per 16 layers
+    kq_cbq_layer small[KQ_MAX_STACK];
+    int32_t ns = 0;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_cbq_layer& s = layers[l];
+        if (mode == KQ_CBQ_WKMEANS && (int64_t)s.k * KQ_DIM >= kCbqWideMin) continue;
+        small[ns++] = s;
+        if (ns == KQ_MAX_STACK) {
+            const kq_status st = kq_quantize_codebook_stack(small, ns, bits, mode, iters, stream);
+            if (st != KQ_OK) return st;
+            ns = 0;
+        }
+    }
+    if (ns > 0) {
+        const kq_status st = kq_quantize_codebook_stack(small, ns, bits, mode, iters, stream);
+        if (st != KQ_OK) return st;
+    }
+    // the large ones one after another on the whole GPU, reusing the workspace (stream order)
+    if (mode != KQ_CBQ_WKMEANS) return KQ_OK;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_cbq_layer& s = layers[l];
+        const int64_t m = (int64_t)s.k * KQ_DIM;
+        if (m < kCbqWideMin) continue;
+        FcParams p;
+        fc_params(p, s.C, s.weights, m, bits, iters, s.codes, s.levels, s.C_hat, nullptr, 0, ws);
+        if (launch_fc_quantize(p, (hipStream_t)stream) != hipSuccess) return KQ_ERR_HIP;
     }
     return KQ_OK;
 }

@@ -198,7 +198,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int half = lane >> 5;
     const long long T = p.total_units;
     int t = (int)((long long)blockIdx.x * T / gridDim.x);
     const int t_end = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);

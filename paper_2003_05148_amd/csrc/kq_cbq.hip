@@ -607,19 +607,26 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     // the same for every scalar of the round
     auto run = [&](auto mode) {
         constexpr int kMode = decltype(mode)::value;
-        // the code of scalar x (old code c); moves its exact contribution when the code changes
-        auto recode = [&](float x, int c) {
+        // the code of scalar r (value x, old code c); moves its exact contribution (weight
+        // times value, and the weight into the count) when the code changes.  A weight of
+        // zero or less contributes nothing, as in the single-workgroup quantizer.
+        auto recode = [&](long long r, float x, int c) {
             const int q = kMode == 0   ? code_from_thresholds<NLEV>(x, s_thr, coarse)
                           : kMode == 1 ? nearest_sorted_fast<NLEV>(x, s_lev, coarse_lev)
                                        : nearest_level(x, s_lev, NLEV);
+            const int wt = p.w ? p.w[r / kDim] : 1;
             if (INIT) {
-                add_exact(s_dig + q * kFcCols, x, 1u);
-                atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+                if (wt > 0) {
+                    add_exact(s_dig + q * kFcCols, x, (unsigned)wt);
+                    atomicAdd(&s_dig[q * kFcCols + kDigits], (unsigned long long)wt);
+                }
             } else if (q != c) {
-                add_exact(s_dig + c * kFcCols, -x, 1u);
-                add_exact(s_dig + q * kFcCols, x, 1u);
-                atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)-1ll);
-                atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+                if (wt > 0) {
+                    add_exact(s_dig + c * kFcCols, -x, (unsigned)wt);
+                    add_exact(s_dig + q * kFcCols, x, (unsigned)wt);
+                    atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)(-(long long)wt));
+                    atomicAdd(&s_dig[q * kFcCols + kDigits], (unsigned long long)wt);
+                }
                 changed = 1;
             }
             return q;
@@ -656,7 +663,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                     unsigned nw = 0u;
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        nw |= (unsigned)recode(xs[e], (int)((cw[j] >> (8 * e)) & 255u)) << (8 * e);
+                        nw |= (unsigned)recode(4 * g + e, xs[e], (int)((cw[j] >> (8 * e)) & 255u)) << (8 * e);
                     if (INIT || nw != cw[j]) c4[g] = nw;
                 }
 #pragma unroll
@@ -667,7 +674,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
             }
             if (blockIdx.x == 0)  // the last m % 4 scalars
                 for (long long r = 4 * ng + tid; r < m; r += kFcThreads) {
-                    const int q = recode(p.v[r], INIT ? 0 : (int)p.codes[r]);
+                    const int q = recode(r, p.v[r], INIT ? 0 : (int)p.codes[r]);
                     if (INIT || q != (int)p.codes[r]) p.codes[r] = (uint8_t)q;
                 }
         } else {
@@ -685,7 +692,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                 for (int j = 0; j < kPer; ++j) {
                     const long long r = r0 + (long long)j * kFcThreads;
                     if (r >= m) continue;
-                    const int q = recode(x[j], c[j]);
+                    const int q = recode(r, x[j], c[j]);
                     if (INIT || q != c[j]) p.codes[r] = (uint8_t)q;
                 }
             }

@@ -274,6 +274,7 @@ constexpr int kFcThreads = 256;
 constexpr int kFcGrid = 1024;  // persistent workgroups
 struct FcParams {
     const float* v;
+    const int32_t* w;      // weight of scalar r: w[r / 9] (a codebook entry's count), or null for 1
     uint8_t* codes;
     float* levels_out;
     float* v_hat;          // levels[codes], or null

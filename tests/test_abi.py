@@ -114,6 +114,23 @@ def test_stack_argument_errors():
     assert lib.kq_update_stack(p, 2, 0, 0, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
 
 
+def test_cbq_stack_workspace_rules():
+    """Only weighted k-means codebooks of at least 16384 scalars need the workspace; its
+    size is that of the largest; a missing or short workspace is refused before any launch."""
+    arr = (kq.KqCbqLayer * 3)()
+    for i, k in enumerate([16, 1821, 1820]):
+        arr[i] = kq.KqCbqLayer(FAKE, k, None, FAKE, FAKE, None)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+    need = lib.kq_quantize_codebook_stack_workspace_bytes(P, 3, 6)
+    assert need == lib.kq_quantize_scalars_workspace_bytes(1821 * 9, 6) > 0
+    assert lib.kq_quantize_codebook_stack_workspace_bytes(P, 1, 6) == 0      # k = 16 alone
+    assert lib.kq_quantize_codebook_stack_workspace_bytes(P, 3, 9) == 0      # bits outside 1..8
+    assert lib.kq_quantize_codebook_stack_ws(P, 3, 6, kq.KQ_CBQ_WKMEANS, 30, None, 0, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_quantize_codebook_stack_ws(P, 3, 6, kq.KQ_CBQ_WKMEANS, 30, FAKE, need - 1, None) == kq.KQ_ERR_WORKSPACE
+    assert lib.kq_quantize_codebook_stack_ws(P, 3, 9, kq.KQ_CBQ_WKMEANS, 30, FAKE, need, None) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_quantize_codebook_stack_ws(P, 0, 6, kq.KQ_CBQ_WKMEANS, 30, FAKE, need, None) == kq.KQ_ERR_ARG
+
+
 def test_cbq_pack_reconstruct_argument_errors():
     q = lambda **kw: lib.kq_quantize_codebook(kw.get("C", FAKE), kw.get("k", 8), kw.get("dim", 9), None,
                                               kw.get("bits", 6), kw.get("mode", 0), kw.get("iters", 30),

@@ -380,6 +380,35 @@ def test_reconstruct_stack_and_errors(packed):
         assert e1 == pytest.approx(single, rel=1e-12), (n, k)
 
 
+@pytest.mark.parametrize("bits", [2, 6, 8])
+def test_quantize_codebook_wide_path(bits):
+    """Codebooks of at least 16384 scalars run on the whole GPU with the entry counts as
+    weights: codes, levels and C_hat bit for bit those of the oracle and of the
+    one-workgroup quantizer, in a stack mixed with small codebooks; integer-valued data
+    (exact ties between levels) and zero weights included."""
+    rng = np.random.default_rng(30 + bits)
+    big = rng.laplace(0, 0.03, (1900, 9)).astype(np.float32)          # 17,100 scalars
+    ints = rng.integers(-40, 41, (4096, 9)).astype(np.float32)        # 36,864, exact ties
+    small = rng.standard_normal((256, 9)).astype(np.float32)
+    Cs = [big, small, ints]
+    ws = [rng.integers(0, 500, len(c)) for c in Cs]
+    ws[0][::13] = 0
+    ws[2][::7] = 0
+    wd = [dev(w.astype(np.int32)) for w in ws]
+    wide = kq.kq_quantize_codebook_stack([dev(c) for c in Cs], wd, bits, kq.KQ_CBQ_WKMEANS, 30)
+    one = kq.kq_quantize_codebook_stack([dev(c) for c in Cs], wd, bits, kq.KQ_CBQ_WKMEANS, 30, wide=False)
+    for C, w, a, b in zip(Cs, ws, wide, one):
+        oc, ol, oh, _ = oracle.cbq_wkmeans(C, w, bits, 30)
+        for got in (a, b):
+            assert np.array_equal(host(got[0]), oc), (len(C), bits)
+            assert np.array_equal(host(got[1]).view(np.uint32), ol.view(np.uint32)), (len(C), bits)
+            assert np.array_equal(host(got[2]).view(np.uint32), oh.view(np.uint32)), (len(C), bits)
+    # uniform grids never take the wide path, and need no workspace
+    uni = kq.kq_quantize_codebook_stack([dev(big)], None, bits, kq.KQ_CBQ_UNIFORM, 0)
+    oc, ol, oh = oracle.cbq_uniform(big, bits)
+    assert np.array_equal(host(uni[0][0]), oc) and np.array_equal(host(uni[0][1]).view(np.uint32), ol.view(np.uint32))
+
+
 @pytest.mark.parametrize("packed", [False, True])
 def test_reconstruct_unaligned_views(packed):
     """Output, reference and index arrays that start 4 bytes past a 16-byte boundary:

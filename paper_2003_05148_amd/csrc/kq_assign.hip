@@ -457,14 +457,24 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                     fj = d < fd ? jj : fj;
                     fd = d < fd ? d : fd;
                 }
-            } else {
-                for (int jj = lane; jj < k; jj += kWave) {
-                    float c[kDim];
+            } else {  // rows from memory: four per lane in flight, taken in index order
+                constexpr int kU = 4;
+                for (int j0 = lane; j0 < k; j0 += kU * kWave) {
+                    float c[kU][kDim];
 #pragma unroll
-                    for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)jj * kDim + d];
-                    const float d = sqdist9(xf, c);
-                    fj = d < fd ? jj : fj;
-                    fd = d < fd ? d : fd;
+                    for (int u = 0; u < kU; ++u) {
+                        const int jj = min(j0 + u * kWave, k - 1);  // a valid row past the end
+#pragma unroll
+                        for (int d = 0; d < kDim; ++d) c[u][d] = C[(size_t)jj * kDim + d];
+                    }
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        const int jj = j0 + u * kWave;
+                        const float d = sqdist9(xf, c[u]);
+                        const bool take = jj < k && d < fd;
+                        fj = take ? jj : fj;
+                        fd = take ? d : fd;
+                    }
                 }
             }
             wave_argmin(fd, fj);

@@ -448,14 +448,28 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             // meet in their lexicographic minimum
             float fd = __builtin_inff();
             int fj = 0x7fffffff;
-            if (resident) {  // the rows are still staged in LDS
-                for (int jj = lane; jj < k; jj += kWave) {
-                    const f32x4 r0 = s_c[jj * 3 + 0], r1 = s_c[jj * 3 + 1];
-                    const float c8 = s_cf[jj * kRowFloats + 8];
-                    const float c[kDim] = {r0[0], r0[1], r0[2], r0[3], r1[0], r1[1], r1[2], r1[3], c8};
-                    const float d = sqdist9(xf, c);
-                    fj = d < fd ? jj : fj;
-                    fd = d < fd ? d : fd;
+            if (resident) {  // the rows are still staged in LDS: four per lane in flight
+                constexpr int kU = 4;
+                for (int j0 = lane; j0 < k; j0 += kU * kWave) {
+                    f32x4 r0[kU], r1[kU];
+                    float c8[kU];
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        const int jj = min(j0 + u * kWave, k - 1);  // a staged row past the end
+                        r0[u] = s_c[jj * 3 + 0];
+                        r1[u] = s_c[jj * 3 + 1];
+                        c8[u] = s_cf[jj * kRowFloats + 8];
+                    }
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        const int jj = j0 + u * kWave;
+                        const float c[kDim] = {r0[u][0], r0[u][1], r0[u][2], r0[u][3], r1[u][0],
+                                               r1[u][1], r1[u][2], r1[u][3], c8[u]};
+                        const float d = sqdist9(xf, c);
+                        const bool take = jj < k && d < fd;
+                        fj = take ? jj : fj;
+                        fd = take ? d : fd;
+                    }
                 }
             } else {  // rows from memory: four per lane in flight, taken in index order
                 constexpr int kU = 4;

@@ -605,8 +605,9 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     const long long m = p.m;
     // one instantiation per search (thresholds, sorted levels, full scan): the choice is
     // the same for every scalar of the round
-    auto run = [&](auto mode) {
+    auto run = [&](auto mode, auto weighted) {
         constexpr int kMode = decltype(mode)::value;
+        constexpr bool kWeighted = decltype(weighted)::value;
         // the code of scalar r (value x, old code c); moves its exact contribution (weight
         // times value, and the weight into the count) when the code changes.  A weight of
         // zero or less contributes nothing, as in the single-workgroup quantizer.
@@ -614,7 +615,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
             const int q = kMode == 0   ? code_from_thresholds<NLEV>(x, s_thr, coarse)
                           : kMode == 1 ? nearest_sorted_fast<NLEV>(x, s_lev, coarse_lev)
                                        : nearest_level(x, s_lev, NLEV);
-            const int wt = p.w ? p.w[r / kDim] : 1;
+            const int wt = kWeighted ? p.w[(unsigned)r / (unsigned)kDim] : 1;  // r < 2^31
             if (INIT) {
                 if (wt > 0) {
                     add_exact(s_dig + q * kFcCols, x, (unsigned)wt);
@@ -698,12 +699,19 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
             }
         }
     };
+    // weights or none: decided once, so unweighted scalars spend nothing on them
+    auto pick = [&](auto mode) {
+        if (p.w)
+            run(mode, std::integral_constant<bool, true>{});
+        else
+            run(mode, std::integral_constant<bool, false>{});
+    };
     if (THR)
-        run(std::integral_constant<int, 0>{});
+        pick(std::integral_constant<int, 0>{});
     else if (sorted)
-        run(std::integral_constant<int, 1>{});
+        pick(std::integral_constant<int, 1>{});
     else
-        run(std::integral_constant<int, 2>{});
+        pick(std::integral_constant<int, 2>{});
     if (changed) s_changed = 1;
     __syncthreads();
     unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * NLEV * kFcCols;

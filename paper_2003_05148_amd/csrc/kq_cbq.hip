@@ -452,6 +452,12 @@ constexpr int kFcCols = kDigits + 1;  // digits, then the count
 // more than the exact search it saves (measured per round: about even at 2^21 scalars,
 // 35 instead of 42 us at 3 * 2^20)
 constexpr long long kFcThresholdMin = 3ll << 20;
+// whether rounds may take their codes from thresholds: unweighted sets only (weighted
+// codebooks stay far below that size), by the size rule unless a flag forces a way; the
+// device's choice and the host's launch of the threshold kernel use the same rule
+__host__ __device__ __forceinline__ bool fc_thr_wanted(const FcParams& p) {
+    return p.w == nullptr && (p.thr_mode == 2 || (p.thr_mode == 0 && p.m >= kFcThresholdMin));
+}
 
 __device__ __forceinline__ bool fc_done(const FcParams& p) { return p.state[0] != 0; }
 
@@ -523,7 +529,7 @@ __device__ void set_thresholds(const FcParams& p, const float* s_lev, int nlev, 
     const int tid = threadIdx.x;
     const float fl = exact_floor(fmaxf(fabsf(vmin), fabsf(vmax)));
     // the boundary search costs a few microseconds per round: worth it only for large sets
-    const bool wanted = p.thr_mode == 2 || (p.thr_mode == 0 && p.m >= kFcThresholdMin);
+    const bool wanted = fc_thr_wanted(p);
     if (tid == 0) *s_bad = (unsorted || vsm < fl || !wanted) ? 1 : 0;
     __syncthreads();
     if (tid < nlev && s_lev[tid] != 0.0f && fabsf(s_lev[tid]) < fl) *s_bad = 1;
@@ -632,7 +638,10 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
             }
             return q;
         };
-        if ((reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 && (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
+        // the grouped loop for threshold rounds (the large sets); the exact searches (small
+        // sets, weighted codebooks, data where thresholds are refused) take one scalar at a time
+        if (kMode == 0 && (reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 &&
+            (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
             // groups of four scalars: one float4 of values and one word of four codes per
             // group, kPer groups per thread, the next step's loaded while this one is coded;
             // a group whose codes change stores its word
@@ -706,12 +715,14 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         else
             run(mode, std::integral_constant<bool, false>{});
     };
-    if (THR)
-        pick(std::integral_constant<int, 0>{});
-    else if (sorted)
-        pick(std::integral_constant<int, 1>{});
-    else
-        pick(std::integral_constant<int, 2>{});
+    if constexpr (THR) {
+        run(std::integral_constant<int, 0>{}, std::integral_constant<bool, false>{});  // never weighted
+    } else {
+        if (sorted)
+            pick(std::integral_constant<int, 1>{});
+        else
+            pick(std::integral_constant<int, 2>{});
+    }
     if (changed) s_changed = 1;
     __syncthreads();
     unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * NLEV * kFcCols;
@@ -722,7 +733,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
 template <bool INIT>
 hipError_t launch_fc_assign(const FcParams& p, int G, hipStream_t s) {
     // the threshold launch only where the state may choose thresholds
-    const bool thr = p.thr_mode == 2 || (p.thr_mode == 0 && p.m >= kFcThresholdMin);
+    const bool thr = fc_thr_wanted(p);
     switch (p.bits) {
 #define KQ_FC_CASE(B)                                                                                          \
     case B:                                                                                                    \

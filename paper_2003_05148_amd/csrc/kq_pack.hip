@@ -207,7 +207,7 @@ __device__ __forceinline__ double recon_steps(const ReconLayer& L, const float* 
             float v = 0.0f;
             if ((unsigned)jq < (unsigned)L.k) v = LDS ? s_cb[jq * kDim + dim[q]] : L.C[jq * kDim + dim[q]];
             if (lane + kWave * q < nf) {
-                out[lane + kWave * q] = v;
+                __builtin_nontemporal_store(v, &out[lane + kWave * q]);  // streamed, not re-read here
                 if (err) {
                     const double df = (double)cur.x[q] - (double)v;
                     acc += df * df;

@@ -24,8 +24,8 @@
 // over at most n values can overflow and the relative resolution is the same for any
 // gradient magnitude; the finish then writes c - gamma * mean instead of the mean.
 // update_finish_kernel: a workgroup of 640 threads owns 8 entries of one layer; eight
-// groups of 80 threads add an eighth of the partials each, sixteen loads in flight per
-// thread (any order gives the same integers), then it divides and writes the codebook
+// groups of 80 threads add an eighth of the partials each, eight loads in flight per
+// thread (any order gives the same integers; 12, 16, 24 or 32 in flight measured slower), then it divides and writes the codebook
 // and the counts (fewer, fuller workgroups measured faster than 2 or 4 entries each:
 // the launch is short and its cost is mostly per workgroup).  One more workgroup
 // per layer adds the distortion partials in a fixed order (those of the assignment kernel
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
 }
 
 #ifndef KQ_FINISH_BATCH
-#define KQ_FINISH_BATCH 16
+#define KQ_FINISH_BATCH 8
 #endif
 constexpr int kFinishGroups = kSumThreads / (10 * kFinishEntries);
 constexpr int kFinishBatch = KQ_FINISH_BATCH;
@@ -209,8 +209,7 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         const int nb = L.nchunks;
         const size_t stride = (size_t)k * 10;
         const unsigned long long* hp = h + (size_t)j * 10 + d;
-        // partials g, g + 8, ...: kFinishBatch loads in flight at a time (one batch covers
-        // 128 partials, every layer of the benchmark stacks)
+        // partials g, g + 8, ...: kFinishBatch loads in flight at a time
 #pragma unroll 1
         for (int q0 = g; q0 < nb; q0 += kFinishBatch * kFinishGroups) {
             unsigned long long v[kFinishBatch];

@@ -305,6 +305,18 @@ def main():
     torch.cuda.synchronize()
     grad_ms = g0.elapsed_time(g1) / 5
 
+    # reconstruction alone (int32 indices, no error; not part of the step): 4 B read and
+    # 36 B written per kernel, five launches between HIP events after a queued step
+    recon_plain = [{"idx": st.idx[i], "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i]} for i, L in enumerate(layers)]
+    step(False)
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for _ in range(5):
+        kq.kq_reconstruct_stack(recon_plain, workspace=recon_ws)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    recon_plain_ms = r0.elapsed_time(r1) / 5
+
     if args.copy_probe > 0:
         src = torch.ones(args.copy_probe << 18, device=dev)
         dst = torch.empty_like(src)
@@ -346,6 +358,8 @@ def main():
         "lloyd_round_ms": assign_ms + update_ms, "final_assign_ms": mean_ms["assign_final"], "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
         "reconstruct_ms": mean_ms["reconstruct"],
         "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9 if mean_ms["reconstruct"] else 0.0,
+        "reconstruct_plain_ms": recon_plain_ms,
+        "reconstruct_plain_GBps": 40.0 * n_total / (recon_plain_ms * 1e-3) / 1e9,
         "grad_step_ms": grad_ms, "grad_step_GBps": 40.0 * n_total / (grad_ms * 1e-3) / 1e9,
         "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
         "beta_K": sum(L.k * 9 * 32 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),

@@ -6,6 +6,9 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 
 What each function follows in the paper:
 
+* ``forgy_select`` -- the initial codebook of the k-means (Sec. 3.1 does not say how it
+  starts): k distinct kernels of the layer in a seeded random order (splitmix64 driving a
+  partial Fisher-Yates shuffle).
 * ``assign`` / ``update`` / ``distortion`` / ``fit`` -- kernel-level
   quantization, Sec. 3.1, Eq. (1): plain Lloyd k-means over the n = p q kernels
   of a layer, each a vector of omega^2 = 9 values (C loops in ``kq_oracle.c``).
@@ -46,7 +49,7 @@ def build(force: bool = True) -> str:
     """Compile the C part of the oracle (plain loops, no FP contraction)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + f".tmp{os.getpid()}"
-        subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-shared", "-fPIC",
+        subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared", "-fPIC",
                         _SRC, "-o", tmp, "-lm"], check=True)
         os.replace(tmp, _LIB)
     return _LIB
@@ -68,8 +71,15 @@ def _load():
         lib.kqo_update.restype = I
         lib.kqo_fit.argtypes = [P, I64, I, I, P, I, P, P, P, P]
         lib.kqo_fit.restype = I
+        lib.kqo_set_threads.argtypes = [I]
+        lib.kqo_set_threads.restype = I
         _lib = lib
     return _lib
+
+
+def set_threads(t: int) -> int:
+    """Host threads of the assignment loop (its results do not depend on the count)."""
+    return int(_load().kqo_set_threads(int(t)))
 
 
 def _ptr(a):
@@ -81,6 +91,56 @@ def _f32(a, shape_last=None):
     if shape_last is not None and (a.ndim != 2 or a.shape[1] != shape_last):
         raise ValueError("expected [*, %d] array" % shape_last)
     return a
+
+
+# ---- Sec. 3.1: the k-means initialisation --------------------------------------------
+
+_MASK64 = (1 << 64) - 1
+
+
+def splitmix64(seed: int):
+    """The splitmix64 generator (Steele, Lea, Flood, OOPSLA 2014): the 64-bit state grows by
+    0x9E3779B97F4A7C15 per draw and each draw returns the new state through the variant-13
+    mixer.  Yields the draws as Python integers."""
+    state = seed & _MASK64
+    while True:
+        state = (state + 0x9E3779B97F4A7C15) & _MASK64
+        z = state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+        yield z ^ (z >> 31)
+
+
+def forgy_select(X, k: int, seed: int) -> np.ndarray:
+    """Indices of k distinct kernels of X in a seeded random order (the reading taken for
+    the k-means initialisation, which the paper leaves open).
+
+    The order is a Fisher-Yates shuffle of 0..n-1 run only as far as needed: at step i a
+    draw d of ``splitmix64(seed)`` picks j = i + (d mod (n - i)), positions i and j swap, and
+    the value now at position i is the next candidate.  A candidate whose nine values equal,
+    bit for bit, those of an already accepted kernel (-0 and +0 counted as equal) is
+    skipped.  Raises ValueError when X holds fewer than k distinct kernels.
+    """
+    X = _f32(X)
+    n = X.shape[0]
+    bits = X.view(np.uint32).copy()
+    bits[bits == 0x80000000] = 0          # -0 reads as +0
+    perm = list(range(n))
+    draws = splitmix64(seed)
+    accepted, seen = [], set()
+    for i in range(n):
+        if len(accepted) == k:
+            break
+        j = i + next(draws) % (n - i)
+        perm[i], perm[j] = perm[j], perm[i]
+        cand = perm[i]
+        key = bits[cand].tobytes()
+        if key not in seen:
+            seen.add(key)
+            accepted.append(cand)
+    if len(accepted) < k:
+        raise ValueError(f"only {len(accepted)} distinct kernels, k={k}")
+    return np.asarray(accepted, dtype=np.int64)
 
 
 # ---- Sec. 3.1: kernel-level quantization (Lloyd k-means, Eq. 1) ----------------------
@@ -307,10 +367,10 @@ def cbq_wkmeans(C, weights, bits: int = 6, iters: int = 30):
 
 
 def quantize_scalars(v, bits: int = 6, iters: int = 30):
-    """Quantization of a fully-connected layer (end of Sec. 3.2), done "with the same
-    layer by layer k-means clustering method" as the codebooks: the k-means of
-    ``cbq_wkmeans`` on one flat set of scalars, every scalar carrying weight 1 (an FC
-    weight is a parameter of its own, so there is no appearance count to weigh with).
+    """Quantization of a fully-connected layer (end of Sec. 3.2), by the layer-by-layer
+    k-means the codebooks are quantized with: the k-means of ``cbq_wkmeans`` on one flat
+    set of scalars, every scalar carrying weight 1 (an FC weight is a parameter of its
+    own, so there is no appearance count to weigh with).
 
     Returns (codes uint8 [m], levels float32 [2^bits], v_hat float32 [m], rounds).
     """

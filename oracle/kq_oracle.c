@@ -26,9 +26,12 @@
  *   - the distortion of an assignment is the fp64 sum, in ascending kernel
  *     order, of the fp64 squared distances to the assigned entries.
  *
- * Build: gcc -O2 -ffp-contract=off -shared -fPIC kq_oracle.c -lm
+ * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC kq_oracle.c -lm
  * (contraction off, so every multiply and add below rounds separately unless
- * fmaf is written out).
+ * fmaf is written out).  The assignment's loop over kernels may run on several
+ * host threads (kqo_set_threads): every kernel's decision is computed alone, so
+ * the results are the same on any number of threads; the distortion and the
+ * update stay sequential sums in ascending kernel order.
  */
 #include <math.h>
 #include <stdint.h>
@@ -55,6 +58,14 @@ static double sqdist_f64(const float* x, const float* c, int dim) {
     return acc;
 }
 
+static int kqo_threads = 1;
+
+/* Host threads for the assignment loop (1 = plain sequential loop).  Returns the count. */
+int kqo_set_threads(int t) {
+    kqo_threads = t < 1 ? 1 : t;
+    return kqo_threads;
+}
+
 /*
  * Assignment step of Eq. (1): nearest codebook entry of every kernel.
  *   X [n][dim], C [k][dim] row-major fp32.
@@ -66,6 +77,7 @@ static double sqdist_f64(const float* x, const float* c, int dim) {
 int kqo_assign(const float* X, int64_t n, int dim, const float* C, int k,
                int32_t* idx32, float* d32, int32_t* idx64, double* d1, double* d2) {
     if (n < 0 || dim < 1 || k < 1) return -1;
+#pragma omp parallel for schedule(static) num_threads(kqo_threads) if (kqo_threads > 1)
     for (int64_t i = 0; i < n; ++i) {
         const float* x = X + i * dim;
         if (idx32 || d32) {

@@ -221,3 +221,21 @@ def test_fit_matches_sklearn_lloyd():
     assert np.array_equal(km.labels_, r["idx"])
     assert np.allclose(km.cluster_centers_, r["C"], rtol=1e-6, atol=1e-7)
     assert km.inertia_ == pytest.approx(r["J"][-1], rel=1e-6)
+
+
+def test_threaded_assignment_is_identical():
+    """The oracle's assignment loop on several host threads gives the same decisions,
+    distances and fits as the sequential loop (each kernel is decided alone)."""
+    L = synth.resnet18_stack(k=64, layers=1)[0]
+    C = synth.random_codebook_state(L.X, 64, 3)
+    try:
+        oracle.set_threads(1)
+        a1, f1 = oracle.assign(L.X, C), oracle.fit(L.X, L.C0, 3)
+        oracle.set_threads(4)
+        a4, f4 = oracle.assign(L.X, C), oracle.fit(L.X, L.C0, 3)
+    finally:
+        oracle.set_threads(1)
+    for key in a1:
+        assert np.array_equal(a1[key], a4[key]), key
+    for key in f1:
+        assert np.array_equal(f1[key], f4[key]), key

@@ -3,7 +3,8 @@
 
 Workload (one step): the ResNet-18-shaped stack of 3x3 convolutions (16 layers,
 1,220,608 kernels, synthetic Laplace weights), one codebook of k = 256 entries per
-layer, then
+layer started from k distinct kernels (kq_forgy_select), then, in one library call
+(kq_compress_stack):
   * 30 Lloyd rounds (assign + update) and a final assignment on every layer,
   * the final member counts,
   * 6-bit weighted k-means quantization of every codebook (Sec. 3.2),
@@ -11,16 +12,20 @@ layer, then
   * reconstruction of every weight tensor from the packed indices and the
     dequantised codebook, and its squared error against the original weights.
 
-value = kernels x Lloyd rounds / step time (everything above inside the step).
-The assignment kernel's own duration is measured with HIP events on the stream it
-runs on, in one instrumented step after the timed ones, and priced against the FP32
-peak.
+value = kernels x Lloyd rounds / step time (everything above inside the step; inputs
+resident in HBM before the timed region).  The dominant kernel, the assignment, is
+timed inside the timed steps: each step has the library record a pair of HIP events
+around one round's assignment launch (round s mod 30 in step s), and the mean of those
+launches prices it against the FP32 peak.  A diagnostic line on stderr adds the other
+launches (warm and after a 1 GiB cache flush), the per-layer report of Sec. 4.2.1
+(l2 error, Eq. 4, 6, 7 for K and K+C) and the codebook-retraining step of Eq. (2).
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -31,38 +36,38 @@ if ROOT not in sys.path:
 METRIC = "kernels assigned/sec per Lloyd iter (ResNet-18 stack, K=256); % FP32 peak; HBM GB/s"
 FP32_PEAK_TFLOPS = 157.3     # MI355X dense FP32 (matrix cores and vector)
 HBM_PEAK_GBS = 8000.0
+FLUSH_BYTES = 1 << 30        # written before a cold measurement: more than the 256 MB Infinity Cache
 
 
-# workloads: layer generator, codebook size, Lloyd rounds, description
+# workloads: layer generator, codebook size, Lloyd rounds, first seed of the initial codebooks, description
 CONFIGS = {
-    "resnet18": ("resnet18_stack", 256, 30, "resnet18-3x3-stack (16 layers, 1,220,608 kernels, Laplace)"),
-    "vgg16": ("vgg16_stack", 256, 30, "vgg16-3x3-stack (13 layers, 1,634,496 kernels, normal; conv1 k clamped to 192)"),
-    "single": ("single_layer", 256, 20, "single 64x64 layer (4096 kernels, normal)"),
-    "stress": ("stress_layer", 4096, 10, "stress 1024x1024 layer (1,048,576 kernels from 4096 clusters)"),
+    "resnet18": ("resnet18_stack", 256, 30, 2000, "resnet18-3x3-stack (16 layers, 1,220,608 kernels, Laplace)"),
+    "vgg16": ("vgg16_stack", 256, 30, 1000,
+              "vgg16-3x3-stack (13 layers, 1,634,496 kernels, normal; conv1 k clamped to 192)"),
+    "single": ("single_layer", 256, 20, 1, "single 64x64 layer (4096 kernels, normal)"),
+    "stress": ("stress_layer", 4096, 10, 4000, "stress 1024x1024 layer (1,048,576 kernels from 4096 clusters)"),
 }
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="resnet18", choices=sorted(CONFIGS),
                     help="workload (default: the ResNet-18-shaped stack, the headline metric)")
     ap.add_argument("--iters", type=int, default=None, help="Lloyd rounds per layer (default: the config's)")
     ap.add_argument("--k", type=int, default=None, help="codebook size (default: the config's)")
     ap.add_argument("--yinyang", action="store_true",
                     help="run each layer's Lloyd rounds with Yinyang assignments (Sec. 4.1; the same result)")
-    ap.add_argument("--unfused", action="store_true",
-                    help="run the update as its own pass over the kernels (the member sums are not fused "
-                         "into the assignment)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-diag", action="store_true", help="skip the diagnostic line")
     ap.add_argument("--cpu-iters", type=int, default=2, help="Lloyd rounds of the oracle sample")
-    ap.add_argument("--row", choices=["lloyd", "fc", "search"], default="lloyd",
+    ap.add_argument("--row", choices=["lloyd", "fc", "search", "report"], default="lloyd",
                     help="lloyd: the step above (default); fc: the fully-connected-layer quantizer "
                          "(kq_quantize_scalars, 6 bits, 30 rounds) on the VGG-16 fc6/fc7/fc8 shapes; "
                          "search: the codebook-size search (kq_search_codebook_size) on the "
-                         "ResNet-18 conv1 shape")
+                         "ResNet-18 conv1 shape; report: only the per-layer compression report")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device to device three times (a plain copy "
                          "kernel of known size, the scale for hardware byte counters)")
@@ -90,24 +95,54 @@ def assign_traffic():
     return rec["bytes_per_launch"]
 
 
-def cpu_baseline(layers, iters, budget=1e9):
-    """The CPU oracle (single-threaded plain C) on a bounded sample: `iters` Lloyd
-    rounds plus the final assignment on every layer, each layer cut to its first rows
-    when the full stack would exceed `budget` (kernel x entry x round) units."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def host_cores() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS")
+    return max(1, min(n, int(env))) if env and env.isdigit() else n
+
+
+def cpu_baseline(layers, C0, iters, budget=1e9):
+    """The CPU oracle (plain C) on a bounded sample: `iters` Lloyd rounds plus the final
+    assignment on every layer, each layer cut to its first rows when the full stack would
+    exceed `budget` (kernel x entry x round) units; once on one thread, once with the
+    assignment loop on all host cores (same results)."""
     import oracle
     work = sum(L.n * L.k * (iters + 1) for L in layers)
     f = min(1.0, budget / work)
-    t0 = time.perf_counter()
-    n = 0
-    for L in layers:
-        m = min(L.n, max(L.k, int(L.n * f)))
-        oracle.fit(L.X[:m], L.C0, iters)
-        n += m
-    dt = time.perf_counter() - t0
+
+    def run(threads):
+        oracle.set_threads(threads)
+        t0 = time.perf_counter()
+        n = 0
+        for L, c in zip(layers, C0):
+            m = min(L.n, max(L.k, int(L.n * f)))
+            oracle.fit(L.X[:m], c, iters)
+            n += m
+        return n, time.perf_counter() - t0
+
+    n, dt1 = run(1)
+    cores = host_cores()
+    _, dtn = run(cores)
+    oracle.set_threads(1)
     rows = "all rows" if f >= 1.0 else f"the first {100 * f:.1f} % of the rows"
-    return {"value": n * iters / dt, "unit": "kernels/s", "cores": 1, "kind": "oracle",
+    return {"value": n * iters / dtn, "unit": "kernels/s", "cores": cores, "kind": "oracle",
+            "single_thread_value": n * iters / dt1, "cpu_model": cpu_model(),
             "sample": f"{iters} Lloyd rounds + final assignment on {rows} of all {len(layers)} layers "
-                      f"({n} kernels, k={layers[0].k}), {dt:.1f} s"}
+                      f"({n} kernels, k={layers[0].k}): {dtn:.1f} s with the assignment loop on {cores} "
+                      f"threads, {dt1:.1f} s on one"}
 
 
 def bench_fc(args, kq, torch):
@@ -146,7 +181,7 @@ def bench_search(args, kq, torch, synth):
     dev = torch.device("cuda:0")
     L = synth.resnet18_stack(k=256, layers=1)[0]
     n_init = int(0.3 * L.n)
-    cand = L.X[synth.distinct_init(L.X, n_init, 7)]
+    cand = L.X[kq.kq_forgy_select(L.X, n_init, 7)]
     Xd, Cd = torch.from_numpy(L.X).to(dev), torch.from_numpy(cand).to(dev)
     kq.kq_search_codebook_size(Xd, Cd, 0.5, 8, 30)
     torch.cuda.synchronize()
@@ -161,6 +196,33 @@ def bench_search(args, kq, torch, synth):
                       "config": {"workload": f"resnet18 conv1 64x64 ({L.n} kernels), n_init {n_init}, "
                                              "r = 0.5, 8 iterations"},
                       "ms_per_search": ms, "k": int(k), "trials": [int(t[0]) for t in trials]}))
+
+
+def layer_report(kq, torch, layers, comp, T):
+    """Sec. 4.2.1 per layer: the l2 reconstruction error (mean squared error per weight) of
+    K (the fp32 codebook: the final distortion / 9n) and of K+C (6-bit codebook, weighted
+    k-means as in Sec. 3.2, and the uniform grid), and Eq. (4), (6), (7) for K and K+C."""
+    dev = comp.device
+    uni = kq.kq_quantize_codebook_stack(comp.C, comp.counts, 6, kq.KQ_CBQ_UNIFORM, 0)
+    sq_uni = torch.zeros(len(layers), dtype=torch.float64, device=dev)
+    recon = [{"idx": comp.idx[i], "n": L.n, "C": uni[i][2], "W_ref": comp.X[i], "sq_error": sq_uni[i:i + 1]}
+             for i, L in enumerate(layers)]
+    kq.kq_reconstruct_stack(recon)
+    torch.cuda.synchronize()
+    sq_w, sq_u = comp.sq_error.cpu().tolist(), sq_uni.cpu().tolist()
+    rows = []
+    for i, L in enumerate(layers):
+        p = 9 * L.n
+        B_k, cr_k, beta_k = kq.kq_accounting(L.n, L.k, 32)
+        B_kc, cr_kc, beta_kc = kq.kq_accounting(L.n, L.k, 6)
+        rows.append({"layer": L.name, "n": L.n, "k": L.k, "index_bits": kq.index_bits(L.k),
+                     "mse_K": float(comp.distortion[i][T].item()) / p, "mse_KC_wkmeans": sq_w[i] / p,
+                     "mse_KC_uniform": sq_u[i] / p, "B_K": B_k, "CR_K": cr_k, "beta_K": beta_k,
+                     "B_KC": B_kc, "CR_KC": cr_kc, "beta_KC": beta_kc})
+    n_tot = sum(L.n for L in layers)
+    tot = {"beta_K": sum(r["B_K"] for r in rows) / (9 * n_tot), "beta_KC": sum(r["B_KC"] for r in rows) / (9 * n_tot)}
+    tot["CR_K"], tot["CR_KC"] = 32 / tot["beta_K"], 32 / tot["beta_KC"]
+    return rows, tot
 
 
 def main():
@@ -182,140 +244,40 @@ def main():
         return bench_fc(args, kq, torch)
     if args.row == "search":
         return bench_search(args, kq, torch, synth)
-    gen, k_default, iters_default, desc = CONFIGS[args.config]
+    gen, k_default, iters_default, seed0, desc = CONFIGS[args.config]
     k = args.k if args.k is not None else k_default
     T = args.iters if args.iters is not None else iters_default
-    layers = getattr(synth, gen)(k=k)
+    layers = getattr(synth, gen)(k=k)            # kernels and codebook sizes (k clamped to the distinct kernels)
     n_total = sum(L.n for L in layers)
+    C0 = [np.ascontiguousarray(L.X[kq.kq_forgy_select(L.X, L.k, seed0 + i)]) for i, L in enumerate(layers)]
 
     # inputs resident in HBM before timing
     X = [torch.from_numpy(L.X).to(dev) for L in layers]
-    sizes = [L.k * 9 for L in layers]
-    C0flat = torch.from_numpy(np.concatenate([L.C0.reshape(-1) for L in layers])).to(dev)
-    st = kq.Stack(X, [torch.empty(L.k, 9, device=dev) for L in layers], iters=T)
-    # make the stack's codebooks views of one flat buffer so a step restarts with one copy
-    Cflat = torch.empty_like(C0flat)
-    views = list(torch.split(Cflat, sizes))
-    for i, v in enumerate(views):
-        st.C[i] = v.view(-1, 9)
-        st.layers[i].C = st.C[i].data_ptr()
-    bits = [kq.index_bits(L.k) for L in layers]
-    cb_out = [(torch.empty(L.k * 9, dtype=torch.uint8, device=dev), torch.empty(64, device=dev),
-               torch.empty(L.k, 9, device=dev)) for L in layers]
-    p_idx = [torch.empty((L.n * b + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L, b in zip(layers, bits)]
-    p_codes = [torch.empty((L.k * 9 * 6 + 7) // 8 + 4, dtype=torch.uint8, device=dev) for L in layers]
-    W_hat = [torch.empty(L.n, 9, device=dev) for L in layers]
-    sq = torch.zeros(len(layers), dtype=torch.float64, device=dev)
-    pack_jobs = [(st.idx[i], bits[i], p_idx[i]) for i in range(len(layers))] + \
-                [(cb_out[i][0], 6, p_codes[i]) for i in range(len(layers))]
-    recon = [{"packed": p_idx[i], "bits": bits[i], "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i], "W_ref": X[i],
-              "sq_error": sq[i:i + 1]} for i, L in enumerate(layers)]
-    recon_ws = torch.zeros(max(256, kq.recon_workspace_bytes(recon)), dtype=torch.uint8, device=dev)
-
-    # the member sums come with the assignment when every codebook fits the fused variant
-    fused = max(L.k for L in layers) <= 256 and not args.unfused
+    C0d = [torch.from_numpy(c).to(dev) for c in C0]
+    comp = kq.Compression(X, C0d, iters=T, bits=6, mode=kq.KQ_CBQ_WKMEANS, cbq_iters=30)
     stream = torch.cuda.current_stream(dev)
-    ev = {"assign": [], "assign_final": [], "update": [], "cbq": [], "pack": [], "reconstruct": [], "fit": []}
+
     if args.yinyang:
-        C0_views = [v.view(-1, 9) for v in torch.split(C0flat, sizes)]
-        yy_ws = [torch.empty(kq.lib.kq_yinyang_workspace_bytes(L.n, L.k, 0), dtype=torch.uint8, device=dev)
-                 for L in layers]
-        yy_stats = [torch.zeros(max(T, 1), 3, dtype=torch.int64, device=dev) for L in layers]
+        return bench_yinyang(args, kq, torch, layers, X, C0d, comp, T, desc, k)
 
-    def timed(name, record, fn):
-        if not record:
-            fn()
-            return
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        fn()
-        e1.record(stream)
-        ev[name].append((e0, e1))
-
-    def yinyang_rounds(record: bool):
-        for i in range(len(layers)):
-            timed("fit", record, lambda i=i: kq.kq_fit_layer_yinyang(
-                X[i], C0_views[i], T, C=st.C[i], idx=st.idx[i], counts=st.counts[i],
-                distortion=st.distortion[i], stats=yy_stats[i], workspace=yy_ws[i]))
-
-    def step(record: bool):
-        if args.yinyang:
-            yinyang_rounds(record)
-            timed("cbq", record, lambda: kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30,
-                                                                       out=cb_out))
-            timed("pack", record, lambda: kq.kq_pack_bits_stack(pack_jobs))
-            timed("reconstruct", record, lambda: kq.kq_reconstruct_stack(recon, workspace=recon_ws))
-            return
-        Cflat.copy_(C0flat)
-        for t in range(T + 1):
-            if record:
-                a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a0.record(stream)
-            kq.kq_assign_stack(st, dist_slot=t, distortion=False, fused_sums=fused and t < T)
-            if record:
-                a1.record(stream)
-                # the rounds' launches (fused when the sums come with them) and the final one apart
-                ev["assign" if t < T else "assign_final"].append((a0, a1))
-            if t < T:
-                if record:
-                    u0, u1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    u0.record(stream)
-                kq.kq_update_stack(st, dist_slot=t, distortion_from_assign=True, sums_from_assign=fused)
-                if record:
-                    u1.record(stream)
-                    ev["update"].append((u0, u1))
-        kq.kq_update_stack(st, dist_slot=T, counts_only=True, distortion_from_assign=True)
-        timed("cbq", record, lambda: kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30,
-                                                                   out=cb_out))
-        timed("pack", record, lambda: kq.kq_pack_bits_stack(pack_jobs))
-        timed("reconstruct", record, lambda: kq.kq_reconstruct_stack(recon, workspace=recon_ws))
-
+    # one event pair per timed step, recorded by the library around one round's assignment
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ev:                              # torch creates its events on their first record
+        a.record(stream)
+        b.record(stream)
     for _ in range(args.warmup):
-        step(False)
+        comp.run()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(False)
+    for s in range(args.steps):
+        comp.run(round_events={s % T: ev[s]} if T > 0 else None)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = 1e3 * elapsed / args.steps
-    # Per-launch durations: one more step with HIP events around every launch on the stream
-    # the kernels run on.  It is kept out of the timed steps above because an event record
-    # between two kernels adds a few microseconds of its own to the step.  Two untimed steps
-    # are queued first: the host then enqueues the event step while the GPU still works
-    # through them, so every event is stamped by the GPU's progress and not by a host that
-    # is slower than the kernels it launches.
-    for _ in range(2):
-        step(False)
-    step(True)
-    torch.cuda.synchronize()
-
-    # Eq. (2) codebook retraining step on the same stack (not part of the step): synthetic
-    # gradients of the kernels' shape, the final assignment, one launch set per step
-    gst = kq.Stack([x * 1e-3 for x in X], [c.view(-1, 9) for c in st.C])
-    for i in range(len(layers)):
-        gst.idx[i].copy_(st.idx[i])
-    kq.kq_codebook_grad_step_stack(gst, 0.01)
-    step(False)  # queued GPU work ahead of the events, as above
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for _ in range(5):
-        kq.kq_codebook_grad_step_stack(gst, 0.01)
-    g1.record(stream)
-    torch.cuda.synchronize()
-    grad_ms = g0.elapsed_time(g1) / 5
-
-    # reconstruction alone (int32 indices, no error; not part of the step): 4 B read and
-    # 36 B written per kernel, five launches between HIP events after a queued step
-    recon_plain = [{"idx": st.idx[i], "n": L.n, "C": cb_out[i][2], "W_hat": W_hat[i]} for i, L in enumerate(layers)]
-    step(False)
-    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    r0.record(stream)
-    for _ in range(5):
-        kq.kq_reconstruct_stack(recon_plain, workspace=recon_ws)
-    r1.record(stream)
-    torch.cuda.synchronize()
-    recon_plain_ms = r0.elapsed_time(r1) / 5
+    assign_ms = float(np.mean([a.elapsed_time(b) for a, b in ev])) if T > 0 else 0.0
+    flops = 18.0 * sum(L.k * L.n for L in layers)   # 9 multiply-adds per (kernel, entry) pair
+    achieved = flops / (assign_ms * 1e-3) / 1e12 if assign_ms > 0 else 0.0
+    fused = max(L.k for L in layers) <= 256
 
     if args.copy_probe > 0:
         src = torch.ones(args.copy_probe << 18, device=dev)
@@ -324,47 +286,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
 
-    mean_ms = {name: float(np.mean([a.elapsed_time(b) for a, b in pairs])) if pairs else 0.0
-               for name, pairs in ev.items()}
-    assign_ms, update_ms = mean_ms["assign"], mean_ms["update"]
-    rec_bytes = sum(L.n * (b / 8 + 36 + 36) for L, b in zip(layers, bits))  # packed index + reference + output row
-    flops = 18.0 * sum(L.k * L.n for L in layers)   # 9 multiply-adds per (kernel, entry) pair
-    achieved = flops / (assign_ms * 1e-3) / 1e12 if assign_ms > 0 else 0.0
-    # the separate update reads a 36-byte kernel and a 4-byte index per kernel; with fused
-    # sums the round's update is only the finish over the assignment's partial sums, so no
-    # kernel bytes are credited to it
-    upd_bytes = 40.0 * n_total
-    upd_gbs = upd_bytes / (update_ms * 1e-3) / 1e9 if update_ms > 0 and not fused else None
-
-    yy_diag = None
-    if args.yinyang:
-        # the fits' own work: the round-0 assignment is a full one (n k distances), rounds
-        # 1..T scan what the bounds leave (per-round counts from the library)
-        stats = [s.cpu().numpy() for s in yy_stats]
-        evals = sum(L.n * L.k + int(s[:T, 2].sum()) for L, s in zip(layers, stats))
-        full = sum(L.n * L.k * (T + 1) for L in layers)
-        fit_ms = sum(a.elapsed_time(b) for a, b in ev["fit"])
-        yy_diag = {"fit_ms": fit_ms, "distance_evaluations": evals, "lloyd_equivalent": full,
-                   "evaluated_fraction": evals / full,
-                   "kernels_scanned_per_round": [int(x) for x in np.sum([s[:T, 0] for s in stats], axis=0)],
-                   "pairs_scanned_per_round": [int(x) for x in np.sum([s[:T, 1] for s in stats], axis=0)]}
-        achieved = 18.0 * evals / (fit_ms * 1e-3) / 1e12
-    J = [float(d[T]) for d in st.distortion]
-    mse_k = [j / (9 * L.n) for j, L in zip(J, layers)]
-    mse_kc = [float(s) / (9 * L.n) for s, L in zip(sq.cpu(), layers)]
-    print(json.dumps({"diag": {
-        "assign_ms": assign_ms, "assign_TFLOPs": achieved, "update_ms": update_ms, "update_is_finish_only": fused,
-        "update_GBps": upd_gbs,
-        "lloyd_round_ms": assign_ms + update_ms, "final_assign_ms": mean_ms["assign_final"], "cbq_ms": mean_ms["cbq"], "pack_ms": mean_ms["pack"],
-        "reconstruct_ms": mean_ms["reconstruct"],
-        "reconstruct_GBps": rec_bytes / (mean_ms["reconstruct"] * 1e-3) / 1e9 if mean_ms["reconstruct"] else 0.0,
-        "reconstruct_plain_ms": recon_plain_ms,
-        "reconstruct_plain_GBps": 40.0 * n_total / (recon_plain_ms * 1e-3) / 1e9,
-        "grad_step_ms": grad_ms, "grad_step_GBps": 40.0 * n_total / (grad_ms * 1e-3) / 1e9,
-        "mse_K_first_last": [mse_k[0], mse_k[-1]], "mse_KC_first_last": [mse_kc[0], mse_kc[-1]],
-        "beta_K": sum(L.k * 9 * 32 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
-        "beta_KC": sum(L.k * 9 * 6 + L.n * b for L, b in zip(layers, bits)) / (9 * n_total),
-        "yinyang": yy_diag}}), file=sys.stderr)
+    if args.row == "report":
+        rows, tot = layer_report(kq, torch, layers, comp, T)
+        print(json.dumps({"report": rows, "stack": tot, "config": desc, "k": k, "lloyd_rounds": T}))
+        return
+    if not args.no_diag:
+        print(json.dumps({"diag": diagnostics(kq, torch, np, layers, comp, T, fused, stream)}), file=sys.stderr,
+              flush=True)
 
     result = {
         "metric": METRIC,
@@ -380,24 +308,156 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{desc} k={k}: {T} Lloyd rounds + final assignment, "
-                               "6-bit weighted codebook quantization, index/code packing, packed reconstruction",
+                               "6-bit weighted codebook quantization, index/code packing, packed reconstruction "
+                               "(one kq_compress_stack call per step)",
                    "layers": len(layers), "kernels": n_total, "k": k, "lloyd_rounds": T, "codebook_bits": 6},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / FP32_PEAK_TFLOPS,
-                     "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) and fused else None,
+                     "traffic": assign_traffic() if (args.config, k) == ("resnet18", 256) else None,
                      "kernel": ("assign_kernel<2, true> (member sums fused)" if fused else "assign_kernel<2, false>")
-                               + " averaged over the Lloyd rounds' launches (one per round, whole stack)"},
+                               + f": one Lloyd round's launch per timed step (rounds 0..{min(args.steps, T) - 1}), "
+                                 "whole stack per launch",
+                     "pricing": "bf16-split MFMA screening + exact fp32 rescoring; the method's fp32 flops "
+                                "(18 k per kernel) priced at the 157.3 TFLOP/s FP32 peak"},
     }
-    if args.yinyang:
-        # distances the Yinyang fits evaluated (matrix-core round 0 + exact fp32 scans), 18 flop
-        # each, over the fits' whole time (updates included); the scans run unpacked fp32 VALU
-        result["config"]["assignment"] = "yinyang"
-        result["roofline"] = {"bound": "alu", "achieved": achieved, "peak": FP32_PEAK_TFLOPS / 2, "unit": "TFLOP/s",
-                              "frac": achieved / (FP32_PEAK_TFLOPS / 2), "traffic": None,
-                              "kernel": "kq_fit_layer_yinyang (all launches of the fits)"}
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(layers, args.cpu_iters)
+        result["cpu_baseline"] = cpu_baseline(layers, C0, args.cpu_iters)
     print(json.dumps(result), flush=True)
+
+
+def head_start(torch, stream, ms=2.0):
+    """Queue about `ms` of GPU spinning (no memory traffic) so that the launches queued
+    after it are timed by the GPU's progress, not by how fast the host enqueues them."""
+    if not hasattr(head_start, "cycles"):          # calibrate the spin once
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        torch.cuda._sleep(1_000_000)
+        b.record(stream)
+        torch.cuda.synchronize()
+        head_start.cycles = int(1_000_000 * ms / max(a.elapsed_time(b), 1e-3))
+    torch.cuda._sleep(head_start.cycles)
+
+
+def timed_launches(torch, stream, fn, reps, prep=None, flush=None):
+    """Mean duration (ms) of fn's launches between two HIP events, `reps` times, all queued
+    behind a head start; `prep` runs (untimed) before each; with `flush`, a 1 GiB buffer
+    is written before each so the launches start from a cold cache."""
+    pairs = []
+    head_start(torch, stream)
+    for _ in range(reps):
+        if prep:
+            prep()
+        if flush is not None:
+            flush.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        pairs.append((a, b))
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in pairs) / reps
+
+
+def diagnostics(kq, torch, np, layers, comp, T, fused, stream):
+    """Per-launch times of the other steps, through the per-step stack calls on the state
+    the timed steps left (the same kernels and launch configurations), warm and after a
+    1 GiB flush; the per-layer report; the Eq. (2) codebook step."""
+    dev = comp.device
+    n_total = sum(L.n for L in layers)
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    st = kq.Stack(comp.X, [c.clone() for c in comp.C], iters=1)
+    reps = 5
+
+    def both(fn, prep=None):
+        if prep:
+            prep()
+        fn()                                       # caches warm
+        return (timed_launches(torch, stream, fn, reps, prep),
+                timed_launches(torch, stream, fn, reps, prep, flush))
+
+    d = {}
+    # the shifts of the layers' sums once (an update that finds them), then each step's launches alone
+    kq.kq_update_stack(st)
+    if fused:
+        d["assign_fused_ms"] = both(lambda: kq.kq_assign_stack(st, distortion=False, fused_sums=True,
+                                                               reuse_shifts=True))
+        d["finish_ms"] = both(lambda: kq.kq_update_stack(st, distortion_from_assign=True, sums_from_assign=True),
+                              prep=lambda: kq.kq_assign_stack(st, distortion=False, fused_sums=True,
+                                                              reuse_shifts=True))
+    d["assign_plain_ms"] = both(lambda: kq.kq_assign_stack(st, distortion=False))
+    upd = both(lambda: kq.kq_update_stack(st, reuse_shifts=True))
+    d["update_separate_ms"] = upd                              # update_kernel + finish, 40 B per kernel read
+    d["update_separate_GBps"] = [40.0 * n_total / (t * 1e-3) / 1e9 for t in upd]
+    d["cbq_wkmeans_ms"] = both(lambda: kq.kq_quantize_codebook_stack(comp.C, comp.counts, 6, kq.KQ_CBQ_WKMEANS, 30))
+    jobs = [(comp.idx[i], comp.index_bits[i], comp.packed_idx[i]) for i in range(len(layers))] + \
+           [(comp.codes[i], 6, comp.packed_codes[i]) for i in range(len(layers))]
+    d["pack_ms"] = both(lambda: kq.kq_pack_bits_stack(jobs))
+    rec_err = [{"packed": comp.packed_idx[i], "bits": comp.index_bits[i], "n": L.n, "C": comp.C_hat[i],
+                "W_hat": comp.W_hat[i], "W_ref": comp.X[i], "sq_error": comp.sq_error[i:i + 1]}
+               for i, L in enumerate(layers)]
+    rec_plain = [{"idx": comp.idx[i], "n": L.n, "C": comp.C_hat[i], "W_hat": comp.W_hat[i]}
+                 for i, L in enumerate(layers)]
+    ws = torch.zeros(max(256, kq.recon_workspace_bytes(rec_err)), dtype=torch.uint8, device=dev)
+    d["reconstruct_packed_with_error_ms"] = both(lambda: kq.kq_reconstruct_stack(rec_err, workspace=ws))
+    rp = both(lambda: kq.kq_reconstruct_stack(rec_plain, workspace=ws))
+    d["reconstruct_plain_ms"] = rp                             # 4 B index read + 36 B row written per kernel
+    d["reconstruct_plain_GBps"] = [40.0 * n_total / (t * 1e-3) / 1e9 for t in rp]
+    d["warm_cold_note"] = ("each pair [warm, cold]: mean of 5 launches queued behind a head start, then of 5 "
+                           "launches each after writing a 1 GiB buffer")
+    # Eq. (2) codebook retraining step on the same stack: synthetic gradients of the kernels'
+    # shape and the final assignment, one launch set per step
+    gst = kq.Stack([x * 1e-3 for x in comp.X], [c.clone() for c in comp.C])
+    for i in range(len(layers)):
+        gst.idx[i].copy_(comp.idx[i])
+    g = both(lambda: kq.kq_codebook_grad_step_stack(gst, 0.01))
+    d["grad_step_ms"] = g
+    d["grad_step_GBps"] = [40.0 * n_total / (t * 1e-3) / 1e9 for t in g]
+    rows, tot = layer_report(kq, torch, layers, comp, T)
+    d["report"] = rows
+    d["report_stack"] = tot
+    del flush
+    return d
+
+
+def bench_yinyang(args, kq, torch, layers, X, C0d, comp, T, desc, k):
+    """Each layer's fit with Yinyang assignments (Sec. 4.1): the same result as the Lloyd
+    path; the distances its bounds leave to evaluate, over its whole time."""
+    import numpy as np
+    dev = comp.device
+    stream = torch.cuda.current_stream(dev)
+    yy_ws = [torch.empty(kq.lib.kq_yinyang_workspace_bytes(L.n, L.k, 0), dtype=torch.uint8, device=dev)
+             for L in layers]
+    stats = [torch.zeros(max(T, 1), 3, dtype=torch.int64, device=dev) for _ in layers]
+
+    def step():
+        for i in range(len(layers)):
+            kq.kq_fit_layer_yinyang(X[i], C0d[i], T, C=comp.C[i], idx=comp.idx[i], counts=comp.counts[i],
+                                    distortion=comp.distortion[i], stats=stats[i], workspace=yy_ws[i])
+        kq.kq_quantize_codebook_stack(comp.C, comp.counts, 6, kq.KQ_CBQ_WKMEANS, 30)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = 1e3 * (time.perf_counter() - t0) / args.steps
+    st = [s.cpu().numpy() for s in stats]
+    evals = sum(L.n * L.k + int(s[:T, 2].sum()) for L, s in zip(layers, st))
+    full = sum(L.n * L.k * (T + 1) for L in layers)
+    achieved = 18.0 * evals / (ms_step * 1e-3) / 1e12
+    n_total = sum(L.n for L in layers)
+    print(json.dumps({"metric": METRIC, "value": n_total * T / (ms_step * 1e-3), "unit": "kernels/s", "n_gpus": 1,
+                      "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+                      "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": f"{desc} k={k}: {T} Yinyang Lloyd rounds + final assignment per layer, "
+                                             "6-bit weighted codebook quantization", "assignment": "yinyang"},
+                      "roofline": {"bound": "alu", "achieved": achieved, "peak": FP32_PEAK_TFLOPS / 2,
+                                   "unit": "TFLOP/s", "frac": achieved / (FP32_PEAK_TFLOPS / 2), "traffic": None,
+                                   "kernel": "kq_fit_layer_yinyang (all launches of the fits, whole step)"},
+                      "yinyang": {"distance_evaluations": evals, "lloyd_equivalent": full,
+                                  "evaluated_fraction": evals / full}}), flush=True)
 
 
 if __name__ == "__main__":

@@ -22,6 +22,9 @@
  *                        fully-connected layer (any size).
  *   kq_pack_bits         Eq. (4): the n * ceil(log2 k)-bit index stream.
  *   kq_reconstruct       end of Sec. 3.2: recover the weight tensor from codebook + indices.
+ *   kq_compress_stack    all of the above for the layers of a network in one call.
+ *   kq_forgy_select      the k-means initialisation (k distinct kernels in a seeded order).
+ *   kq_accounting        Eq. (4), (6), (7): storage bits, compression ratio, bits per parameter.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -31,7 +34,8 @@
  *    this is the tensor itself (kernel i = o * C_in + c).  Codebooks C are k rows of 9.
  *  - Pointers named device are device memory (hipMalloc / torch.cuda); pointers named
  *    host are host memory.  Every buffer belongs to the caller.  The library never
- *    allocates memory and keeps no global state.
+ *    allocates device memory and keeps no global state (kq_forgy_select, a host-only
+ *    helper, uses host memory while it runs).
  *  - stream is a hipStream_t (NULL = the null stream).  Device calls only enqueue work
  *    on that stream and return; outputs are valid once the stream has been synchronised.
  *  - Arguments are checked on the host before anything is enqueued.  On an error
@@ -42,9 +46,12 @@
  *    query returns, 256-byte aligned.  Its contents need no initialisation: every
  *    call writes what it later reads.  Calls that share a workspace must be ordered on one
  *    stream (concurrent calls on one workspace race).
- *  - Kernel values must be finite with |x| < 32 for kq_update / kq_fit_* (the member
- *    sums are exact 64-bit fixed-point sums, see kq_update).  Real CNN weights are
- *    orders of magnitude smaller.
+ *  - The member sums of the update are exact 64-bit fixed-point sums at a per-layer scale
+ *    taken from the layer's largest magnitude (see kq_update), so any finite kernel values
+ *    are supported.  Non-finite values make the sums meaningless: calls that form sums accept
+ *    KQ_F_VALIDATE, which checks every value first (one pass over the kernels, then a wait
+ *    for the result) and returns KQ_ERR_RANGE, with no output written, if any is NaN or
+ *    infinite.  Without the flag such inputs give unspecified codebooks (no fault).
  */
 #ifndef KQ_H
 #define KQ_H
@@ -61,7 +68,7 @@ typedef enum kq_status {
     KQ_ERR_ARG = 1,          /* null pointer, bad size, misaligned pointer */
     KQ_ERR_UNSUPPORTED = 2,  /* dim != 9, k above KQ_MAX_K, bits outside 1..16 */
     KQ_ERR_WORKSPACE = 3,    /* workspace missing, too small or misaligned */
-    KQ_ERR_RANGE = 4,        /* reserved: input outside the supported value range */
+    KQ_ERR_RANGE = 4,        /* KQ_F_VALIDATE: a kernel (or gradient) value is NaN or infinite */
     KQ_ERR_HIP = 5           /* a HIP runtime call failed */
 } kq_status;
 
@@ -91,6 +98,15 @@ typedef enum kq_status {
 #define KQ_F_EXACT_SEARCH 16u /* kq_quantize_scalars: every code by the exact fp64 search (reference) */
 #define KQ_F_THRESHOLDS 32u  /* kq_quantize_scalars: codes from level thresholds at any size, wherever
                                 they are valid (by default only from 3 * 2^20 scalars on) */
+#define KQ_F_VALIDATE 64u    /* kq_update, kq_update_stack, kq_assign_stack, kq_fit_layer,
+                                kq_fit_stack, kq_compress_stack: check that every kernel value
+                                is finite before anything is written; KQ_ERR_RANGE otherwise.
+                                The call then waits on the stream for the check. */
+#define KQ_F_REUSE_SHIFTS 128u /* kq_assign_stack (with KQ_F_FUSED_SUMS), kq_update_stack: the
+                                layers' fixed-point shifts are those the preceding stack call on
+                                the same layers and workspace found (a fused assignment, or an
+                                update without this flag); the kernels must not have changed
+                                since.  Saves the pass over the kernels that finds them. */
 #define KQ_F_SUMS_FROM_ASSIGN 8u
                              /* kq_update_stack: finish the update from the sums the preceding
                                 kq_assign_stack with KQ_F_FUSED_SUMS left (same layers and
@@ -116,10 +132,10 @@ const char* kq_status_string(kq_status s);
 int32_t kq_abi_version(void);
 
 /*
- * Workspace bytes for one layer of n kernels and k entries for op (KQ_OP_*).
- * Returns 0 for invalid sizes.
+ * Workspace bytes for one layer of n kernels of dim values and k entries for op (KQ_OP_*;
+ * KQ_OP_SQ_ERROR: n values, k = 1, dim = 1).  Returns 0 for invalid or unsupported sizes.
  */
-size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k);
+size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k, int32_t dim);
 
 /* Workspace bytes for a stack call (kq_assign_stack / kq_update_stack / kq_fit_stack). */
 size_t kq_stack_workspace_bytes(const kq_layer* layers /* host [n_layers] */, int32_t n_layers);
@@ -151,9 +167,11 @@ kq_status kq_assign(const float* X, int64_t n, int32_t dim, const float* C, int3
  *
  *   counts[j] = |S_j| = #{i : idx[i] == j}
  *   C_new[j]  = mean of the kernels in S_j, or C_old[j] when S_j is empty.
- *   The member sums are exact integer sums of q(x) = rint(x * 2^s), s = 57 -
- *   ceil(log2 n), so they do not depend on summation order; the mean is
- *   fp32( (double(sum) * 2^-s) / |S_j| ).
+ *   The member sums are exact integer sums of q(x) = rint(x * 2^s) with
+ *   s = 62 - ceil(log2 n) - e, e the smallest integer with max_i |x_i| < 2^e (-126 if that
+ *   maximum is subnormal; a first pass over X finds it), so no sum can overflow and the resolution is
+ *   2^-(62 - ceil(log2 n)) of the largest magnitude at any scale of the weights; the sums
+ *   do not depend on summation order, and the mean is fp32( (double(sum) * 2^-s) / |S_j| ).
  *
  *   *distortion = the Eq. (1) objective of the given assignment against C_old:
  *               sum_i d(x_i, C_old[idx[i]]) with d the fp32 distance of kq_assign,
@@ -161,7 +179,7 @@ kq_status kq_assign(const float* X, int64_t n, int32_t dim, const float* C, int3
  *
  *   X device [n][9]; idx device [n] values in [0, k) (out-of-range indices are
  *   ignored); C_old, C_new device [k][9] (may alias); counts device [k] or NULL.
- *   flags: 0, or KQ_F_COUNTS_ONLY to compute only the counts (C_new untouched).
+ *   flags: KQ_F_COUNTS_ONLY to compute only the counts (C_new untouched); KQ_F_VALIDATE.
  */
 kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
                     const float* C_old, float* C_new, int32_t* counts, double* distortion,
@@ -175,7 +193,7 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
  *   C [k][9] ends as the codebook after `iters` updates, idx [n] the final
  *   assignment, counts [k] (may be NULL) its member counts, distortion
  *   device [iters+1] (may be NULL) the distortion of every assignment.
- *   Requires 1 <= k <= n.  C_init may equal C.
+ *   Requires 1 <= k <= n.  C_init may equal C (it is only read).  flags: 0 or KQ_F_VALIDATE.
  */
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init,
                        int32_t iters, float* C, int32_t* idx, int32_t* counts, double* distortion,
@@ -194,7 +212,7 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
  *   fp64(sum) / z and c - gamma * mean is evaluated in fp64 and rounded once to fp32.
  *   counts [k] (may be NULL) receives z.  C_old and C_new may alias (in-place step).
  *   G, C_old, C_new device [.][9] fp32; idx device [n]; gamma finite (else KQ_ERR_ARG).
- *   workspace: kq_workspace_bytes(KQ_OP_GRAD, n, k).
+ *   workspace: kq_workspace_bytes(KQ_OP_GRAD, n, k, 9).
  *   kq_codebook_grad_step_stack: the same for every layer of a stack in one launch set;
  *   layers[l].X holds the layer's gradients and layers[l].C is stepped in place
  *   (workspace: kq_stack_workspace_bytes).
@@ -207,7 +225,7 @@ kq_status kq_codebook_grad_step_stack(const kq_layer* layers, int32_t n_layers, 
 
 /*
  * kq_quantize_scalars -- end of Sec. 3.2: the 6-bit quantization of a fully-connected
- * layer "with the same k-means clustering method" as the codebooks, i.e. the algorithm of
+ * layer by the k-means the codebooks are quantized with, i.e. the algorithm of
  * kq_quantize_codebook (KQ_CBQ_WKMEANS) on one flat set of `count` scalars, every weight 1,
  * for sets far larger than a codebook (a VGG-16 fc6 weight has 102,760,448 scalars).
  *
@@ -288,7 +306,7 @@ kq_status kq_search_codebook_size(const float* X, int64_t n, int32_t dim, const 
  *                      (device int64 [iters][3] or NULL): the scan counts of rounds 1..iters.
  *   X device [n][9]; C, C_prev, C_init device [k][9]; idx device [n]; best_d device [n];
  *   counts device [k].  Requires 1 <= k <= n.  Kernel and codebook values must be finite
- *   with |x| < 32 (the grouping and the fit run kq_update's fixed-point sums).
+ *   (the grouping and the fit run kq_update's fixed-point sums).
  *   workspace: kq_yinyang_workspace_bytes(n, k, groups) bytes (about 20 bytes per kernel
  *   and group plus kq_workspace_bytes); it carries the state from one call to the next,
  *   so the calls of one fit must use one workspace, in order, on one stream.
@@ -398,7 +416,7 @@ kq_status kq_unpack_bits(const uint8_t* in, int64_t count, int32_t bits, int32_t
  * kq_reconstruct -- end of Sec. 3.2: W_hat[i][d] = C[idx[i]][d].
  *   Pass the 6-bit dequantised codebook (C_hat of kq_quantize_codebook) for K+C.
  *   idx device [n] values in [0, k) (others give zeros); C device [k][9];
- *   W_hat device [n][9], 16-byte aligned.
+ *   W_hat device [n][9]; every pointer 4-byte aligned.
  */
 kq_status kq_reconstruct(const int32_t* idx, int64_t n, const float* C, int32_t k, int32_t dim,
                          float* W_hat, void* stream);
@@ -416,7 +434,7 @@ kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, 
  *   *out = sum_i (double(A[i]) - double(B[i]))^2 over `count` fp32 values, in fp64,
  *   in a fixed order (the same bits on every run).
  *   A, B device [count] fp32, 4-byte aligned; out device fp64 scalar;
- *   workspace of kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1) bytes.
+ *   workspace of kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1, 1) bytes.
  */
 kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out,
                       void* ws, size_t ws_bytes, void* stream);
@@ -463,6 +481,79 @@ size_t kq_reconstruct_stack_workspace_bytes(const kq_recon_layer* layers /* host
  * every layer of a host array, 1 <= n_layers <= KQ_MAX_STACK; all pointers 4-byte aligned. */
 kq_status kq_reconstruct_stack(const kq_recon_layer* layers, int32_t n_layers, void* ws, size_t ws_bytes,
                                void* stream);
+
+/*
+ * kq_compress_stack -- the whole compression pass of Sec. 3 for the layers of a network, in
+ * one call (one stream-ordered sequence of launches; nothing waits on the host unless
+ * KQ_F_VALIDATE is set):
+ *   1. Sec. 3.1, Eq. (1): `iters` Lloyd rounds from C_init and a final assignment
+ *      (kq_fit_stack): C, idx, counts, distortion [iters + 1];
+ *   2. Sec. 3.2: quantization of every codebook to 2^bits levels with the entry counts as
+ *      weights (kq_quantize_codebook_stack_ws, `mode`, `cbq_iters` rounds): codes, levels,
+ *      C_hat;
+ *   3. Eq. (4): the ceil(log2 k)-bit index stream and the `bits`-bit code stream
+ *      (kq_pack_bits; each optional);
+ *   4. end of Sec. 3.2: W_hat = C_hat[idx] from the packed stream when there is one
+ *      (kq_reconstruct_stack; optional), and the squared error of W_hat against X.
+ *   Every output is bit for bit what the separate calls give.
+ *   All pointers are device pointers; C_init is only read (it may equal C).  1 <= k <= n;
+ *   1 <= bits <= 8; n_layers >= 1 (processed KQ_MAX_STACK layers at a time).
+ *   flags: 0 or KQ_F_VALIDATE.  workspace: kq_compress_workspace_bytes(layers, n_layers, bits).
+ *   round_events: NULL, or a host array of 2 * (iters + 1) hipEvent_t handles created by the
+ *   caller, any of them NULL: entries 2t and 2t + 1 are recorded on the stream just before and
+ *   just after the assignment launch of Lloyd round t (t = iters: the final assignment) of the
+ *   first KQ_MAX_STACK layers, so the caller can time that launch inside the pass.
+ */
+typedef struct kq_compress_layer {
+    const float* X;          /* [n][9] kernels */
+    int64_t n;
+    int32_t k;
+    const float* C_init;     /* [k][9] initial codebook */
+    float* C;                /* [k][9] codebook after `iters` rounds */
+    int32_t* idx;            /* [n] final assignment */
+    int32_t* counts;         /* [k] kernels per entry (final assignment) */
+    double* distortion;      /* [iters + 1] or NULL */
+    uint8_t* codes;          /* [k * 9] */
+    float* levels;           /* [2^bits] */
+    float* C_hat;            /* [k][9] levels[codes] */
+    uint8_t* packed_idx;     /* ceil(n * ceil(log2 k) / 8) bytes, 4-byte aligned, or NULL */
+    uint8_t* packed_codes;   /* ceil(9 k bits / 8) bytes, 4-byte aligned, or NULL */
+    float* W_hat;            /* [n][9] or NULL */
+    double* sq_error;        /* scalar or NULL (needs W_hat): sum of (X - W_hat)^2 over 9n values, fp64 */
+} kq_compress_layer;
+
+size_t kq_compress_workspace_bytes(const kq_compress_layer* layers, int32_t n_layers, int32_t bits);
+kq_status kq_compress_stack(const kq_compress_layer* layers, int32_t n_layers, int32_t iters, int32_t mode,
+                            int32_t bits, int32_t cbq_iters, uint32_t flags, void* const* round_events, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/*
+ * Host-only helpers (no HIP call, no device memory).
+ *
+ * kq_index_bits: ceil(log2 k), the index width of Eq. (4) (0 for k = 1; -1 for k < 1).
+ *
+ * kq_accounting -- storage of a quantized layer of n kernels of dim = omega^2 values with a
+ *   codebook of k entries stored at bc bits per value:
+ *     Eq. (4): B = k * dim * bc + n * ceil(log2 k) bits;
+ *     Eq. (6): C_KQ = 32 * n * dim / B (against fp32 weights);
+ *     Eq. (7): beta = B / (n * dim) bits per parameter.
+ *   bc = 32 for the fp32 codebook (K), 6 for the 6-bit one (K+C); the table of 2^bits levels
+ *   is not counted.  Each output pointer may be NULL.  n, k, dim >= 1, 1 <= bc <= 64.
+ *
+ * kq_forgy_select -- the initial codebook of the k-means: k bitwise-distinct kernels of X
+ *   (-0 and +0 count as equal) in a seeded random order.  Generator: splitmix64 (state +=
+ *   0x9E3779B97F4A7C15, output mixed by the variant-13 finalizer), state = seed.  Order: a
+ *   partial Fisher-Yates shuffle of 0 .. n-1: for i = 0, 1, ...: j = i + (next() mod (n - i)),
+ *   swap positions i and j, candidate = the value now at position i; a candidate whose
+ *   kernel equals an accepted one is skipped; stop at k accepted.  sel[q] = the q-th
+ *   accepted kernel.  X host [n][9]; sel host [k].  KQ_ERR_ARG when X has fewer than k
+ *   distinct kernels (sel untouched).  Host memory of O(k + draws) entries is used while it
+ *   runs and released before it returns.
+ */
+int32_t kq_index_bits(int32_t k);
+kq_status kq_accounting(int64_t n, int32_t k, int32_t dim, int32_t bc, int64_t* storage_bits, double* ratio,
+                        double* bits_per_param);
+kq_status kq_forgy_select(const float* X, int64_t n, int32_t dim, int32_t k, uint64_t seed, int64_t* sel);
 
 #ifdef __cplusplus
 }

@@ -51,12 +51,18 @@ class KqReconLayer(ctypes.Structure):
                 ("W_hat", _P), ("W_ref", _P), ("sq_error", _P)]
 
 
+class KqCompressLayer(ctypes.Structure):
+    _fields_ = [("X", _P), ("n", _I64), ("k", _I32), ("C_init", _P), ("C", _P), ("idx", _P), ("counts", _P),
+                ("distortion", _P), ("codes", _P), ("levels", _P), ("C_hat", _P), ("packed_idx", _P),
+                ("packed_codes", _P), ("W_hat", _P), ("sq_error", _P)]
+
+
 def _load():
     lib = ctypes.CDLL(LIB_PATH)
     sig = {
         "kq_status_string": ([_I32], ctypes.c_char_p),
         "kq_abi_version": ([], _I32),
-        "kq_workspace_bytes": ([_I32, _I64, _I32], _SZ),
+        "kq_workspace_bytes": ([_I32, _I64, _I32, _I32], _SZ),
         "kq_stack_workspace_bytes": ([_P, _I32], _SZ),
         "kq_workspace_init": ([_P, _SZ, _P], _I32),
         "kq_assign": ([_P, _I64, _I32, _P, _I32, _P, _P, _P, _U32, _P, _SZ, _P], _I32),
@@ -88,6 +94,11 @@ def _load():
         "kq_yinyang_init": ([_P, _I64, _I32, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_yinyang_assign": ([_P, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P, _P, _P, _SZ, _P], _I32),
         "kq_fit_layer_yinyang": ([_P, _I64, _I32, _I32, _P, _I32, _I32, _P, _P, _P, _P, _P, _P, _SZ, _P], _I32),
+        "kq_compress_workspace_bytes": ([_P, _I32, _I32], _SZ),
+        "kq_compress_stack": ([_P, _I32, _I32, _I32, _I32, _I32, _U32, _P, _P, _SZ, _P], _I32),
+        "kq_index_bits": ([_I32], _I32),
+        "kq_accounting": ([_I64, _I32, _I32, _I32, _P, _P, _P], _I32),
+        "kq_forgy_select": ([_P, _I64, _I32, _I32, ctypes.c_uint64, _P], _I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -111,6 +122,8 @@ KQ_F_FUSED_SUMS = 4
 KQ_F_SUMS_FROM_ASSIGN = 8
 KQ_F_EXACT_SEARCH = 16
 KQ_F_THRESHOLDS = 32
+KQ_F_VALIDATE = 64
+KQ_F_REUSE_SHIFTS = 128
 EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stack_workspace_bytes",
             "kq_workspace_init", "kq_assign", "kq_update", "kq_fit_layer", "kq_assign_stack",
             "kq_update_stack", "kq_fit_stack", "kq_quantize_codebook", "kq_quantize_codebook_stack",
@@ -119,7 +132,9 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_pack_bits_stack", "kq_reconstruct_stack_workspace_bytes", "kq_reconstruct_stack",
             "kq_yinyang_workspace_bytes", "kq_yinyang_init", "kq_yinyang_assign", "kq_fit_layer_yinyang",
             "kq_codebook_grad_step", "kq_codebook_grad_step_stack", "kq_quantize_scalars_workspace_bytes",
-            "kq_quantize_scalars", "kq_search_workspace_bytes", "kq_search_codebook_size"]
+            "kq_quantize_scalars", "kq_search_workspace_bytes", "kq_search_codebook_size",
+            "kq_compress_workspace_bytes", "kq_compress_stack", "kq_index_bits", "kq_accounting",
+            "kq_forgy_select"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -205,7 +220,7 @@ def kq_assign(X, C, idx=None, best_d=None, distortion=None, workspace=None):
     _dev(idx, torch.int32, "idx", (n,))
     _dev(best_d, torch.float32, "best_d", (n,))
     _dev(distortion, torch.float64, "distortion")
-    nb = lib.kq_workspace_bytes(KQ_OP_ASSIGN, n, k)
+    nb = lib.kq_workspace_bytes(KQ_OP_ASSIGN, n, k, KQ_DIM)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_assign(X.data_ptr(), n, KQ_DIM, C.data_ptr(), k, idx.data_ptr(), best_d.data_ptr(),
                          distortion.data_ptr(), 0, ws.data_ptr(), ws.numel(), _stream(dev)), "kq_assign")
@@ -213,7 +228,7 @@ def kq_assign(X, C, idx=None, best_d=None, distortion=None, workspace=None):
 
 
 def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace=None, counts_only: bool = False,
-              with_distortion: bool = True):
+              with_distortion: bool = True, validate: bool = False):
     """Mean of every kernel set (empty sets keep their entry) and the distortion of the
     assignment against C_old.  Returns (C_new, counts, distortion float64 [1]), the
     distortion None when `with_distortion` is False (the library is then passed NULL)."""
@@ -231,11 +246,12 @@ def kq_update(X, idx, C_old, C_new=None, counts=None, distortion=None, workspace
         _dev(distortion, torch.float64, "distortion")
     else:
         distortion = None
-    nb = lib.kq_workspace_bytes(KQ_OP_UPDATE, n, k)
+    nb = lib.kq_workspace_bytes(KQ_OP_UPDATE, n, k, KQ_DIM)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_update(X.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), C_new.data_ptr(),
                          counts.data_ptr(), distortion.data_ptr() if distortion is not None else None,
-                         KQ_F_COUNTS_ONLY if counts_only else 0, ws.data_ptr(), ws.numel(), _stream(dev)),
+                         (KQ_F_COUNTS_ONLY if counts_only else 0) | (KQ_F_VALIDATE if validate else 0), ws.data_ptr(),
+                         ws.numel(), _stream(dev)),
            "kq_update")
     return C_new, counts, distortion
 
@@ -325,7 +341,7 @@ def kq_codebook_grad_step(G, idx, C_old, gamma: float, C_new=None, counts=None, 
     counts = counts if counts is not None else torch.empty(k, dtype=torch.int32, device=dev)
     _dev(C_new, torch.float32, "C_new", (k, KQ_DIM))
     _dev(counts, torch.int32, "counts", (k,))
-    nb = lib.kq_workspace_bytes(KQ_OP_GRAD, n, k)
+    nb = lib.kq_workspace_bytes(KQ_OP_GRAD, n, k, KQ_DIM)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_codebook_grad_step(G.data_ptr(), n, KQ_DIM, idx.data_ptr(), k, C_old.data_ptr(), float(gamma),
                                      C_new.data_ptr(), counts.data_ptr(), ws.data_ptr(), ws.numel(),
@@ -401,7 +417,8 @@ def kq_search_codebook_size(X, C_cand, r: float, max_iter: int, lloyd_iters: int
     return k_out.value, C[:k_out.value], idx, trials, d0.value
 
 
-def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None):
+def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortion=None, workspace=None,
+                 validate: bool = False):
     """`iters` Lloyd rounds then a final assignment.  Returns (C, idx, counts, distortion[iters+1])."""
     X = _kernels(X)
     C_init = _kernels(C_init, "C_init")
@@ -415,11 +432,11 @@ def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortio
     _dev(idx, torch.int32, "idx", (n,))
     _dev(counts, torch.int32, "counts", (k,))
     _dev(distortion, torch.float64, "distortion", (iters + 1,))
-    nb = lib.kq_workspace_bytes(KQ_OP_FIT, n, k)
+    nb = lib.kq_workspace_bytes(KQ_OP_FIT, n, k, KQ_DIM)
     ws = workspace if workspace is not None else _ws(dev, nb)
     _check(lib.kq_fit_layer(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, C.data_ptr(), idx.data_ptr(),
-                            counts.data_ptr(), distortion.data_ptr(), 0, ws.data_ptr(), ws.numel(),
-                            _stream(dev)), "kq_fit_layer")
+                            counts.data_ptr(), distortion.data_ptr(), KQ_F_VALIDATE if validate else 0,
+                            ws.data_ptr(), ws.numel(), _stream(dev)), "kq_fit_layer")
     return C, idx, counts, distortion
 
 
@@ -453,11 +470,21 @@ class Stack:
             c.copy_(src)
 
 
-def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True, fused_sums: bool = False):
+def _check_slot(stack, dist_slot: int):
+    if not 0 <= dist_slot < stack.distortion[0].numel():
+        raise ValueError(f"dist_slot {dist_slot} outside the stack's distortion history "
+                         f"(length {stack.distortion[0].numel()})")
+
+
+def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True, fused_sums: bool = False,
+                    validate: bool = False, reuse_shifts: bool = False):
     """Assign every layer of the stack; the distortion (if asked) goes to slot dist_slot.
     fused_sums also accumulates the member sums of the new assignment (every k <= 256),
-    for a following kq_update_stack(..., sums_from_assign=True)."""
-    flags = KQ_F_FUSED_SUMS if fused_sums else 0
+    for a following kq_update_stack(..., sums_from_assign=True); reuse_shifts takes the
+    layers' fixed-point shifts from the preceding call on the stack instead of a new pass."""
+    _check_slot(stack, dist_slot)
+    flags = (KQ_F_FUSED_SUMS if fused_sums else 0) | (KQ_F_VALIDATE if validate else 0)
+    flags |= KQ_F_REUSE_SHIFTS if reuse_shifts else 0
     if not distortion:
         saved = [(l.distortion) for l in stack.layers]
         for l in stack.layers:
@@ -475,23 +502,25 @@ def kq_assign_stack(stack: Stack, dist_slot: int = 0, distortion: bool = True, f
 
 
 def kq_update_stack(stack: Stack, dist_slot: int = 0, counts_only: bool = False, distortion_from_assign=False,
-                    sums_from_assign: bool = False):
+                    sums_from_assign: bool = False, validate: bool = False, reuse_shifts: bool = False):
     """Update every codebook of the stack.  The distortion of the assignment goes to slot
     dist_slot; with distortion_from_assign it is the value the preceding kq_assign_stack
     left in the workspace (no second pass over the old codebook).  With sums_from_assign
     the update is finished from the member sums of the preceding fused assignment (the
     kernels are not read again; the distortion then also comes from the assignment)."""
     flags = (KQ_F_COUNTS_ONLY if counts_only else 0) | (KQ_F_DISTORTION_FROM_ASSIGN if distortion_from_assign else 0)
-    flags |= KQ_F_SUMS_FROM_ASSIGN if sums_from_assign else 0
+    flags |= (KQ_F_SUMS_FROM_ASSIGN if sums_from_assign else 0) | (KQ_F_VALIDATE if validate else 0)
+    flags |= KQ_F_REUSE_SHIFTS if reuse_shifts else 0
+    _check_slot(stack, dist_slot)
     _check(lib.kq_update_stack(ctypes.cast(stack.layers, _P), stack.n_layers, dist_slot, flags,
                                stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)), "kq_update_stack")
 
 
-def kq_fit_stack(stack: Stack, iters: int):
+def kq_fit_stack(stack: Stack, iters: int, validate: bool = False):
     if stack.distortion[0].numel() < iters + 1:
         raise ValueError("the stack's distortion history is shorter than iters + 1")
-    _check(lib.kq_fit_stack(ctypes.cast(stack.layers, _P), stack.n_layers, iters, 0, stack.ws.data_ptr(),
-                            stack.ws.numel(), _stream(stack.device)), "kq_fit_stack")
+    _check(lib.kq_fit_stack(ctypes.cast(stack.layers, _P), stack.n_layers, iters, KQ_F_VALIDATE if validate else 0,
+                            stack.ws.data_ptr(), stack.ws.numel(), _stream(stack.device)), "kq_fit_stack")
 
 
 # ---- Sec. 3.2 --------------------------------------------------------------------------
@@ -545,7 +574,35 @@ def kq_quantize_codebook_stack(Cs, weights, bits: int = 6, mode: int = KQ_CBQ_WK
 # ---- Eq. (4) and test-time reconstruction -------------------------------------------------
 
 def index_bits(k: int) -> int:
-    return 0 if k <= 1 else int(math.ceil(math.log2(k)))
+    """ceil(log2 k), the Eq. (4) index width (kq_index_bits)."""
+    b = lib.kq_index_bits(int(k))
+    if b < 0:
+        raise ValueError("k must be >= 1")
+    return b
+
+
+def kq_accounting(n: int, k: int, bc: int, dim: int = KQ_DIM):
+    """Eq. (4), (6), (7) for a layer of n kernels and a k-entry codebook stored at bc bits
+    per value: (storage bits B, compression ratio C_KQ, bits per parameter beta)."""
+    B, r, beta = ctypes.c_int64(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(lib.kq_accounting(int(n), int(k), int(dim), int(bc), ctypes.byref(B), ctypes.byref(r),
+                             ctypes.byref(beta)), "kq_accounting")
+    return B.value, r.value, beta.value
+
+
+def kq_forgy_select(X, k: int, seed: int):
+    """k distinct kernels of X (host: a numpy array or CPU tensor [n, 9] float32) in the
+    seeded splitmix64 partial Fisher-Yates order.  Returns their row indices (int64 numpy)."""
+    import numpy as np
+    if isinstance(X, torch.Tensor):
+        if X.is_cuda:
+            raise TypeError("kq_forgy_select takes host kernels")
+        X = X.numpy()
+    X = np.ascontiguousarray(X, dtype=np.float32).reshape(-1, KQ_DIM)
+    sel = np.empty(max(int(k), 1), np.int64)
+    _check(lib.kq_forgy_select(X.ctypes.data_as(_P), X.shape[0], KQ_DIM, int(k), int(seed) & ((1 << 64) - 1),
+                               sel.ctypes.data_as(_P)), "kq_forgy_select")
+    return sel[:k]
 
 
 def kq_pack_bits(values, bits: int, out=None):
@@ -595,7 +652,7 @@ def kq_sq_error(A, B, out=None, workspace=None):
     _dev(A, torch.float32, "A")
     _dev(B, torch.float32, "B", tuple(A.shape))
     out = out if out is not None else torch.empty(1, dtype=torch.float64, device=A.device)
-    nb = lib.kq_workspace_bytes(KQ_OP_SQ_ERROR, A.numel(), 1)
+    nb = lib.kq_workspace_bytes(KQ_OP_SQ_ERROR, A.numel(), 1, 1)
     ws = workspace if workspace is not None else _ws(A.device, nb)
     _check(lib.kq_sq_error(A.data_ptr(), B.data_ptr(), A.numel(), out.data_ptr(), ws.data_ptr(), ws.numel(),
                            _stream(A.device)), "kq_sq_error")
@@ -679,3 +736,81 @@ def kq_reconstruct_stack(layers, workspace=None):
     _check(lib.kq_reconstruct_stack(ctypes.cast(arr, _P), len(layers), _ptr(ws), 0 if ws is None else ws.numel(),
                                     _stream(dev)), "kq_reconstruct_stack")
     return outs
+
+
+# ---- the whole compression pass in one call ------------------------------------------------
+
+class Compression:
+    """Device buffers of kq_compress_stack for the layers of a network: per layer X, C_init,
+    the fitted C, idx, counts, the distortion history, the quantized codebook (codes, levels,
+    C_hat), the packed index and code streams, W_hat and its squared error; plus the layer
+    descriptor array and the workspace.  ``run()`` makes the one library call."""
+
+    def __init__(self, Xs, C_inits, iters: int, bits: int = 6, mode: int = KQ_CBQ_WKMEANS, cbq_iters: int = 30,
+                 pack: bool = True, reconstruct: bool = True, sq_error: bool = True):
+        self.X = [_kernels(x) for x in Xs]
+        self.C_init = [_kernels(c, "C_init") for c in C_inits]
+        dev = self.X[0].device
+        self.device, self.iters, self.bits, self.mode, self.cbq_iters = dev, int(iters), int(bits), int(mode), int(cbq_iters)
+        ks = [c.shape[0] for c in self.C_init]
+        ns = [x.shape[0] for x in self.X]
+        self.C = [torch.empty(k, KQ_DIM, device=dev) for k in ks]
+        self.idx = [torch.empty(n, dtype=torch.int32, device=dev) for n in ns]
+        self.counts = [torch.empty(k, dtype=torch.int32, device=dev) for k in ks]
+        self.distortion = [torch.zeros(self.iters + 1, dtype=torch.float64, device=dev) for _ in ns]
+        self.codes = [torch.empty(k * KQ_DIM, dtype=torch.uint8, device=dev) for k in ks]
+        self.levels = [torch.empty(1 << self.bits, device=dev) for _ in ks]
+        self.C_hat = [torch.empty(k, KQ_DIM, device=dev) for k in ks]
+        self.index_bits = [index_bits(k) for k in ks]
+        # stream buffers rounded up to whole dwords (the packers store 32-bit words)
+        self.packed_idx = [torch.zeros(((n * b + 7) // 8 + 3) // 4 * 4 + 4, dtype=torch.uint8, device=dev)
+                           for n, b in zip(ns, self.index_bits)] if pack else None
+        self.packed_codes = [torch.zeros(((k * KQ_DIM * self.bits + 7) // 8 + 3) // 4 * 4 + 4, dtype=torch.uint8,
+                                         device=dev) for k in ks] if pack else None
+        self.W_hat = [torch.empty(n, KQ_DIM, device=dev) for n in ns] if reconstruct else None
+        self.sq_error = torch.zeros(len(ns), dtype=torch.float64, device=dev) if (reconstruct and sq_error) else None
+        arr = (KqCompressLayer * len(ns))()
+        for i in range(len(ns)):
+            if self.C_init[i].shape != (ks[i], KQ_DIM):
+                raise ValueError("C_init must be [k, 9]")
+            arr[i] = KqCompressLayer(
+                self.X[i].data_ptr(), ns[i], ks[i], self.C_init[i].data_ptr(), self.C[i].data_ptr(),
+                self.idx[i].data_ptr(), self.counts[i].data_ptr(), self.distortion[i].data_ptr(),
+                self.codes[i].data_ptr(), self.levels[i].data_ptr(), self.C_hat[i].data_ptr(),
+                self.packed_idx[i].data_ptr() if pack else None, self.packed_codes[i].data_ptr() if pack else None,
+                self.W_hat[i].data_ptr() if reconstruct else None,
+                self.sq_error[i:i + 1].data_ptr() if self.sq_error is not None else None)
+        self.layers = arr
+        self.n_layers = len(ns)
+        nb = lib.kq_compress_workspace_bytes(ctypes.cast(arr, _P), self.n_layers, self.bits)
+        if nb == 0:
+            raise ValueError("invalid compression layers")
+        self.ws = torch.zeros(nb, dtype=torch.uint8, device=dev)
+
+    def packed_index_stream(self, i: int):
+        return self.packed_idx[i][:(self.X[i].shape[0] * self.index_bits[i] + 7) // 8]
+
+    def packed_code_stream(self, i: int):
+        return self.packed_codes[i][:(self.C[i].shape[0] * KQ_DIM * self.bits + 7) // 8]
+
+    def run(self, validate: bool = False, round_events=None):
+        kq_compress_stack(self, validate, round_events)
+
+
+def kq_compress_stack(comp: Compression, validate: bool = False, round_events=None):
+    """The compression pass of every layer of ``comp`` in one library call: Lloyd fit,
+    codebook quantization, index/code packing, reconstruction and its error.
+    round_events: None, or {round t: (start, end) torch.cuda.Event with timing} -- the
+    library records them around the assignment launch of those Lloyd rounds."""
+    ev = None
+    if round_events:
+        ev = (_P * (2 * (comp.iters + 1)))()
+        for t, (a, b) in round_events.items():
+            if not 0 <= t <= comp.iters:
+                raise ValueError(f"round {t} outside 0..{comp.iters}")
+            if not a.cuda_event or not b.cuda_event:
+                raise ValueError("record each event once through torch first (torch creates them lazily)")
+            ev[2 * t], ev[2 * t + 1] = a.cuda_event, b.cuda_event
+    _check(lib.kq_compress_stack(ctypes.cast(comp.layers, _P), comp.n_layers, comp.iters, comp.mode, comp.bits,
+                                 comp.cbq_iters, KQ_F_VALIDATE if validate else 0, ev, comp.ws.data_ptr(),
+                                 comp.ws.numel(), _stream(comp.device)), "kq_compress_stack")

@@ -6,13 +6,17 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
 #include "kq_internal.h"
 
 using namespace kq;
 
 namespace {
 
-constexpr int32_t kAbiVersion = 9;
+constexpr int32_t kAbiVersion = 10;
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 bool valid_n(int64_t n) { return n >= 1 && n < (int64_t(1) << 31); }
@@ -34,9 +38,11 @@ kq_status check_ws(void* ws, size_t ws_bytes, size_t need) {
 enum class Op { Assign, Update };
 
 // Launch parameters for layers [l0, l1) of a stack.  `base` points at the workspace
-// of layer 0 (the regions of the layers follow each other in order).
+// of layer 0 (the regions of the layers follow each other in order).  C_alt (nullable):
+// for an assignment the codebook of each layer to assign against instead of its C; for an
+// update the previous codebook (entries kept when empty, the distortion's codebook).
 void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* base, Op op,
-                  int32_t dist_slot, const float* const* C_old, uint32_t kflags, bool from_assign = false) {
+                  int32_t dist_slot, const float* const* C_alt, uint32_t kflags, bool from_assign = false) {
     memset(&p, 0, sizeof(p));
     size_t off = 0;
     for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
@@ -50,13 +56,19 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
         unsigned char* w = base + off;
         d.X = s.X;
         d.C = s.C;
-        d.C_old = C_old ? C_old[l] : s.C;
+        d.C_old = s.C;
+        if (C_alt && C_alt[l]) {
+            if (op == Op::Assign) d.C = const_cast<float*>(C_alt[l]);
+            else d.C_old = C_alt[l];
+        }
         d.idx = s.idx;
         d.n = (int)s.n;
         d.k = s.k;
-        d.shift = fixed_shift(s.n);
+        d.shift = base_shift(s.n);
         d.dist = s.distortion ? s.distortion + dist_slot : nullptr;
         d.hist = (long long*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k));
+        d.xmax = base ? (unsigned*)(w + ws_xmax_offset(s.n, s.k)) : nullptr;
+        d.nxmax = absmax_blocks(s.n);
         if (op == Op::Assign) {
             d.best_d = s.best_d;
             d.part = base ? (double*)w : nullptr;  // partials whenever there is a workspace
@@ -75,8 +87,6 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
             d.nchunks = (int)((s.n + d.chunk - 1) / d.chunk);
             d.nunits = d.ranges * d.nchunks;
             d.flags = (int)kflags;
-            d.gmax = (unsigned*)(w + ws_assign_part(s.n) + ws_update_part(s.n, s.k) + ws_hist(s.n, s.k));
-            d.ngmax = grad_max_blocks(s.n);
         }
         d.unit_begin = unit;
         unit += d.nunits;
@@ -85,6 +95,25 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
     p.nlayers = l1 - l0;
     p.total_units = unit;
     set_unit_table(p);
+}
+
+// The largest magnitudes of layers [l0, l1) (their X: kernels, or gradients) and from them
+// the fixed-point shift of each layer's sums, in the workspace.  With `validate` the call
+// waits for them and returns KQ_ERR_RANGE when any value is NaN or infinite.
+kq_status run_xmax(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, hipStream_t s, bool validate) {
+    StackParams p;
+    stack_params(p, layers, l0, l1, ws, Op::Update, 0, nullptr, 0);
+    unsigned* flags = p.L[0].xmax + p.L[0].nxmax + 1;  // the first layer's region holds the call's flags
+    p.range_flags = validate ? flags : nullptr;
+    if (launch_absmax(p, s) != hipSuccess) return KQ_ERR_HIP;
+    if (!validate) return KQ_OK;
+    unsigned h[KQ_MAX_STACK] = {0};
+    if (hipMemcpyAsync(h, flags, sizeof(unsigned) * (size_t)p.nlayers, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return KQ_ERR_HIP;
+    for (int l = 0; l < p.nlayers; ++l)
+        if (h[l] != 0u) return KQ_ERR_RANGE;
+    return KQ_OK;
 }
 
 kq_status check_layers(const kq_layer* layers, int32_t n_layers, bool fit) {
@@ -137,11 +166,12 @@ void fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, in
 }
 
 // assignment of layers [l0, l1) (+ the distortion finish when any layer asks for it);
-// `fused` also leaves the member sums of the new assignment in the workspace
+// `fused` also leaves the member sums of the new assignment in the workspace (the layers'
+// shifts must be in place: run_xmax)
 kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s,
-                     bool fused = false) {
+                     bool fused = false, const float* const* C_alt = nullptr) {
     StackParams p;
-    stack_params(p, layers, l0, l1, ws, Op::Assign, slot, nullptr, 0);
+    stack_params(p, layers, l0, l1, ws, Op::Assign, slot, C_alt, 0);
     if (fused) {
         int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
         fused_slots(layers, l0, l1, wf, ns);
@@ -153,7 +183,8 @@ kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
 }
 
 // `sums_from_assign`: the preceding fused assignment of the same layers left the member
-// sums (and the distortion partials): only the finishing launch runs
+// sums (and the distortion partials): only the finishing launch runs.  Otherwise the
+// layers' shifts must be in place (run_xmax) unless only counts are asked for.
 kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot,
                      const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false,
                      bool sums_from_assign = false) {
@@ -170,8 +201,8 @@ kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
     return KQ_OK;
 }
 
-// Eq. (2) on layers [l0, l1): per-block maxima of |g|, the segmented sums of the gradients
-// (layers[l].X holds them), then c - gamma * mean into layers[l].C
+// Eq. (2) on layers [l0, l1): the largest |g| and the shift of each layer, the segmented
+// sums of the gradients (layers[l].X holds them), then c - gamma * mean into layers[l].C
 kq_status run_grad(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, const float* const* C_old,
                    float gamma, hipStream_t s) {
     kq_layer quiet[KQ_MAX_STACK];
@@ -181,10 +212,11 @@ kq_status run_grad(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char
     }
     size_t off = 0;
     for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
+    kq_status st = run_xmax(quiet, 0, l1 - l0, ws + off, s, false);
+    if (st != KQ_OK) return st;
     StackParams p;
     stack_params(p, quiet, 0, l1 - l0, ws + off, Op::Update, 0, C_old ? C_old + l0 : nullptr, kFlagGrad);
     for (int l = 0; l < p.nlayers; ++l) p.L[l].gamma = gamma;
-    if (launch_grad_absmax(p, s) != hipSuccess) return KQ_ERR_HIP;
     if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
     if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;
@@ -192,10 +224,19 @@ kq_status run_grad(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char
 
 bool finite_gamma(float g) { return g == g && g < 3.4e38f && g > -3.4e38f; }
 
-// Lloyd rounds: assign (leaving distortion partials in the workspace), then update,
-// whose finishing kernel adds those partials; the final assignment is followed by a
-// counts-only update that does the same.
-kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsigned char* ws, hipStream_t s) {
+// Lloyd rounds on a stack: the shifts of the layers' sums once (one pass over the kernels),
+// then per round the assignment (leaving distortion partials, and with every k <= 256 the
+// member sums, in the workspace) and the update, whose finishing kernel adds those partials;
+// the final assignment is followed by a counts-only update that does the same.  C_init
+// (nullable, per layer nullable): round 0 assigns against C_init[l] and keeps its entries
+// when empty, so layers[l].C need not hold the start.
+kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsigned char* ws, hipStream_t s,
+                  const float* const* C_init = nullptr, bool validate = false, void* const* round_events = nullptr) {
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {  // every layer's shift (and range check) first
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        const kq_status st = run_xmax(layers, l0, l1, ws, s, validate);
+        if (st != KQ_OK) return st;
+    }
     kq_layer quiet[KQ_MAX_STACK];
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
@@ -205,21 +246,35 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
         }
         size_t off = 0;
         for (int32_t l = 0; l < l0; ++l) off += layer_ws_bytes(layers[l].n, layers[l].k);
+        unsigned char* w = ws + off;
+        const float* const* init = C_init ? C_init + l0 : nullptr;
         bool need_last = false;
         for (int32_t l = l0; l < l1; ++l) need_last |= layers[l].counts != nullptr || layers[l].distortion != nullptr;
+        if (iters == 0 && init) {  // no update will write C: it takes the start as it is
+            for (int32_t l = l0; l < l1; ++l) {
+                if (!C_init[l] || C_init[l] == layers[l].C) continue;
+                if (hipMemcpyAsync(layers[l].C, C_init[l], sizeof(float) * KQ_DIM * (size_t)layers[l].k,
+                                   hipMemcpyDeviceToDevice, s) != hipSuccess)
+                    return KQ_ERR_HIP;
+            }
+            init = nullptr;
+        }
         const bool fused = fusable(layers, l0, l1);  // the member sums come with the assignment
         for (int32_t t = 0; t <= iters; ++t) {
             const bool last = (t == iters);
-            kq_status st = run_assign(quiet, 0, l1 - l0, ws + off, 0, s, fused && !(last && !need_last));
+            const float* const* from = t == 0 ? init : nullptr;
+            void* const* ev = (round_events && l0 == 0) ? round_events + 2 * t : nullptr;
+            if (ev && ev[0] && hipEventRecord((hipEvent_t)ev[0], s) != hipSuccess) return KQ_ERR_HIP;
+            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from);
             if (st != KQ_OK) return st;
+            if (ev && ev[1] && hipEventRecord((hipEvent_t)ev[1], s) != hipSuccess) return KQ_ERR_HIP;
             if (last && !need_last) break;
-            st = run_update(layers, l0, l1, ws, t, nullptr, last ? kFlagCountsOnly : 0, s, true, fused);
+            st = run_update(layers + l0, 0, l1 - l0, w, t, from, last ? kFlagCountsOnly : 0, s, true, fused);
             if (st != KQ_OK) return st;
         }
     }
     return KQ_OK;
 }
-
 
 // ---- Yinyang workspace: the layer's own region (assignment partials, update partials and
 // histograms), then the grouping fit's region, then the Yinyang state ----------------------
@@ -358,12 +413,12 @@ const char* kq_status_string(kq_status st) {
 
 int32_t kq_abi_version(void) { return kAbiVersion; }
 
-size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k) {
+size_t kq_workspace_bytes(int32_t op, int64_t n, int32_t k, int32_t dim) {
     if (op == KQ_OP_SQ_ERROR) {
-        if (n < 1 || n >= (int64_t(1) << 40)) return 0;
+        if (n < 1 || n >= (int64_t(1) << 40) || k != 1 || dim != 1) return 0;
         return align256(sizeof(double) * (size_t)sq_error_blocks(n));
     }
-    if (!valid_n(n) || !valid_k(k)) return 0;
+    if (!valid_n(n) || !valid_k(k) || dim != KQ_DIM) return 0;
     if (op != KQ_OP_ASSIGN && op != KQ_OP_UPDATE && op != KQ_OP_FIT && op != KQ_OP_GRAD) return 0;
     return layer_ws_bytes(n, k);
 }
@@ -400,7 +455,7 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
                     void* stream) {
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
-    if (!valid_n(n) || !valid_k(k) || (flags & ~KQ_F_COUNTS_ONLY) != 0) return KQ_ERR_ARG;
+    if (!valid_n(n) || !valid_k(k) || (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_VALIDATE)) != 0) return KQ_ERR_ARG;
     if (!X || !idx || !C_old || !C_new || !aligned(X, 4) || !aligned(idx, 4) || !aligned(C_old, 4) ||
         !aligned(C_new, 4))
         return KQ_ERR_ARG;
@@ -409,8 +464,13 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
     if (w != KQ_OK) return w;
     const kq_layer l = {X, n, k, C_new, const_cast<int32_t*>(idx), nullptr, counts, distortion};
     const float* olds[1] = {C_old};
-    return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0,
-                      (hipStream_t)stream);
+    const bool counts_only = (flags & KQ_F_COUNTS_ONLY) != 0, validate = (flags & KQ_F_VALIDATE) != 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (!counts_only || validate) {  // the shift of the layer's sums (and the range check)
+        const kq_status st = run_xmax(&l, 0, 1, (unsigned char*)ws, s, validate);
+        if (st != KQ_OK) return st;
+    }
+    return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, counts_only ? kFlagCountsOnly : 0, s);
 }
 
 kq_status kq_codebook_grad_step(const float* G, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
@@ -506,7 +566,7 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
 size_t fit_ws_upto(int64_t n, int32_t kmax) {
     const size_t c1024 = (size_t)((n + 1023) / 1024);
     return ws_assign_part(n) + align256(sizeof(double) * (size_t)update_ranges(kmax) * c1024) +
-           align256(sizeof(int64_t) * 10 * (size_t)kmax * (size_t)assign_tiles(n)) + ws_grad(n);
+           align256(sizeof(int64_t) * 10 * (size_t)kmax * (size_t)assign_tiles(n)) + ws_xmax(n);
 }
 
 size_t kq_search_workspace_bytes(int64_t n, int32_t n_init, int32_t lloyd_iters) {
@@ -584,19 +644,15 @@ kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const 
                        void* stream) {
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
-    if (!valid_n(n) || !valid_k(k) || k > n || iters < 0 || flags != 0) return KQ_ERR_ARG;
+    if (!valid_n(n) || !valid_k(k) || k > n || iters < 0 || (flags & ~KQ_F_VALIDATE) != 0) return KQ_ERR_ARG;
     if (!C_init || !aligned(C_init, 4)) return KQ_ERR_ARG;
     const kq_layer l = {X, n, k, C, idx, nullptr, counts, distortion};
     kq_status st = check_layers(&l, 1, true);
     if (st != KQ_OK) return st;
     st = check_ws(ws, ws_bytes, layer_ws_bytes(n, k));
     if (st != KQ_OK) return st;
-    hipStream_t s = (hipStream_t)stream;
-    if (C_init != C) {
-        if (hipMemcpyAsync(C, C_init, sizeof(float) * (size_t)k * KQ_DIM, hipMemcpyDeviceToDevice, s) != hipSuccess)
-            return KQ_ERR_HIP;
-    }
-    return run_fit(&l, 1, iters, (unsigned char*)ws, s);
+    const float* init[1] = {C_init};
+    return run_fit(&l, 1, iters, (unsigned char*)ws, (hipStream_t)stream, init, (flags & KQ_F_VALIDATE) != 0);
 }
 
 size_t kq_yinyang_workspace_bytes(int64_t n, int32_t k, int32_t groups) {
@@ -654,6 +710,7 @@ kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k
     const kq_layer l0 = {X, n, k, C, idx, nullptr, nullptr, nullptr};
     if ((st = run_assign(&l0, 0, 1, w, 0, s)) != KQ_OK) return st;
     if ((st = yy_start(w, L, X, n, C, k, t, s)) != KQ_OK) return st;
+    if (iters > 0 && (st = run_xmax(&l0, 0, 1, w, s, false)) != KQ_OK) return st;  // the shift of the sums
     // rounds 1..iters: update from `cur` into `nxt` (the distortion of the assignment
     // before it from its partials), then the Yinyang assignment against `nxt`
     float* cur = C;
@@ -681,14 +738,21 @@ kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
                           size_t ws_bytes, void* stream) {
     kq_status st = check_layers(layers, n_layers, false);
     if (st != KQ_OK) return st;
-    if (dist_slot < 0 || (flags & ~KQ_F_FUSED_SUMS) != 0) return KQ_ERR_ARG;
-    const bool fused = (flags & KQ_F_FUSED_SUMS) != 0;
+    if (dist_slot < 0 || (flags & ~(KQ_F_FUSED_SUMS | KQ_F_VALIDATE | KQ_F_REUSE_SHIFTS)) != 0) return KQ_ERR_ARG;
+    const bool fused = (flags & KQ_F_FUSED_SUMS) != 0, validate = (flags & KQ_F_VALIDATE) != 0;
+    const bool reuse = (flags & KQ_F_REUSE_SHIFTS) != 0;
     if (fused && !fusable(layers, 0, n_layers)) return KQ_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {  // range checks before anything is written
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        if ((validate || (fused && !reuse)) && (st = run_xmax(layers, l0, l1, (unsigned char*)ws, s, validate)) != KQ_OK)
+            return st;
+    }
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, (hipStream_t)stream, fused);
+        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, s, fused);
         if (st != KQ_OK) return st;
     }
     return KQ_OK;
@@ -699,16 +763,25 @@ kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
     kq_status st = check_layers(layers, n_layers, false);
     if (st != KQ_OK) return st;
     if (dist_slot < 0 ||
-        (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_DISTORTION_FROM_ASSIGN | KQ_F_SUMS_FROM_ASSIGN)) != 0)
+        (flags & ~(KQ_F_COUNTS_ONLY | KQ_F_DISTORTION_FROM_ASSIGN | KQ_F_SUMS_FROM_ASSIGN | KQ_F_VALIDATE |
+                   KQ_F_REUSE_SHIFTS)) != 0)
         return KQ_ERR_ARG;
-    const bool from_sums = (flags & KQ_F_SUMS_FROM_ASSIGN) != 0;
+    const bool from_sums = (flags & KQ_F_SUMS_FROM_ASSIGN) != 0, validate = (flags & KQ_F_VALIDATE) != 0;
+    const bool counts_only = (flags & KQ_F_COUNTS_ONLY) != 0, reuse = (flags & KQ_F_REUSE_SHIFTS) != 0;
     if (from_sums && !fusable(layers, 0, n_layers)) return KQ_ERR_UNSUPPORTED;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    // the shifts of the sums (the fused assignment left its own), and the range checks, first
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        st = run_update(layers, l0, l1, (unsigned char*)ws, dist_slot, nullptr,
-                        (flags & KQ_F_COUNTS_ONLY) ? kFlagCountsOnly : 0, (hipStream_t)stream,
+        if ((validate || (!from_sums && !counts_only && !reuse)) &&
+            (st = run_xmax(layers, l0, l1, (unsigned char*)ws, s, validate)) != KQ_OK)
+            return st;
+    }
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        st = run_update(layers, l0, l1, (unsigned char*)ws, dist_slot, nullptr, counts_only ? kFlagCountsOnly : 0, s,
                         (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0, from_sums);
         if (st != KQ_OK) return st;
     }
@@ -719,10 +792,11 @@ kq_status kq_fit_stack(const kq_layer* layers, int32_t n_layers, int32_t iters, 
                        size_t ws_bytes, void* stream) {
     kq_status st = check_layers(layers, n_layers, true);
     if (st != KQ_OK) return st;
-    if (iters < 0 || flags != 0) return KQ_ERR_ARG;
+    if (iters < 0 || (flags & ~KQ_F_VALIDATE) != 0) return KQ_ERR_ARG;
     st = check_ws(ws, ws_bytes, stack_ws_bytes(layers, n_layers));
     if (st != KQ_OK) return st;
-    return run_fit(layers, n_layers, iters, (unsigned char*)ws, (hipStream_t)stream);
+    return run_fit(layers, n_layers, iters, (unsigned char*)ws, (hipStream_t)stream, nullptr,
+                   (flags & KQ_F_VALIDATE) != 0);
 }
 
 static kq_status check_cbq(const kq_cbq_layer& l, int32_t bits, int32_t mode, int32_t iters) {
@@ -846,7 +920,7 @@ kq_status kq_reconstruct(const int32_t* idx, int64_t n, const float* C, int32_t 
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k)) return KQ_ERR_ARG;
-    if (!idx || !C || !W_hat || !aligned(idx, 4) || !aligned(C, 4) || !aligned(W_hat, 16)) return KQ_ERR_ARG;
+    if (!idx || !C || !W_hat || !aligned(idx, 4) || !aligned(C, 4) || !aligned(W_hat, 4)) return KQ_ERR_ARG;
     const kq_recon_layer l = {idx, nullptr, 0, k, n, C, W_hat, nullptr, nullptr};
     return kq_reconstruct_stack(&l, 1, nullptr, 0, stream);
 }
@@ -856,7 +930,7 @@ kq_status kq_reconstruct_packed(const uint8_t* packed, int32_t bits, int64_t n, 
     if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
     if (k > KQ_MAX_K || bits < 0 || bits > 16) return KQ_ERR_UNSUPPORTED;
     if (!valid_n(n) || !valid_k(k)) return KQ_ERR_ARG;
-    if ((bits > 0 && (!packed || !aligned(packed, 4))) || !C || !W_hat || !aligned(C, 4) || !aligned(W_hat, 16))
+    if ((bits > 0 && (!packed || !aligned(packed, 4))) || !C || !W_hat || !aligned(C, 4) || !aligned(W_hat, 4))
         return KQ_ERR_ARG;
     const kq_recon_layer l = {nullptr, packed, bits, k, n, C, W_hat, nullptr, nullptr};
     return kq_reconstruct_stack(&l, 1, nullptr, 0, stream);
@@ -866,7 +940,7 @@ kq_status kq_sq_error(const float* A, const float* B, int64_t count, double* out
                       void* stream) {
     if (count < 1 || count >= (int64_t(1) << 40)) return KQ_ERR_ARG;
     if (!A || !B || !out || !aligned(A, 4) || !aligned(B, 4) || !aligned(out, 8)) return KQ_ERR_ARG;
-    const kq_status w = check_ws(ws, ws_bytes, kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1));
+    const kq_status w = check_ws(ws, ws_bytes, kq_workspace_bytes(KQ_OP_SQ_ERROR, count, 1, 1));
     if (w != KQ_OK) return w;
     return hip_status(launch_sq_error(A, B, count, out, ws, (hipStream_t)stream));
 }
@@ -969,6 +1043,208 @@ kq_status kq_reconstruct_stack(const kq_recon_layer* layers, int32_t n_layers, v
     for (int32_t l = n_layers; l < KQ_MAX_STACK; ++l) p.unit_begin[l] = 0x7fffffff;
     p.total_blocks = blk;
     return hip_status(launch_reconstruct_stack(p, (hipStream_t)stream));
+}
+
+// ---- the whole compression pass of a stack (Sec. 3.1 fit, Sec. 3.2 codebook quantization,
+// Eq. 4 index stream, test-time reconstruction) in one call ----------------------------------
+
+static kq_status compress_layer_views(const kq_compress_layer& c, int32_t bits, kq_layer& fit, kq_cbq_layer& cbq,
+                                      kq_pack_job (&jobs)[2], int& njobs, kq_recon_layer& rec) {
+    fit = kq_layer{c.X, c.n, c.k, c.C, c.idx, nullptr, c.counts, c.distortion};
+    cbq = kq_cbq_layer{c.C, c.k, c.counts, c.codes, c.levels, c.C_hat};
+    const int32_t b = kq_index_bits(c.k);
+    njobs = 0;
+    if (c.packed_idx) jobs[njobs++] = kq_pack_job{c.idx, 4, b, c.n, c.packed_idx};
+    if (c.packed_codes) jobs[njobs++] = kq_pack_job{c.codes, 1, bits, (int64_t)c.k * KQ_DIM, c.packed_codes};
+    rec = kq_recon_layer{c.packed_idx ? nullptr : c.idx, c.packed_idx, b, c.k, c.n, c.C_hat, c.W_hat,
+                         c.sq_error ? c.X : nullptr, c.sq_error};
+    return KQ_OK;
+}
+
+static kq_status check_compress(const kq_compress_layer* layers, int32_t n_layers, int32_t iters, int32_t mode,
+                                int32_t bits, int32_t cbq_iters, uint32_t flags) {
+    if (layers == nullptr || n_layers < 1) return KQ_ERR_ARG;
+    if (bits < 1 || bits > 8) return KQ_ERR_UNSUPPORTED;
+    if (iters < 0 || cbq_iters < 0 || (mode != KQ_CBQ_WKMEANS && mode != KQ_CBQ_UNIFORM) ||
+        (flags & ~KQ_F_VALIDATE) != 0)
+        return KQ_ERR_ARG;
+    for (int32_t l = 0; l < n_layers; ++l) {
+        const kq_compress_layer& c = layers[l];
+        if (!c.C_init || !aligned(c.C_init, 4) || !c.counts || !c.codes || !c.levels || !c.C_hat) return KQ_ERR_ARG;
+        if (c.sq_error && !c.W_hat) return KQ_ERR_ARG;
+        kq_layer fit;
+        kq_cbq_layer cbq;
+        kq_pack_job jobs[2];
+        int njobs = 0;
+        kq_recon_layer rec;
+        compress_layer_views(c, bits, fit, cbq, jobs, njobs, rec);
+        kq_status st = check_layers(&fit, 1, true);
+        if (st != KQ_OK) return st;
+        if ((st = check_cbq(cbq, bits, mode, cbq_iters)) != KQ_OK) return st;
+        for (int q = 0; q < njobs; ++q)
+            if ((st = check_pack_job(jobs[q])) != KQ_OK) return st;
+        if (c.W_hat && (st = check_recon_layer(rec)) != KQ_OK) return st;
+    }
+    return KQ_OK;
+}
+
+// workspace regions: the fit of one chunk of up to KQ_MAX_STACK layers, the wide codebook
+// quantizer, the reconstruction's error partials (chunks run one after another and share them)
+struct CompressLayout {
+    size_t fit, cbq, recon, total;
+};
+
+static CompressLayout compress_layout(const kq_compress_layer* layers, int32_t n_layers, int32_t bits) {
+    CompressLayout L = {0, 0, 0, 0};
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        kq_layer fit[KQ_MAX_STACK];
+        kq_cbq_layer cbq[KQ_MAX_STACK];
+        kq_recon_layer rec[KQ_MAX_STACK];
+        int nrec = 0;
+        for (int32_t l = l0; l < l1; ++l) {
+            kq_pack_job jobs[2];
+            int njobs = 0;
+            kq_recon_layer r;
+            compress_layer_views(layers[l], bits, fit[l - l0], cbq[l - l0], jobs, njobs, r);
+            if (layers[l].W_hat) rec[nrec++] = r;
+        }
+        const size_t f = stack_ws_bytes(fit, l1 - l0);
+        const size_t c = kq_quantize_codebook_stack_workspace_bytes(cbq, l1 - l0, bits);
+        const size_t r = nrec ? recon_ws_bytes(rec, nrec) : 0;
+        L.fit = f > L.fit ? f : L.fit;
+        L.cbq = align256(c) > L.cbq ? align256(c) : L.cbq;
+        L.recon = align256(r) > L.recon ? align256(r) : L.recon;
+    }
+    L.total = L.fit + L.cbq + L.recon;
+    return L;
+}
+
+size_t kq_compress_workspace_bytes(const kq_compress_layer* layers, int32_t n_layers, int32_t bits) {
+    if (check_compress(layers, n_layers, 0, KQ_CBQ_WKMEANS, bits, 0, 0) != KQ_OK) return 0;
+    return compress_layout(layers, n_layers, bits).total;
+}
+
+kq_status kq_compress_stack(const kq_compress_layer* layers, int32_t n_layers, int32_t iters, int32_t mode,
+                            int32_t bits, int32_t cbq_iters, uint32_t flags, void* const* round_events, void* ws,
+                            size_t ws_bytes, void* stream) {
+    kq_status st = check_compress(layers, n_layers, iters, mode, bits, cbq_iters, flags);
+    if (st != KQ_OK) return st;
+    const CompressLayout L = compress_layout(layers, n_layers, bits);
+    if ((st = check_ws(ws, ws_bytes, L.total)) != KQ_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    unsigned char* w = (unsigned char*)ws;
+    kq_layer fit[KQ_MAX_STACK];
+    const float* init[KQ_MAX_STACK];
+    kq_cbq_layer cbq[KQ_MAX_STACK];
+    kq_pack_job jobs[KQ_MAX_PACK_JOBS];
+    kq_recon_layer rec[KQ_MAX_STACK];
+    if (flags & KQ_F_VALIDATE) {  // every layer checked before any output is written
+        for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
+            const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+            for (int32_t l = l0; l < l1; ++l) {
+                kq_pack_job j2[2];
+                int nj = 0;
+                kq_recon_layer r;
+                compress_layer_views(layers[l], bits, fit[l - l0], cbq[l - l0], j2, nj, r);
+            }
+            if ((st = run_xmax(fit, 0, l1 - l0, w, s, true)) != KQ_OK) return st;
+        }
+    }
+    for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
+        const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
+        int njobs = 0, nrec = 0;
+        for (int32_t l = l0; l < l1; ++l) {
+            kq_pack_job j2[2];
+            int nj = 0;
+            kq_recon_layer r;
+            compress_layer_views(layers[l], bits, fit[l - l0], cbq[l - l0], j2, nj, r);
+            init[l - l0] = layers[l].C_init;
+            for (int q = 0; q < nj; ++q) jobs[njobs++] = j2[q];
+            if (layers[l].W_hat) rec[nrec++] = r;
+        }
+        if ((st = run_fit(fit, l1 - l0, iters, w, s, init, false, l0 == 0 ? round_events : nullptr)) != KQ_OK)
+            return st;
+        if ((st = kq_quantize_codebook_stack_ws(cbq, l1 - l0, bits, mode, cbq_iters, L.cbq ? w + L.fit : nullptr,
+                                                L.cbq, stream)) != KQ_OK)
+            return st;
+        if (njobs > 0 && (st = kq_pack_bits_stack(jobs, njobs, stream)) != KQ_OK) return st;
+        if (nrec > 0 && (st = kq_reconstruct_stack(rec, nrec, L.recon ? w + L.fit + L.cbq : nullptr, L.recon,
+                                                   stream)) != KQ_OK)
+            return st;
+    }
+    return KQ_OK;
+}
+
+// ---- host-only helpers ----------------------------------------------------------------------
+
+int32_t kq_index_bits(int32_t k) {
+    if (k < 1) return -1;
+    int32_t b = 0;
+    while ((int64_t(1) << b) < (int64_t)k) ++b;
+    return b;
+}
+
+kq_status kq_accounting(int64_t n, int32_t k, int32_t dim, int32_t bc, int64_t* storage_bits, double* ratio,
+                        double* bits_per_param) {
+    if (n < 1 || k < 1 || dim < 1 || bc < 1 || bc > 64) return KQ_ERR_ARG;
+    const int64_t B = (int64_t)k * dim * bc + n * kq_index_bits(k);  // Eq. (4)
+    const double params = (double)n * (double)dim;
+    if (storage_bits) *storage_bits = B;
+    if (ratio) *ratio = params * 32.0 / (double)B;  // Eq. (6), fp32 weights
+    if (bits_per_param) *bits_per_param = (double)B / params;  // Eq. (7)
+    return KQ_OK;
+}
+
+// splitmix64: the state advances by the golden-ratio increment and each output is the
+// state through the variant-13 mixer (Steele, Lea and Flood, OOPSLA 2014)
+static uint64_t splitmix64_next(uint64_t& state) {
+    state += 0x9E3779B97F4A7C15ull;
+    uint64_t z = state;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+namespace {
+struct KernelKey {
+    uint32_t v[KQ_DIM];
+    bool operator==(const KernelKey& o) const { return memcmp(v, o.v, sizeof(v)) == 0; }
+};
+struct KernelKeyHash {
+    size_t operator()(const KernelKey& k) const {
+        uint64_t h = 0x243F6A8885A308D3ull;
+        for (int d = 0; d < KQ_DIM; ++d) h = (h ^ k.v[d]) * 0x100000001B3ull;
+        return (size_t)(h ^ (h >> 29));
+    }
+};
+}  // namespace
+
+kq_status kq_forgy_select(const float* X, int64_t n, int32_t dim, int32_t k, uint64_t seed, int64_t* sel) {
+    if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
+    if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(n) || !valid_k(k) || k > n || !X || !sel) return KQ_ERR_ARG;
+    std::unordered_map<int64_t, int64_t> moved;  // positions of the permutation that a swap changed
+    std::unordered_set<KernelKey, KernelKeyHash> seen;
+    std::vector<int64_t> out;
+    out.reserve((size_t)k);
+    uint64_t state = seed;
+    for (int64_t i = 0; i < n && (int32_t)out.size() < k; ++i) {
+        const int64_t j = i + (int64_t)(splitmix64_next(state) % (uint64_t)(n - i));
+        const auto pi = moved.find(i), pj = moved.find(j);
+        const int64_t vi = pi == moved.end() ? i : pi->second;
+        const int64_t vj = pj == moved.end() ? j : pj->second;
+        moved[j] = vi;  // swap positions i and j; position i is final from here on
+        const int64_t cand = vj;
+        KernelKey key;
+        memcpy(key.v, X + cand * KQ_DIM, sizeof(key.v));
+        for (int d = 0; d < KQ_DIM; ++d)
+            if (key.v[d] == 0x80000000u) key.v[d] = 0u;  // -0 and +0 are the same kernel value
+        if (seen.insert(key).second) out.push_back(cand);
+    }
+    if ((int32_t)out.size() < k) return KQ_ERR_ARG;  // fewer than k distinct kernels
+    memcpy(sel, out.data(), sizeof(int64_t) * (size_t)k);
+    return KQ_OK;
 }
 
 }  // extern "C"

@@ -501,11 +501,11 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             }
         }
 
-        if (FUSED && valid) {  // the update's exact member sums of this kernel
-            const float sc = __builtin_ldexpf(1.0f, L.shift);
+        if (FUSED && valid) {  // the update's exact member sums of this kernel, at the layer's shift
+            const int sh = (int)L.xmax[L.nxmax];
             atomicAdd(&s_cnt[myj], 1u);
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_point(xo[d], sc));
+            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_point(xo[d], sh));
         }
 
         if (L.part) {

@@ -20,18 +20,12 @@ constexpr int kWave = 64;
 // the K = 10 fp32 contraction, 9 dims + norm, into three cross terms).
 // A "tile" of the grid is the 256 kernels one workgroup scores at a time; the grid is
 // persistent (at most kAssignGridMax workgroups, each walking a contiguous run of tiles).
-#ifndef KQ_ASSIGN_WAVES
-#define KQ_ASSIGN_WAVES 4
-#endif
-constexpr int kAssignWaves = KQ_ASSIGN_WAVES;
+constexpr int kAssignWaves = 4;
 constexpr int kAssignTilesPerWave = 2;
 constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
-#ifndef KQ_ASSIGN_OCC
-#define KQ_ASSIGN_OCC 3
-#endif
-constexpr int kAssignOcc = KQ_ASSIGN_OCC;  // workgroups resident per CU
+constexpr int kAssignOcc = 3;  // workgroups resident per CU
 // codebook entries staged in LDS at a time (64 B of operands + 48 B of fp32 row each)
-constexpr int kAssignChunk = kAssignOcc <= 2 ? 512 : (kAssignOcc == 3 ? 384 : 320);
+constexpr int kAssignChunk = 384;
 constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every CU full
 
 // ---- update kernel geometry ---------------------------------------------------------
@@ -43,15 +37,9 @@ constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every 
 // most update_max_chunks(n, k) of them (that bounds its partial histograms).
 constexpr int kUpdateThreads = 1024;
 constexpr int kUpdateMinKernelsPerBlock = 1024;
-#ifndef KQ_UPDATE_BLOCKS
-#define KQ_UPDATE_BLOCKS 256
-#endif
-constexpr int kUpdateTargetBlocks = KQ_UPDATE_BLOCKS;
+constexpr int kUpdateTargetBlocks = 256;
 constexpr int kUpdateLdsMaxK = 768;     // LDS histogram [768][9] int64 + [768] u32
-#ifndef KQ_FINISH_ENTRIES
-#define KQ_FINISH_ENTRIES 8
-#endif
-constexpr int kFinishEntries = KQ_FINISH_ENTRIES;  // codebook entries per finishing workgroup
+constexpr int kFinishEntries = 8;  // codebook entries per finishing workgroup
 constexpr size_t kUpdatePartialBudget = size_t(1) << 24;  // bytes of partials per layer above 768 entries
 
 inline int update_ranges(int32_t k) { return (k + kUpdateLdsMaxK - 1) / kUpdateLdsMaxK; }
@@ -83,19 +71,28 @@ constexpr int kSqPerBlock = 8192;
 inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1) / kAssignKernelsPerTile); }
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
 
-// fixed-point scale of the exact member sums: q(x) = rint(x * 2^s), s = 57 - ceil(log2 n)
-inline int fixed_shift(int64_t n) {
+// Fixed-point scale of the exact member sums.  A layer's sums use q(x) = rint(x * 2^s) with
+//     s = 62 - ceil(log2 n) - e,   e the smallest integer with max |x| < 2^e (-126 when the
+//                                  largest magnitude is subnormal, 62 - ceil(log2 n) for an
+//                                  all-zero layer),
+// so |q| <= 2^(62 - ceil(log2 n)) and no sum over at most n values can leave int64, while the
+// resolution stays 2^-(62 - ceil(log2 n)) of the layer's largest magnitude whatever that
+// magnitude is.  base_shift(n) = 57 - ceil(log2 n) is s for 16 <= max |x| < 32; the device
+// derives s from it and the layer's maxima of |x| (the same rule serves the gradient sums
+// of Eq. 2).
+inline int base_shift(int64_t n) {
     int c = 0;
     while ((int64_t(1) << c) < n) ++c;
     return 57 - c;
 }
 
-// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is exact in fp32 (|x| * 2^s < 2^62,
-// a power-of-two scaling) and so is its rounding to an integer v; v = hi * 2^32 + lo with
-// hi = floor(v * 2^-32) (|hi| < 2^30) and 0 <= lo < 2^32, where lo = v - hi * 2^32 has
-// fewer significant bits than v and is exact in fp32 too, so both convert exactly.
-__device__ __forceinline__ unsigned long long fixed_point(float x, float scale) {
-    const float v = __builtin_rintf(x * scale);
+// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is one exact v_ldexp_f32 (a power-of-two
+// scaling that stays below 2^62 in magnitude by the choice of s) and so is its rounding to an
+// integer v; v = hi * 2^32 + lo with hi = floor(v * 2^-32) (|hi| <= 2^30) and 0 <= lo < 2^32,
+// where lo = v - hi * 2^32 has fewer significant bits than v and is exact in fp32 too, so both
+// convert exactly.
+__device__ __forceinline__ unsigned long long fixed_point(float x, int shift) {
+    const float v = __builtin_rintf(__builtin_ldexpf(x, shift));
     const float hi = __builtin_floorf(v * 0x1p-32f);
     const float lo = __builtin_fmaf(hi, -0x1p32f, v);
     return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
@@ -114,6 +111,7 @@ constexpr int kFuseChunk = 256;  // codebook entries staged at a time by the fus
 //   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]           (overwritten each call)
 //   update distortion partials : fp64 [ranges * max chunks]                      (overwritten each call)
 //   update histograms          : int64 [max chunks][k][10] per-chunk partial sums (overwritten each call)
+//   magnitudes                 : u32 [absmax_blocks(n) + 1 + KQ_MAX_STACK] (below)
 inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 inline size_t ws_assign_part(int64_t n) { return align256(sizeof(double) * (size_t)assign_tiles(n) * kAssignWaves); }
 inline size_t ws_update_part(int64_t n, int32_t k) {
@@ -124,13 +122,17 @@ inline size_t ws_hist(int64_t n, int32_t k) {
     if (k <= kFuseMaxK && (size_t)assign_tiles(n) > parts) parts = (size_t)assign_tiles(n);  // fused partials
     return align256(sizeof(int64_t) * 10 * (size_t)k * parts);
 }
-// codebook gradient step: per-block maxima of |g| (fp32 bits) and the layer's fixed-point shift
-constexpr int kGradMaxPerBlock = 8192;  // gradient values per block of the |g| maximum
-inline int grad_max_blocks(int64_t n) { return (int)((n * kDim + kGradMaxPerBlock - 1) / kGradMaxPerBlock); }
-inline size_t ws_grad(int64_t n) { return align256(sizeof(unsigned) * ((size_t)grad_max_blocks(n) + 1)); }
-inline size_t layer_ws_bytes(int64_t n, int32_t k) {
-    return ws_assign_part(n) + ws_update_part(n, k) + ws_hist(n, k) + ws_grad(n);
+// Largest magnitudes of the values whose fixed-point sums a call forms (the kernels, or the
+// gradients of Eq. 2): one maximum of |v| per block of 8192 values (fp32 bits with the sign
+// cleared, so a NaN orders above +inf and every finite value), then the layer's shift, then
+// -- used in the first layer's region of a call -- one non-finite flag per layer of the call.
+constexpr int kAbsMaxPerBlock = 8192;
+inline int absmax_blocks(int64_t n) { return (int)((n * kDim + kAbsMaxPerBlock - 1) / kAbsMaxPerBlock); }
+inline size_t ws_xmax(int64_t n) {
+    return align256(sizeof(unsigned) * ((size_t)absmax_blocks(n) + 1 + KQ_MAX_STACK));
 }
+inline size_t ws_xmax_offset(int64_t n, int32_t k) { return ws_assign_part(n) + ws_update_part(n, k) + ws_hist(n, k); }
+inline size_t layer_ws_bytes(int64_t n, int32_t k) { return ws_xmax_offset(n, k) + ws_xmax(n); }
 
 enum : int { kFlagCountsOnly = 1, kFlagGrad = 2 };
 
@@ -149,7 +151,7 @@ struct DevLayer {
     int k;
     int unit_begin;           // first tile (assign) or workgroup (update) of this layer
     int nunits;               // tiles or workgroups of this layer
-    int shift;                // fixed-point scale (update)
+    int shift;                // base_shift(n); the device turns it into the layer's fixed-point shift
     int flags;                // kFlag*
     int napart;               // number of assignment partials
     int ranges;               // update: codebook ranges (workgroups per chunk)
@@ -157,8 +159,8 @@ struct DevLayer {
     int chunk;                // update: kernels per chunk
     int nchunks;              // update: chunks (= partial histograms)
     float gamma;              // gradient step: learning rate
-    unsigned* gmax;           // gradient step: per-block maxima of |g| as fp32 bits, then the shift
-    int ngmax;                // gradient step: number of those blocks
+    unsigned* xmax;           // per-block maxima of |x| (or |g|) as fp32 bits, then the shift (xmax[nxmax])
+    int nxmax;                // number of those blocks
     int wfirst;               // fused assignment: first workgroup whose tiles touch the layer
 };
 
@@ -169,6 +171,7 @@ struct DevLayer {
 struct StackParams {
     int nlayers;
     int total_units;
+    unsigned* range_flags;    // per layer: a non-finite value was seen (absmax launches), or null
     int unit_begin[KQ_MAX_STACK];
     DevLayer L[KQ_MAX_STACK];
 };
@@ -250,7 +253,7 @@ hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_fill_zero(void* ws, size_t bytes, hipStream_t s);
-hipError_t launch_grad_absmax(const StackParams& p, hipStream_t s);
+hipError_t launch_absmax(const StackParams& p, hipStream_t s);
 
 struct CbqLayer {
     const float* C;
@@ -333,14 +336,8 @@ struct ReconParams {
     int unit_begin[KQ_MAX_STACK];  // first workgroup of each layer, INT_MAX past the last
     ReconLayer L[KQ_MAX_STACK];
 };
-#ifndef KQ_RECON_THREADS
-#define KQ_RECON_THREADS 512
-#endif
-#ifndef KQ_RECON_ROWS
-#define KQ_RECON_ROWS 2048
-#endif
-constexpr int kReconThreads = KQ_RECON_THREADS;
-constexpr int kReconRows = KQ_RECON_ROWS;  // rows per workgroup of the stack reconstruction
+constexpr int kReconThreads = 512;
+constexpr int kReconRows = 2048;  // rows per workgroup of the stack reconstruction
 constexpr int kReconLdsFloats = 16384;  // codebooks up to this many values are gathered from LDS
 inline int recon_blocks(int64_t n) { return (int)((n + kReconRows - 1) / kReconRows); }
 hipError_t launch_pack_stack(const PackParams& p, hipStream_t s);

@@ -1,10 +1,13 @@
 // Update step of kernel-level quantization (Sec. 3.1, Eq. 1): every codebook entry
 // becomes the mean of its kernel set S_j; an empty set keeps its entry.
 //
-// The member sums are exact integers: each value is mapped to q(x) = rint(x * 2^s)
-// with s = 57 - ceil(log2 n), so |q| < 2^62 / n and no sum over at most n kernels can
-// overflow int64 (|x| < 32).  Integer addition is associative, so the sums, and with
-// them the new codebook, do not depend on the order in which blocks or lanes add.
+// The member sums are exact integers: each value is mapped to q(x) = rint(x * 2^s) with a
+// per-layer shift s = 62 - ceil(log2 n) - e, max |x| < 2^e, so |q| <= 2^62 / n and
+// no sum over at most n kernels can overflow int64, at any magnitude of the weights.
+// Integer addition is associative, so the sums, and with them the new codebook, do not
+// depend on the order in which blocks or lanes add.  absmax_kernel takes the maxima of |x|
+// per block of 8192 values and shift_kernel turns them into each layer's s (and flags
+// non-finite values); both run once per call, or once per fit, before any sum is formed.
 //
 // update_kernel: one launch covers every layer of a stack.  A layer's kernels are cut
 // into chunks and its codebook into ranges of at most 768 entries; a workgroup of 1024
@@ -19,10 +22,8 @@
 // assignment, it also sums, in a fixed order, the fp32 distances of its rows to their old
 // entries.
 // Codebook gradient step (Eq. 2): the same sums over a gradient tensor G instead of the
-// kernels, with a per-layer scale s = min(100, 62 - ceil(log2 n) - e) where 2^e > max |g|
-// (a first launch takes per-block maxima of |g|; every workgroup reduces them), so no sum
-// over at most n values can overflow and the relative resolution is the same for any
-// gradient magnitude; the finish then writes c - gamma * mean instead of the mean.
+// kernels, with the same shift rule applied to max |g|; the finish then writes
+// c - gamma * mean instead of the mean.
 // update_finish_kernel: a workgroup of 640 threads owns 8 entries of one layer; eight
 // groups of 80 threads add an eighth of the partials each, eight loads in flight per
 // thread (any order gives the same integers; 12, 16, 24 or 32 in flight measured slower), then it divides and writes the codebook
@@ -45,21 +46,21 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
     return acc;
 }
 
-// shift of the gradient sums: s = 62 - ceil(log2 n) - e with max |g| < 2^e, i.e. the kernel
-// shift (57 - ceil(log2 n), for |x| < 32 = 2^5) moved by 5 - e, kept in [-100, 100]
-__device__ __forceinline__ int grad_shift(float gmax, int kernel_shift) {
-    if (!(gmax > 0.0f)) return 100;
-    const int be = (int)((__float_as_uint(gmax) >> 23) & 255u);
-    const int e = be == 0 ? -126 : be - 126;  // gmax < 2^e (subnormal maxima: below 2^-126)
-    const int s = kernel_shift + 5 - e;
-    return s > 100 ? 100 : (s < -100 ? -100 : s);
+// the layer's shift from its largest magnitude (fp32 bits, sign cleared):
+// s = base + 5 - e with max < 2^e, where base = 57 - ceil(log2 n) (e = -126 for a subnormal
+// maximum, e = 0 for an all-zero layer; a non-finite maximum gives e >= 129 and a shift
+// that keeps the sums finite but meaningless, which KQ_F_VALIDATE reports)
+__device__ __forceinline__ int layer_shift(unsigned maxbits, int base) {
+    const int be = (int)(maxbits >> 23);                          // biased exponent (255: inf or NaN)
+    const int e = maxbits == 0u ? 0 : (be == 0 ? -126 : be - 126);  // max < 2^e
+    return base + 5 - e;
 }
 
 struct UpdateCtx {
     unsigned long long* s_sum;  // [krange][9]
     unsigned* s_cnt;            // [krange]
     const float* C_old;
-    float scale;                // 2^s
+    int shift;                  // s of q(x) = rint(x * 2^s)
     int j0, kr;                 // the entry range [j0, j0 + kr)
     bool sums, want_dist;
 };
@@ -72,7 +73,7 @@ __device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[
     atomicAdd(&c.s_cnt[jr], 1u);
     if (c.sums) {
 #pragma unroll
-        for (int d = 0; d < kDim; ++d) atomicAdd(&c.s_sum[jr * kDim + d], fixed_point(x[d], c.scale));
+        for (int d = 0; d < kDim; ++d) atomicAdd(&c.s_sum[jr * kDim + d], fixed_point(x[d], c.shift));
     }
 }
 
@@ -123,20 +124,8 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     c.s_sum = s_dyn;
     c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
-    int shift = L.shift;
-    if (L.flags & kFlagGrad) {  // the scale of the gradient sums, from the per-block maxima of |g|
-        __shared__ unsigned s_mx;
-        if (tid == 0) s_mx = 0u;
-        __syncthreads();
-        unsigned m = 0u;
-        for (int q = tid; q < L.ngmax; q += kUpdateThreads) m = max(m, L.gmax[q]);
-        atomicMax(&s_mx, m);  // LDS; non-negative floats order as their bits
-        __syncthreads();
-        shift = grad_shift(__uint_as_float(s_mx), L.shift);
-        if (u == 0 && tid == 0) L.gmax[L.ngmax] = (unsigned)shift;  // for the finish
-    }
-    c.scale = __builtin_ldexpf(1.0f, shift);
     c.sums = (L.flags & kFlagCountsOnly) == 0;
+    c.shift = c.sums ? (int)L.xmax[L.nxmax] : 0;  // set by shift_kernel before this launch
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;
 
@@ -173,11 +162,8 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     }
 }
 
-#ifndef KQ_FINISH_BATCH
-#define KQ_FINISH_BATCH 8
-#endif
 constexpr int kFinishGroups = kSumThreads / (10 * kFinishEntries);
-constexpr int kFinishBatch = KQ_FINISH_BATCH;
+constexpr int kFinishBatch = 8;
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
 
@@ -236,62 +222,83 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         } else if ((L.flags & kFlagCountsOnly) == 0) {
             const float old = L.C_old[(size_t)j * kDim + d];
             float c = old;
-            if (z > 0 && (L.flags & kFlagGrad)) {  // Eq. (2): c - gamma * mean gradient
-                const int sh = (int)L.gmax[L.ngmax];
-                const double mean = ((double)S * ldexp(1.0, -sh)) / (double)z;
-                c = (float)((double)old - (double)L.gamma * mean);
-            } else if (z > 0) {
-                c = (float)(((double)S * ldexp(1.0, -L.shift)) / (double)z);
+            if (z > 0) {
+                const double mean = ((double)S * ldexp(1.0, -(int)L.xmax[L.nxmax])) / (double)z;
+                // Eq. (2): c - gamma * mean gradient; Eq. (1): the mean of the kernels
+                c = (L.flags & kFlagGrad) ? (float)((double)old - (double)L.gamma * mean) : (float)mean;
             }
             L.C[(size_t)j * kDim + d] = c;
         }
     }
 }
 
-// per-block maximum of |g| over 8192 gradient values of a layer (fp32 bits; NaN ignored)
-__global__ __launch_bounds__(256) void grad_absmax_kernel(const StackParams p) {
+// per-block maximum of |v| over 8192 values of a layer (the kernels, or the gradients of
+// Eq. 2) as fp32 bits with the sign cleared: an integer maximum, so a NaN counts as the
+// largest value and shift_kernel can flag it
+__global__ __launch_bounds__(256) void absmax_kernel(const StackParams p) {
     __shared__ unsigned s_mx;
     const int li = find_layer(p, blockIdx.x);
     const DevLayer& L = p.L[li];
     const int b = blockIdx.x - L.unit_begin;
     const long long count = (long long)L.n * kDim;
-    const long long base = (long long)b * kGradMaxPerBlock;
+    const long long base = (long long)b * kAbsMaxPerBlock;
     if (threadIdx.x == 0) s_mx = 0u;
     __syncthreads();
-    float m = 0.0f;
-    if ((reinterpret_cast<uintptr_t>(L.X) & 15u) == 0 && base + kGradMaxPerBlock <= count) {
-        // a whole block from a 16-byte aligned tensor: eight float4 loads per thread in flight
-        const float4* __restrict__ X4 = reinterpret_cast<const float4*>(L.X + base);
-        float4 v[kGradMaxPerBlock / 1024];
+    unsigned m = 0u;
+    const unsigned* __restrict__ V = reinterpret_cast<const unsigned*>(L.X);
+    if ((reinterpret_cast<uintptr_t>(L.X) & 15u) == 0 && base + kAbsMaxPerBlock <= count) {
+        // a whole block from a 16-byte aligned tensor: eight 16-byte loads per thread in flight
+        const uint4* __restrict__ V4 = reinterpret_cast<const uint4*>(V + base);
+        uint4 v[kAbsMaxPerBlock / 1024];
 #pragma unroll
-        for (int u = 0; u < kGradMaxPerBlock / 1024; ++u) v[u] = X4[threadIdx.x + 256 * u];
+        for (int u = 0; u < kAbsMaxPerBlock / 1024; ++u) v[u] = V4[threadIdx.x + 256 * u];
 #pragma unroll
-        for (int u = 0; u < kGradMaxPerBlock / 1024; ++u)
-            m = fmaxf(m, fmaxf(fmaxf(fabsf(v[u].x), fabsf(v[u].y)), fmaxf(fabsf(v[u].z), fabsf(v[u].w))));
+        for (int u = 0; u < kAbsMaxPerBlock / 1024; ++u)
+            m = max(m, max(max(v[u].x & 0x7fffffffu, v[u].y & 0x7fffffffu), max(v[u].z & 0x7fffffffu, v[u].w & 0x7fffffffu)));
     } else {
 #pragma unroll 4
-        for (int q = threadIdx.x; q < kGradMaxPerBlock; q += 256) {
+        for (int q = threadIdx.x; q < kAbsMaxPerBlock; q += 256) {
             const long long e = base + q;
-            if (e < count) m = fmaxf(m, fabsf(L.X[e]));
+            if (e < count) m = max(m, V[e] & 0x7fffffffu);
         }
     }
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-    if ((threadIdx.x & 63) == 0) atomicMax(&s_mx, __float_as_uint(m));
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, off));
+    if ((threadIdx.x & 63) == 0) atomicMax(&s_mx, m);  // LDS
     __syncthreads();
-    if (threadIdx.x == 0) L.gmax[b] = s_mx;
+    if (threadIdx.x == 0) L.xmax[b] = s_mx;
 }
 
-hipError_t launch_grad_absmax(const StackParams& p, hipStream_t s) {
+// one workgroup per layer: the largest of its block maxima gives the layer's shift
+// (xmax[nxmax]); range_flags[layer] records whether any value was NaN or infinite
+__global__ __launch_bounds__(256) void shift_kernel(const StackParams p) {
+    __shared__ unsigned s_mx;
+    const DevLayer& L = p.L[blockIdx.x];
+    if (threadIdx.x == 0) s_mx = 0u;
+    __syncthreads();
+    unsigned m = 0u;
+    for (int q = threadIdx.x; q < L.nxmax; q += 256) m = max(m, L.xmax[q]);
+    atomicMax(&s_mx, m);  // LDS
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        L.xmax[L.nxmax] = (unsigned)layer_shift(s_mx, L.shift);
+        if (p.range_flags) p.range_flags[blockIdx.x] = s_mx >= 0x7f800000u ? 1u : 0u;
+    }
+}
+
+hipError_t launch_absmax(const StackParams& p, hipStream_t s) {
     StackParams q = p;
     int blk = 0;
     for (int l = 0; l < q.nlayers; ++l) {
         q.L[l].unit_begin = blk;
-        blk += q.L[l].ngmax;
+        blk += q.L[l].nxmax;
     }
     q.total_units = blk;
     set_unit_table(q);
-    hipLaunchKernelGGL(grad_absmax_kernel, dim3(blk), dim3(256), 0, s, q);
+    hipLaunchKernelGGL(absmax_kernel, dim3(blk), dim3(256), 0, s, q);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(shift_kernel, dim3(q.nlayers), dim3(256), 0, s, q);
     return hipGetLastError();
 }
 
@@ -308,9 +315,6 @@ hipError_t launch_update(const StackParams& p, hipStream_t s) {
         const size_t b = (size_t)p.L[l].krange * (kDim * sizeof(unsigned long long) + sizeof(unsigned));
         lds = b > lds ? b : lds;
     }
-#ifdef KQ_UPDATE_LDS_MIN
-    if (lds < KQ_UPDATE_LDS_MIN) lds = KQ_UPDATE_LDS_MIN;
-#endif
     hipLaunchKernelGGL(update_kernel, dim3(p.total_units), dim3(kUpdateThreads), lds, s, p);
     return hipGetLastError();
 }

@@ -29,21 +29,21 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert lib.kq_abi_version() == 9
+    assert lib.kq_abi_version() == 10
     for s in range(6):
         assert len(lib.kq_status_string(s)) > 0
     assert lib.kq_status_string(99) == b"unknown status"
 
 
 def test_workspace_sizes():
-    a = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 4096, 256)
+    a = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 4096, 256, 9)
     assert a > 0 and a % 256 == 0
-    assert lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256) == a
-    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 0, 256) == 0
-    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, 0) == 0
-    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, kq.KQ_MAX_K + 1) == 0
-    assert lib.kq_workspace_bytes(7, 10, 4) == 0
-    big = lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 1 << 20, 4096)
+    assert lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256, 9) == a
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 0, 256, 9) == 0
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, 0, 9) == 0
+    assert lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 10, kq.KQ_MAX_K + 1, 9) == 0
+    assert lib.kq_workspace_bytes(7, 10, 4, 9) == 0
+    big = lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 1 << 20, 4096, 9)
     assert big >= 8 * 10 * 4096
 
 
@@ -72,7 +72,7 @@ def test_assign_argument_errors():
     assert assign(flags=1) == kq.KQ_ERR_ARG
     # a distortion output needs a workspace of the queried size
     assert assign(dist=FAKE) == kq.KQ_ERR_WORKSPACE
-    need = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 100, 8)
+    need = lib.kq_workspace_bytes(kq.KQ_OP_ASSIGN, 100, 8, 9)
     assert assign(dist=FAKE, ws=FAKE, wsb=need - 1) == kq.KQ_ERR_WORKSPACE
     assert assign(dist=FAKE, ws=FAKE + 128, wsb=need) == kq.KQ_ERR_WORKSPACE
 
@@ -104,7 +104,7 @@ def test_stack_argument_errors():
     arr[1] = kq.KqLayer(FAKE, 100, 200, FAKE, FAKE, None, FAKE, None)
     p = ctypes.cast(arr, ctypes.c_void_p)
     need = lib.kq_stack_workspace_bytes(p, 2)
-    assert need == lib.kq_workspace_bytes(0, 4096, 256) + lib.kq_workspace_bytes(0, 100, 200)
+    assert need == lib.kq_workspace_bytes(0, 4096, 256, 9) + lib.kq_workspace_bytes(0, 100, 200, 9)
     assert lib.kq_fit_stack(p, 2, 3, 0, FAKE, need, None) == kq.KQ_ERR_ARG      # k > n in layer 1
     assert lib.kq_assign_stack(p, 2, 0, 0, FAKE, need - 1, None) == kq.KQ_ERR_WORKSPACE
     assert lib.kq_assign_stack(p, 0, 0, 0, FAKE, need, None) == kq.KQ_ERR_ARG
@@ -149,7 +149,7 @@ def test_cbq_pack_reconstruct_argument_errors():
     assert lib.kq_pack_bits(None, 4, 0, 4, None, None) == kq.KQ_OK             # nothing to do
     assert lib.kq_pack_bits(None, 4, 10, 0, None, None) == kq.KQ_OK            # zero-bit fields
     assert lib.kq_unpack_bits(None, 10, 4, FAKE, None) == kq.KQ_ERR_ARG
-    assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 9, FAKE + 4, None) == kq.KQ_ERR_ARG   # W_hat 16-B aligned
+    assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 9, FAKE + 2, None) == kq.KQ_ERR_ARG   # W_hat 4-B aligned
     assert lib.kq_reconstruct(FAKE, 10, FAKE, 4, 8, FAKE, None) == kq.KQ_ERR_UNSUPPORTED
     assert lib.kq_reconstruct_packed(None, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG
     assert lib.kq_reconstruct_packed(FAKE + 2, 4, 10, FAKE, 4, 9, FAKE, None) == kq.KQ_ERR_ARG  # stream read as dwords
@@ -207,7 +207,7 @@ def test_stack_pack_and_reconstruct_argument_errors():
 
 def test_yinyang_workspace_and_argument_errors():
     a = lib.kq_yinyang_workspace_bytes(4096, 256, 0)
-    assert a > lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256) and a % 256 == 0
+    assert a > lib.kq_workspace_bytes(kq.KQ_OP_FIT, 4096, 256, 9) and a % 256 == 0
     assert lib.kq_yinyang_workspace_bytes(4096, 256, 8) > lib.kq_yinyang_workspace_bytes(4096, 256, 4)
     assert lib.kq_yinyang_workspace_bytes(4096, 256, 65) == 0      # more groups than mask bits
     assert lib.kq_yinyang_workspace_bytes(100, 8, 9) == 0          # more groups than entries
@@ -253,8 +253,8 @@ def test_yinyang_workspace_and_argument_errors():
 
 
 def test_grad_step_argument_errors():
-    nb = lib.kq_workspace_bytes(kq.KQ_OP_GRAD, 100, 8)
-    assert nb == lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 100, 8) and nb > 0
+    nb = lib.kq_workspace_bytes(kq.KQ_OP_GRAD, 100, 8, 9)
+    assert nb == lib.kq_workspace_bytes(kq.KQ_OP_UPDATE, 100, 8, 9) and nb > 0
 
     def step(**kw):
         a = dict(G=FAKE, n=100, dim=9, idx=FAKE, k=8, C0=FAKE, gamma=0.1, C=FAKE, z=None, ws=FAKE, wsb=nb)
@@ -301,7 +301,7 @@ def test_quantize_scalars_argument_errors():
 
 def test_search_argument_errors():
     nb = lib.kq_search_workspace_bytes(1000, 300, 10)
-    assert nb >= lib.kq_workspace_bytes(kq.KQ_OP_FIT, 1000, 256)     # covers every trial size
+    assert nb >= lib.kq_workspace_bytes(kq.KQ_OP_FIT, 1000, 256, 9)     # covers every trial size
     assert lib.kq_search_workspace_bytes(100, 101, 10) == 0
     k = ctypes.c_int32(0)
 
@@ -319,3 +319,108 @@ def test_search_argument_errors():
     assert srch(mi=-1) == kq.KQ_ERR_ARG
     assert srch(k=None) == kq.KQ_ERR_ARG
     assert srch(wsb=nb - 1) == kq.KQ_ERR_WORKSPACE
+
+
+# ---- host-only helpers: computed on the host, checked without a GPU -------------------------
+
+def test_forgy_select_matches_the_oracle():
+    """kq_forgy_select (host C) picks the same kernels as the oracle's reading of the
+    initialisation, bit for bit, on the hand-worked case and on stacks with copies, signed
+    zeros and NaN kernels; k above the number of distinct kernels is refused."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from test_oracle_forgy import HAND_X, golden
+
+    for seed, k, expected in golden()[1]:
+        assert kq.kq_forgy_select(HAND_X, k, seed).tolist() == expected
+    rng = np.random.default_rng(11)
+    X = rng.standard_normal((3000, 9)).astype(np.float32)
+    X[1000:1500] = X[:500]
+    X[2000] = 0.0
+    X[2001] = -0.0
+    X[2002, 3] = np.nan
+    cases = [(X, 2499, 0), (X, 64, 2 ** 64 - 1), (X, 1, 5), (synth.resnet18_stack(k=16, layers=1)[0].X, 4096, 2000),
+             (synth.stress_layer(n=100000, k=4096, n_centers=4096, seed=4)[0].X, 4096, 4000)]
+    for Xc, k, seed in cases:
+        assert np.array_equal(kq.kq_forgy_select(Xc, k, seed), oracle.forgy_select(Xc, k, seed)), (k, seed)
+    sel = np.zeros(3, np.int64)
+    P = ctypes.c_void_p
+    xp = np.ascontiguousarray(HAND_X).ctypes.data_as(P)
+    assert lib.kq_forgy_select(xp, 7, 9, 6, 1234567, sel.ctypes.data_as(P)) == kq.KQ_ERR_ARG   # 5 distinct
+    assert sel.tolist() == [0, 0, 0]                                                           # untouched
+    assert lib.kq_forgy_select(xp, 7, 9, 8, 1, sel.ctypes.data_as(P)) == kq.KQ_ERR_ARG         # k > n
+    assert lib.kq_forgy_select(xp, 7, 8, 3, 1, sel.ctypes.data_as(P)) == kq.KQ_ERR_UNSUPPORTED
+    assert lib.kq_forgy_select(None, 7, 9, 3, 1, sel.ctypes.data_as(P)) == kq.KQ_ERR_ARG
+    assert lib.kq_forgy_select(xp, 7, 9, 3, 1, None) == kq.KQ_ERR_ARG
+
+
+def test_accounting_matches_the_paper_and_the_oracle():
+    """Eq. (4), (6), (7) in the library: the figures of Sec. 4.2.1 (golden file) and the
+    oracle's formulas, which the golden tables pin, on a grid of sizes."""
+    import oracle
+    from test_oracle_pack_accounting import rows
+
+    for _layer, n, k, cr_k, cr_kc, beta_kc in rows("vgg_k128_ratios.txt"):
+        B, r32, _ = kq.kq_accounting(int(n), int(k), 32)
+        _, r6, b6 = kq.kq_accounting(int(n), int(k), 6)
+        assert abs(r32 - float(cr_k)) <= 0.01 and abs(r6 - float(cr_kc)) <= 0.01 and abs(b6 - float(beta_kc)) <= 0.001
+    for k in (1, 2, 3, 4, 5, 60, 192, 255, 256, 257, 4096, 7679, 65536):
+        assert kq.index_bits(k) == oracle.index_bits(k)
+        for n in (1, 192, 4096, 262144):
+            for bc in (6, 32):
+                B, r, beta = kq.kq_accounting(n, k, bc)
+                assert B == oracle.storage_bits(n, k, bc)
+                assert r == oracle.compression_ratio(n, k, bc) and beta == oracle.bits_per_param(n, k, bc)
+    assert kq.kq_accounting(10 ** 9, 2, 32)[1] == pytest.approx(288, rel=1e-6)   # the limit of Sec. 3.3
+    assert lib.kq_index_bits(0) == -1
+    assert lib.kq_accounting(0, 4, 9, 6, None, None, None) == kq.KQ_ERR_ARG
+    assert lib.kq_accounting(4, 4, 9, 0, None, None, None) == kq.KQ_ERR_ARG
+
+
+def test_validate_flag_and_compress_argument_errors():
+    # KQ_F_VALIDATE is accepted by the calls that form member sums, refused elsewhere
+    assert lib.kq_assign(FAKE, 100, 9, FAKE, 8, FAKE, None, None, kq.KQ_F_VALIDATE, None, 0, None) == kq.KQ_ERR_ARG
+    up = lambda f: lib.kq_update(FAKE, 100, 9, FAKE, 8, FAKE, FAKE, None, None, f, None, 0, None)
+    assert up(kq.KQ_F_VALIDATE) == kq.KQ_ERR_WORKSPACE and up(kq.KQ_F_VALIDATE | 128) == kq.KQ_ERR_ARG
+    fit = lambda f: lib.kq_fit_layer(FAKE, 100, 9, 8, FAKE, 3, FAKE, FAKE, None, None, f, None, 0, None)
+    assert fit(kq.KQ_F_VALIDATE) == kq.KQ_ERR_WORKSPACE and fit(kq.KQ_F_FUSED_SUMS) == kq.KQ_ERR_ARG
+    # the compression pass
+    arr = (kq.KqCompressLayer * 2)()
+    good = dict(X=FAKE, n=4096, k=256, C_init=FAKE, C=FAKE, idx=FAKE, counts=FAKE, distortion=None, codes=FAKE,
+                levels=FAKE, C_hat=FAKE, packed_idx=FAKE, packed_codes=FAKE, W_hat=FAKE, sq_error=FAKE)
+    arr[0] = kq.KqCompressLayer(**good)
+    arr[1] = kq.KqCompressLayer(**dict(good, n=100, k=16))
+    P = ctypes.cast(arr, ctypes.c_void_p)
+    need = lib.kq_compress_workspace_bytes(P, 2, 6)
+    fit_need = lib.kq_workspace_bytes(0, 4096, 256, 9) + lib.kq_workspace_bytes(0, 100, 16, 9)
+    assert need >= fit_need and need % 256 == 0
+    run = lambda n_layers=2, iters=30, mode=0, bits=6, cit=30, flags=0, ws=FAKE, wsb=need: lib.kq_compress_stack(
+        P, n_layers, iters, mode, bits, cit, flags, None, ws, wsb, None)
+    assert run(bits=9) == kq.KQ_ERR_UNSUPPORTED
+    assert run(n_layers=0) == kq.KQ_ERR_ARG and run(iters=-1) == kq.KQ_ERR_ARG and run(mode=3) == kq.KQ_ERR_ARG
+    assert run(cit=-1) == kq.KQ_ERR_ARG and run(flags=kq.KQ_F_FUSED_SUMS) == kq.KQ_ERR_ARG
+    assert run(wsb=need - 1) == kq.KQ_ERR_WORKSPACE and run(ws=FAKE + 64) == kq.KQ_ERR_WORKSPACE
+    for field, value in [("k", 4097), ("C_init", None), ("counts", None), ("C_hat", None), ("X", FAKE + 2),
+                         ("packed_idx", FAKE + 2), ("W_hat", None)]:
+        arr[0] = kq.KqCompressLayer(**dict(good, **{field: value}))
+        assert run() == kq.KQ_ERR_ARG, field            # (W_hat None with sq_error set)
+    arr[0] = kq.KqCompressLayer(**dict(good, k=kq.KQ_MAX_K + 1, n=1 << 20))
+    assert run() == kq.KQ_ERR_UNSUPPORTED
+    arr[0] = kq.KqCompressLayer(**dict(good, packed_idx=None, packed_codes=None, W_hat=None, sq_error=None))
+    assert lib.kq_compress_workspace_bytes(P, 2, 6) >= fit_need
+
+
+def test_python_stack_wrappers_check_the_distortion_slot():
+    """kq_assign_stack / kq_update_stack refuse a slot outside the distortion history before
+    calling the library (the C side only sees device pointers and cannot check it)."""
+    import types
+
+    import torch
+    fake = types.SimpleNamespace(distortion=[torch.zeros(4, dtype=torch.float64)], layers=None, n_layers=1)
+    for slot in (4, 17, -1):
+        with pytest.raises(ValueError):
+            kq.kq_assign_stack(fake, dist_slot=slot)
+        with pytest.raises(ValueError):
+            kq.kq_update_stack(fake, dist_slot=slot)

@@ -555,6 +555,27 @@ kq_status kq_accounting(int64_t n, int32_t k, int32_t dim, int32_t bc, int64_t* 
                         double* bits_per_param);
 kq_status kq_forgy_select(const float* X, int64_t n, int32_t dim, int32_t k, uint64_t seed, int64_t* sel);
 
+/*
+ * kq_fit_layer_noalloc -- kq_fit_layer for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc): the same
+ * arguments without the workspace, and the same outputs bit for bit.  Its scratch is a
+ * static device array of KQ_NOALLOC_SCRATCH_BYTES (32 MiB) in the library, one per GPU the
+ * library runs on, held until the process ends; its address is looked up once per device
+ * (hipGetSymbolAddress, on the first call with that device current).  The call allocates
+ * nothing.  The stream must belong to the current device.
+ *   Sizes whose kq_workspace_bytes(KQ_OP_FIT, n, k, 9) exceeds the scratch (for k = 256, n
+ *   above 418,560 kernels) return KQ_ERR_WORKSPACE, before anything is enqueued.
+ *   All calls on one GPU share that GPU's scratch: calls that overlap on one device (two
+ *   streams, two host threads) race and give unspecified results; order them on one stream.
+ *   Nothing in the scratch needs to start at zero (every call writes what it reads).
+ *   kq_fit_layer_noalloc_max_bytes() returns the scratch size.
+ */
+#define KQ_NOALLOC_SCRATCH_BYTES (32u << 20)
+size_t kq_fit_layer_noalloc_max_bytes(void);
+kq_status kq_fit_layer_noalloc(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters,
+                               float* C, int32_t* idx, int32_t* counts, double* distortion, uint32_t flags,
+                               void* stream);
+
 #ifdef __cplusplus
 }
 #endif

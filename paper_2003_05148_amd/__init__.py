@@ -99,6 +99,8 @@ def _load():
         "kq_index_bits": ([_I32], _I32),
         "kq_accounting": ([_I64, _I32, _I32, _I32, _P, _P, _P], _I32),
         "kq_forgy_select": ([_P, _I64, _I32, _I32, ctypes.c_uint64, _P], _I32),
+        "kq_fit_layer_noalloc_max_bytes": ([], _SZ),
+        "kq_fit_layer_noalloc": ([_P, _I64, _I32, _I32, _P, _I32, _P, _P, _P, _P, _U32, _P], _I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -134,7 +136,7 @@ EXPORTED = ["kq_status_string", "kq_abi_version", "kq_workspace_bytes", "kq_stac
             "kq_codebook_grad_step", "kq_codebook_grad_step_stack", "kq_quantize_scalars_workspace_bytes",
             "kq_quantize_scalars", "kq_search_workspace_bytes", "kq_search_codebook_size",
             "kq_compress_workspace_bytes", "kq_compress_stack", "kq_index_bits", "kq_accounting",
-            "kq_forgy_select"]
+            "kq_forgy_select", "kq_fit_layer_noalloc_max_bytes", "kq_fit_layer_noalloc"]
 KQ_MAX_PACK_JOBS = 32
 
 
@@ -437,6 +439,22 @@ def kq_fit_layer(X, C_init, iters: int, C=None, idx=None, counts=None, distortio
     _check(lib.kq_fit_layer(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, C.data_ptr(), idx.data_ptr(),
                             counts.data_ptr(), distortion.data_ptr(), KQ_F_VALIDATE if validate else 0,
                             ws.data_ptr(), ws.numel(), _stream(dev)), "kq_fit_layer")
+    return C, idx, counts, distortion
+
+
+def kq_fit_layer_noalloc(X, C_init, iters: int, C, idx, counts, distortion, validate: bool = False):
+    """kq_fit_layer with the library's static scratch instead of a workspace (the library
+    allocates nothing; the outputs must be given).  Returns (C, idx, counts, distortion)."""
+    X = _kernels(X)
+    C_init = _kernels(C_init, "C_init")
+    n, k = X.shape[0], C_init.shape[0]
+    _dev(C, torch.float32, "C", (k, KQ_DIM))
+    _dev(idx, torch.int32, "idx", (n,))
+    _dev(counts, torch.int32, "counts", (k,))
+    _dev(distortion, torch.float64, "distortion", (iters + 1,))
+    _check(lib.kq_fit_layer_noalloc(X.data_ptr(), n, KQ_DIM, k, C_init.data_ptr(), iters, C.data_ptr(),
+                                    idx.data_ptr(), counts.data_ptr(), distortion.data_ptr(),
+                                    KQ_F_VALIDATE if validate else 0, _stream(X.device)), "kq_fit_layer_noalloc")
     return C, idx, counts, distortion
 
 

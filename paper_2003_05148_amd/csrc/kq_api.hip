@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <unordered_map>
 #include <unordered_set>
 #include <vector>
@@ -639,6 +640,30 @@ kq_status kq_search_codebook_size(const float* X, int64_t n, int32_t dim, const 
     return hip_status(hipStreamSynchronize(s));
 }
 
+// ---- kq_fit_layer_noalloc: the fit with its scratch in a static device array -------------
+// Each device the library runs on holds one copy of `scratch` (until the process ends); host
+// code must never pass the array's name to a kernel or a copy (on the host it names a
+// stand-in, not device memory).  The device address comes from hipGetSymbolAddress, taken
+// once per device with that device current, and is kept here.
+static __device__ __align__(256) unsigned char scratch[KQ_NOALLOC_SCRATCH_BYTES];
+constexpr int kNoAllocMaxDevices = 64;
+static void* g_scratch_ptr[kNoAllocMaxDevices];
+static std::mutex g_scratch_mutex;
+
+static kq_status scratch_for_current_device(unsigned char** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return KQ_ERR_HIP;
+    if (dev >= kNoAllocMaxDevices) return KQ_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return KQ_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = (unsigned char*)g_scratch_ptr[dev];
+    return KQ_OK;
+}
+
 kq_status kq_fit_layer(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters, float* C,
                        int32_t* idx, int32_t* counts, double* distortion, uint32_t flags, void* ws, size_t ws_bytes,
                        void* stream) {
@@ -1245,6 +1270,25 @@ kq_status kq_forgy_select(const float* X, int64_t n, int32_t dim, int32_t k, uin
     if ((int32_t)out.size() < k) return KQ_ERR_ARG;  // fewer than k distinct kernels
     memcpy(sel, out.data(), sizeof(int64_t) * (size_t)k);
     return KQ_OK;
+}
+
+size_t kq_fit_layer_noalloc_max_bytes(void) { return (size_t)KQ_NOALLOC_SCRATCH_BYTES; }
+
+kq_status kq_fit_layer_noalloc(const float* X, int64_t n, int32_t dim, int32_t k, const float* C_init, int32_t iters,
+                               float* C, int32_t* idx, int32_t* counts, double* distortion, uint32_t flags,
+                               void* stream) {
+    if (dim != KQ_DIM) return KQ_ERR_UNSUPPORTED;
+    if (k > KQ_MAX_K) return KQ_ERR_UNSUPPORTED;
+    if (!valid_n(n) || !valid_k(k) || k > n || iters < 0 || (flags & ~KQ_F_VALIDATE) != 0) return KQ_ERR_ARG;
+    if (!C_init || !aligned(C_init, 4)) return KQ_ERR_ARG;
+    const kq_layer l = {X, n, k, C, idx, nullptr, counts, distortion};
+    kq_status st = check_layers(&l, 1, true);
+    if (st != KQ_OK) return st;
+    if (layer_ws_bytes(n, k) > (size_t)KQ_NOALLOC_SCRATCH_BYTES) return KQ_ERR_WORKSPACE;  // beyond the static scratch
+    unsigned char* ws = nullptr;
+    if ((st = scratch_for_current_device(&ws)) != KQ_OK) return st;
+    const float* init[1] = {C_init};
+    return run_fit(&l, 1, iters, ws, (hipStream_t)stream, init, (flags & KQ_F_VALIDATE) != 0);
 }
 
 }  // extern "C"

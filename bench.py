@@ -36,7 +36,7 @@ if ROOT not in sys.path:
 METRIC = "kernels assigned/sec per Lloyd iter (ResNet-18 stack, K=256); % FP32 peak; HBM GB/s"
 FP32_PEAK_TFLOPS = 157.3     # MI355X dense FP32 (matrix cores and vector)
 HBM_PEAK_GBS = 8000.0
-FLUSH_BYTES = 1 << 30        # written before a cold measurement: more than the 256 MB Infinity Cache
+FLUSH_BYTES = 1 << 30        # a cold measurement writes this much, then reads as much of another buffer
 
 
 # workloads: layer generator, codebook size, Lloyd rounds, first seed of the initial codebooks, description
@@ -328,34 +328,45 @@ def main():
 def head_start(torch, stream, ms=2.0):
     """Queue about `ms` of GPU spinning (no memory traffic) so that the launches queued
     after it are timed by the GPU's progress, not by how fast the host enqueues them."""
-    if not hasattr(head_start, "cycles"):          # calibrate the spin once
+    if not hasattr(head_start, "cycles_per_ms"):   # calibrate the spin once, on a long spin
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        torch.cuda._sleep(1_000_000)
+        torch.cuda._sleep(5_000_000)
         b.record(stream)
         torch.cuda.synchronize()
-        head_start.cycles = int(1_000_000 * ms / max(a.elapsed_time(b), 1e-3))
-    torch.cuda._sleep(head_start.cycles)
+        head_start.cycles_per_ms = 5_000_000 / max(a.elapsed_time(b), 1e-3)
+    torch.cuda._sleep(int(head_start.cycles_per_ms * ms))
 
 
-def timed_launches(torch, stream, fn, reps, prep=None, flush=None):
-    """Mean duration (ms) of fn's launches between two HIP events, `reps` times, all queued
-    behind a head start; `prep` runs (untimed) before each; with `flush`, a 1 GiB buffer
-    is written before each so the launches start from a cold cache."""
-    pairs = []
-    head_start(torch, stream)
-    for _ in range(reps):
-        if prep:
-            prep()
-        if flush is not None:
-            flush.zero_()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        fn()
-        b.record(stream)
-        pairs.append((a, b))
-    torch.cuda.synchronize()
-    return sum(a.elapsed_time(b) for a, b in pairs) / reps
+class LaunchTimer:
+    """Median duration (ms) of a call's launches between two HIP events, over `reps`
+    calls queued behind a head start; `prep` runs (untimed) before each call; with the
+    flush buffers, 1 GiB is written and another 1 GiB read before each call, so that it
+    starts from caches that hold none of its data and nothing dirty.  The events are
+    created once and reused."""
+
+    def __init__(self, torch, stream, reps=5):
+        self.torch, self.stream = torch, stream
+        self.ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in self.ev:
+            a.record(stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+
+    def __call__(self, fn, prep=None, flush=None):
+        import statistics
+        head_start(self.torch, self.stream)
+        for a, b in self.ev:
+            if prep:
+                prep()
+            if flush is not None:      # 1 GiB written, then 1 GiB of another buffer read: the caches
+                flush[0].zero_()         # end up holding clean lines of the second buffer only
+                flush[1].sum()
+            a.record(self.stream)
+            fn()
+            b.record(self.stream)
+        self.torch.cuda.synchronize()
+        return statistics.median(a.elapsed_time(b) for a, b in self.ev)
 
 
 def diagnostics(kq, torch, np, layers, comp, T, fused, stream):
@@ -364,16 +375,18 @@ def diagnostics(kq, torch, np, layers, comp, T, fused, stream):
     1 GiB flush; the per-layer report; the Eq. (2) codebook step."""
     dev = comp.device
     n_total = sum(L.n for L in layers)
-    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    flush = (torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev),
+             torch.zeros(FLUSH_BYTES, dtype=torch.uint8, device=dev))
     st = kq.Stack(comp.X, [c.clone() for c in comp.C], iters=1)
     reps = 5
+
+    timer = LaunchTimer(torch, stream, reps)
 
     def both(fn, prep=None):
         if prep:
             prep()
         fn()                                       # caches warm
-        return (timed_launches(torch, stream, fn, reps, prep),
-                timed_launches(torch, stream, fn, reps, prep, flush))
+        return timer(fn, prep), timer(fn, prep, flush)
 
     d = {}
     # the shifts of the layers' sums once (an update that finds them), then each step's launches alone
@@ -402,8 +415,8 @@ def diagnostics(kq, torch, np, layers, comp, T, fused, stream):
     rp = both(lambda: kq.kq_reconstruct_stack(rec_plain, workspace=ws))
     d["reconstruct_plain_ms"] = rp                             # 4 B index read + 36 B row written per kernel
     d["reconstruct_plain_GBps"] = [40.0 * n_total / (t * 1e-3) / 1e9 for t in rp]
-    d["warm_cold_note"] = ("each pair [warm, cold]: mean of 5 launches queued behind a head start, then of 5 "
-                           "launches each after writing a 1 GiB buffer")
+    d["warm_cold_note"] = ("each pair [warm, cold] in ms: median of 5 calls queued behind a head start, then of "
+                           "5 calls each after writing 1 GiB and reading another 1 GiB (events around the call)")
     # Eq. (2) codebook retraining step on the same stack: synthetic gradients of the kernels'
     # shape and the final assignment, one launch set per step
     gst = kq.Stack([x * 1e-3 for x in comp.X], [c.clone() for c in comp.C])

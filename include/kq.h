@@ -500,9 +500,9 @@ kq_status kq_reconstruct_stack(const kq_recon_layer* layers, int32_t n_layers, v
  *   1 <= bits <= 8; n_layers >= 1 (processed KQ_MAX_STACK layers at a time).
  *   flags: 0 or KQ_F_VALIDATE.  workspace: kq_compress_workspace_bytes(layers, n_layers, bits).
  *   round_events: NULL, or a host array of 2 * (iters + 1) hipEvent_t handles created by the
- *   caller, any of them NULL: entries 2t and 2t + 1 are recorded on the stream just before and
- *   just after the assignment launch of Lloyd round t (t = iters: the final assignment) of the
- *   first KQ_MAX_STACK layers, so the caller can time that launch inside the pass.
+ *   caller, any of them NULL: entries 2t and 2t + 1 take the start and the end time of the
+ *   assignment kernel of Lloyd round t (t = iters: the final assignment) of the first
+ *   KQ_MAX_STACK layers (hipExtLaunchKernel), so the caller can time that kernel inside the pass.
  */
 typedef struct kq_compress_layer {
     const float* X;          /* [n][9] kernels */

@@ -170,7 +170,7 @@ void fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, in
 // `fused` also leaves the member sums of the new assignment in the workspace (the layers'
 // shifts must be in place: run_xmax)
 kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s,
-                     bool fused = false, const float* const* C_alt = nullptr) {
+                     bool fused = false, const float* const* C_alt = nullptr, void* const* events = nullptr) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Assign, slot, C_alt, 0);
     if (fused) {
@@ -178,7 +178,8 @@ kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
         fused_slots(layers, l0, l1, wf, ns);
         for (int l = 0; l < p.nlayers; ++l) p.L[l].wfirst = wf[l];
     }
-    if (launch_assign(p, s, fused) != hipSuccess) return KQ_ERR_HIP;
+    hipEvent_t e0 = events ? (hipEvent_t)events[0] : nullptr, e1 = events ? (hipEvent_t)events[1] : nullptr;
+    if (launch_assign(p, s, fused, e0, e1) != hipSuccess) return KQ_ERR_HIP;
     if (any_distortion(layers, l0, l1) && launch_assign_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
     return KQ_OK;
 }
@@ -265,10 +266,8 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
             const bool last = (t == iters);
             const float* const* from = t == 0 ? init : nullptr;
             void* const* ev = (round_events && l0 == 0) ? round_events + 2 * t : nullptr;
-            if (ev && ev[0] && hipEventRecord((hipEvent_t)ev[0], s) != hipSuccess) return KQ_ERR_HIP;
-            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from);
+            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from, ev);
             if (st != KQ_OK) return st;
-            if (ev && ev[1] && hipEventRecord((hipEvent_t)ev[1], s) != hipSuccess) return KQ_ERR_HIP;
             if (last && !need_last) break;
             st = run_update(layers + l0, 0, l1 - l0, w, t, from, last ? kFlagCountsOnly : 0, s, true, fused);
             if (st != KQ_OK) return st;

@@ -36,6 +36,8 @@
 // tile's kernels are loaded while the current one is scored.  After the scoring each wave
 // settles its own 64 kernels (no workgroup barrier) and, when asked, writes an fp64
 // distortion partial; a second kernel sums the partials in a fixed order.
+#include <hip/hip_ext.h>
+
 #include "kq_internal.h"
 
 namespace kq {
@@ -530,13 +532,19 @@ __global__ __launch_bounds__(kSumThreads) void assign_finish_kernel(const StackP
 
 int assign_grid(int total_units) { return total_units < kAssignGridMax ? total_units : kAssignGridMax; }
 
-hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused) {
+hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused, hipEvent_t start, hipEvent_t stop) {
     const int grid = assign_grid(p.total_units);
-    if (fused)
-        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, true>), dim3(grid), dim3(kAssignWaves * kWave), 0, s, p);
-    else
-        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, false>), dim3(grid), dim3(kAssignWaves * kWave), 0, s,
-                           p);
+    const dim3 g(grid), b(kAssignWaves * kWave);
+    if (start || stop) {  // the events take the kernel's own start and end times
+        if (fused)
+            hipExtLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, true>), g, b, 0, s, start, stop, 0, p);
+        else
+            hipExtLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, false>), g, b, 0, s, start, stop, 0, p);
+    } else if (fused) {
+        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, true>), g, b, 0, s, p);
+    } else {
+        hipLaunchKernelGGL((assign_kernel<kAssignTilesPerWave, false>), g, b, 0, s, p);
+    }
     return hipGetLastError();
 }
 

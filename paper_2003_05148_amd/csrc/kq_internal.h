@@ -247,7 +247,8 @@ __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src
 constexpr int kSumThreads = 640;
 
 // launchers (return hipSuccess or the launch error)
-hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused = false);
+hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused = false, hipEvent_t start = nullptr,
+                         hipEvent_t stop = nullptr);
 int assign_grid(int total_units);
 hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);

@@ -197,7 +197,14 @@ def test_compress_stack_full_resnet18_matches_fit_and_validates():
     T = 3
     Xs, C0s = [dev(L.X) for L in layers], [dev(L.C0) for L in layers]
     comp = kq.Compression(Xs, C0s, iters=T)
-    comp.run(validate=True)
+    ev = {t: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for t in (0, 2, T)}
+    for a, b in ev.values():
+        a.record()
+        b.record()
+    comp.run(validate=True, round_events=ev)     # events on the kernel launches change nothing
+    torch.cuda.synchronize()
+    for t, (a, b) in ev.items():
+        assert 0.001 < a.elapsed_time(b) < 50.0, t   # the assignment kernel's own duration, in ms
     st = kq.Stack(Xs, C0s, iters=T)
     kq.kq_fit_stack(st, T)
     out = kq.kq_quantize_codebook_stack(st.C, st.counts, 6, kq.KQ_CBQ_WKMEANS, 30)

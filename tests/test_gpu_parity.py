@@ -479,3 +479,30 @@ def test_fused_sums_need_small_codebooks():
         kq.kq_assign_stack(st, fused_sums=True)
     with pytest.raises(kq.KqError):
         kq.kq_update_stack(st, sums_from_assign=True)
+
+
+@pytest.mark.parametrize("bits", [1, 3, 6])
+def test_quantize_codebook_edge_weights_and_magnitudes(bits):
+    """Weighted k-means codebooks bit for bit the oracle's at 1, 3 and 6 bits: codebooks on
+    both sides of the size up to which the scalars are held in LDS (910 and 911 entries),
+    zero weights, a level that lands a few 1e-10 from zero after the first round (weights
+    near 2^30), and a value far below the largest magnitude."""
+    rng = np.random.default_rng(40 + bits)
+    cases = []
+    for k in (1, 7, 255, 910, 911):
+        C = rng.laplace(0, 0.03, (k, 9)).astype(np.float32)
+        w = rng.integers(0, 300, k)
+        w[::5] = 0
+        cases.append((C, w))
+    # the middle cell holds -1 and 1 with weights 2^30 and 2^30 + 1: its level is 1 / (2^31 + 1)
+    C = np.array([[-5.0] * 9, [-1.0] * 9, [1.0] * 9, [7.0] * 9], np.float32)
+    cases.append((C, np.array([1, 1 << 30, (1 << 30) + 1, 1])))
+    C = rng.standard_normal((200, 9)).astype(np.float32)
+    C[3, 4] = np.float32(1e-12)                                   # a value far below the largest
+    cases.append((C, rng.integers(1, 50, 200)))
+    for C, w in cases:
+        codes, levels, C_hat = kq.kq_quantize_codebook(dev(C), dev(w.astype(np.int32)), bits, kq.KQ_CBQ_WKMEANS, 30)
+        oc, ol, oh, _ = oracle.cbq_wkmeans(C, w, bits, 30)
+        assert np.array_equal(host(codes), oc), (C.shape, bits)
+        assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), (C.shape, bits)
+        assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32)), (C.shape, bits)

@@ -13,17 +13,27 @@
 // the 32 rows of a kernel are its "slots", slot r holding entries r, r + 32, r + 64, ...
 // Each lane keeps the minimum score of each slot, one v_min3 per two scores.
 //
-// Exactness.  Let Q = (|x| + max_j |c_j|)^2 and u = 2^-24; every |s_j| <= Q.  A screened
-// score is within 842 u Q of its exact value (dropped cross terms 3 * 2^-16 Q, at most
-// 33 fp32 roundings in the MFMA sums, 9 u Q in the fp32 norm) plus 32 u Q where a slot
-// minimum carries its slot number in its 4 lowest mantissa bits, and the fp32 distance
-// of any entry is within 12 u Q of its exact value.  The entries of the slot with the
-// smallest minimum are rescored in the plain fp32 form; when every other slot's minimum
-// exceeds it by more than theta = 2^-13 Q + 2^-100 (2048 u Q, against
-// 2 (842 + 32 + 12) u Q = 1772 u Q needed), no entry outside that slot can reach the
-// slot's fp32 minimum, so the slot's fp32 argmin (lowest index on ties) is the answer.
-// Kernels below that gap are rescored over the whole codebook in the exact fp32 form by
-// their wave.  The output is therefore the plain fp32 argmin, bit for bit.
+// Exactness.  Write u = 2^-24 and P_j = 2 |x| |c_j| + |c_j|^2 <= (|x| + |c_j|)^2.  A
+// screened score differs from s_j by at most 823 u P_j (dropped cross terms
+// 3 * 2^-16 (1 + 2^-7), at most 33 fp32 roundings in the MFMA sums, 9 u in the fp32
+// norm), and a slot minimum that carries its slot number in its 4 lowest mantissa bits
+// moves by at most 30 u of its magnitude.  The entries of the slot with the smallest
+// minimum are rescored in the plain fp32 form: d* is their smallest distance, taken at
+// the lowest index; M2 is the smallest minimum of the other slots, so every entry j
+// outside the slot has a screened score >= M2.  With R = 2 |x| + (1 + 2^-9) sqrt(d*) +
+// 2^-61 and Q = R^2, such an entry either has |c_j| > R - |x|, and then lies farther
+// than (1 + 2^-9) sqrt(d*) from x, so that its fp32 distance (every term positive,
+// relative error <= 12 u) exceeds d*; or has P_j <= Q, and then its fp32 distance is at
+// least (1 - 12 u) (M2 + |x|^2 - 823 u Q), which exceeds d* once
+// M2 + |x|^2 - d* > 870 u Q (packing, the fp32 |x|^2, the distance's rounding and the
+// guard's own two roundings included).  The guard asks for more than
+// theta = 2^-14 Q' + 2^-100 with Q' = 1.03 (2 sqrt(fl |x|^2) + sqrt(d*) + 2^-60)^2 >= Q
+// (1024 u Q; the hardware square roots' errors sit far inside the factor 1.03, and
+// 2^-100 covers underflow).  A kernel that passes ends with the slot's fp32 argmin;
+// the others are rescored over the whole codebook in the exact fp32 form by their
+// wave.  The output is therefore the plain fp32 argmin, bit for bit.  Q' < 1e37 is also
+// asked for: every entry with P_j <= Q then has finite partial sums, while a screened
+// score of a farther entry may overflow to +inf or NaN, which the slot minima skip.
 //
 // Grid.  Kernels are cut into tiles of 256 (one per workgroup pass); tiles of all
 // layers of a stack are numbered layer after layer and a persistent grid of at most
@@ -51,7 +61,7 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRowFloats = 12;      // fp32 codebook rows in LDS: 9 values, padded to 48 bytes
 constexpr float kPadScore = 1e38f;  // score of padding entries: finite and above any trusted score
-constexpr float kTrustQ = 1e37f;    // Q at or above this: no screening result is trusted
+constexpr float kTrustQ = 1e37f;    // Q' at or above this: rescored over the whole codebook
 static_assert(kAssignChunk % 64 == 0, "chunks hold whole pairs of 32-entry tiles");
 
 // two fp32 values split exactly: v = h + m + l with h = bf16(v), m = bf16(v - h); H and M
@@ -194,7 +204,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     constexpr int kAssignChunk = FUSED ? kFuseChunk : ::kq::kAssignChunk;
     __shared__ u32x4 s_a[kAssignChunk / 32 * 2 * kWave];  // [tile][k-step][lane] A operands
     __shared__ f32x4 s_c[kAssignChunk * kRowFloats / 4];   // fp32 rows of the staged entries
-    __shared__ float s_wmax[kAssignWaves];                 // per-wave max |c|^2 of the staged codebook
     __shared__ unsigned long long s_sum[FUSED ? kFuseMaxK * kDim : 1];  // fused: member sums
     __shared__ unsigned s_cnt[FUSED ? kFuseMaxK : 1];                   // fused: member counts
 
@@ -211,7 +220,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     load_kernel(p.L[li], t - p.unit_begin[li], wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
     int hl = li;      // fused: the layer whose sums the histogram holds
-    float cnorm = 0.0f;  // square root of the largest |c|^2 of the staged layer's codebook
     if (FUSED) {
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
@@ -275,7 +283,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         int rj = 0x7fffffff;
         const int kpad = (k + 63) & ~63;
         const bool resident = kpad <= kAssignChunk;
-        float tmax = 0.0f;
 #pragma unroll 1
         for (int c0 = 0; c0 < kpad; c0 += kAssignChunk) {
             const int cn = min(kAssignChunk, kpad - c0);
@@ -294,7 +301,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                             w[d] = -2.0f * c[d];
                         }
                         w[9] = nn;
-                        tmax = fmaxf(tmax, nn);
                     } else {  // padding: screened far away, and never taken by the rescoring
 #pragma unroll
                         for (int d = 0; d < kDim; ++d) {
@@ -328,20 +334,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                     s_c[jl * 3 + 1] = r1;
                     s_c[jl * 3 + 2] = r2;
                 }
-                if (c0 + cn >= kpad) {  // last chunk: publish this wave's max norm
-                    float wm = tmax;
-#pragma unroll
-                    for (int off = 32; off >= 1; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
-                    if (lane == 0) s_wmax[wave] = wm;
-                }
                 __syncthreads();
                 staged = resident ? li : -1;
-                if (c0 + cn >= kpad) {  // the whole codebook has been seen: its largest norm
-                    float cm2 = s_wmax[0];
-#pragma unroll
-                    for (int w = 1; w < kAssignWaves; ++w) cm2 = fmaxf(cm2, s_wmax[w]);
-                    cnorm = __builtin_amdgcn_sqrtf(cm2);
-                }
             }
 
             // slot minima over the chunk (cn >= 64), two codebook tiles per step; the first
@@ -422,12 +416,13 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         float xn2 = 0.0f;
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xn2 = __fmaf_rn(xo[d], xo[d], xn2);
-        // Q only scales the guard, which has a 13 % margin: the hardware square root will do
-        const float rr = __builtin_amdgcn_sqrtf(xn2) + cnorm;
-        const float q2 = rr * rr;
-        const float theta = 0x1p-13f * q2 + 0x1p-100f;
+        // the local bound Q' from |x| and the rescored distance; the hardware square roots
+        // will do (their errors are far below the factor 1.03)
+        const float rr = 2.0f * __builtin_amdgcn_sqrtf(xn2) + __builtin_amdgcn_sqrtf(rd) + 0x1p-60f;
+        const float q2 = rr * rr * 1.03f;
+        const float theta = 0x1p-14f * q2 + 0x1p-100f;
 
-        const bool sure = valid && (q2 < kTrustQ) && (rs - rb > theta) && (rj < k);
+        const bool sure = valid && (q2 < kTrustQ) && (rs - (rd - xn2) > theta) && (rj < k);
         float dist = 0.0f;
         int myj = rj;  // the entry this lane's kernel ends with
         if (sure) {

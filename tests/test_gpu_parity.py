@@ -77,6 +77,34 @@ def test_assign_exact_ties_and_near_ties():
     check_assign(X, C, "midpoint")
 
 
+def test_assign_far_entries_and_mixed_scales():
+    """The guard's bound is local (|x| and the rescored distance): entries far from every
+    kernel, up to norms whose fp32 |c|^2 overflows, must neither be chosen nor hide a
+    nearer entry, and kernels of very different scales (zero, 1e-25, 1e-6, 1) share one
+    codebook.  Bit for bit the oracle's plain fp32 argmin."""
+    rng = np.random.default_rng(77)
+    base = rng.laplace(0, 0.02, (256, 9)).astype(np.float32)
+    far = np.zeros((12, 9), np.float32)
+    for r, mag in enumerate([1e3, -1e6, 1e12, -1e15, 1e18, 3e18, -1e19, 2e19, 3e19, 1e30, -1e35, 3e38]):
+        far[r] = mag * np.sign(rng.standard_normal(9)).astype(np.float32)
+    far[5, 4] = 0.0  # mixed zero and huge coordinates
+    C = np.concatenate([base[:100], far[:6], base[100:], far[6:]])
+    X = rng.laplace(0, 0.02, (6000, 9)).astype(np.float32)
+    X[:500] *= np.float32(1e-6)
+    X[500:700] *= np.float32(1e-25)
+    X[700:800] = 0.0
+    X[800:1000] *= np.float32(50.0)
+    X[1000:1064] = C[rng.integers(0, C.shape[0] - 12, 64)]  # exact hits
+    check_assign(X, C, "far entries, mixed scales")
+    # the same kernels against a codebook scaled down to the tiny kernels' range
+    Ct = (base * np.float32(1e-6)).astype(np.float32)
+    check_assign(X, Ct, "codebook at 1e-6")
+    # large kernels (|x|^2 near 1e36) against far entries: Q' passes 1e37 for some
+    Xl = (rng.standard_normal((3000, 9)) * 2e17).astype(np.float32)
+    Cl = np.concatenate([(rng.standard_normal((200, 9)) * 2e17).astype(np.float32), far])
+    check_assign(Xl, Cl, "large kernels")
+
+
 def test_assign_nonfinite_inputs_match_plain_scan():
     X = synth.normal_layer(8, 8, 5)
     X[3, 2] = np.nan

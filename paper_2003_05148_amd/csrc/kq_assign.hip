@@ -499,10 +499,10 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         }
 
         if (FUSED && valid) {  // the update's exact member sums of this kernel, at the layer's shift
-            const int sh = (int)L.xmax[L.nxmax];
+            const double sc = fixed_scale((int)L.xmax[L.nxmax]);
             atomicAdd(&s_cnt[myj], 1u);
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_point(xo[d], sh));
+            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_bits(xo[d], sc));
         }
 
         if (L.part) {

@@ -72,30 +72,29 @@ inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
 
 // Fixed-point scale of the exact member sums.  A layer's sums use q(x) = rint(x * 2^s) with
-//     s = 62 - ceil(log2 n) - e,   e the smallest integer with max |x| < 2^e (-126 when the
-//                                  largest magnitude is subnormal, 62 - ceil(log2 n) for an
+//     s = min(62 - ceil(log2 n), 51) - e,   e the smallest integer with max |x| < 2^e (-126
+//                                  when the largest magnitude is subnormal, 0 for an
 //                                  all-zero layer),
-// so |q| <= 2^(62 - ceil(log2 n)) and no sum over at most n values can leave int64, while the
-// resolution stays 2^-(62 - ceil(log2 n)) of the layer's largest magnitude whatever that
-// magnitude is.  base_shift(n) = 57 - ceil(log2 n) is s for 16 <= max |x| < 32; the device
-// derives s from it and the layer's maxima of |x| (the same rule serves the gradient sums
-// of Eq. 2).
+// so |q| < 2^51 and |q| <= 2^(62 - ceil(log2 n)): no sum over at most n values can leave
+// int64, while the resolution stays 2^-min(62 - ceil(log2 n), 51) of the layer's largest
+// magnitude whatever that magnitude is.  base_shift(n) = min(57 - ceil(log2 n), 46) is s for
+// 16 <= max |x| < 32; the device derives s from it and the layer's maxima of |x| (the same
+// rule serves the gradient sums of Eq. 2).
 inline int base_shift(int64_t n) {
     int c = 0;
     while ((int64_t(1) << c) < n) ++c;
-    return 57 - c;
+    return 57 - c < 46 ? 57 - c : 46;
 }
 
-// q(x) = rint(x * 2^s) as a 64-bit integer.  x * 2^s is one exact v_ldexp_f32 (a power-of-two
-// scaling that stays below 2^62 in magnitude by the choice of s) and so is its rounding to an
-// integer v; v = hi * 2^32 + lo with hi = floor(v * 2^-32) (|hi| <= 2^30) and 0 <= lo < 2^32,
-// where lo = v - hi * 2^32 has fewer significant bits than v and is exact in fp32 too, so both
-// convert exactly.
-__device__ __forceinline__ unsigned long long fixed_point(float x, int shift) {
-    const float v = __builtin_rintf(__builtin_ldexpf(x, shift));
-    const float hi = __builtin_floorf(v * 0x1p-32f);
-    const float lo = __builtin_fmaf(hi, -0x1p32f, v);
-    return ((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo;
+// q(x) travels in the low bits of a double: fma(x, 2^s, 1.5 * 2^52) rounds x * 2^s to an
+// integer (ties to even, as rint) inside the binade [2^52, 2^53), where doubles are one
+// apart, so its bit pattern is kFixedBias + q(x) for |q| < 2^51.  Sums of these patterns
+// in wrapping 64-bit integer arithmetic, less count * kFixedBias, are the exact sums of q.
+// Two full-rate instructions per value (a conversion and an fma in fp64).
+constexpr unsigned long long kFixedBias = 0x4338000000000000ull;  // the bits of 1.5 * 2^52
+__device__ __forceinline__ double fixed_scale(int shift) { return __builtin_ldexp(1.0, shift); }
+__device__ __forceinline__ unsigned long long fixed_bits(float x, double scale) {
+    return __builtin_bit_cast(unsigned long long, __builtin_fma((double)x, scale, 0x1.8p52));
 }
 
 // ---- fused assignment + member sums ------------------------------------------------------

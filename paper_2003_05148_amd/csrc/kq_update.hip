@@ -2,8 +2,10 @@
 // becomes the mean of its kernel set S_j; an empty set keeps its entry.
 //
 // The member sums are exact integers: each value is mapped to q(x) = rint(x * 2^s) with a
-// per-layer shift s = 62 - ceil(log2 n) - e, max |x| < 2^e, so |q| <= 2^62 / n and
-// no sum over at most n kernels can overflow int64, at any magnitude of the weights.
+// per-layer shift s = min(62 - ceil(log2 n), 51) - e, max |x| < 2^e, so |q| <= 2^62 / n
+// and no sum over at most n kernels can overflow int64, at any magnitude of the weights
+// (each q is added as kFixedBias + q, the bit pattern of one fp64 fma, and the finish
+// takes count * kFixedBias back off).
 // Integer addition is associative, so the sums, and with them the new codebook, do not
 // depend on the order in which blocks or lanes add.  absmax_kernel takes the maxima of |x|
 // per block of 8192 values and shift_kernel turns them into each layer's s (and flags
@@ -47,7 +49,7 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
 }
 
 // the layer's shift from its largest magnitude (fp32 bits, sign cleared):
-// s = base + 5 - e with max < 2^e, where base = 57 - ceil(log2 n) (e = -126 for a subnormal
+// s = base + 5 - e with max < 2^e, where base = min(57 - ceil(log2 n), 46) (e = -126 for a subnormal
 // maximum, e = 0 for an all-zero layer; a non-finite maximum gives e >= 129 and a shift
 // that keeps the sums finite but meaningless, which KQ_F_VALIDATE reports)
 __device__ __forceinline__ int layer_shift(unsigned maxbits, int base) {
@@ -60,7 +62,7 @@ struct UpdateCtx {
     unsigned long long* s_sum;  // [krange][9]
     unsigned* s_cnt;            // [krange]
     const float* C_old;
-    int shift;                  // s of q(x) = rint(x * 2^s)
+    double scale;               // 2^s of q(x) = rint(x * 2^s)
     int j0, kr;                 // the entry range [j0, j0 + kr)
     bool sums, want_dist;
 };
@@ -73,7 +75,7 @@ __device__ __forceinline__ void add_kernel(const UpdateCtx& c, const float (&x)[
     atomicAdd(&c.s_cnt[jr], 1u);
     if (c.sums) {
 #pragma unroll
-        for (int d = 0; d < kDim; ++d) atomicAdd(&c.s_sum[jr * kDim + d], fixed_point(x[d], c.shift));
+        for (int d = 0; d < kDim; ++d) atomicAdd(&c.s_sum[jr * kDim + d], fixed_bits(x[d], c.scale));
     }
 }
 
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
     c.sums = (L.flags & kFlagCountsOnly) == 0;
-    c.shift = c.sums ? (int)L.xmax[L.nxmax] : 0;  // set by shift_kernel before this launch
+    c.scale = fixed_scale(c.sums ? (int)L.xmax[L.nxmax] : 0);  // set by shift_kernel before this launch
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;
 
@@ -168,7 +170,7 @@ constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
 
 __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const StackParams p) {
-    __shared__ long long s_S[kFinishGroups][kFinishEntries * 10];
+    __shared__ unsigned long long s_S[kFinishGroups][kFinishEntries * 10];
     __shared__ double s_w[kSumThreads / kWave];
     const int b = blockIdx.x;
     if (b >= p.total_units) {  // the last nlayers workgroups: the distortion of layer b - total
@@ -208,22 +210,23 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
             for (int r = 0; r < kFinishBatch; ++r) s += v[r];
         }
     }
-    s_S[g][v] = (long long)s;
+    s_S[g][v] = s;
     __syncthreads();
     if (g == 0 && j < k) {
-        long long S = 0, z = 0;
+        unsigned long long S = 0, z = 0;  // wrapping sums
 #pragma unroll
         for (int q = 0; q < kFinishGroups; ++q) {
             S += s_S[q][v];
             z += s_S[q][(v / 10) * 10 + 9];
         }
+        S -= z * kFixedBias;  // the exact sum of q(x) over the entry's kernels
         if (d == 9) {
             if (L.counts) L.counts[j] = (int32_t)z;
         } else if ((L.flags & kFlagCountsOnly) == 0) {
             const float old = L.C_old[(size_t)j * kDim + d];
             float c = old;
             if (z > 0) {
-                const double mean = ((double)S * ldexp(1.0, -(int)L.xmax[L.nxmax])) / (double)z;
+                const double mean = ((double)(long long)S * ldexp(1.0, -(int)L.xmax[L.nxmax])) / (double)z;
                 // Eq. (2): c - gamma * mean gradient; Eq. (1): the mean of the kernels
                 c = (L.flags & kFlagGrad) ? (float)((double)old - (double)L.gamma * mean) : (float)mean;
             }

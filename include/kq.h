@@ -564,7 +564,7 @@ kq_status kq_forgy_select(const float* X, int64_t n, int32_t dim, int32_t k, uin
  * (hipGetSymbolAddress, on the first call with that device current).  The call allocates
  * nothing.  The stream must belong to the current device.
  *   Sizes whose kq_workspace_bytes(KQ_OP_FIT, n, k, 9) exceeds the scratch (for k = 256, n
- *   above 418,560 kernels) return KQ_ERR_WORKSPACE, before anything is enqueued.
+ *   above 1,666,048 kernels) return KQ_ERR_WORKSPACE, before anything is enqueued.
  *   All calls on one GPU share that GPU's scratch: calls that overlap on one device (two
  *   streams, two host threads) race and give unspecified results; order them on one stream.
  *   Nothing in the scratch needs to start at zero (every call writes what it reads).

@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <unordered_map>
 #include <unordered_set>
@@ -73,12 +74,12 @@ void stack_params(StackParams& p, const kq_layer* layers, int32_t l0, int32_t l1
         if (op == Op::Assign) {
             d.best_d = s.best_d;
             d.part = base ? (double*)w : nullptr;  // partials whenever there is a workspace
-            d.nunits = assign_tiles(s.n);
+            d.nunits = assign_units(s.n);
         } else {
             d.counts = s.counts;
             if (d.dist && from_assign) {
                 d.apart = (const double*)w;
-                d.napart = assign_tiles(s.n) * kAssignWaves;
+                d.napart = assign_units(s.n);
             } else if (d.dist) {
                 d.part = (double*)(w + ws_assign_part(s.n));
             }
@@ -145,16 +146,16 @@ bool fusable(const kq_layer* layers, int32_t l0, int32_t l1) {
 }
 
 // The fused assignment's partials: with the persistent grid of the assignment launch over
-// layers [l0, l1), workgroup w walks tiles [w T / G, (w + 1) T / G); a layer's partials
-// are those of the workgroups whose runs touch its tiles.  For every layer: the first such
+// layers [l0, l1), workgroup w walks units [w T / G, (w + 1) T / G); a layer's partials
+// are those of the workgroups whose runs touch its units.  For every layer: the first such
 // workgroup and their number.
 void fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, int* nslots) {
     long long T = 0;
-    for (int32_t l = l0; l < l1; ++l) T += assign_tiles(layers[l].n);
+    for (int32_t l = l0; l < l1; ++l) T += assign_units(layers[l].n);
     const long long G = assign_grid((int)T);
     long long b = 0;
     for (int32_t l = l0; l < l1; ++l) {
-        const long long e = b + assign_tiles(layers[l].n);  // tiles [b, e)
+        const long long e = b + assign_units(layers[l].n);  // units [b, e)
         long long w0 = b * G / T;                           // a first guess, then exact
         while (w0 > 0 && w0 * T / G > b) --w0;
         while ((w0 + 1) * T / G <= b) ++w0;
@@ -348,7 +349,7 @@ YyParams yy_params(unsigned char* ws, const YyLayout& L, const float* X, int64_t
     p.n = (int)n;
     p.k = k;
     p.t = t;
-    p.npart = assign_tiles(n) * kAssignWaves;
+    p.npart = assign_units(n);
     return p;
 }
 
@@ -378,7 +379,7 @@ kq_status yy_distortion(const YyParams& p, double* distortion, hipStream_t s) {
     q.nlayers = 1;
     q.L[0].part = p.part;
     q.L[0].dist = distortion;
-    q.L[0].nunits = assign_tiles(p.n);
+    q.L[0].nunits = assign_units(p.n);
     set_unit_table(q);
     return hip_status(launch_assign_finish(q, s));
 }
@@ -562,11 +563,12 @@ kq_status kq_quantize_scalars(const float* v, int64_t count, int32_t bits, int32
 }
 
 // a fit workspace large enough for every codebook size up to kmax (the per-layer layout
-// is not monotone in k: small codebooks keep one fused partial per assignment tile)
+// is not monotone in k: small codebooks keep one fused partial per assignment workgroup)
 size_t fit_ws_upto(int64_t n, int32_t kmax) {
     const size_t c1024 = (size_t)((n + 1023) / 1024);
     return ws_assign_part(n) + align256(sizeof(double) * (size_t)update_ranges(kmax) * c1024) +
-           align256(sizeof(int64_t) * 10 * (size_t)kmax * (size_t)assign_tiles(n)) + ws_xmax(n);
+           align256(sizeof(int64_t) * 10 * (size_t)kmax * (size_t)std::max<int64_t>(fused_parts(n), (n + kUpdateMinKernelsPerBlock - 1) / kUpdateMinKernelsPerBlock)) +
+           ws_xmax(n);
 }
 
 size_t kq_search_workspace_bytes(int64_t n, int32_t n_init, int32_t lloyd_iters) {

@@ -155,9 +155,9 @@ __device__ __forceinline__ void lds_a(u32x4 (&a)[2][2], const u32x4* s_a, int p,
         for (int kk = 0; kk < 2; ++kk) a[t][kk] = s_a[((2 * p + t) * 2 + kk) * kWave + lane];
 }
 
-// this lane's kernel (kernel 256 t + 64 wave + lane of the layer); a valid row past the end
-__device__ __forceinline__ void load_kernel(const DevLayer& L, int tile, int wave, int lane, float (&x)[kDim]) {
-    const int i = tile * kAssignKernelsPerTile + wave * kWave + lane;
+// this lane's kernel of unit u of the layer (kernel 64 u + lane); a valid row past the end
+__device__ __forceinline__ void load_kernel(const DevLayer& L, int u, int lane, float (&x)[kDim]) {
+    const int i = u * kWave + lane;
     const int ic = i < L.n ? i : L.n - 1;
 #pragma unroll
     for (int d = 0; d < kDim; ++d) x[d] = L.X[(size_t)ic * kDim + d];
@@ -177,7 +177,7 @@ __device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d,
 
 // Fused variant (every codebook of at most kFuseMaxK entries): each lane also adds its
 // settled kernel to the workgroup's LDS histogram of exact fixed-point member sums, which
-// is stored as the partial of (layer, workgroup) whenever the workgroup's run of tiles
+// is stored as the partial of (layer, workgroup) whenever the workgroup's run of units
 // leaves a layer; the update then needs only its finishing launch.
 template <int CHUNK, bool FUSED>
 __device__ __forceinline__ void fused_flush(const StackParams& p, int l, unsigned long long* s_sum, unsigned* s_cnt,
@@ -199,7 +199,7 @@ __device__ __forceinline__ void fused_flush(const StackParams& p, int l, unsigne
 }
 
 template <int R, bool FUSED>
-__global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kernel(const StackParams p) {
+__global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const StackParams p) {
     static_assert(R == 2, "one kernel per lane and the half exchange need two kernel tiles per wave");
     constexpr int kAssignChunk = FUSED ? kFuseChunk : ::kq::kAssignChunk;
     __shared__ u32x4 s_a[kAssignChunk / 32 * 2 * kWave];  // [tile][k-step][lane] A operands
@@ -210,14 +210,23 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const long long T = p.total_units;
-    int t = (int)((long long)blockIdx.x * T / gridDim.x);
-    const int t_end = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);
-    if (t >= t_end) return;
+    const int u_end = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);
+    int ub = (int)((long long)blockIdx.x * T / gridDim.x);
+    if (ub >= u_end) return;
 
-    int li = find_layer(p, t);
+    // Rounds: up to kAssignWaves consecutive units of one layer, unit ub + wave for each wave
+    // (a wave past the round's end idles, but takes part in every barrier).  [ub, r_end) is
+    // the round, li its layer.
+    auto round_end = [&](int u0, int l) {
+        const int le = l + 1 < KQ_MAX_STACK ? p.unit_begin[l + 1] : 0x7fffffff;
+        return min(min(u0 + kAssignWaves, u_end), le);
+    };
+    int li = find_layer(p, ub);
+    int r_end = round_end(ub, li);
+    bool active = ub + wave < r_end;
     int staged = -1;  // layer whose whole codebook is resident in LDS
-    float xo[kDim];   // this lane's kernel of the current tile
-    load_kernel(p.L[li], t - p.unit_begin[li], wave, lane, xo);
+    float xo[kDim];   // this lane's kernel of the current round
+    load_kernel(p.L[li], ub + wave - p.unit_begin[li], lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
     int hl = li;      // fused: the layer whose sums the histogram holds
     if (FUSED) {
@@ -227,8 +236,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
     }
 
 #pragma unroll 1
-    for (; t < t_end; ++t) {
-        while (li + 1 < p.nlayers && t >= p.unit_begin[li + 1]) ++li;
+    while (ub < u_end) {
         if (FUSED && li != hl) {  // the run left layer hl: store its sums
             fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
             hl = li;
@@ -236,19 +244,25 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
         const DevLayer& L = p.L[li];
         const int n = L.n, k = L.k;
         const float* __restrict__ C = L.C;
-        const int lt = t - L.unit_begin;
-        const int i = lt * kAssignKernelsPerTile + wave * kWave + lane;
-        const bool valid = i < n;
+        const int lu = ub + wave - L.unit_begin;  // this wave's unit of the layer
+        const int i = lu * kWave + lane;
+        const bool valid = active && i < n;
 
-        // prefetch the next tile's kernel; it arrives while this tile is scored
+        // the next round; its kernel is prefetched while this one is scored
+        const int u2 = r_end;
+        int l2 = li;
+        while (l2 + 1 < p.nlayers && u2 >= p.unit_begin[l2 + 1]) ++l2;
+        const int r2 = u2 < u_end ? round_end(u2, l2) : u_end;
+        const bool active2 = u2 + wave < r2;
         float xn[kDim];
-        if (t + 1 < t_end) {
-            int ln = li;
-            while (ln + 1 < p.nlayers && t + 1 >= p.unit_begin[ln + 1]) ++ln;
-            load_kernel(p.L[ln], t + 1 - p.unit_begin[ln], wave, lane, xn);
+        if (active2) {
+            load_kernel(p.L[l2], u2 + wave - p.unit_begin[l2], lane, xn);
+        } else {
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) xn[d] = 0.0f;
         }
 
-        // B operands.  Kernel tile r of this wave is kernels 64 wave + 32 r + (lane % 32), the
+        // B operands.  Kernel tile r of this wave is kernels 64 lu + 32 r + (lane % 32), the
         // kernels of lanes 32 r .. 32 r + 31.  A lane past the end holds a copy of the last
         // kernel and its results are dropped.  Lane (col, half) needs, for k-step kk, dwords
         // 8 kk + 4 half .. + 3 of the column's kernel; dword e packs terms 2e, 2e + 1:
@@ -338,6 +352,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
                 staged = resident ? li : -1;
             }
 
+            if (!active) continue;  // an idle wave only helps to stage
+
             // slot minima over the chunk (cn >= 64), two codebook tiles per step; the first
             // pair starts them, capped at the largest finite float so that packing keeps a number
             float best[R][16];
@@ -412,106 +428,111 @@ __global__ __launch_bounds__(kAssignWaves * kWave, kAssignOcc) void assign_kerne
             const int bj = bt < 0 ? 0x7fffffff : c0 + slot + 32 * bt;
             merge_top2(rb, rs, rj, rd, M1, M2, bj, bd);
         }
-
-        float xn2 = 0.0f;
+        if (active) {  // settle this wave's unit
+            float xn2 = 0.0f;
 #pragma unroll
-        for (int d = 0; d < kDim; ++d) xn2 = __fmaf_rn(xo[d], xo[d], xn2);
-        // the local bound Q' from |x| and the rescored distance; the hardware square roots
-        // will do (their errors are far below the factor 1.03)
-        const float rr = 2.0f * __builtin_amdgcn_sqrtf(xn2) + __builtin_amdgcn_sqrtf(rd) + 0x1p-60f;
-        const float q2 = rr * rr * 1.03f;
-        const float theta = 0x1p-14f * q2 + 0x1p-100f;
+            for (int d = 0; d < kDim; ++d) xn2 = __fmaf_rn(xo[d], xo[d], xn2);
+            // the local bound Q' from |x| and the rescored distance; the hardware square roots
+            // will do (their errors are far below the factor 1.03)
+            const float rr = 2.0f * __builtin_amdgcn_sqrtf(xn2) + __builtin_amdgcn_sqrtf(rd) + 0x1p-60f;
+            const float q2 = rr * rr * 1.03f;
+            const float theta = 0x1p-14f * q2 + 0x1p-100f;
 
-        const bool sure = valid && (q2 < kTrustQ) && (rs - (rd - xn2) > theta) && (rj < k);
-        float dist = 0.0f;
-        int myj = rj;  // the entry this lane's kernel ends with
-        if (sure) {
-            dist = rd;
-            L.idx[i] = rj;
-            if (L.best_d) L.best_d[i] = rd;
-        }
+            const bool sure = valid && (q2 < kTrustQ) && (rs - (rd - xn2) > theta) && (rj < k);
+            float dist = 0.0f;
+            int myj = rj;  // the entry this lane's kernel ends with
+            if (sure) {
+                dist = rd;
+                L.idx[i] = rj;
+                if (L.best_d) L.best_d[i] = rd;
+            }
 
-        // exact fp32 rescoring of the kernels the guard could not settle, one at a time
-        unsigned long long fl = __ballot(valid && !sure);
-        while (fl) {
-            const int f = __ffsll((long long)fl) - 1;
-            fl &= fl - 1;
-            float xf[kDim];  // lane f's kernel, the same in every lane (f is uniform)
+            // exact fp32 rescoring of the kernels the guard could not settle, one at a time
+            unsigned long long fl = __ballot(valid && !sure);
+            while (fl) {
+                const int f = __ffsll((long long)fl) - 1;
+                fl &= fl - 1;
+                float xf[kDim];  // lane f's kernel, the same in every lane (f is uniform)
 #pragma unroll
-            for (int d = 0; d < kDim; ++d)
-                xf[d] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xo[d]), f));
-            // each lane scans entries lane, lane + 64, ... in increasing order (strict <: the
-            // lowest index among equal distances), then the lanes' (distance, index) pairs
-            // meet in their lexicographic minimum
-            float fd = __builtin_inff();
-            int fj = 0x7fffffff;
-            if (resident) {  // the rows are still staged in LDS: four per lane in flight
-                constexpr int kU = 4;
-                for (int j0 = lane; j0 < k; j0 += kU * kWave) {
-                    f32x4 r0[kU], r1[kU];
-                    float c8[kU];
+                for (int d = 0; d < kDim; ++d)
+                    xf[d] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xo[d]), f));
+                // each lane scans entries lane, lane + 64, ... in increasing order (strict <: the
+                // lowest index among equal distances), then the lanes' (distance, index) pairs
+                // meet in their lexicographic minimum
+                float fd = __builtin_inff();
+                int fj = 0x7fffffff;
+                if (resident) {  // the rows are still staged in LDS: four per lane in flight
+                    constexpr int kU = 4;
+                    for (int j0 = lane; j0 < k; j0 += kU * kWave) {
+                        f32x4 r0[kU], r1[kU];
+                        float c8[kU];
 #pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        const int jj = min(j0 + u * kWave, k - 1);  // a staged row past the end
-                        r0[u] = s_c[jj * 3 + 0];
-                        r1[u] = s_c[jj * 3 + 1];
-                        c8[u] = s_cf[jj * kRowFloats + 8];
+                        for (int u = 0; u < kU; ++u) {
+                            const int jj = min(j0 + u * kWave, k - 1);  // a staged row past the end
+                            r0[u] = s_c[jj * 3 + 0];
+                            r1[u] = s_c[jj * 3 + 1];
+                            c8[u] = s_cf[jj * kRowFloats + 8];
+                        }
+#pragma unroll
+                        for (int u = 0; u < kU; ++u) {
+                            const int jj = j0 + u * kWave;
+                            const float c[kDim] = {r0[u][0], r0[u][1], r0[u][2], r0[u][3], r1[u][0],
+                                                   r1[u][1], r1[u][2], r1[u][3], c8[u]};
+                            const float d = sqdist9(xf, c);
+                            const bool take = jj < k && d < fd;
+                            fj = take ? jj : fj;
+                            fd = take ? d : fd;
+                        }
                     }
+                } else {  // rows from memory: four per lane in flight, taken in index order
+                    constexpr int kU = 4;
+                    for (int j0 = lane; j0 < k; j0 += kU * kWave) {
+                        float c[kU][kDim];
 #pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        const int jj = j0 + u * kWave;
-                        const float c[kDim] = {r0[u][0], r0[u][1], r0[u][2], r0[u][3], r1[u][0],
-                                               r1[u][1], r1[u][2], r1[u][3], c8[u]};
-                        const float d = sqdist9(xf, c);
-                        const bool take = jj < k && d < fd;
-                        fj = take ? jj : fj;
-                        fd = take ? d : fd;
+                        for (int u = 0; u < kU; ++u) {
+                            const int jj = min(j0 + u * kWave, k - 1);  // a valid row past the end
+#pragma unroll
+                            for (int d = 0; d < kDim; ++d) c[u][d] = C[(size_t)jj * kDim + d];
+                        }
+#pragma unroll
+                        for (int u = 0; u < kU; ++u) {
+                            const int jj = j0 + u * kWave;
+                            const float d = sqdist9(xf, c[u]);
+                            const bool take = jj < k && d < fd;
+                            fj = take ? jj : fj;
+                            fd = take ? d : fd;
+                        }
                     }
                 }
-            } else {  // rows from memory: four per lane in flight, taken in index order
-                constexpr int kU = 4;
-                for (int j0 = lane; j0 < k; j0 += kU * kWave) {
-                    float c[kU][kDim];
-#pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        const int jj = min(j0 + u * kWave, k - 1);  // a valid row past the end
-#pragma unroll
-                        for (int d = 0; d < kDim; ++d) c[u][d] = C[(size_t)jj * kDim + d];
-                    }
-#pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        const int jj = j0 + u * kWave;
-                        const float d = sqdist9(xf, c[u]);
-                        const bool take = jj < k && d < fd;
-                        fj = take ? jj : fj;
-                        fd = take ? d : fd;
-                    }
+                wave_argmin(fd, fj);
+                if (lane == f) {
+                    if (fj == 0x7fffffff) fj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
+                    L.idx[i] = fj;
+                    if (L.best_d) L.best_d[i] = fd;
+                    dist = fd;
+                    myj = fj;
                 }
             }
-            wave_argmin(fd, fj);
-            if (lane == f) {
-                if (fj == 0x7fffffff) fj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
-                L.idx[i] = fj;
-                if (L.best_d) L.best_d[i] = fd;
-                dist = fd;
-                myj = fj;
-            }
-        }
 
-        if (FUSED && valid) {  // the update's exact member sums of this kernel, at the layer's shift
-            const double sc = fixed_scale((int)L.xmax[L.nxmax]);
-            atomicAdd(&s_cnt[myj], 1u);
+            if (FUSED && valid) {  // the update's exact member sums of this kernel, at the layer's shift
+                const double sc = fixed_scale((int)L.xmax[L.nxmax]);
+                atomicAdd(&s_cnt[myj], 1u);
 #pragma unroll
-            for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_bits(xo[d], sc));
-        }
+                for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_bits(xo[d], sc));
+            }
 
-        if (L.part) {
-            const double v = wave_sum_f64(valid ? (double)dist : 0.0);
-            if (lane == 0) L.part[lt * kAssignWaves + wave] = v;
+            if (L.part) {
+                const double v = wave_sum_f64(valid ? (double)dist : 0.0);
+                if (lane == 0) L.part[lu] = v;
+            }
         }
 
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xo[d] = xn[d];
+        ub = u2;
+        li = l2;
+        r_end = r2;
+        active = active2;
     }
     if (FUSED) fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
 }
@@ -521,7 +542,7 @@ __global__ __launch_bounds__(kSumThreads) void assign_finish_kernel(const StackP
     __shared__ double s_w[kSumThreads / kWave];
     const DevLayer& L = p.L[blockIdx.x];
     if (L.dist == nullptr) return;
-    const double v = block_fixed_sum<kSumThreads>(L.part, L.nunits * kAssignWaves, s_w);
+    const double v = block_fixed_sum<kSumThreads>(L.part, L.nunits, s_w);
     if (threadIdx.x == 0) *L.dist = v;
 }
 

@@ -15,18 +15,16 @@ constexpr int kDim = 9;
 constexpr int kWave = 64;
 
 // ---- assignment kernel geometry -----------------------------------------------------
-// A workgroup is 4 waves; each wave scores kAssignTilesPerWave tiles of 32 kernels
-// against 32-entry codebook tiles with v_mfma_f32_32x32x16_bf16 (an exact bf16 split of
-// the K = 10 fp32 contraction, 9 dims + norm, into three cross terms).
-// A "tile" of the grid is the 256 kernels one workgroup scores at a time; the grid is
-// persistent (at most kAssignGridMax workgroups, each walking a contiguous run of tiles).
-constexpr int kAssignWaves = 4;
+// A wave scores kAssignTilesPerWave tiles of 32 kernels (a "unit" of 64 kernels, one per
+// lane) against 32-entry codebook tiles with v_mfma_f32_32x32x16_bf16 (an exact bf16 split
+// of the K = 10 fp32 contraction, 9 dims + norm, into three cross terms).  The grid is
+// persistent: one workgroup of kAssignWaves waves per CU (three per SIMD), each walking a
+// contiguous run of the stack's units, one unit per wave at a time.
+constexpr int kAssignWaves = 12;
 constexpr int kAssignTilesPerWave = 2;
-constexpr int kAssignKernelsPerTile = kAssignWaves * kAssignTilesPerWave * 32;   // 256
-constexpr int kAssignOcc = 3;  // workgroups resident per CU
 // codebook entries staged in LDS at a time (64 B of operands + 48 B of fp32 row each)
 constexpr int kAssignChunk = 384;
-constexpr int kAssignGridMax = 256 * kAssignOcc;  // the persistent grid: every CU full
+constexpr int kAssignGridMax = 256;  // the persistent grid: one workgroup per CU
 
 // ---- update kernel geometry ---------------------------------------------------------
 // One launch updates every layer of a stack.  A layer's kernels are cut into chunks and
@@ -68,7 +66,10 @@ inline int update_chunk(int64_t n, int32_t k, int kpb) {
 constexpr int kSqThreads = 256;
 constexpr int kSqPerBlock = 8192;
 
-inline int assign_tiles(int64_t n) { return (int)((n + kAssignKernelsPerTile - 1) / kAssignKernelsPerTile); }
+// units of 64 kernels of a layer (one wave's work at a time; one distortion partial each)
+inline int assign_units(int64_t n) { return (int)((n + kWave - 1) / kWave); }
+// fused partials of a layer: one per workgroup whose run touches it, at most one per unit
+inline int fused_parts(int64_t n) { return assign_units(n) < kAssignGridMax ? assign_units(n) : kAssignGridMax; }
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
 
 // Fixed-point scale of the exact member sums.  A layer's sums use q(x) = rint(x * 2^s) with
@@ -101,24 +102,24 @@ __device__ __forceinline__ unsigned long long fixed_bits(float x, double scale) 
 // With every codebook of at most kFuseMaxK entries, the assignment kernel can also add each
 // settled kernel to a per-workgroup LDS histogram of exact member sums (the update's
 // fixed-point sums) and store it per (layer, workgroup) as a partial, so the update needs
-// only its finishing launch.  A layer's partials are those of the workgroups whose tile
-// runs touch it: at most one per tile.
+// only its finishing launch.  A layer's partials are those of the workgroups whose unit
+// runs touch it (fused_parts(n) at most).
 constexpr int kFuseMaxK = 256;
 constexpr int kFuseChunk = 256;  // codebook entries staged at a time by the fused variant
 
 // ---- per-layer workspace ---------------------------------------------------------------
-//   assign distortion partials : fp64 [assign_tiles(n) * kAssignWaves]           (overwritten each call)
+//   assign distortion partials : fp64 [assign_units(n)]                          (overwritten each call)
 //   update distortion partials : fp64 [ranges * max chunks]                      (overwritten each call)
 //   update histograms          : int64 [max chunks][k][10] per-chunk partial sums (overwritten each call)
 //   magnitudes                 : u32 [absmax_blocks(n) + 1 + KQ_MAX_STACK] (below)
 inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
-inline size_t ws_assign_part(int64_t n) { return align256(sizeof(double) * (size_t)assign_tiles(n) * kAssignWaves); }
+inline size_t ws_assign_part(int64_t n) { return align256(sizeof(double) * (size_t)assign_units(n)); }
 inline size_t ws_update_part(int64_t n, int32_t k) {
     return align256(sizeof(double) * (size_t)update_ranges(k) * (size_t)update_max_chunks(n, k));
 }
 inline size_t ws_hist(int64_t n, int32_t k) {
     size_t parts = (size_t)update_max_chunks(n, k);
-    if (k <= kFuseMaxK && (size_t)assign_tiles(n) > parts) parts = (size_t)assign_tiles(n);  // fused partials
+    if (k <= kFuseMaxK && (size_t)fused_parts(n) > parts) parts = (size_t)fused_parts(n);  // fused partials
     return align256(sizeof(int64_t) * 10 * (size_t)k * parts);
 }
 // Largest magnitudes of the values whose fixed-point sums a call forms (the kernels, or the
@@ -149,7 +150,7 @@ struct DevLayer {
     int n;
     int k;
     int unit_begin;           // first tile (assign) or workgroup (update) of this layer
-    int nunits;               // tiles or workgroups of this layer
+    int nunits;               // units or workgroups of this layer
     int shift;                // base_shift(n); the device turns it into the layer's fixed-point shift
     int flags;                // kFlag*
     int napart;               // number of assignment partials

@@ -44,7 +44,7 @@ def test_noalloc_fit_equals_workspace_fit_twice_then_smaller():
 
 def test_noalloc_refuses_sizes_beyond_the_scratch():
     assert kq.lib.kq_fit_layer_noalloc_max_bytes() == 32 << 20
-    n = 418561                                                   # one kernel past the limit at k = 256
+    n = 1666049                                                  # one kernel past the limit at k = 256
     assert kq.lib.kq_workspace_bytes(kq.KQ_OP_FIT, n, 256, 9) > kq.lib.kq_fit_layer_noalloc_max_bytes()
     assert kq.lib.kq_workspace_bytes(kq.KQ_OP_FIT, n - 1, 256, 9) <= kq.lib.kq_fit_layer_noalloc_max_bytes()
     X = torch.zeros(n, 9, device=DEV)

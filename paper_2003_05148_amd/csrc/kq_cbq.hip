@@ -279,6 +279,246 @@ __device__ __forceinline__ int code_from_thresholds(float x, const float* s_thr,
     return 8 * c + (f4 ? 4 : 0) + (f2 ? 2 : 0) + (f1 ? 1 : 0);
 }
 
+// ---- codebooks of at most kCbqFastMax scalars whose values all meet the exactness condition
+// (finite, no nonzero magnitude below 2^(e(M) - 29), M the largest magnitude): the rounds
+// in integers.  Every value is then a multiple of 2^-S with S = 52 - e(M) (149 when M is
+// subnormal), so w v 2^S is an integer below 2^84 in magnitude, held as a 2^42 + b with
+// 0 <= b < 2^42; a level keeps the sums A of the a and B of the b of its members (below
+// 2^54 for 4096 scalars) and W of their weights in three 64-bit LDS accumulators.  Its new
+// value is the exact integer A 2^42 + B rounded once to fp64, times 2^-S, over W in fp64,
+// rounded to fp32: the value the digit sums give, bit for bit.  When a round's levels are
+// sorted and none is a nonzero value below 2^(e(M) - 29) either, every fp64 distance is
+// exact, the nearest level of v (lowest index on ties) changes from q to q + 1 exactly
+// above the midpoint of L_q and L_{q+1} (exact in fp64), and the code of v is the number of
+// thresholds t_q <= v, t_q the smallest fp32 value above that midpoint (t_q = t_{q+1} when
+// L_q = L_{q+1}, whose upper level never wins).  Other rounds search the levels as
+// cbq_kernel does.  The scalars, their weights, codes and (a, b) stay in registers, one
+// wave computes the levels and thresholds, and a round takes two barriers.
+constexpr int kCbqFastPer = 4;                              // scalars per thread
+constexpr int kCbqFastMax = kCbqThreads * kCbqFastPer;      // 4096
+constexpr int kCbqFastLevels = 64;                          // six bits
+
+// an int128 rounded to nearest-even fp64
+__device__ __forceinline__ double i128_to_double(__int128 x) {
+    const bool neg = x < 0;
+    const unsigned __int128 u = neg ? (unsigned __int128)(-x) : (unsigned __int128)x;
+    const unsigned long long hi = (unsigned long long)(u >> 64), lo = (unsigned long long)u;
+    double r;
+    if (hi == 0) {
+        r = (double)lo;  // correctly rounded conversion of 64 bits
+    } else {
+        const int lz = __clzll((long long)hi);  // 0..63
+        const unsigned long long top = lz ? (hi << lz) | (lo >> (64 - lz)) : hi;
+        const bool sticky = (lz ? (lo << lz) : lo) != 0ull;
+        unsigned long long mant = top >> 11;
+        const unsigned rnd = (unsigned)(top & 0x7ffull);
+        if (rnd > 0x400u || (rnd == 0x400u && (sticky || (mant & 1ull)))) ++mant;
+        r = ldexp((double)mant, 64 + 63 - lz - 52);
+    }
+    return neg ? -r : r;
+}
+
+// the smallest fp32 value above y (y finite, within fp32 range)
+__device__ __forceinline__ float fp32_above(double y) {
+    const float f = (float)y;  // nearest; a larger fp32 below y cannot exist
+    if ((double)f > y) return f;
+    const unsigned u = __float_as_uint(f);
+    if (u == 0x80000000u || u == 0u) return __uint_as_float(1u);  // above a zero: the smallest subnormal
+    return __uint_as_float((u & 0x80000000u) ? u - 1u : u + 1u);
+}
+
+__device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, float lo, float hi, float M) {
+    __shared__ __attribute__((aligned(16))) float s_flev[kCbqFastLevels];
+    __shared__ __attribute__((aligned(16))) float s_thr[kCbqFastLevels];
+    __shared__ __attribute__((aligned(16))) float s_coarse[kCbqFastLevels / 8];  // every eighth of s_flev or s_thr
+    __shared__ unsigned long long s_A[kCbqFastLevels], s_B[kCbqFastLevels], s_W[kCbqFastLevels];
+    __shared__ int s_mode;
+    __shared__ int s_chg[2];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int beM = (int)((__float_as_uint(M) >> 23) & 255u);
+    const int S = beM == 0 ? 149 : 179 - beM;
+    const float fl = exact_floor(M);
+
+    float x[kCbqFastPer];
+    unsigned wt[kCbqFastPer];
+    int cd[kCbqFastPer];
+#pragma unroll
+    for (int u = 0; u < kCbqFastPer; ++u) {
+        const int r = tid + u * kCbqThreads;
+        x[u] = r < m ? L.C[r] : 0.0f;
+        const int w = r < m && L.w ? L.w[r / kDim] : 1;
+        wt[u] = r < m && w > 0 ? (unsigned)w : 0u;  // weights <= 0 add nothing
+        cd[u] = 0;
+    }
+    // w v 2^S as a 2^42 + b: v 2^S from the bits (the integer mantissa shifted into place,
+    // 0 <= shift <= 29 for every value that meets the condition), times w in 128 bits
+    auto contrib = [&](float xv, unsigned w, long long& a, unsigned long long& b) {
+        const unsigned bits = __float_as_uint(xv);
+        const int be = (int)((bits >> 23) & 255u);
+        const unsigned long long mant = (unsigned long long)((bits & 0x7fffffu) | (be ? 0x800000u : 0u));
+        const long long vs = mant ? (long long)(mant << ((be ? be : 1) - 150 + S)) : 0ll;
+        const __int128 X = (__int128)((bits >> 31) ? -vs : vs) * (__int128)w;
+        a = (long long)(X >> 42);
+        b = (unsigned long long)X & ((1ull << 42) - 1ull);
+    };
+    if (tid < kCbqFastLevels) {
+        s_A[tid] = s_B[tid] = s_W[tid] = 0ull;
+        const double delta = ((double)hi - (double)lo) / (double)(kCbqFastLevels - 1);
+        s_flev[tid] = (float)__dadd_rn((double)lo, __dmul_rn((double)tid, delta));
+    }
+    if (tid < 2) s_chg[tid] = 0;
+
+    // wave 0: the levels (from the sums, when `update`), whether they are sorted and exact,
+    // and then the thresholds; s_mode = 2 (thresholds), 1 (sorted levels) or 0 (unsorted)
+    // level q from its sums (unchanged when empty or without `update`): N = A 2^42 + B with
+    // B's carries moved into A; while |A| <= 2^53 both parts are exact doubles and one fp64
+    // addition rounds N correctly
+    auto level_of = [&](int q, bool update) {
+        float Lq = s_flev[q];
+        const unsigned long long W = s_W[q];
+        if (update && W > 0ull) {
+            const unsigned long long B = s_B[q];
+            const long long A = (long long)s_A[q] + (long long)(B >> 42);
+            const unsigned long long Bl = B & ((1ull << 42) - 1ull);
+            double N;
+            if (A <= (1ll << 53) && A >= -(1ll << 53))
+                N = __builtin_ldexp((double)A, 42) + (double)Bl;
+            else
+                N = i128_to_double(((__int128)A << 42) + (__int128)Bl);
+            Lq = (float)(ldexp(N, -S) / (double)W);
+        }
+        return Lq;
+    };
+    auto levels = [&](bool update) {
+        const int q = lane;
+        const float Lq = level_of(q, update);
+        s_flev[q] = Lq;
+        const float Ln = __shfl_down(Lq, 1);  // the level above (lane 63: its own)
+        const bool srt = __all(q == kCbqFastLevels - 1 || Lq <= Ln);
+        const bool ex = __all(Lq == 0.0f || fabsf(Lq) >= fl);
+        float t = __builtin_inff();
+        int src = -1;  // a duplicate takes the threshold of the next level up
+        if (q < kCbqFastLevels - 1) {
+            if (Lq == Ln)
+                src = q + 1;
+            else
+                t = fp32_above(0.5 * ((double)Lq + (double)Ln));
+        }
+        if (__any(src >= 0)) {
+#pragma unroll
+            for (int st = 0; st < 6; ++st) {  // pointer jumping over runs of equal levels
+                const float ts = __shfl(t, src < 0 ? q : src);
+                const int ss = __shfl(src, src < 0 ? q : src);
+                if (src >= 0) {
+                    t = ts;
+                    src = ss;
+                }
+            }
+        }
+        const int mode = srt ? (ex ? 2 : 1) : 0;
+        s_thr[q] = t;
+        if ((q & 7) == 7) s_coarse[q >> 3] = mode == 2 ? t : Lq;
+        if (q == 0) s_mode = mode;
+    };
+    if (wave == 0) levels(false);
+    __syncthreads();
+
+    // codes against the current levels; with `move`, a changed code moves the scalar's
+    // contribution between the two levels' sums
+    auto code_all = [&](bool first) {
+        const int mode = __builtin_amdgcn_readfirstlane(s_mode);  // the same in every lane
+        bool need[kCbqFastPer];
+        if (!first && mode == 2) {
+            // code c stays while t_{c-1} <= v < t_c: every bound loaded first, then the tests
+            float tl[kCbqFastPer], th[kCbqFastPer];
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u) {
+                const int c = cd[u];
+                tl[u] = s_thr[c > 0 ? c - 1 : 0];
+                th[u] = s_thr[c];
+            }
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u)
+                need[u] = tid + u * kCbqThreads < m && !((cd[u] == 0 || tl[u] <= x[u]) && x[u] < th[u]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u) need[u] = tid + u * kCbqThreads < m;
+        }
+        bool any = false;
+#pragma unroll
+        for (int u = 0; u < kCbqFastPer; ++u) any |= need[u];
+        int chg = 0;
+        if (!__any(any)) return chg;
+        float coarse[kCbqFastLevels / 8 + 1];
+        {
+            typedef float f32x4 __attribute__((ext_vector_type(4)));
+            const f32x4 c0 = reinterpret_cast<const f32x4*>(s_coarse)[0], c1 = reinterpret_cast<const f32x4*>(s_coarse)[1];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                coarse[i] = c0[i];
+                coarse[4 + i] = c1[i];
+            }
+            coarse[kCbqFastLevels / 8] = 0.0f;
+        }
+        int q[kCbqFastPer];
+        if (mode == 2) {
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u)
+                q[u] = need[u] ? code_from_thresholds<kCbqFastLevels>(x[u], s_thr, coarse) : cd[u];
+        } else if (mode == 1) {
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u)
+                q[u] = need[u] ? nearest_sorted_fast<kCbqFastLevels>(x[u], s_flev, coarse) : cd[u];
+        } else {
+#pragma unroll
+            for (int u = 0; u < kCbqFastPer; ++u) q[u] = need[u] ? nearest_level(x[u], s_flev, kCbqFastLevels) : cd[u];
+        }
+#pragma unroll
+        for (int u = 0; u < kCbqFastPer; ++u) {
+            if (!need[u] || (!first && q[u] == cd[u])) continue;
+            if (wt[u]) {
+                long long a;
+                unsigned long long b;
+                contrib(x[u], wt[u], a, b);
+                if (!first) {  // out of the old level
+                    const int c = cd[u];
+                    atomicAdd(&s_A[c], (unsigned long long)(-a));
+                    atomicAdd(&s_B[c], (unsigned long long)(-(long long)b));
+                    atomicAdd(&s_W[c], (unsigned long long)(-(long long)wt[u]));
+                }
+                atomicAdd(&s_A[q[u]], (unsigned long long)a);
+                atomicAdd(&s_B[q[u]], b);
+                atomicAdd(&s_W[q[u]], (unsigned long long)wt[u]);
+            }
+            chg |= first ? 0 : 1;
+            cd[u] = q[u];
+        }
+        return chg;
+    };
+    code_all(true);
+    __syncthreads();
+
+    for (int it = 0; it < p.iters; ++it) {
+        if (wave == 0) {
+            levels(true);
+            if (lane == 0) s_chg[it & 1] = 0;  // last read before the previous round's first barrier
+        }
+        __syncthreads();
+        if (code_all(false)) s_chg[it & 1] = 1;
+        __syncthreads();
+        if (!s_chg[it & 1]) break;
+    }
+
+    if (tid < kCbqFastLevels) L.levels[tid] = s_flev[tid];
+#pragma unroll
+    for (int u = 0; u < kCbqFastPer; ++u) {
+        const int r = tid + u * kCbqThreads;
+        if (r >= m) continue;
+        L.codes[r] = (uint8_t)cd[u];
+        if (L.C_hat) L.C_hat[r] = s_flev[cd[u]];
+    }
+}
+
 // Thread tid handles scalars r = tid, tid + 1024, ...  With LDS (codebooks of at most
 // kCbqLdsScalars scalars) the scalars, their weights and codes are copied into LDS once;
 // otherwise every pass reads them from memory.  The level sums are kept up to date
@@ -293,7 +533,7 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     __shared__ __attribute__((aligned(16))) float s_lev[kCbqMaxLevels];
     __shared__ unsigned long long s_dig[kCbqMaxLevels * kDigits];
     __shared__ unsigned long long s_w[kCbqMaxLevels];
-    __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave];
+    __shared__ float s_lo[kCbqThreads / kWave], s_hi[kCbqThreads / kWave], s_sm[kCbqThreads / kWave];
     __shared__ int s_changed;
     __shared__ int s_unsorted;
     __shared__ float s_v[LDS ? kCbqLdsScalars : 1];
@@ -317,6 +557,46 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
             codes[r] = (uint8_t)q;
     };
 
+    // grid on [min, max]; for the integer rounds also the smallest nonzero magnitude and
+    // whether a value is not finite
+    float lo = __builtin_inff(), hi = -__builtin_inff(), sm = __builtin_inff();
+    bool nonfinite = false;
+    for (int r = tid; r < m; r += kCbqThreads) {
+        const float x = v[r];
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
+        if (x != 0.0f) sm = fminf(sm, fabsf(x));
+        nonfinite |= !(fabsf(x) <= 3.402823466e38f);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, off));
+        hi = fmaxf(hi, __shfl_xor(hi, off));
+        sm = fminf(sm, __shfl_xor(sm, off));
+    }
+    nonfinite = __any(nonfinite);
+    if (lane == 0) {
+        s_lo[wave] = lo;
+        s_hi[wave] = hi;
+        s_sm[wave] = nonfinite ? -1.0f : sm;
+    }
+    if (tid == 0) s_unsorted = 0;
+    __syncthreads();
+    lo = s_lo[0];
+    hi = s_hi[0];
+    sm = s_sm[0];
+    for (int w = 1; w < kCbqThreads / kWave; ++w) {
+        lo = fminf(lo, s_lo[w]);
+        hi = fmaxf(hi, s_hi[w]);
+        sm = s_sm[w] < 0.0f || sm < 0.0f ? -1.0f : fminf(sm, s_sm[w]);
+    }
+    if (FAST64 && wk && m <= kCbqFastMax && sm >= 0.0f) {
+        const float M = fmaxf(fabsf(lo), fabsf(hi));
+        if (!(sm < exact_floor(M))) {  // every value meets the exactness condition
+            cbq_exact_rounds(p, L, m, lo, hi, M);
+            return;
+        }
+    }
     if (LDS) {
         for (int r = tid; r < m; r += kCbqThreads) {
             s_v[r] = v[r];
@@ -325,31 +605,6 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     }
     for (int e = tid; e < nlev * kDigits; e += kCbqThreads) s_dig[e] = 0ull;
     for (int e = tid; e < nlev; e += kCbqThreads) s_w[e] = 0ull;
-
-    // grid on [min, max]
-    float lo = __builtin_inff(), hi = -__builtin_inff();
-    for (int r = tid; r < m; r += kCbqThreads) {
-        const float x = v[r];
-        lo = fminf(lo, x);
-        hi = fmaxf(hi, x);
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        lo = fminf(lo, __shfl_xor(lo, off));
-        hi = fmaxf(hi, __shfl_xor(hi, off));
-    }
-    if (lane == 0) {
-        s_lo[wave] = lo;
-        s_hi[wave] = hi;
-    }
-    if (tid == 0) s_unsorted = 0;
-    __syncthreads();
-    lo = s_lo[0];
-    hi = s_hi[0];
-    for (int w = 1; w < kCbqThreads / kWave; ++w) {
-        lo = fminf(lo, s_lo[w]);
-        hi = fmaxf(hi, s_hi[w]);
-    }
     if (tid < nlev) {
         const double delta = ((double)hi - (double)lo) / (double)(nlev - 1);
         s_lev[tid] = (float)__dadd_rn((double)lo, __dmul_rn((double)tid, delta));

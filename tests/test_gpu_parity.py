@@ -534,3 +534,35 @@ def test_quantize_codebook_edge_weights_and_magnitudes(bits):
         assert np.array_equal(host(codes), oc), (C.shape, bits)
         assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), (C.shape, bits)
         assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32)), (C.shape, bits)
+
+
+def test_quantize_codebook_6bit_rounds_bit_exact_over_many_codebooks():
+    """6-bit weighted k-means codebooks whose values meet the exactness condition run their
+    rounds in integers (two 64-bit sums per level, codes from thresholds); rounds whose levels
+    are unsorted or come near zero search the levels instead, and codebooks whose values do
+    not meet the condition take the digit sums.  Bit for bit the oracle's over many seeds:
+    sizes up to and past the 4096-scalar limit (455 and 456 entries), constant and
+    few-valued codebooks (equal levels), zero and huge weights, mixed magnitudes."""
+    rng = np.random.default_rng(2024)
+    cases = []
+    for t in range(24):
+        k = int(rng.integers(1, 460))
+        C = rng.laplace(0, 10.0 ** rng.uniform(-4, 1), (k, 9)).astype(np.float32)
+        w = rng.integers(0, 1 << int(rng.integers(1, 31)), k)
+        if t % 3 == 0:
+            w[rng.random(k) < 0.3] = 0
+        cases.append((C, w))
+    cases.append((np.full((40, 9), 0.25, np.float32), np.ones(40, np.int64)))           # one value
+    cases.append((rng.choice(np.float32([-1, 0.5, 3]), (90, 9)), rng.integers(1, 9, 90)))  # three values
+    cases.append((np.zeros((7, 9), np.float32), np.ones(7, np.int64)))                   # all zero
+    for k in (455, 456):
+        cases.append((rng.standard_normal((k, 9)).astype(np.float32), rng.integers(1, 1000, k)))
+    C = rng.standard_normal((300, 9)).astype(np.float32)
+    C[17, 2] = np.float32(3e-9)                                 # below 2^(e(M) - 29): digit sums
+    cases.append((C, rng.integers(1, 100, 300)))
+    for i, (C, w) in enumerate(cases):
+        codes, levels, C_hat = kq.kq_quantize_codebook(dev(C), dev(w.astype(np.int32)), 6, kq.KQ_CBQ_WKMEANS, 30)
+        oc, ol, oh, _ = oracle.cbq_wkmeans(C, w, 6, 30)
+        assert np.array_equal(host(codes), oc), i
+        assert np.array_equal(host(levels).view(np.uint32), ol.view(np.uint32)), i
+        assert np.array_equal(host(C_hat).view(np.uint32), oh.view(np.uint32)), i

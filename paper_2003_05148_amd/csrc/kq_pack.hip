@@ -124,11 +124,13 @@ __global__ __launch_bounds__(kWave) void sq_finish_kernel(const double* part, in
 // as dwords by the first 2 * bits lanes and each lane extracts its field with two
 // ds_bpermute); each float then takes its row's index from that row's lane (ds_bpermute)
 // and gathers its value from the codebook, copied into LDS first when it holds at most
-// kReconLdsFloats values.  Loads and stores are all full 256-byte wave accesses, and the
+// kReconLdsFloats values (48-byte rows).  Loads and stores are all full 256-byte wave accesses, and the
 // next step's index and reference values load while the current step is rebuilt.  When the
 // layer asks for it, each lane also sums (W_ref - W_hat)^2 in fp64 over its floats in a
 // fixed order; the lanes of a wave are combined by a butterfly, the waves in order, and a
 // second kernel adds the workgroup partials in order.
+
+constexpr int kReconRowFloats = 12;  // staged codebook rows: 9 values, padded to 48 bytes
 
 // the index of the step's row `lane` (rows b0 .. b0 + cnt - 1), or -1 past the end of the layer
 __device__ __forceinline__ int recon_step_index(const ReconLayer& L, int b0, int cnt, int lane) {
@@ -205,7 +207,7 @@ __device__ __forceinline__ double recon_steps(const ReconLayer& L, const float* 
         for (int q = 0; q < kDim; ++q) {
             const int jq = __builtin_amdgcn_ds_bpermute(src[q], cur.j);
             float v = 0.0f;
-            if ((unsigned)jq < (unsigned)L.k) v = LDS ? s_cb[jq * kDim + dim[q]] : L.C[jq * kDim + dim[q]];
+            if ((unsigned)jq < (unsigned)L.k) v = LDS ? s_cb[jq * kReconRowFloats + dim[q]] : L.C[jq * kDim + dim[q]];
             if (lane + kWave * q < nf) {
                 __builtin_nontemporal_store(v, &out[lane + kWave * q]);  // streamed, not re-read here
                 if (err) {
@@ -221,8 +223,104 @@ __device__ __forceinline__ double recon_steps(const ReconLayer& L, const float* 
     return acc;
 }
 
+// The same with 16-byte accesses, for W_hat (and W_ref) aligned to 16 bytes: lane r gathers
+// its row's codeword (three ds_read_b128 from 48-byte rows) into the wave's stage, a
+// 576-float row-major tile of the step (rows 9 dwords apart: no bank conflicts), and the
+// tile leaves as 144 float4 stores (lane l takes float4s l, l + 64, l + 128), with the
+// reference read as the same float4s for the error.
+typedef float rf32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void recon_ref4(rf32x4 (&x)[3], const ReconLayer& L, int b0, int nf, int lane) {
+    const float* __restrict__ ref = L.W_ref + (size_t)b0 * kDim;
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+        const int t = lane + kWave * u;
+        if (4 * t + 4 <= nf) {
+            x[u] = reinterpret_cast<const rf32x4*>(ref)[t];
+        } else {
+            rf32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (4 * t + e < nf) v[e] = ref[4 * t + e];
+            x[u] = v;
+        }
+    }
+}
+
+template <bool LDS>
+__device__ __forceinline__ double recon_steps_vec(const ReconLayer& L, const float* __restrict__ s_cb,
+                                                  float* __restrict__ s_st, int i0, int i1, int lane, int wave,
+                                                  bool err) {
+    constexpr int kWaves = kReconThreads / kWave;
+    const int nsteps = (i1 - i0 + kWave - 1) / kWave;
+    double acc = 0.0;
+    int st = wave;
+    if (st >= nsteps) return acc;
+    int j = recon_step_index(L, i0 + st * kWave, min(kWave, i1 - i0 - st * kWave), lane);
+    rf32x4 xr[3];
+    if (err) recon_ref4(xr, L, i0 + st * kWave, min(kWave, i1 - i0 - st * kWave) * kDim, lane);
+    for (;;) {
+        const int b0 = i0 + st * kWave;
+        const int nf = min(kWave, i1 - b0) * kDim;
+        const int sn = st + kWaves;
+        const bool more = sn < nsteps;
+        int jn = 0;
+        rf32x4 xn[3];
+        if (more) {
+            jn = recon_step_index(L, i0 + sn * kWave, min(kWave, i1 - i0 - sn * kWave), lane);
+            if (err) recon_ref4(xn, L, i0 + sn * kWave, min(kWave, i1 - i0 - sn * kWave) * kDim, lane);
+        }
+        float c[kDim];  // this lane's row (zeros for an index outside the codebook)
+        if ((unsigned)j < (unsigned)L.k) {
+            if (LDS) {
+                const rf32x4* __restrict__ r = reinterpret_cast<const rf32x4*>(s_cb) + (size_t)j * 3;
+                const rf32x4 r0 = r[0], r1 = r[1], r2 = r[2];
+                c[0] = r0[0]; c[1] = r0[1]; c[2] = r0[2]; c[3] = r0[3];
+                c[4] = r1[0]; c[5] = r1[1]; c[6] = r1[2]; c[7] = r1[3];
+                c[8] = r2[0];
+            } else {
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) c[d] = L.C[(size_t)j * kDim + d];
+            }
+        } else {
+#pragma unroll
+            for (int d = 0; d < kDim; ++d) c[d] = 0.0f;
+        }
+#pragma unroll
+        for (int d = 0; d < kDim; ++d) s_st[lane * kDim + d] = c[d];
+        float* __restrict__ out = L.W + (size_t)b0 * kDim;
+#pragma unroll
+        for (int u = 0; u < 3; ++u) {
+            const int t = lane + kWave * u;
+            if (4 * t >= nf) continue;
+            const rf32x4 v = reinterpret_cast<const rf32x4*>(s_st)[t];
+            if (4 * t + 4 <= nf) {
+                __builtin_nontemporal_store(v, reinterpret_cast<rf32x4*>(out) + t);  // streamed, not re-read here
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * t + e < nf) __builtin_nontemporal_store(v[e], out + 4 * t + e);
+            }
+            if (err) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * t + e < nf) {
+                        const double df = (double)xr[u][e] - (double)v[e];
+                        acc += df * df;
+                    }
+            }
+        }
+        if (!more) break;
+        j = jn;
+#pragma unroll
+        for (int u = 0; u < 3; ++u) xr[u] = xn[u];
+        st = sn;
+    }
+    return acc;
+}
+
 __global__ __launch_bounds__(kReconThreads) void reconstruct_stack_kernel(const ReconParams p) {
-    extern __shared__ float s_cb[];  // the codebook, when it is staged
+    extern __shared__ __attribute__((aligned(16))) float s_cb[];  // the codebook in 48-byte rows when it is staged, then the waves' stages
     __shared__ double s_w[kReconThreads / kWave];
     constexpr int kWaves = kReconThreads / kWave;
     int li = 0;
@@ -234,13 +332,19 @@ __global__ __launch_bounds__(kReconThreads) void reconstruct_stack_kernel(const 
     const int i0 = lb * kReconRows;
     const int i1 = min(L.n, i0 + kReconRows);
     const bool err = L.part != nullptr;
+    const bool staged = L.k * kReconRowFloats <= kReconLdsFloats;
+    // 16-byte stores where W_hat (and W_ref) allow them
+    const bool vec = ((reinterpret_cast<uintptr_t>(L.W) | (err ? reinterpret_cast<uintptr_t>(L.W_ref) : 0)) & 15u) == 0;
+    float* s_st = s_cb + (staged ? L.k * kReconRowFloats : 0) + wave * kWave * kDim;
     double acc;
-    if (L.k * kDim <= kReconLdsFloats) {
-        for (int e = tid; e < L.k * kDim; e += kReconThreads) s_cb[e] = L.C[e];
+    if (staged) {
+        for (int e = tid; e < L.k * kDim; e += kReconThreads) s_cb[(e / kDim) * kReconRowFloats + e % kDim] = L.C[e];
         __syncthreads();
-        acc = recon_steps<true>(L, s_cb, i0, i1, lane, wave, err);
+        acc = vec ? recon_steps_vec<true>(L, s_cb, s_st, i0, i1, lane, wave, err)
+                  : recon_steps<true>(L, s_cb, i0, i1, lane, wave, err);
     } else {
-        acc = recon_steps<false>(L, s_cb, i0, i1, lane, wave, err);
+        acc = vec ? recon_steps_vec<false>(L, s_cb, s_st, i0, i1, lane, wave, err)
+                  : recon_steps<false>(L, s_cb, i0, i1, lane, wave, err);
     }
     if (!err) return;
 #pragma unroll
@@ -293,11 +397,12 @@ hipError_t launch_pack_stack(const PackParams& p, hipStream_t s) {
 }
 
 hipError_t launch_reconstruct_stack(const ReconParams& p, hipStream_t s) {
-    size_t lds = 0;  // the largest codebook that is staged
+    size_t lds = 0;  // the largest codebook that is staged (48-byte rows), then the waves' stages
     for (int l = 0; l < p.nlayers; ++l) {
-        const size_t f = (size_t)p.L[l].k * kDim;
+        const size_t f = (size_t)p.L[l].k * kReconRowFloats;
         if (f <= (size_t)kReconLdsFloats && f * sizeof(float) > lds) lds = f * sizeof(float);
     }
+    lds += sizeof(float) * kReconThreads * kDim;
     hipLaunchKernelGGL(reconstruct_stack_kernel, dim3(p.total_blocks), dim3(kReconThreads), lds, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

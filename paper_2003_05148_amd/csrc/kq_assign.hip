@@ -113,8 +113,8 @@ __device__ __forceinline__ void argmin_take(float& d, int& j, float od, int oj) 
 }
 template <int CTL>
 __device__ __forceinline__ void argmin_dpp(float& d, int& j) {
-    const float od = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(d), CTL, 0xF, 0xF, false));
-    const int oj = __builtin_amdgcn_update_dpp(0, j, CTL, 0xF, 0xF, false);
+    const float od = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(d), CTL, 0xF, 0xF, true));
+    const int oj = __builtin_amdgcn_mov_dpp(j, CTL, 0xF, 0xF, true);
     argmin_take(d, j, od, oj);
 }
 // the wave's lexicographic minimum of the lanes' (distance, index) pairs, in every lane:

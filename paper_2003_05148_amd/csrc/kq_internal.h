@@ -192,8 +192,9 @@ __device__ __forceinline__ int find_layer(const StackParams& p, int u) {
 // v plus the value that DPP control CTL brings from another lane of the row
 template <int CTL>
 __device__ __forceinline__ double dpp_add(double v) {
-    const unsigned plo = __builtin_amdgcn_update_dpp(0u, (unsigned)__double2loint(v), CTL, 0xF, 0xF, false);
-    const unsigned phi = __builtin_amdgcn_update_dpp(0u, (unsigned)__double2hiint(v), CTL, 0xF, 0xF, false);
+    // every source lane of these row moves exists: no "old" value is needed
+    const unsigned plo = __builtin_amdgcn_mov_dpp((unsigned)__double2loint(v), CTL, 0xF, 0xF, true);
+    const unsigned phi = __builtin_amdgcn_mov_dpp((unsigned)__double2hiint(v), CTL, 0xF, 0xF, true);
     return v + __hiloint2double((int)phi, (int)plo);
 }
 // v summed over the 64 lanes by the butterfly of partner offsets 32, 16, 8, 4, 2, 1; every

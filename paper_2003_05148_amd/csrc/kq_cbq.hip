@@ -35,6 +35,22 @@ __device__ __forceinline__ int nearest_level(float v, const float* lev, int nlev
     return bq;
 }
 
+// the same, kept as a loop (for rare rounds, where a fully unrolled scan would only cost registers)
+__device__ __forceinline__ int nearest_level_loop(float v, const float* lev, int nlev) {
+    const double vd = (double)v;
+    double best = fabs(vd - (double)lev[0]);
+    int bq = 0;
+#pragma unroll 1
+    for (int q = 1; q < nlev; ++q) {
+        const double d = fabs(vd - (double)lev[q]);
+        if (d < best) {
+            best = d;
+            bq = q;
+        }
+    }
+    return bq;
+}
+
 // the same when the levels are sorted (L_0 <= L_1 <= ...): the distances in fp64 do not
 // grow towards v from either side, so the answer is the first level >= v or, if not
 // farther, the lowest-indexed level whose distance equals that of the last level < v
@@ -292,10 +308,11 @@ __device__ __forceinline__ int code_from_thresholds(float x, const float* s_thr,
 // above the midpoint of L_q and L_{q+1} (exact in fp64), and the code of v is the number of
 // thresholds t_q <= v, t_q the smallest fp32 value above that midpoint (t_q = t_{q+1} when
 // L_q = L_{q+1}, whose upper level never wins).  Other rounds search the levels as
-// cbq_kernel does.  The scalars, their weights, codes and (a, b) stay in registers, one
-// wave computes the levels and thresholds, and a round takes two barriers.
-constexpr int kCbqFastPer = 4;                              // scalars per thread
-constexpr int kCbqFastMax = kCbqThreads * kCbqFastPer;      // 4096
+// cbq_kernel does.  The scalars, their weights and codes live in LDS; one wave computes the
+// levels and thresholds; in a threshold round every scalar checks that it still lies in its
+// code's interval [t_{c-1}, t_c), and the few that left it are queued and searched by dense
+// lanes, which move their (a, b, w) between the two levels' sums (three barriers a round).
+constexpr int kCbqFastMax = 4096;                           // scalars of a codebook
 constexpr int kCbqFastLevels = 64;                          // six bits
 
 // an int128 rounded to nearest-even fp64
@@ -327,28 +344,25 @@ __device__ __forceinline__ float fp32_above(double y) {
     return __uint_as_float((u & 0x80000000u) ? u - 1u : u + 1u);
 }
 
-__device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, float lo, float hi, float M) {
+__device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, float lo, float hi, float M, float* s_x,
+                                 unsigned* s_wt, uint8_t* s_cd, unsigned short* s_q) {
     __shared__ __attribute__((aligned(16))) float s_flev[kCbqFastLevels];
     __shared__ __attribute__((aligned(16))) float s_thr[kCbqFastLevels];
     __shared__ __attribute__((aligned(16))) float s_coarse[kCbqFastLevels / 8];  // every eighth of s_flev or s_thr
     __shared__ unsigned long long s_A[kCbqFastLevels], s_B[kCbqFastLevels], s_W[kCbqFastLevels];
     __shared__ int s_mode;
     __shared__ int s_chg[2];
+    __shared__ unsigned s_qn;  // scalars queued this round
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int beM = (int)((__float_as_uint(M) >> 23) & 255u);
     const int S = beM == 0 ? 149 : 179 - beM;
     const float fl = exact_floor(M);
 
-    float x[kCbqFastPer];
-    unsigned wt[kCbqFastPer];
-    int cd[kCbqFastPer];
-#pragma unroll
-    for (int u = 0; u < kCbqFastPer; ++u) {
-        const int r = tid + u * kCbqThreads;
-        x[u] = r < m ? L.C[r] : 0.0f;
-        const int w = r < m && L.w ? L.w[r / kDim] : 1;
-        wt[u] = r < m && w > 0 ? (unsigned)w : 0u;  // weights <= 0 add nothing
-        cd[u] = 0;
+    // the scalars, their weights (those <= 0 add nothing) and, later, their codes in LDS
+    for (int r = tid; r < m; r += kCbqThreads) {
+        s_x[r] = L.C[r];
+        const int w = L.w ? L.w[r / kDim] : 1;
+        s_wt[r] = w > 0 ? (unsigned)w : 0u;
     }
     // w v 2^S as a 2^42 + b: v 2^S from the bits (the integer mantissa shifted into place,
     // 0 <= shift <= 29 for every value that meets the condition), times w in 128 bits
@@ -361,6 +375,22 @@ __device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, f
         a = (long long)(X >> 42);
         b = (unsigned long long)X & ((1ull << 42) - 1ull);
     };
+    // scalar r moves into level q (and, unless `first`, out of level c)
+    auto move = [&](int r, int c, int q, bool first) {
+        const unsigned w = s_wt[r];
+        if (!w) return;
+        long long a;
+        unsigned long long b;
+        contrib(s_x[r], w, a, b);
+        if (!first) {
+            atomicAdd(&s_A[c], (unsigned long long)(-a));
+            atomicAdd(&s_B[c], (unsigned long long)(-(long long)b));
+            atomicAdd(&s_W[c], (unsigned long long)(-(long long)w));
+        }
+        atomicAdd(&s_A[q], (unsigned long long)a);
+        atomicAdd(&s_B[q], b);
+        atomicAdd(&s_W[q], (unsigned long long)w);
+    };
     if (tid < kCbqFastLevels) {
         s_A[tid] = s_B[tid] = s_W[tid] = 0ull;
         const double delta = ((double)hi - (double)lo) / (double)(kCbqFastLevels - 1);
@@ -368,8 +398,6 @@ __device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, f
     }
     if (tid < 2) s_chg[tid] = 0;
 
-    // wave 0: the levels (from the sums, when `update`), whether they are sorted and exact,
-    // and then the thresholds; s_mode = 2 (thresholds), 1 (sorted levels) or 0 (unsorted)
     // level q from its sums (unchanged when empty or without `update`): N = A 2^42 + B with
     // B's carries moved into A; while |A| <= 2^53 both parts are exact doubles and one fp64
     // addition rounds N correctly
@@ -389,6 +417,8 @@ __device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, f
         }
         return Lq;
     };
+    // wave 0: the levels (from the sums, when `update`), whether they are sorted and exact,
+    // and then the thresholds; s_mode = 2 (thresholds), 1 (sorted levels) or 0 (unsorted)
     auto levels = [&](bool update) {
         const int q = lane;
         const float Lq = level_of(q, update);
@@ -418,84 +448,42 @@ __device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, f
         const int mode = srt ? (ex ? 2 : 1) : 0;
         s_thr[q] = t;
         if ((q & 7) == 7) s_coarse[q >> 3] = mode == 2 ? t : Lq;
-        if (q == 0) s_mode = mode;
+        if (q == 0) {
+            s_mode = mode;
+            s_qn = 0u;
+        }
     };
+    __syncthreads();  // scalars and grid in place
     if (wave == 0) levels(false);
     __syncthreads();
 
-    // codes against the current levels; with `move`, a changed code moves the scalar's
-    // contribution between the two levels' sums
-    auto code_all = [&](bool first) {
-        const int mode = __builtin_amdgcn_readfirstlane(s_mode);  // the same in every lane
-        bool need[kCbqFastPer];
-        if (!first && mode == 2) {
-            // code c stays while t_{c-1} <= v < t_c: every bound loaded first, then the tests
-            float tl[kCbqFastPer], th[kCbqFastPer];
+    auto load_coarse = [&](float (&coarse)[kCbqFastLevels / 8 + 1]) {
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        const f32x4 c0 = reinterpret_cast<const f32x4*>(s_coarse)[0], c1 = reinterpret_cast<const f32x4*>(s_coarse)[1];
 #pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u) {
-                const int c = cd[u];
-                tl[u] = s_thr[c > 0 ? c - 1 : 0];
-                th[u] = s_thr[c];
-            }
-#pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u)
-                need[u] = tid + u * kCbqThreads < m && !((cd[u] == 0 || tl[u] <= x[u]) && x[u] < th[u]);
-        } else {
-#pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u) need[u] = tid + u * kCbqThreads < m;
+        for (int i = 0; i < 4; ++i) {
+            coarse[i] = c0[i];
+            coarse[4 + i] = c1[i];
         }
-        bool any = false;
-#pragma unroll
-        for (int u = 0; u < kCbqFastPer; ++u) any |= need[u];
-        int chg = 0;
-        if (!__any(any)) return chg;
-        float coarse[kCbqFastLevels / 8 + 1];
-        {
-            typedef float f32x4 __attribute__((ext_vector_type(4)));
-            const f32x4 c0 = reinterpret_cast<const f32x4*>(s_coarse)[0], c1 = reinterpret_cast<const f32x4*>(s_coarse)[1];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                coarse[i] = c0[i];
-                coarse[4 + i] = c1[i];
-            }
-            coarse[kCbqFastLevels / 8] = 0.0f;
-        }
-        int q[kCbqFastPer];
-        if (mode == 2) {
-#pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u)
-                q[u] = need[u] ? code_from_thresholds<kCbqFastLevels>(x[u], s_thr, coarse) : cd[u];
-        } else if (mode == 1) {
-#pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u)
-                q[u] = need[u] ? nearest_sorted_fast<kCbqFastLevels>(x[u], s_flev, coarse) : cd[u];
-        } else {
-#pragma unroll
-            for (int u = 0; u < kCbqFastPer; ++u) q[u] = need[u] ? nearest_level(x[u], s_flev, kCbqFastLevels) : cd[u];
-        }
-#pragma unroll
-        for (int u = 0; u < kCbqFastPer; ++u) {
-            if (!need[u] || (!first && q[u] == cd[u])) continue;
-            if (wt[u]) {
-                long long a;
-                unsigned long long b;
-                contrib(x[u], wt[u], a, b);
-                if (!first) {  // out of the old level
-                    const int c = cd[u];
-                    atomicAdd(&s_A[c], (unsigned long long)(-a));
-                    atomicAdd(&s_B[c], (unsigned long long)(-(long long)b));
-                    atomicAdd(&s_W[c], (unsigned long long)(-(long long)wt[u]));
-                }
-                atomicAdd(&s_A[q[u]], (unsigned long long)a);
-                atomicAdd(&s_B[q[u]], b);
-                atomicAdd(&s_W[q[u]], (unsigned long long)wt[u]);
-            }
-            chg |= first ? 0 : 1;
-            cd[u] = q[u];
-        }
-        return chg;
+        coarse[kCbqFastLevels / 8] = 0.0f;
     };
-    code_all(true);
+    // code of x against the current levels (the mode decides how)
+    auto search = [&](float x, int mode, const float (&coarse)[kCbqFastLevels / 8 + 1]) {
+        return mode == 2 ? code_from_thresholds<kCbqFastLevels>(x, s_thr, coarse)
+                         : (mode == 1 ? nearest_sorted_fast<kCbqFastLevels>(x, s_flev, coarse)
+                                      : nearest_level_loop(x, s_flev, kCbqFastLevels));
+    };
+
+    {  // the first codes, and with them the sums
+        const int mode = __builtin_amdgcn_readfirstlane(s_mode);
+        float coarse[kCbqFastLevels / 8 + 1];
+        load_coarse(coarse);
+        for (int r = tid; r < m; r += kCbqThreads) {
+            const int q = search(s_x[r], mode, coarse);
+            s_cd[r] = (uint8_t)q;
+            move(r, 0, q, true);
+        }
+    }
     __syncthreads();
 
     for (int it = 0; it < p.iters; ++it) {
@@ -504,18 +492,70 @@ __device__ void cbq_exact_rounds(const CbqParams& p, const CbqLayer& L, int m, f
             if (lane == 0) s_chg[it & 1] = 0;  // last read before the previous round's first barrier
         }
         __syncthreads();
-        if (code_all(false)) s_chg[it & 1] = 1;
+        const int mode = __builtin_amdgcn_readfirstlane(s_mode);
+        int chg = 0;
+        if (mode == 2) {
+            // code c stays while t_{c-1} <= v < t_c; the scalars that left their interval are
+            // queued and searched by dense lanes (a few per round: no wave runs the search for
+            // one lane)
+            // (a thread's up to four scalars: every code read first, then every bound)
+            constexpr int kPer = kCbqFastMax / kCbqThreads;
+            int c[kPer];
+            float x[kPer], tl[kPer], th[kPer];
+#pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                const int r = tid + u * kCbqThreads;
+                c[u] = r < m ? s_cd[r] : 0;
+                x[u] = r < m ? s_x[r] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                tl[u] = s_thr[c[u] > 0 ? c[u] - 1 : 0];
+                th[u] = s_thr[c[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < kPer; ++u) {
+                const int r = tid + u * kCbqThreads;
+                if (r < m && !((c[u] == 0 || tl[u] <= x[u]) && x[u] < th[u]))
+                    s_q[atomicAdd(&s_qn, 1u)] = (unsigned short)r;
+            }
+            __syncthreads();
+            const int n = (int)s_qn;
+            if (tid < n) {
+                float coarse[kCbqFastLevels / 8 + 1];
+                load_coarse(coarse);
+                for (int e = tid; e < n; e += kCbqThreads) {
+                    const int r = s_q[e];
+                    const int c = s_cd[r];
+                    const int q = code_from_thresholds<kCbqFastLevels>(s_x[r], s_thr, coarse);  // differs from c
+                    move(r, c, q, false);
+                    s_cd[r] = (uint8_t)q;
+                }
+                chg = 1;
+            }
+        } else {
+            float coarse[kCbqFastLevels / 8 + 1];
+            load_coarse(coarse);
+            for (int r = tid; r < m; r += kCbqThreads) {
+                const int c = s_cd[r];
+                const int q = search(s_x[r], mode, coarse);
+                if (q != c) {
+                    move(r, c, q, false);
+                    s_cd[r] = (uint8_t)q;
+                    chg = 1;
+                }
+            }
+        }
+        if (chg) s_chg[it & 1] = 1;
         __syncthreads();
         if (!s_chg[it & 1]) break;
     }
 
     if (tid < kCbqFastLevels) L.levels[tid] = s_flev[tid];
-#pragma unroll
-    for (int u = 0; u < kCbqFastPer; ++u) {
-        const int r = tid + u * kCbqThreads;
-        if (r >= m) continue;
-        L.codes[r] = (uint8_t)cd[u];
-        if (L.C_hat) L.C_hat[r] = s_flev[cd[u]];
+    for (int r = tid; r < m; r += kCbqThreads) {
+        const int c = s_cd[r];
+        L.codes[r] = (uint8_t)c;
+        if (L.C_hat) L.C_hat[r] = s_flev[c];
     }
 }
 
@@ -593,8 +633,11 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
     if (FAST64 && wk && m <= kCbqFastMax && sm >= 0.0f) {
         const float M = fmaxf(fabsf(lo), fabsf(hi));
         if (!(sm < exact_floor(M))) {  // every value meets the exactness condition
-            cbq_exact_rounds(p, L, m, lo, hi, M);
-            return;
+            if constexpr (LDS) {
+                cbq_exact_rounds(p, L, m, lo, hi, M, s_v, reinterpret_cast<unsigned*>(s_wt), s_code,
+                                 reinterpret_cast<unsigned short*>(s_dig));
+                return;
+            }
         }
     }
     if (LDS) {

@@ -84,6 +84,13 @@ __device__ __forceinline__ float sqdist9(const float* x, const float* c) {
 }
 
 __device__ __forceinline__ float min2(float a, float b) { return __builtin_amdgcn_fmed3f(a, b, -3.402823466e38f); }
+// the smallest of three finite values (v_min3_f32 without the compiler's NaN canonicalisation:
+// the operands are never NaN)
+__device__ __forceinline__ float min3f(float a, float b, float c) {
+    float r;
+    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
 
 // scores of codebook tiles 2p and 2p + 1 (A operands a) against one kernel tile (B operands b)
 __device__ __forceinline__ void score_pair(f32x16 (&acc)[2], const u32x4 (&a)[2][2], const u32x4 (&b)[2]) {
@@ -167,7 +174,7 @@ __device__ __forceinline__ void load_kernel(const DevLayer& L, int u, int lane, 
 // equal to the best, which the guard rejects, so either winner may be kept
 __device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d, float ob, float os, int oj,
                                            float od) {
-    const float mx = fmaxf(b, ob);
+    const float mx = __builtin_amdgcn_fmed3f(b, ob, __builtin_inff());  // the larger (neither is NaN)
     s = fminf(fminf(s, os), mx);
     const bool lt = ob < b;
     b = lt ? ob : b;
@@ -254,12 +261,12 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
         while (l2 + 1 < p.nlayers && u2 >= p.unit_begin[l2 + 1]) ++l2;
         const int r2 = u2 < u_end ? round_end(u2, l2) : u_end;
         const bool active2 = u2 + wave < r2;
+        // (every wave loads: past the round's end a clamped row of the layer holding u2, after the
+        // last round this unit's rows again; neither is used)
         float xn[kDim];
-        if (active2) {
-            load_kernel(p.L[l2], u2 + wave - p.unit_begin[l2], lane, xn);
-        } else {
-#pragma unroll
-            for (int d = 0; d < kDim; ++d) xn[d] = 0.0f;
+        {
+            const bool more = u2 < u_end;
+            load_kernel(p.L[more ? l2 : li], more ? u2 + wave - p.unit_begin[l2] : lu, lane, xn);
         }
 
         // B operands.  Kernel tile r of this wave is kernels 64 lu + 32 r + (lane % 32), the
@@ -385,19 +392,29 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             }
 
             // per kernel tile: smallest and second smallest slot minimum, the slot number q
-            // (rows 8 (q / 4) + 4 half + q % 4) packed into the low bits
+            // (rows 8 (q / 4) + 4 half + q % 4) packed into the low bits.  A tournament: the
+            // smallest and second smallest of each triple (min3, med3); for groups with such
+            // pairs (m, s), the set's smallest is the least m and its second smallest the
+            // smaller of the groups' second-least m and the least s (an s of a group that does
+            // not hold the minimum is at least that group's m)
             float m1[R], m2[R];
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                float a1 = __builtin_inff(), a2 = __builtin_inff();
+                float pq[16];
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const float pq = __uint_as_float((__float_as_uint(best[r][q]) & ~15u) | (unsigned)q);
-                    a2 = __builtin_amdgcn_fmed3f(a1, a2, pq);
-                    a1 = min2(a1, pq);
+                for (int q = 0; q < 16; ++q) pq[q] = __uint_as_float((__float_as_uint(best[r][q]) & ~15u) | (unsigned)q);
+                float tm[5], ts[5];
+#pragma unroll
+                for (int t = 0; t < 5; ++t) {
+                    tm[t] = min3f(pq[3 * t], pq[3 * t + 1], pq[3 * t + 2]);
+                    ts[t] = __builtin_amdgcn_fmed3f(pq[3 * t], pq[3 * t + 1], pq[3 * t + 2]);
                 }
-                m1[r] = a1;
-                m2[r] = a2;
+                const float ma = min3f(tm[0], tm[1], tm[2]);
+                const float sa = min2(__builtin_amdgcn_fmed3f(tm[0], tm[1], tm[2]), min3f(ts[0], ts[1], ts[2]));
+                const float mb = min3f(tm[3], tm[4], pq[15]);
+                const float sb = min2(__builtin_amdgcn_fmed3f(tm[3], tm[4], pq[15]), min2(ts[3], ts[4]));
+                m1[r] = min2(ma, mb);
+                m2[r] = __builtin_amdgcn_fmed3f(ma, mb, min2(sa, sb));
             }
             // own kernel: lanes < 32 tile 0, lanes >= 32 tile 1; first from the lower half's rows
             const auto x1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m1[0]), __float_as_uint(m1[1]), false, false);
@@ -414,8 +431,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             float bd = __builtin_inff();
             int bt = -1;  // tile of the best entry so far
             const int ntile = cn >> 5;  // the same trip count in every lane
-#pragma unroll 4
-            for (int tq = 0; tq < ntile; ++tq) {
+            auto rescore = [&](int tq) {
                 const int jl = slot + 32 * tq;
                 const f32x4 r0 = s_c[jl * 3 + 0], r1 = s_c[jl * 3 + 1];
                 const float c8 = s_cf[jl * kRowFloats + 8];
@@ -424,9 +440,23 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
                 const bool take = d < bd;
                 bd = take ? d : bd;
                 bt = take ? tq : bt;
+            };
+            if (ntile == 8) {  // 256 entries: constant tile numbers
+#pragma unroll
+                for (int tq = 0; tq < 8; ++tq) rescore(tq);
+            } else {
+#pragma unroll 4
+                for (int tq = 0; tq < ntile; ++tq) rescore(tq);
             }
             const int bj = bt < 0 ? 0x7fffffff : c0 + slot + 32 * bt;
-            merge_top2(rb, rs, rj, rd, M1, M2, bj, bd);
+            if (c0 == 0) {  // the first chunk starts the summary
+                rb = M1;
+                rs = M2;
+                rj = bj;
+                rd = bd;
+            } else {
+                merge_top2(rb, rs, rj, rd, M1, M2, bj, bd);
+            }
         }
         if (active) {  // settle this wave's unit
             float xn2 = 0.0f;

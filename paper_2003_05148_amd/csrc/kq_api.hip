@@ -537,6 +537,8 @@ static void fc_params(FcParams& p, const float* v, const int32_t* w, int64_t cou
     p.state = (int*)b;
     b += align256(sizeof(int) * 4);
     p.wg_changed = (int*)b;
+    b += align256(sizeof(int) * G);
+    p.tbl = (unsigned*)b;
 }
 
 size_t kq_quantize_scalars_workspace_bytes(int64_t count, int32_t bits) {

@@ -738,7 +738,8 @@ __global__ __launch_bounds__(kCbqThreads) void cbq_kernel(const CbqParams p) {
 //                     (subtracted from the old level, added to the new); it stores the
 //                     per-level digits and counts as its partial and whether it changed
 //                     any code;
-//   fc_sum_kernel     one workgroup per level adds the partials to the level's running
+//   fc_sum_kernel     one workgroup per level adds the partials (stored per level, one per
+//                     coding workgroup) to the level's running
 //                     exact sum and forms the candidate level fp32(round64(sum) / count);
 //   fc_state_kernel   one workgroup: a round that changed no code ends the run (every
 //                     later launch returns at once); otherwise the candidates become the
@@ -819,9 +820,21 @@ __global__ __launch_bounds__(kFcThreads) void fc_minmax_kernel(const FcParams p)
     }
 }
 
+// the bucket of x: (x - lo) * sc clamped to [0, kFcBuckets - 1] (NaN to 0), truncated.  Each
+// step is monotone, so x <= y gives bucket(x) <= bucket(y); the table and the coding launch
+// compute it with the same operations on the same lo and sc.
+__device__ __forceinline__ int fc_bucket(float x, float lo, float sc) {
+    const float t = (x - lo) * sc;
+    return (int)fminf(fmaxf(t, 0.0f), (float)(kFcBuckets - 1));
+}
+
 // thresholds of the levels s_lev (sorted unless s_unsorted) when every distance from the
 // data range to them is exact in fp64 (state[3]); otherwise state[3] = 0 and the codes
-// are found by the exact search.  Every thread of the workgroup calls it.
+// are found by the exact search.  With thresholds and a finite bucket scale the bucket
+// table follows: for bucket b, c = the number of thresholds whose bucket is below b (all
+// of them below every value of b) and n = the number inside b; entry b = (c | n << 8,
+// threshold c or +inf).  A value's code is then c plus the count of the n thresholds
+// c .. c + n - 1 at or below it.  Every thread of the workgroup calls it.
 __device__ void set_thresholds(const FcParams& p, const float* s_lev, int nlev, int unsorted, int* s_bad, float vmin,
                                float vmax, float vsm) {
     const int tid = threadIdx.x;
@@ -833,8 +846,52 @@ __device__ void set_thresholds(const FcParams& p, const float* s_lev, int nlev, 
     if (tid < nlev && s_lev[tid] != 0.0f && fabsf(s_lev[tid]) < fl) *s_bad = 1;
     __syncthreads();
     const int ok = *s_bad == 0;
-    if (tid < nlev) p.thr[tid] = (ok && tid + 1 < nlev) ? code_threshold(tid, s_lev, nlev, vmin, vmax) : __builtin_inff();
+    float t = __builtin_inff();
+    if (tid < nlev) {
+        t = (ok && tid + 1 < nlev) ? code_threshold(tid, s_lev, nlev, vmin, vmax) : __builtin_inff();
+        p.thr[tid] = t;
+    }
     if (tid == 0) p.state[3] = ok;
+    __shared__ float s_t[kCbqMaxLevels];
+    const float sc = (float)kFcBuckets / (vmax - vmin);
+    const bool table = ok && vmax > vmin && sc > 0.0f && sc < __builtin_inff();  // the same in every thread
+    if (tid == 0) p.range[3] = table ? sc : 0.0f;
+    if (!table) return;
+    // per bucket the number of thresholds in it; then each thread takes kPerThread consecutive
+    // buckets, and c of its first bucket is the exclusive prefix sum of the threads before it
+    static_assert(kFcBuckets % kCbqMaxLevels == 0, "whole runs of buckets per thread");
+    constexpr int kPerThread = kFcBuckets / kCbqMaxLevels;
+    __shared__ int s_n[kFcBuckets];
+    __shared__ int s_wsum[kCbqMaxLevels / kWave];
+    for (int b = tid; b < kFcBuckets; b += kCbqMaxLevels) s_n[b] = 0;
+    if (tid < nlev) s_t[tid] = t;
+    __syncthreads();
+    if (tid + 1 < nlev) atomicAdd(&s_n[fc_bucket(t, vmin, sc)], 1);  // thresholds 0 .. nlev - 2
+    __syncthreads();
+    int n[kPerThread], tot = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        n[i] = s_n[kPerThread * tid + i];
+        tot += n[i];
+    }
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    int inc = tot;  // inclusive scan over the wave
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(inc, off);
+        if (lane >= off) inc += o;
+    }
+    if (lane == kWave - 1) s_wsum[wave] = inc;
+    __syncthreads();
+    int c = inc - tot;
+    for (int w = 0; w < wave; ++w) c += s_wsum[w];
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+        const int b = kPerThread * tid + i;
+        p.tbl[2 * b] = (unsigned)c | ((unsigned)n[i] << 8);
+        p.tbl[2 * b + 1] = __float_as_uint(n[i] > 0 ? s_t[c] : __builtin_inff());
+        c += n[i];
+    }
 }
 
 // the uniform grid on [min, max]; clears the run state and the running sums
@@ -842,13 +899,34 @@ __global__ __launch_bounds__(kCbqMaxLevels) void fc_grid_kernel(const FcParams p
     __shared__ float s_lo, s_hi, s_sm;
     __shared__ float s_lev[kCbqMaxLevels];
     __shared__ int s_unsorted, s_bad;
+    __shared__ float s_w[3][kCbqMaxLevels / kWave];
     const int tid = threadIdx.x, nlev = 1 << p.bits;
-    if (tid == 0) {
+    {  // the workgroups' minima and maxima: strided per thread, then across the wave and the waves
         float lo = __builtin_inff(), hi = -__builtin_inff(), sm = __builtin_inff();
-        for (int b = 0; b < nblk; ++b) {
+        for (int b = tid; b < nblk; b += kCbqMaxLevels) {
             lo = fminf(lo, p.minmax[3 * b]);
             hi = fmaxf(hi, p.minmax[3 * b + 1]);
             sm = fminf(sm, p.minmax[3 * b + 2]);
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            lo = fminf(lo, __shfl_xor(lo, off));
+            hi = fmaxf(hi, __shfl_xor(hi, off));
+            sm = fminf(sm, __shfl_xor(sm, off));
+        }
+        if ((tid & (kWave - 1)) == 0) {
+            s_w[0][tid / kWave] = lo;
+            s_w[1][tid / kWave] = hi;
+            s_w[2][tid / kWave] = sm;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float lo = s_w[0][0], hi = s_w[1][0], sm = s_w[2][0];
+        for (int w = 1; w < kCbqMaxLevels / kWave; ++w) {
+            lo = fminf(lo, s_w[0][w]);
+            hi = fmaxf(hi, s_w[1][w]);
+            sm = fminf(sm, s_w[2][w]);
         }
         s_lo = lo;
         s_hi = hi;
@@ -885,6 +963,12 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     __shared__ __attribute__((aligned(16))) float s_lev[NLEV < 8 ? 8 : NLEV];
     __shared__ __attribute__((aligned(16))) float s_thr[NLEV < 8 ? 8 : NLEV];
     __shared__ unsigned long long s_dig[NLEV * kFcCols];
+    __shared__ uint2 s_tbl[THR ? kFcBuckets : 1];
+    // threshold rounds: per wave a queue of the scalars whose code changed (value, old and new
+    // code), whose sums are moved 64 at a time by the whole wave
+    constexpr int kQCap = 4 * kWave + kWave;  // a group step adds at most 4 per lane
+    __shared__ float s_qv[THR ? kFcThreads / kWave : 1][THR ? kQCap : 1];
+    __shared__ unsigned short s_qc[THR ? kFcThreads / kWave : 1][THR ? kQCap : 1];
     __shared__ int s_changed;
     if (fc_done(p)) return;
     if ((p.state[3] != 0) != THR) return;  // the other launch codes this round
@@ -893,6 +977,10 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         s_lev[e] = p.lev[e];
         s_thr[e] = p.thr[e];  // thr[NLEV - 1] is +inf
     }
+    const float blo = p.range[0], bsc = p.range[3];
+    const bool table = THR && bsc > 0.0f;  // the bucket table of this round's thresholds
+    if (table)
+        for (int e = tid; e < kFcBuckets; e += kFcThreads) s_tbl[e] = make_uint2(p.tbl[2 * e], p.tbl[2 * e + 1]);
     for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) s_dig[e] = 0ull;
     if (tid == 0) s_changed = 0;
     __syncthreads();
@@ -907,7 +995,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     int changed = 0;
     constexpr int kPer = 4;
     const long long m = p.m;
-    // one instantiation per search (thresholds, sorted levels, full scan): the choice is
+    // one instantiation per search (bucket table, thresholds, sorted levels, full scan): the choice is
     // the same for every scalar of the round
     auto run = [&](auto mode, auto weighted) {
         constexpr int kMode = decltype(mode)::value;
@@ -915,10 +1003,29 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         // the code of scalar r (value x, old code c); moves its exact contribution (weight
         // times value, and the weight into the count) when the code changes.  A weight of
         // zero or less contributes nothing, as in the single-workgroup quantizer.
-        auto recode = [&](long long r, float x, int c) {
-            const int q = kMode == 0   ? code_from_thresholds<NLEV>(x, s_thr, coarse)
-                          : kMode == 1 ? nearest_sorted_fast<NLEV>(x, s_lev, coarse_lev)
-                                       : nearest_level(x, s_lev, NLEV);
+        // the code of value x: the bucket table (two or more thresholds in the bucket: the
+        // rest one by one), or a search of the thresholds or levels
+        auto table_fixup = [&](float x, uint2 e, int q) {
+            if (e.x >= 512u) {  // two or more thresholds in the bucket
+                const int c = (int)(e.x & 255u), n = (int)(e.x >> 8);
+                for (int j = 1; j < n; ++j) q += s_thr[c + j] <= x ? 1 : 0;
+            }
+            return q;
+        };
+        auto search = [&](float x) {
+            if constexpr (kMode == 3) {
+                const uint2 e = s_tbl[fc_bucket(x, blo, bsc)];
+                return table_fixup(x, e, (int)(e.x & 255u) + (__uint_as_float(e.y) <= x ? 1 : 0));
+            } else {
+                return kMode == 0   ? code_from_thresholds<NLEV>(x, s_thr, coarse)
+                       : kMode == 1 ? nearest_sorted_fast<NLEV>(x, s_lev, coarse_lev)
+                                    : nearest_level(x, s_lev, NLEV);
+            }
+        };
+        // scalar r (value x, old code c) takes code q: its exact contribution (weight times
+        // value, and the weight into the count) moves when the code changes.  A weight of
+        // zero or less contributes nothing, as in the single-workgroup quantizer.
+        auto recode = [&](long long r, float x, int c, int q) {
             const int wt = kWeighted ? p.w[(unsigned)r / (unsigned)kDim] : 1;  // r < 2^31
             if (INIT) {
                 if (wt > 0) {
@@ -936,9 +1043,49 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
             }
             return q;
         };
+        // the wave's queue of changed scalars (threshold rounds, unweighted): a lane whose scalar
+        // changed appends (value, old code, new code) at the wave's count plus the number of
+        // lower lanes appending; drain moves the sums of 64 entries at a time from the queue's
+        // end, one per lane (all of them when `all`)
+        const int wv = tid / kWave, ln = tid & (kWave - 1);
+        int qn = 0;  // the same in every lane of the wave
+        auto enqueue = [&](bool ch, float x, int c, int q) {
+            if constexpr (THR) {
+                const unsigned long long mk = __ballot(ch);
+                if (mk == 0ull) return;
+                changed = 1;
+                if (ch) {
+                    const int pos = qn + (int)__builtin_amdgcn_mbcnt_hi((unsigned)(mk >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((unsigned)mk, 0u));
+                    s_qv[wv][pos] = x;
+                    s_qc[wv][pos] = (unsigned short)(c | (q << 8));
+                }
+                qn += __popcll(mk);
+            }
+        };
+        auto drain = [&](bool all) {
+            if constexpr (THR) {
+                while (qn >= kWave || (all && qn > 0)) {
+                    __builtin_amdgcn_wave_barrier();  // this wave's queue writes come first
+                    const int take = qn < kWave ? qn : kWave;
+                    if (ln < take) {
+                        const int at = qn - take + ln;
+                        const float x = s_qv[wv][at];
+                        const unsigned cq = s_qc[wv][at];
+                        const int c = (int)(cq & 255u), q = (int)(cq >> 8);
+                        add_exact(s_dig + c * kFcCols, -x, 1u);
+                        add_exact(s_dig + q * kFcCols, x, 1u);
+                        atomicAdd(&s_dig[c * kFcCols + kDigits], (unsigned long long)-1ll);
+                        atomicAdd(&s_dig[q * kFcCols + kDigits], 1ull);
+                    }
+                    __builtin_amdgcn_wave_barrier();  // read before the slots are reused
+                    qn -= take;
+                }
+            }
+        };
         // the grouped loop for threshold rounds (the large sets); the exact searches (small
         // sets, weighted codebooks, data where thresholds are refused) take one scalar at a time
-        if (kMode == 0 && (reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 &&
+        if ((kMode == 0 || kMode == 3) && (reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 &&
             (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
             // groups of four scalars: one float4 of values and one word of four codes per
             // group, kPer groups per thread, the next step's loaded while this one is coded;
@@ -963,16 +1110,53 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                 float4 xn[kPer];
                 unsigned cn[kPer];
                 if (g0 + step < ng) load(g0 + step, xn, cn);
+                float xs[kPer][4];
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    xs[j][0] = xv[j].x;
+                    xs[j][1] = xv[j].y;
+                    xs[j][2] = xv[j].z;
+                    xs[j][3] = xv[j].w;
+                }
+                int qs[kPer][4];
+                if constexpr (kMode == 3) {  // the step's sixteen table reads issued together
+                    uint2 te[kPer][4];
+#pragma unroll
+                    for (int j = 0; j < kPer; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) te[j][e] = s_tbl[fc_bucket(xs[j][e], blo, bsc)];
+                    unsigned many = 0u;
+#pragma unroll
+                    for (int j = 0; j < kPer; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            qs[j][e] = (int)(te[j][e].x & 255u) + (__uint_as_float(te[j][e].y) <= xs[j][e] ? 1 : 0);
+                            many |= te[j][e].x;
+                        }
+                    if (many >= 512u)
+#pragma unroll
+                        for (int j = 0; j < kPer; ++j)
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) qs[j][e] = table_fixup(xs[j][e], te[j][e], qs[j][e]);
+                }
 #pragma unroll
                 for (int j = 0; j < kPer; ++j) {
                     const long long g = g0 + (long long)j * kFcThreads;
-                    if (g >= ng) continue;
-                    const float xs[4] = {xv[j].x, xv[j].y, xv[j].z, xv[j].w};
+                    const bool have = g < ng;
                     unsigned nw = 0u;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        nw |= (unsigned)recode(4 * g + e, xs[e], (int)((cw[j] >> (8 * e)) & 255u)) << (8 * e);
-                    if (INIT || nw != cw[j]) c4[g] = nw;
+                    for (int e = 0; e < 4; ++e) {
+                        const int q = kMode == 3 ? qs[j][e] : search(xs[j][e]);
+                        const int c = (int)((cw[j] >> (8 * e)) & 255u);
+                        if (INIT) {
+                            if (have) recode(4 * g + e, xs[j][e], c, q);
+                        } else {
+                            enqueue(have && q != c, xs[j][e], c, q);
+                        }
+                        nw |= (unsigned)q << (8 * e);
+                    }
+                    if (have && (INIT || nw != cw[j])) c4[g] = nw;
+                    if (!INIT) drain(false);
                 }
 #pragma unroll
                 for (int j = 0; j < kPer; ++j) {
@@ -980,9 +1164,11 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                     cw[j] = cn[j];
                 }
             }
+            if (!INIT) drain(true);
             if (blockIdx.x == 0)  // the last m % 4 scalars
                 for (long long r = 4 * ng + tid; r < m; r += kFcThreads) {
-                    const int q = recode(r, p.v[r], INIT ? 0 : (int)p.codes[r]);
+                    const float x = p.v[r];
+                    const int q = recode(r, x, INIT ? 0 : (int)p.codes[r], search(x));
                     if (INIT || q != (int)p.codes[r]) p.codes[r] = (uint8_t)q;
                 }
         } else {
@@ -1000,7 +1186,7 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                 for (int j = 0; j < kPer; ++j) {
                     const long long r = r0 + (long long)j * kFcThreads;
                     if (r >= m) continue;
-                    const int q = recode(r, x[j], c[j]);
+                    const int q = recode(r, x[j], c[j], search(x[j]));
                     if (INIT || q != c[j]) p.codes[r] = (uint8_t)q;
                 }
             }
@@ -1013,8 +1199,11 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         else
             run(mode, std::integral_constant<bool, false>{});
     };
-    if constexpr (THR) {
-        run(std::integral_constant<int, 0>{}, std::integral_constant<bool, false>{});  // never weighted
+    if constexpr (THR) {  // never weighted
+        if (table)
+            run(std::integral_constant<int, 3>{}, std::integral_constant<bool, false>{});
+        else
+            run(std::integral_constant<int, 0>{}, std::integral_constant<bool, false>{});
     } else {
         if (sorted)
             pick(std::integral_constant<int, 1>{});
@@ -1023,8 +1212,12 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
     }
     if (changed) s_changed = 1;
     __syncthreads();
-    unsigned long long* part = (unsigned long long*)p.part + (size_t)blockIdx.x * NLEV * kFcCols;
-    for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) part[e] = s_dig[e];
+    // partial of level q at [q][workgroup]: a level's partials are contiguous for fc_sum_kernel
+    unsigned long long* part = (unsigned long long*)p.part;
+    for (int e = tid; e < NLEV * kFcCols; e += kFcThreads) {
+        const int q = e / kFcCols, c = e - q * kFcCols;
+        part[((size_t)q * gridDim.x + blockIdx.x) * kFcCols + c] = s_dig[e];
+    }
     if (tid == 0) p.wg_changed[blockIdx.x] = INIT ? 1 : s_changed;
 }
 
@@ -1054,42 +1247,71 @@ hipError_t launch_fc_assign(const FcParams& p, int G, hipStream_t s) {
 }
 
 // one workgroup per level: running exact sum += the partials; candidate level
-__global__ __launch_bounds__(kFcThreads) void fc_sum_kernel(const FcParams p, int nblk) {
-    __shared__ long long s_acc[kFcThreads / kWave][kFcCols];
+// v summed over the wave's 64 lanes (wrapping integer adds, any order), in every lane: the half
+// and row swaps, then DPP moves inside a row (the butterfly of the fp64 wave sum)
+__device__ __forceinline__ long long wave_sum_i64(long long v) {
+    auto add_pair = [](long long x, unsigned lo, unsigned hi) {
+        return x + (long long)(((unsigned long long)hi << 32) | lo);
+    };
+    {
+        const auto a = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+        const auto b = __builtin_amdgcn_permlane32_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
+        v = add_pair(add_pair(0, a[0], b[0]), a[1], b[1]);
+    }
+    {
+        const auto a = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+        const auto b = __builtin_amdgcn_permlane16_swap((unsigned)(v >> 32), (unsigned)(v >> 32), false, false);
+        v = add_pair(add_pair(0, a[0], b[0]), a[1], b[1]);
+    }
+    auto dpp = [&](auto ctl) {
+        constexpr int C = decltype(ctl)::value;
+        const unsigned lo = __builtin_amdgcn_mov_dpp((unsigned)v, C, 0xF, 0xF, true);
+        const unsigned hi = __builtin_amdgcn_mov_dpp((unsigned)(v >> 32), C, 0xF, 0xF, true);
+        v = add_pair(v, lo, hi);
+    };
+    dpp(std::integral_constant<int, 0x128>{});  // row_ror:8
+    dpp(std::integral_constant<int, 0x124>{});  // row_ror:4
+    dpp(std::integral_constant<int, 0x4E>{});   // quad_perm [2,3,0,1]
+    dpp(std::integral_constant<int, 0xB1>{});   // quad_perm [1,0,3,2]
+    return v;
+}
+
+// one 1024-thread workgroup per level: thread b reads partial b (the partials of a level are
+// contiguous); a workgroup whose codes did not change added nothing and is skipped (every
+// first-pass partial is read)
+constexpr int kFcSumThreads = kFcGrid;
+__global__ __launch_bounds__(kFcSumThreads) void fc_sum_kernel(const FcParams p, int nblk) {
+    __shared__ long long s_acc[kFcSumThreads / kWave][kFcCols];
     if (fc_done(p)) return;
     const int q = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nlev = 1 << p.bits;
-    long long a[kFcCols];
+    long long a[kFcCols], run[kFcCols];
 #pragma unroll
     for (int c = 0; c < kFcCols; ++c) a[c] = 0;
-    for (int b = tid; b < nblk; b += kFcThreads) {
-        const long long* src = p.part + ((size_t)b * nlev + q) * kFcCols;
+    if (tid == 0)  // the level's running sums, loaded while the partials are
 #pragma unroll
-        for (int c = 0; c < kFcCols; ++c) a[c] += src[c];
+        for (int c = 0; c < kFcCols; ++c) run[c] = p.S[q * kFcCols + c];
+    if (tid < nblk && p.wg_changed[tid] != 0) {
+        const long long* src = p.part + ((size_t)q * nblk + tid) * kFcCols;
+#pragma unroll
+        for (int c = 0; c < kFcCols; ++c) a[c] = src[c];
     }
 #pragma unroll
-    for (int c = 0; c < kFcCols; ++c) {
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) a[c] += __shfl_xor(a[c], off);
-    }
+    for (int c = 0; c < kFcCols; ++c) a[c] = wave_sum_i64(a[c]);
     if (lane == 0)
         for (int c = 0; c < kFcCols; ++c) s_acc[wave][c] = a[c];
     __syncthreads();
     if (tid == 0) {
         unsigned long long S[kDigits];
-        long long W = p.S[q * kFcCols + kDigits];
+#pragma unroll
         for (int c = 0; c < kFcCols; ++c) {
-            long long t = 0;
-            for (int w = 0; w < kFcThreads / kWave; ++w) t += s_acc[w][c];
-            if (c < kDigits) {
-                const long long v = p.S[q * kFcCols + c] + t;
-                p.S[q * kFcCols + c] = v;
-                S[c] = (unsigned long long)v;
-            } else {
-                W += t;
-                p.S[q * kFcCols + kDigits] = W;
-            }
+            long long t = run[c];
+            for (int w = 0; w < kFcSumThreads / kWave; ++w) t += s_acc[w][c];
+            run[c] = t;
+            if (c < kDigits) S[c] = (unsigned long long)t;
         }
+#pragma unroll
+        for (int c = 0; c < kFcCols; ++c) p.S[q * kFcCols + c] = run[c];
+        const long long W = run[kDigits];
         p.lev_next[q] = W > 0 ? (float)(digits_to_double(S) / (double)W) : p.lev[q];
     }
 }
@@ -1183,7 +1405,7 @@ hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s) {
         e = r == 0 ? launch_fc_assign<true>(p, G, s) : launch_fc_assign<false>(p, G, s);
         if (e != hipSuccess) return e;
         if (r == p.iters) break;  // the last codes need no further levels
-        hipLaunchKernelGGL(fc_sum_kernel, dim3(nlev), dim3(kFcThreads), 0, s, p, G);
+        hipLaunchKernelGGL(fc_sum_kernel, dim3(nlev), dim3(kFcSumThreads), 0, s, p, G);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(fc_state_kernel, dim3(1), dim3(kCbqMaxLevels), 0, s, p, G);
         if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -288,7 +288,7 @@ struct FcParams {
     int bits, iters;
     int thr_mode;          // codes from thresholds: 0 from 2^23 scalars on, 1 never, 2 whenever valid
     float* minmax;         // [grid][3] per-workgroup min, max, smallest nonzero magnitude
-    float* range;          // [3] the data's min, max, smallest nonzero magnitude
+    float* range;          // [4] the data's min, max, smallest nonzero magnitude; the bucket scale
     long long* part;       // [grid][levels][12] per-workgroup digits and counts
     long long* S;          // [levels][12] running exact sums and counts
     float* lev;            // [levels] current levels
@@ -296,13 +296,17 @@ struct FcParams {
     float* thr;            // [levels] code thresholds of the current levels (last one +inf)
     int* state;            // [0] converged, [1] level updates made, [2] levels unsorted, [3] thresholds valid
     int* wg_changed;       // [grid] a code changed in the workgroup
+    unsigned* tbl;         // [kFcBuckets][2] bucket table of the thresholds (range[3] > 0: valid)
 };
+// threshold rounds: the data range is cut into this many buckets of equal width; a scalar's
+// bucket gives the count of the thresholds below the bucket and the first one inside it
+constexpr int kFcBuckets = 2048;
 int fc_grid(long long m);
 inline size_t fc_ws_bytes(long long m, int bits) {
     const size_t G = (size_t)fc_grid(m), nlev = (size_t)1 << bits;
     return align256(sizeof(float) * (3 * G + 4)) + align256(sizeof(long long) * G * nlev * 12) +
            align256(sizeof(long long) * nlev * 12) + 3 * align256(sizeof(float) * nlev) + align256(sizeof(int) * 4) +
-           align256(sizeof(int) * G);
+           align256(sizeof(int) * G) + align256(sizeof(unsigned) * 2 * kFcBuckets);
 }
 hipError_t launch_fc_quantize(const FcParams& p, hipStream_t s);
 

@@ -1088,46 +1088,52 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
         if ((kMode == 0 || kMode == 3) && (reinterpret_cast<uintptr_t>(p.v) & 15u) == 0 &&
             (reinterpret_cast<uintptr_t>(p.codes) & 3u) == 0) {
             // groups of four scalars: one float4 of values and one word of four codes per
-            // group, kPer groups per thread, the next step's loaded while this one is coded;
-            // a group whose codes change stores its word
+            // group, kGPer groups per thread and step, the next step's loaded while this one is
+            // coded; a group whose codes change stores its word
+            constexpr int kGPer = 2;
             const long long ng = m >> 2;
-            const long long step = (long long)gridDim.x * kFcThreads * kPer;
+            const long long step = (long long)gridDim.x * kFcThreads * kGPer;
             const float4* __restrict__ v4 = reinterpret_cast<const float4*>(p.v);
             unsigned* __restrict__ c4 = reinterpret_cast<unsigned*>(p.codes);
-            auto load = [&](long long g0, float4 (&xv)[kPer], unsigned (&cw)[kPer]) {
+            auto load = [&](long long g0, float4 (&xv)[kGPer], unsigned (&cw)[kGPer]) {
 #pragma unroll
-                for (int j = 0; j < kPer; ++j) {
+                for (int j = 0; j < kGPer; ++j) {
                     const long long g = g0 + (long long)j * kFcThreads;
                     xv[j] = g < ng ? v4[g] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
                     cw[j] = (!INIT && g < ng) ? c4[g] : 0u;
                 }
             };
-            long long g0 = (long long)blockIdx.x * kFcThreads * kPer + tid;
-            float4 xv[kPer];
-            unsigned cw[kPer];
-            if (g0 < ng) load(g0, xv, cw);
-            for (; g0 < ng; g0 += step) {
-                float4 xn[kPer];
-                unsigned cn[kPer];
-                if (g0 + step < ng) load(g0 + step, xn, cn);
-                float xs[kPer][4];
+            long long g0 = (long long)blockIdx.x * kFcThreads * kGPer + tid;
+            // kDepth steps in flight: this one and the next (a sweep of groups per step and
+            // depth kept 2 and 2)
+            constexpr int kDepth = 2;
+            float4 xb[kDepth][kGPer];
+            unsigned cb[kDepth][kGPer];
 #pragma unroll
-                for (int j = 0; j < kPer; ++j) {
+            for (int d = 0; d < kDepth - 1; ++d)
+                if (g0 + d * step < ng) load(g0 + d * step, xb[d], cb[d]);
+            for (; g0 < ng; g0 += step) {
+                if (g0 + (kDepth - 1) * step < ng) load(g0 + (kDepth - 1) * step, xb[kDepth - 1], cb[kDepth - 1]);
+                float4 (&xv)[kGPer] = xb[0];
+                unsigned (&cw)[kGPer] = cb[0];
+                float xs[kGPer][4];
+#pragma unroll
+                for (int j = 0; j < kGPer; ++j) {
                     xs[j][0] = xv[j].x;
                     xs[j][1] = xv[j].y;
                     xs[j][2] = xv[j].z;
                     xs[j][3] = xv[j].w;
                 }
-                int qs[kPer][4];
-                if constexpr (kMode == 3) {  // the step's sixteen table reads issued together
-                    uint2 te[kPer][4];
+                int qs[kGPer][4];
+                if constexpr (kMode == 3) {  // the step's table reads issued together
+                    uint2 te[kGPer][4];
 #pragma unroll
-                    for (int j = 0; j < kPer; ++j)
+                    for (int j = 0; j < kGPer; ++j)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) te[j][e] = s_tbl[fc_bucket(xs[j][e], blo, bsc)];
                     unsigned many = 0u;
 #pragma unroll
-                    for (int j = 0; j < kPer; ++j)
+                    for (int j = 0; j < kGPer; ++j)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             qs[j][e] = (int)(te[j][e].x & 255u) + (__uint_as_float(te[j][e].y) <= xs[j][e] ? 1 : 0);
@@ -1135,12 +1141,12 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                         }
                     if (many >= 512u)
 #pragma unroll
-                        for (int j = 0; j < kPer; ++j)
+                        for (int j = 0; j < kGPer; ++j)
 #pragma unroll
                             for (int e = 0; e < 4; ++e) qs[j][e] = table_fixup(xs[j][e], te[j][e], qs[j][e]);
                 }
 #pragma unroll
-                for (int j = 0; j < kPer; ++j) {
+                for (int j = 0; j < kGPer; ++j) {
                     const long long g = g0 + (long long)j * kFcThreads;
                     const bool have = g < ng;
                     unsigned nw = 0u;
@@ -1159,10 +1165,12 @@ __global__ __launch_bounds__(kFcThreads) void fc_assign_kernel(const FcParams p)
                     if (!INIT) drain(false);
                 }
 #pragma unroll
-                for (int j = 0; j < kPer; ++j) {
-                    xv[j] = xn[j];
-                    cw[j] = cn[j];
-                }
+                for (int d = 0; d + 1 < kDepth; ++d)
+#pragma unroll
+                    for (int j = 0; j < kGPer; ++j) {
+                        xb[d][j] = xb[d + 1][j];
+                        cb[d][j] = cb[d + 1][j];
+                    }
             }
             if (!INIT) drain(true);
             if (blockIdx.x == 0)  // the last m % 4 scalars

@@ -235,12 +235,69 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     float xo[kDim];   // this lane's kernel of the current round
     load_kernel(p.L[li], ub + wave - p.unit_begin[li], lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
+    // entries c0 .. c0 + cn - 1 of layer L into LDS: A operands [w_h | w_h | w_m] of w = (-2c, |c|^2)
+    // and the fp32 rows (padding entries: screened far away, never taken by the rescoring)
+    auto stage = [&](const DevLayer& L, int c0, int cn) {
+        const int k = L.k;
+        for (int jl = tid; jl < cn; jl += kAssignWaves * kWave) {
+            const int j = c0 + jl;
+            float c[kDim], w[10];
+            if (j < k) {
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) c[d] = L.C[(size_t)j * kDim + d];
+                float nn = 0.0f;
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) {
+                    nn = __fmaf_rn(c[d], c[d], nn);
+                    w[d] = -2.0f * c[d];
+                }
+                w[9] = nn;
+            } else {  // padding: screened far away, and never taken by the rescoring
+#pragma unroll
+                for (int d = 0; d < kDim; ++d) {
+                    c[d] = __builtin_inff();
+                    w[d] = 0.0f;
+                }
+                w[9] = kPadScore;
+            }
+            unsigned H[5], M[5], A[16];
+#pragma unroll
+            for (int q = 0; q < 5; ++q) split2(w[2 * q], w[2 * q + 1], H[q], M[q]);
+            // [w_h pairs 0..4 | w_h pairs 0..4 | w_m pairs 0..4 | 0]
+#pragma unroll
+            for (int q = 0; q < 5; ++q) {
+                A[q] = H[q];
+                A[5 + q] = H[q];
+                A[10 + q] = M[q];
+            }
+            A[15] = 0u;
+            const int tl = jl >> 5, row = jl & 31;
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int e0 = 8 * kk + 4 * h;
+                    const u32x4 v = {A[e0], A[e0 + 1], A[e0 + 2], A[e0 + 3]};
+                    s_a[(tl * 2 + kk) * kWave + row + 32 * h] = v;
+                }
+            const f32x4 r0 = {c[0], c[1], c[2], c[3]}, r1 = {c[4], c[5], c[6], c[7]}, r2 = {c[8], 0.f, 0.f, 0.f};
+            s_c[jl * 3 + 0] = r0;
+            s_c[jl * 3 + 1] = r1;
+            s_c[jl * 3 + 2] = r2;
+        }
+    };
+    // the first layer's codebook, staged now so that its loads and the first kernels' are in
+    // flight together
+    if (((p.L[li].k + 63) & ~63) <= kAssignChunk) {
+        stage(p.L[li], 0, (p.L[li].k + 63) & ~63);
+        staged = li;
+    }
     int hl = li;      // fused: the layer whose sums the histogram holds
     if (FUSED) {
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
-        __syncthreads();
     }
+    __syncthreads();
 
 #pragma unroll 1
     while (ub < u_end) {
@@ -309,52 +366,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             const int cn = min(kAssignChunk, kpad - c0);
             if (!resident || staged != li) {
                 __syncthreads();  // every wave is done with the previous contents
-                for (int jl = tid; jl < cn; jl += kAssignWaves * kWave) {
-                    const int j = c0 + jl;
-                    float c[kDim], w[10];
-                    if (j < k) {
-#pragma unroll
-                        for (int d = 0; d < kDim; ++d) c[d] = C[(size_t)j * kDim + d];
-                        float nn = 0.0f;
-#pragma unroll
-                        for (int d = 0; d < kDim; ++d) {
-                            nn = __fmaf_rn(c[d], c[d], nn);
-                            w[d] = -2.0f * c[d];
-                        }
-                        w[9] = nn;
-                    } else {  // padding: screened far away, and never taken by the rescoring
-#pragma unroll
-                        for (int d = 0; d < kDim; ++d) {
-                            c[d] = __builtin_inff();
-                            w[d] = 0.0f;
-                        }
-                        w[9] = kPadScore;
-                    }
-                    unsigned H[5], M[5], A[16];
-#pragma unroll
-                    for (int q = 0; q < 5; ++q) split2(w[2 * q], w[2 * q + 1], H[q], M[q]);
-                    // [w_h pairs 0..4 | w_h pairs 0..4 | w_m pairs 0..4 | 0]
-#pragma unroll
-                    for (int q = 0; q < 5; ++q) {
-                        A[q] = H[q];
-                        A[5 + q] = H[q];
-                        A[10 + q] = M[q];
-                    }
-                    A[15] = 0u;
-                    const int tl = jl >> 5, row = jl & 31;
-#pragma unroll
-                    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            const int e0 = 8 * kk + 4 * h;
-                            const u32x4 v = {A[e0], A[e0 + 1], A[e0 + 2], A[e0 + 3]};
-                            s_a[(tl * 2 + kk) * kWave + row + 32 * h] = v;
-                        }
-                    const f32x4 r0 = {c[0], c[1], c[2], c[3]}, r1 = {c[4], c[5], c[6], c[7]}, r2 = {c[8], 0.f, 0.f, 0.f};
-                    s_c[jl * 3 + 0] = r0;
-                    s_c[jl * 3 + 1] = r1;
-                    s_c[jl * 3 + 2] = r2;
-                }
+                stage(L, c0, cn);
                 __syncthreads();
                 staged = resident ? li : -1;
             }

@@ -41,6 +41,10 @@ def data(kind, m, seed):
         return np.full(m, -0.375, np.float32)
     if kind == "integers":                     # exact ties and midpoints between levels
         return rng.integers(-40, 41, m).astype(np.float32)
+    if kind == "outliers":                      # a few far values: many thresholds share a bucket
+        v = 1.0 + rng.standard_normal(m) * 0.01  # (no tiny values, so thresholds are allowed)
+        v[rng.choice(m, min(m, 8), replace=False)] = rng.choice([-500.0, 500.0], min(m, 8))
+        return v.astype(np.float32)
     if kind == "tiny":                          # subnormal and zero values among normal ones
         v = (rng.standard_normal(m) * 1e-3).astype(np.float32)
         v[::7] = np.float32(3e-42)
@@ -60,7 +64,7 @@ def check(v, bits, iters, tag):
 
 
 @pytest.mark.parametrize("m", [1, 2, 9, 1000, 65537])
-@pytest.mark.parametrize("kind", ["normal", "heavy", "integers", "tiny"])
+@pytest.mark.parametrize("kind", ["normal", "heavy", "integers", "tiny", "outliers"])
 def test_fc_quantizer_bit_exact(m, kind):
     check(data(kind, m, m + len(kind)), 6, 30, f"{kind} m={m}")
 
@@ -103,12 +107,14 @@ def test_fc_quantizer_full_size_fc6_properties():
                 assert L[q] == np.float32(math.fsum(mem.tolist()) / mem.size), q
 
 
-@pytest.mark.parametrize("kind", ["normal", "integers", "tiny"])
+@pytest.mark.parametrize("kind", ["normal", "integers", "tiny", "outliers"])
 def test_fc_threshold_path_equals_the_exact_search(kind):
-    """From 3 * 2^20 scalars on, codes come from per-level thresholds (fp32 comparisons);
-    with KQ_F_EXACT_SEARCH every code comes from the exact fp64 search.  Both agree bit
-    for bit, also on integer data (exact midpoints between levels) and on data whose tiny
-    values make fp64 distances inexact (the thresholds are then not used)."""
+    """From 3 * 2^20 scalars on, codes come from per-level thresholds (a bucket table over
+    the data range, fp32 comparisons); with KQ_F_EXACT_SEARCH every code comes from the
+    exact fp64 search.  Both agree bit for bit, also on integer data (exact midpoints
+    between levels), on data whose tiny values make fp64 distances inexact (the thresholds
+    are then not used) and on data with a few far values, where most thresholds fall into
+    one bucket and are compared one by one."""
     m = 9 * 932068                                            # 8,388,612 >= 3 * 2^20
     vd = dev(data(kind, m, 77))
     a = kq.kq_quantize_scalars(vd, 6, 30)

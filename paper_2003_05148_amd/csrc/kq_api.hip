@@ -145,26 +145,19 @@ bool fusable(const kq_layer* layers, int32_t l0, int32_t l1) {
     return true;
 }
 
-// The fused assignment's partials: with the persistent grid of the assignment launch over
-// layers [l0, l1), workgroup w walks units [w T / G, (w + 1) T / G); a layer's partials
-// are those of the workgroups whose runs touch its units.  For every layer: the first such
-// workgroup and their number.
-void fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, int* nslots) {
-    long long T = 0;
-    for (int32_t l = l0; l < l1; ++l) T += assign_units(layers[l].n);
-    const long long G = assign_grid((int)T);
-    long long b = 0;
-    for (int32_t l = l0; l < l1; ++l) {
-        const long long e = b + assign_units(layers[l].n);  // units [b, e)
-        long long w0 = b * G / T;                           // a first guess, then exact
-        while (w0 > 0 && w0 * T / G > b) --w0;
-        while ((w0 + 1) * T / G <= b) ++w0;
-        long long w1 = w0;
-        while ((w1 + 1) * T / G <= e - 1) ++w1;
-        wfirst[l - l0] = (int)w0;
-        nslots[l - l0] = (int)(w1 - w0 + 1);
-        b = e;
+// The assignment's workgroups over layers [l0, l1): each layer gets its own workgroups
+// (assign_partition), which split its units evenly; a layer's fused partials are those of
+// its workgroups.  For every layer: its first workgroup and their number; returns the grid.
+int fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, int* nslots) {
+    int units[KQ_MAX_STACK];
+    for (int32_t l = l0; l < l1; ++l) units[l - l0] = assign_units(layers[l].n);
+    const int grid = assign_partition(units, l1 - l0, nslots);
+    int w = 0;
+    for (int32_t l = 0; l < l1 - l0; ++l) {
+        wfirst[l] = w;
+        w += nslots[l];
     }
+    return grid;
 }
 
 // assignment of layers [l0, l1) (+ the distortion finish when any layer asks for it);
@@ -174,9 +167,10 @@ kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
                      bool fused = false, const float* const* C_alt = nullptr, void* const* events = nullptr) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Assign, slot, C_alt, 0);
-    if (fused) {
+    {
         int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
-        fused_slots(layers, l0, l1, wf, ns);
+        p.assign_grid = fused_slots(layers, l0, l1, wf, ns);
+        for (int l = 0; l < KQ_MAX_STACK; ++l) p.wg_begin[l] = l < p.nlayers ? wf[l] : 0x7fffffff;
         for (int l = 0; l < p.nlayers; ++l) p.L[l].wfirst = wf[l];
     }
     hipEvent_t e0 = events ? (hipEvent_t)events[0] : nullptr, e1 = events ? (hipEvent_t)events[1] : nullptr;

@@ -216,9 +216,16 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const long long T = p.total_units;
-    const int u_end = (int)((long long)(blockIdx.x + 1) * T / gridDim.x);
-    int ub = (int)((long long)blockIdx.x * T / gridDim.x);
+    // this workgroup's run: a share of one layer's units (the layer's workgroups split them evenly)
+    int lb = 0;
+#pragma unroll
+    for (int l = 1; l < KQ_MAX_STACK; ++l) lb += (int)blockIdx.x >= p.wg_begin[l] ? 1 : 0;
+    const int g0 = p.wg_begin[lb];
+    const int gl = (lb + 1 < p.nlayers ? p.wg_begin[lb + 1] : (int)gridDim.x) - g0;
+    const int U = p.L[lb].nunits, j = (int)blockIdx.x - g0;
+    const int q = U / gl, r = U - q * gl;  // workgroup j: q units, one more for the first r
+    int ub = p.unit_begin[lb] + j * q + min(j, r);
+    const int u_end = ub + q + (j < r ? 1 : 0);
     if (ub >= u_end) return;
 
     // Rounds: up to kAssignWaves consecutive units of one layer, unit ub + wave for each wave
@@ -590,8 +597,37 @@ __global__ __launch_bounds__(kSumThreads) void assign_finish_kernel(const StackP
 
 int assign_grid(int total_units) { return total_units < kAssignGridMax ? total_units : kAssignGridMax; }
 
+int assign_partition(const int* units, int nlayers, int* g) {
+    long long T = 0;
+    int umax = 1;
+    for (int l = 0; l < nlayers; ++l) {
+        T += units[l];
+        umax = units[l] > umax ? units[l] : umax;
+    }
+    auto count = [&](long long t) {
+        long long c = 0;
+        for (int l = 0; l < nlayers; ++l) c += (units[l] + t - 1) / t;
+        return c;
+    };
+    long long lo = (T + kAssignGridMax - 1) / kAssignGridMax, hi = umax;  // count(hi) = nlayers <= the grid
+    if (lo < 1) lo = 1;
+    while (lo < hi) {
+        const long long mid = (lo + hi) / 2;
+        if (count(mid) <= kAssignGridMax)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    int grid = 0;
+    for (int l = 0; l < nlayers; ++l) {
+        g[l] = (int)((units[l] + lo - 1) / lo);
+        grid += g[l];
+    }
+    return grid;
+}
+
 hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused, hipEvent_t start, hipEvent_t stop) {
-    const int grid = assign_grid(p.total_units);
+    const int grid = p.assign_grid;
     const dim3 g(grid), b(kAssignWaves * kWave);
     if (start || stop) {  // the events take the kernel's own start and end times
         if (fused)

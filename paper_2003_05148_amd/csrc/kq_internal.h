@@ -173,6 +173,8 @@ struct StackParams {
     int total_units;
     unsigned* range_flags;    // per layer: a non-finite value was seen (absmax launches), or null
     int unit_begin[KQ_MAX_STACK];
+    int wg_begin[KQ_MAX_STACK];  // assignment: first workgroup of each layer (0x7fffffff past the last)
+    int assign_grid;             // assignment: the number of workgroups
     DevLayer L[KQ_MAX_STACK];
 };
 
@@ -248,6 +250,9 @@ __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src
 constexpr int kSumThreads = 640;
 
 // launchers (return hipSuccess or the launch error)
+// the assignment's workgroups per layer (every workgroup works on one layer): g[l] =
+// ceil(units_l / t) for the smallest t with sum g[l] <= kAssignGridMax; returns the grid
+int assign_partition(const int* units, int nlayers, int* g);
 hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused = false, hipEvent_t start = nullptr,
                          hipEvent_t stop = nullptr);
 int assign_grid(int total_units);

@@ -35,15 +35,17 @@
 // asked for: every entry with P_j <= Q then has finite partial sums, while a screened
 // score of a farther entry may overflow to +inf or NaN, which the slot minima skip.
 //
-// Grid.  Kernels are cut into tiles of 256 (one per workgroup pass); tiles of all
-// layers of a stack are numbered layer after layer and a persistent grid of at most
-// kAssignGridMax workgroups walks contiguous runs of them.  A codebook of up to
-// kAssignChunk entries is split and staged once per layer in LDS, in the MFMA A-operand
+// Grid.  Kernels are cut into units of 64 (one kernel per lane of a wave).  The grid of
+// at most kAssignGridMax workgroups is split per layer: layer l gets ceil(U_l / t)
+// workgroups, t the smallest unit count per workgroup for which the total fits, and its
+// U_l units are spread evenly over them, so a workgroup works within one layer; its waves
+// take consecutive units round by round.  A codebook of up to kAssignChunk entries is
+// split and staged once in LDS, in the MFMA A-operand
 // order [tile][k-step][lane][8 x bf16] (one conflict-free ds_read_b128 per MFMA
 // operand) and as fp32 rows for the slot rescoring; larger ones are streamed through LDS
 // chunk by chunk.  Each lane splits its own kernel; the B operands of the two 32-kernel
 // tiles of a wave are exchanged between the lane halves with v_permlane32_swap.  The next
-// tile's kernels are loaded while the current one is scored.  After the scoring each wave
+// round's kernels are loaded while the current ones are scored.  After the scoring each wave
 // settles its own 64 kernels (no workgroup barrier) and, when asked, writes an fp64
 // distortion partial; a second kernel sums the partials in a fixed order.
 #include <hip/hip_ext.h>
@@ -184,25 +186,16 @@ __device__ __forceinline__ void merge_top2(float& b, float& s, int& j, float& d,
 
 // Fused variant (every codebook of at most kFuseMaxK entries): each lane also adds its
 // settled kernel to the workgroup's LDS histogram of exact fixed-point member sums, which
-// is stored as the partial of (layer, workgroup) whenever the workgroup's run of units
-// leaves a layer; the update then needs only its finishing launch.
-template <int CHUNK, bool FUSED>
-__device__ __forceinline__ void fused_flush(const StackParams& p, int l, unsigned long long* s_sum, unsigned* s_cnt,
+// is stored as the partial of (layer, workgroup) when the workgroup's units are done; the
+// update then needs only its finishing launch.
+__device__ __forceinline__ void fused_store(const DevLayer& H, const unsigned long long* s_sum, const unsigned* s_cnt,
                                             int tid) {
     __syncthreads();  // every wave has added its kernels
-    const DevLayer& H = p.L[l];
     unsigned long long* out = (unsigned long long*)H.hist + (size_t)(blockIdx.x - H.wfirst) * H.k * 10;
     for (int e = tid; e < H.k * 10; e += kAssignWaves * kWave) {
         const int j = e / 10, d = e - 10 * j;
-        if (d == 9) {
-            out[e] = s_cnt[j];
-            s_cnt[j] = 0u;
-        } else {
-            out[e] = s_sum[j * kDim + d];
-            s_sum[j * kDim + d] = 0ull;
-        }
+        out[e] = d == 9 ? (unsigned long long)s_cnt[j] : s_sum[j * kDim + d];
     }
-    __syncthreads();  // cleared before the next kernels are added
 }
 
 template <int R, bool FUSED>
@@ -222,25 +215,17 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     for (int l = 1; l < KQ_MAX_STACK; ++l) lb += (int)blockIdx.x >= p.wg_begin[l] ? 1 : 0;
     const int g0 = p.wg_begin[lb];
     const int gl = (lb + 1 < p.nlayers ? p.wg_begin[lb + 1] : (int)gridDim.x) - g0;
-    const int U = p.L[lb].nunits, j = (int)blockIdx.x - g0;
+    const DevLayer& L = p.L[lb];
+    const int U = L.nunits, j = (int)blockIdx.x - g0;
     const int q = U / gl, r = U - q * gl;  // workgroup j: q units, one more for the first r
-    int ub = p.unit_begin[lb] + j * q + min(j, r);
+    int ub = j * q + min(j, r);            // units of the layer, [ub, u_end)
     const int u_end = ub + q + (j < r ? 1 : 0);
     if (ub >= u_end) return;
 
-    // Rounds: up to kAssignWaves consecutive units of one layer, unit ub + wave for each wave
-    // (a wave past the round's end idles, but takes part in every barrier).  [ub, r_end) is
-    // the round, li its layer.
-    auto round_end = [&](int u0, int l) {
-        const int le = l + 1 < KQ_MAX_STACK ? p.unit_begin[l + 1] : 0x7fffffff;
-        return min(min(u0 + kAssignWaves, u_end), le);
-    };
-    int li = find_layer(p, ub);
-    int r_end = round_end(ub, li);
-    bool active = ub + wave < r_end;
-    int staged = -1;  // layer whose whole codebook is resident in LDS
-    float xo[kDim];   // this lane's kernel of the current round
-    load_kernel(p.L[li], ub + wave - p.unit_begin[li], lane, xo);
+    // Rounds: up to kAssignWaves consecutive units, unit ub + wave for each wave (a wave past
+    // the run's end idles, but takes part in every barrier).
+    float xo[kDim];  // this lane's kernel of the current round
+    load_kernel(L, ub + wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
     // entries c0 .. c0 + cn - 1 of layer L into LDS: A operands [w_h | w_h | w_m] of w = (-2c, |c|^2)
     // and the fp32 rows (padding entries: screened far away, never taken by the rescoring)
@@ -293,13 +278,12 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             s_c[jl * 3 + 2] = r2;
         }
     };
-    // the first layer's codebook, staged now so that its loads and the first kernels' are in
-    // flight together
-    if (((p.L[li].k + 63) & ~63) <= kAssignChunk) {
-        stage(p.L[li], 0, (p.L[li].k + 63) & ~63);
-        staged = li;
-    }
-    int hl = li;      // fused: the layer whose sums the histogram holds
+    // the codebook, staged now so that its loads and the first kernels' are in flight together
+    const int n = L.n, k = L.k;
+    const float* __restrict__ C = L.C;
+    const int kpad = (k + 63) & ~63;
+    const bool resident = kpad <= kAssignChunk;  // the whole codebook stays in LDS
+    if (resident) stage(L, 0, kpad);
     if (FUSED) {
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
@@ -308,30 +292,17 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 
 #pragma unroll 1
     while (ub < u_end) {
-        if (FUSED && li != hl) {  // the run left layer hl: store its sums
-            fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
-            hl = li;
-        }
-        const DevLayer& L = p.L[li];
-        const int n = L.n, k = L.k;
-        const float* __restrict__ C = L.C;
-        const int lu = ub + wave - L.unit_begin;  // this wave's unit of the layer
+        const int lu = ub + wave;  // this wave's unit of the layer
         const int i = lu * kWave + lane;
+        const bool active = lu < u_end;
         const bool valid = active && i < n;
 
-        // the next round; its kernel is prefetched while this one is scored
-        const int u2 = r_end;
-        int l2 = li;
-        while (l2 + 1 < p.nlayers && u2 >= p.unit_begin[l2 + 1]) ++l2;
-        const int r2 = u2 < u_end ? round_end(u2, l2) : u_end;
-        const bool active2 = u2 + wave < r2;
-        // (every wave loads: past the round's end a clamped row of the layer holding u2, after the
-        // last round this unit's rows again; neither is used)
+        // the next round's kernel, prefetched while this one is scored (every wave loads: past
+        // the run's end a clamped row, after the last round this unit's rows again; neither is
+        // used)
+        const int u2 = ub + kAssignWaves;
         float xn[kDim];
-        {
-            const bool more = u2 < u_end;
-            load_kernel(p.L[more ? l2 : li], more ? u2 + wave - p.unit_begin[l2] : lu, lane, xn);
-        }
+        load_kernel(L, u2 < u_end ? u2 + wave : lu, lane, xn);
 
         // B operands.  Kernel tile r of this wave is kernels 64 lu + 32 r + (lane % 32), the
         // kernels of lanes 32 r .. 32 r + 31.  A lane past the end holds a copy of the last
@@ -366,16 +337,13 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 
         float rb = __builtin_inff(), rs = __builtin_inff(), rd = __builtin_inff();  // running summary
         int rj = 0x7fffffff;
-        const int kpad = (k + 63) & ~63;
-        const bool resident = kpad <= kAssignChunk;
 #pragma unroll 1
         for (int c0 = 0; c0 < kpad; c0 += kAssignChunk) {
             const int cn = min(kAssignChunk, kpad - c0);
-            if (!resident || staged != li) {
+            if (!resident) {
                 __syncthreads();  // every wave is done with the previous contents
                 stage(L, c0, cn);
                 __syncthreads();
-                staged = resident ? li : -1;
             }
 
             if (!active) continue;  // an idle wave only helps to stage
@@ -579,11 +547,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xo[d] = xn[d];
         ub = u2;
-        li = l2;
-        r_end = r2;
-        active = active2;
     }
-    if (FUSED) fused_flush<kAssignChunk, FUSED>(p, hl, s_sum, s_cnt, tid);
+    if (FUSED) fused_store(L, s_sum, s_cnt, tid);
 }
 
 // distortion of each layer: its per-wave partials summed in a fixed order

@@ -206,6 +206,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     __shared__ f32x4 s_c[kAssignChunk * kRowFloats / 4];   // fp32 rows of the staged entries
     __shared__ unsigned long long s_sum[FUSED ? kFuseMaxK * kDim : 1];  // fused: member sums
     __shared__ unsigned s_cnt[FUSED ? kFuseMaxK : 1];                   // fused: member counts
+    __shared__ int s_next;                                              // fused: the next unit to hand out
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
@@ -222,8 +223,11 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     const int u_end = ub + q + (j < r ? 1 : 0);
     if (ub >= u_end) return;
 
-    // Rounds: up to kAssignWaves consecutive units, unit ub + wave for each wave (a wave past
-    // the run's end idles, but takes part in every barrier).
+    // The plain kernel goes in rounds of kAssignWaves consecutive units, unit ub + wave for
+    // each wave (a wave past the run's end idles, but takes part in every barrier: a streamed
+    // codebook is staged chunk by chunk).  The fused kernel's codebook is always resident, so
+    // its loop has no barrier: each wave starts with unit ub + wave and then takes the next
+    // unit from an LDS counter, so that a wave its SIMD serves less often takes fewer units.
     float xo[kDim];  // this lane's kernel of the current round
     load_kernel(L, ub + wave, lane, xo);
     const float* s_cf = reinterpret_cast<const float*>(s_c);
@@ -283,26 +287,37 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     const float* __restrict__ C = L.C;
     const int kpad = (k + 63) & ~63;
     const bool resident = kpad <= kAssignChunk;  // the whole codebook stays in LDS
+    if (FUSED && !resident) return;              // (the host fuses only codebooks that fit)
     if (resident) stage(L, 0, kpad);
     if (FUSED) {
+        if (tid == 0) s_next = ub + kAssignWaves;
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
     }
     __syncthreads();
 
+    // fused: this wave's unit (uniform over the wave); plain: the round's first unit
+    int cur = FUSED ? __builtin_amdgcn_readfirstlane(ub + wave) : ub;
 #pragma unroll 1
-    while (ub < u_end) {
-        const int lu = ub + wave;  // this wave's unit of the layer
+    while (cur < u_end) {
+        const int lu = FUSED ? cur : cur + wave;  // this wave's unit of the layer
         const int i = lu * kWave + lane;
-        const bool active = lu < u_end;
+        const bool active = FUSED || lu < u_end;
         const bool valid = active && i < n;
 
-        // the next round's kernel, prefetched while this one is scored (every wave loads: past
-        // the run's end a clamped row, after the last round this unit's rows again; neither is
-        // used)
-        const int u2 = ub + kAssignWaves;
+        // the next unit's kernel, prefetched while this one is scored (every wave loads: past
+        // the run's end a clamped row or another workgroup's, after its last unit this unit's
+        // rows again; none is used)
+        int nxt;
+        if constexpr (FUSED) {
+            int g = 0;
+            if (lane == 0) g = atomicAdd(&s_next, 1);
+            nxt = __builtin_amdgcn_readfirstlane(g);
+        } else {
+            nxt = cur + kAssignWaves;
+        }
         float xn[kDim];
-        load_kernel(L, u2 < u_end ? u2 + wave : lu, lane, xn);
+        load_kernel(L, nxt < u_end ? (FUSED ? nxt : nxt + wave) : lu, lane, xn);
 
         // B operands.  Kernel tile r of this wave is kernels 64 lu + 32 r + (lane % 32), the
         // kernels of lanes 32 r .. 32 r + 31.  A lane past the end holds a copy of the last
@@ -340,7 +355,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 #pragma unroll 1
         for (int c0 = 0; c0 < kpad; c0 += kAssignChunk) {
             const int cn = min(kAssignChunk, kpad - c0);
-            if (!resident) {
+            if (!FUSED && !resident) {
                 __syncthreads();  // every wave is done with the previous contents
                 stage(L, c0, cn);
                 __syncthreads();
@@ -546,7 +561,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
 
 #pragma unroll
         for (int d = 0; d < kDim; ++d) xo[d] = xn[d];
-        ub = u2;
+        cur = nxt;
     }
     if (FUSED) fused_store(L, s_sum, s_cnt, tid);
 }

@@ -78,6 +78,19 @@ def test_fused_rounds_vgg16_k256_full_size():
     step_locked_fused(layers, 1, "vgg16 k=256")
 
 
+def test_fused_rounds_ragged_long_stack():
+    """20 layers (two launches of at most 16), from one kernel to 50,000: layers of fewer
+    64-kernel units than a workgroup has waves, unit counts that do not divide evenly over a
+    layer's workgroups, and codebooks of 1 to 256 entries."""
+    sizes = [1, 5, 63, 64, 65, 700, 4096, 4097, 20000, 3, 128, 129, 777, 50000, 10, 2, 9000, 837, 1000, 31]
+    ks = [1, 2, 17, 64, 200, 256, 256, 255, 256, 3, 128, 64, 100, 256, 7, 2, 256, 37, 160, 31]
+    layers = []
+    for i, (n, k) in enumerate(zip(sizes, ks)):
+        X = synth.laplace_layer(1, n, 900 + i) * np.float32(1 + 0.5 * i)
+        layers.append(synth.make_layer(f"r{i}", X, k, 50 + i))
+    step_locked_fused(layers, 2, "ragged")
+
+
 def test_fit_stack_step_locked_resnet18():
     """kq_fit_stack itself (one Lloyd round and the final assignment per call) from the
     oracle's codebook, twice: its C, final indices, counts and both distortions."""

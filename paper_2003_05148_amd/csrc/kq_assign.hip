@@ -211,13 +211,22 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     // this workgroup's run: a share of one layer's units (the layer's workgroups split them evenly)
-    int lb = 0;
+    // (the table of first workgroups is read once, and the layer's fields in one batch after
+    // it: every dependent load of the arguments is a memory round trip before any work)
+    int lb = 0, g0 = 0, g1 = (int)gridDim.x;
 #pragma unroll
     for (int l = 1; l < KQ_MAX_STACK; ++l) lb += (int)blockIdx.x >= p.wg_begin[l] ? 1 : 0;
-    const int g0 = p.wg_begin[lb];
-    const int gl = (lb + 1 < p.nlayers ? p.wg_begin[lb + 1] : (int)gridDim.x) - g0;
+#pragma unroll
+    for (int l = 0; l < KQ_MAX_STACK; ++l) {  // past the last layer the table holds 0x7fffffff
+        g0 = l == lb ? p.wg_begin[l] : g0;
+        g1 = l == lb + 1 ? min(p.wg_begin[l], (int)gridDim.x) : g1;
+    }
+    const int gl = g1 - g0;
     const DevLayer& L = p.L[lb];
-    const int U = L.nunits, j = (int)blockIdx.x - g0;
+    const int n = L.n, k = L.k, U = L.nunits, j = (int)blockIdx.x - g0;
+    const float* __restrict__ C = L.C;
+    const float* const Xl = L.X;
+    asm volatile("" ::"s"(n), "s"(k), "s"(U), "s"(C), "s"(Xl));
     const int q = U / gl, r = U - q * gl;  // workgroup j: q units, one more for the first r
     int ub = j * q + min(j, r);            // units of the layer, [ub, u_end)
     const int u_end = ub + q + (j < r ? 1 : 0);
@@ -283,8 +292,6 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
         }
     };
     // the codebook, staged now so that its loads and the first kernels' are in flight together
-    const int n = L.n, k = L.k;
-    const float* __restrict__ C = L.C;
     const int kpad = (k + 63) & ~63;
     const bool resident = kpad <= kAssignChunk;  // the whole codebook stays in LDS
     if (FUSED && !resident) return;              // (the host fuses only codebooks that fit)
@@ -294,6 +301,8 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
     }
+    // fused: the scale of the layer's fixed-point sums, read once
+    const double fsc = FUSED ? fixed_scale((int)L.xmax[L.nxmax]) : 0.0;
     __syncthreads();
 
     // fused: this wave's unit (uniform over the wave); plain: the round's first unit
@@ -547,10 +556,9 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             }
 
             if (FUSED && valid) {  // the update's exact member sums of this kernel, at the layer's shift
-                const double sc = fixed_scale((int)L.xmax[L.nxmax]);
                 atomicAdd(&s_cnt[myj], 1u);
 #pragma unroll
-                for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_bits(xo[d], sc));
+                for (int d = 0; d < kDim; ++d) atomicAdd(&s_sum[myj * kDim + d], fixed_bits(xo[d], fsc));
             }
 
             if (L.part) {

@@ -173,28 +173,45 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
     __shared__ unsigned long long s_S[kFinishGroups][kFinishEntries * 10];
     __shared__ double s_w[kSumThreads / kWave];
     const int b = blockIdx.x;
-    if (b >= p.total_units) {  // the last nlayers workgroups: the distortion of layer b - total
-        const DevLayer& L = p.L[b - p.total_units];
-        if (L.dist == nullptr) return;
-        const double* src = L.apart ? L.apart : L.part;
-        const int m = L.apart ? L.napart : L.nunits;
+    // (the launch is short: the unit table and then the layer's fields are read in one batch
+    // each, since every dependent load of the arguments is a memory round trip)
+    const int total = p.total_units, li = find_layer(p, b);
+    asm volatile("" ::"s"(total), "s"(li));
+    if (b >= total) {  // the last nlayers workgroups: the distortion of layer b - total
+        const DevLayer& L = p.L[b - total];
+        double* const dist = L.dist;
+        const double *const ap = L.apart, *const pp = L.part;
+        const int na = L.napart, nu = L.nunits;
+        asm volatile("" ::"s"(dist), "s"(ap), "s"(pp), "s"(na), "s"(nu));
+        const double* const src = ap ? ap : pp;
+        const int m = ap ? na : nu;
+        if (dist == nullptr) return;
         const double a = block_fixed_sum<kSumThreads>(src, m, s_w);
-        if (threadIdx.x == 0) *L.dist = a;
+        if (threadIdx.x == 0) *dist = a;
         return;
     }
-    // layer and entry range of this workgroup: each layer owns ceil(k / 4) workgroups
-    const int li = find_layer(p, b);
+    // layer and entry range of this workgroup: each layer owns ceil(k / 8) workgroups
     const DevLayer& L = p.L[li];
-    const int j0 = (b - L.unit_begin) * kFinishEntries;
+    const int k = L.k, nb = L.nchunks, flags = L.flags, nx = L.nxmax, ub = L.unit_begin;
+    const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;
+    const unsigned* const xm = L.xmax;
+    const float* const C_old = L.C_old;
+    asm volatile("" ::"s"(k), "s"(nb), "s"(flags), "s"(nx), "s"(ub), "s"(h), "s"(xm), "s"(C_old));
+    const int j0 = (b - ub) * kFinishEntries;
     const int tid = threadIdx.x;
     const int g = tid / (kFinishEntries * 10), v = tid - g * (kFinishEntries * 10);
     const int j = j0 + v / 10, d = v - 10 * (v / 10);
-    const int k = L.k;
-    const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;
+    // the entry's old value and the layer's shift, in flight with the partials
+    const bool writes_c = g == 0 && j < k && d < kDim && (flags & kFlagCountsOnly) == 0;
+    float old = 0.0f;
+    int shift = 0;
+    if (writes_c) {
+        old = C_old[(size_t)j * kDim + d];
+        shift = (int)xm[nx];
+    }
 
     unsigned long long s = 0ull;
     if (j < k) {
-        const int nb = L.nchunks;
         const size_t stride = (size_t)k * 10;
         const unsigned long long* hp = h + (size_t)j * 10 + d;
         // partials g, g + 8, ...: kFinishBatch loads in flight at a time
@@ -222,13 +239,12 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         S -= z * kFixedBias;  // the exact sum of q(x) over the entry's kernels
         if (d == 9) {
             if (L.counts) L.counts[j] = (int32_t)z;
-        } else if ((L.flags & kFlagCountsOnly) == 0) {
-            const float old = L.C_old[(size_t)j * kDim + d];
+        } else if (writes_c) {
             float c = old;
             if (z > 0) {
-                const double mean = ((double)(long long)S * ldexp(1.0, -(int)L.xmax[L.nxmax])) / (double)z;
+                const double mean = ((double)(long long)S * ldexp(1.0, -shift)) / (double)z;
                 // Eq. (2): c - gamma * mean gradient; Eq. (1): the mean of the kernels
-                c = (L.flags & kFlagGrad) ? (float)((double)old - (double)L.gamma * mean) : (float)mean;
+                c = (flags & kFlagGrad) ? (float)((double)old - (double)L.gamma * mean) : (float)mean;
             }
             L.C[(size_t)j * kDim + d] = c;
         }

@@ -68,7 +68,7 @@ constexpr int kSqPerBlock = 8192;
 
 // units of 64 kernels of a layer (one wave's work at a time; one distortion partial each)
 inline int assign_units(int64_t n) { return (int)((n + kWave - 1) / kWave); }
-// fused partials of a layer: one per workgroup whose run touches it, at most one per unit
+// fused partials of a layer: one per workgroup of the layer, at most one per unit
 inline int fused_parts(int64_t n) { return assign_units(n) < kAssignGridMax ? assign_units(n) : kAssignGridMax; }
 inline int sq_error_blocks(int64_t count) { return (int)((count + kSqPerBlock - 1) / kSqPerBlock); }
 
@@ -102,8 +102,8 @@ __device__ __forceinline__ unsigned long long fixed_bits(float x, double scale) 
 // With every codebook of at most kFuseMaxK entries, the assignment kernel can also add each
 // settled kernel to a per-workgroup LDS histogram of exact member sums (the update's
 // fixed-point sums) and store it per (layer, workgroup) as a partial, so the update needs
-// only its finishing launch.  A layer's partials are those of the workgroups whose unit
-// runs touch it (fused_parts(n) at most).
+// only its finishing launch.  A layer's partials are those of its workgroups (the grid is
+// split per layer; fused_parts(n) at most).
 constexpr int kFuseMaxK = 256;
 constexpr int kFuseChunk = 256;  // codebook entries staged at a time by the fused variant
 
@@ -161,7 +161,7 @@ struct DevLayer {
     float gamma;              // gradient step: learning rate
     unsigned* xmax;           // per-block maxima of |x| (or |g|) as fp32 bits, then the shift (xmax[nxmax])
     int nxmax;                // number of those blocks
-    int wfirst;               // fused assignment: first workgroup whose tiles touch the layer
+    int wfirst;               // fused assignment: the layer's first workgroup
 };
 
 // Kernel arguments of a stack launch.  The first unit of every layer is repeated in a

@@ -107,8 +107,8 @@ kq_status run_xmax(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char
     stack_params(p, layers, l0, l1, ws, Op::Update, 0, nullptr, 0);
     unsigned* flags = p.L[0].xmax + p.L[0].nxmax + 1;  // the first layer's region holds the call's flags
     p.range_flags = validate ? flags : nullptr;
-    if (launch_absmax(p, s) != hipSuccess) return KQ_ERR_HIP;
-    if (!validate) return KQ_OK;
+    if (launch_absmax(p, s, validate) != hipSuccess) return KQ_ERR_HIP;
+    if (!validate) return KQ_OK;  // the first launch that forms sums derives the shifts
     unsigned h[KQ_MAX_STACK] = {0};
     if (hipMemcpyAsync(h, flags, sizeof(unsigned) * (size_t)p.nlayers, hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
@@ -164,9 +164,11 @@ int fused_slots(const kq_layer* layers, int32_t l0, int32_t l1, int* wfirst, int
 // `fused` also leaves the member sums of the new assignment in the workspace (the layers'
 // shifts must be in place: run_xmax)
 kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot, hipStream_t s,
-                     bool fused = false, const float* const* C_alt = nullptr, void* const* events = nullptr) {
+                     bool fused = false, const float* const* C_alt = nullptr, void* const* events = nullptr,
+                     bool derive = false) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Assign, slot, C_alt, 0);
+    p.derive_shift = derive ? 1 : 0;
     {
         int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
         p.assign_grid = fused_slots(layers, l0, l1, wf, ns);
@@ -184,9 +186,10 @@ kq_status run_assign(const kq_layer* layers, int32_t l0, int32_t l1, unsigned ch
 // layers' shifts must be in place (run_xmax) unless only counts are asked for.
 kq_status run_update(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char* ws, int32_t slot,
                      const float* const* C_old, uint32_t kflags, hipStream_t s, bool from_assign = false,
-                     bool sums_from_assign = false) {
+                     bool sums_from_assign = false, bool derive = false) {
     StackParams p;
     stack_params(p, layers, l0, l1, ws, Op::Update, slot, C_old, kflags, from_assign || sums_from_assign);
+    p.derive_shift = derive ? 1 : 0;
     if (sums_from_assign) {
         int wf[KQ_MAX_STACK], ns[KQ_MAX_STACK];
         fused_slots(layers, l0, l1, wf, ns);
@@ -213,6 +216,7 @@ kq_status run_grad(const kq_layer* layers, int32_t l0, int32_t l1, unsigned char
     if (st != KQ_OK) return st;
     StackParams p;
     stack_params(p, quiet, 0, l1 - l0, ws + off, Op::Update, 0, C_old ? C_old + l0 : nullptr, kFlagGrad);
+    p.derive_shift = 1;  // the shift pass above left the block maxima of |g|
     for (int l = 0; l < p.nlayers; ++l) p.L[l].gamma = gamma;
     if (launch_update(p, s) != hipSuccess) return KQ_ERR_HIP;
     if (launch_update_finish(p, s) != hipSuccess) return KQ_ERR_HIP;
@@ -261,10 +265,12 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
             const bool last = (t == iters);
             const float* const* from = t == 0 ? init : nullptr;
             void* const* ev = (round_events && l0 == 0) ? round_events + 2 * t : nullptr;
-            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from, ev);
+            // round 0 forms the shifts (from the block maxima) unless the range check did
+            const bool derive = t == 0 && !validate;
+            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from, ev, derive);
             if (st != KQ_OK) return st;
             if (last && !need_last) break;
-            st = run_update(layers + l0, 0, l1 - l0, w, t, from, last ? kFlagCountsOnly : 0, s, true, fused);
+            st = run_update(layers + l0, 0, l1 - l0, w, t, from, last ? kFlagCountsOnly : 0, s, true, fused, derive);
             if (st != KQ_OK) return st;
         }
     }
@@ -465,7 +471,8 @@ kq_status kq_update(const float* X, int64_t n, int32_t dim, const int32_t* idx, 
         const kq_status st = run_xmax(&l, 0, 1, (unsigned char*)ws, s, validate);
         if (st != KQ_OK) return st;
     }
-    return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, counts_only ? kFlagCountsOnly : 0, s);
+    return run_update(&l, 0, 1, (unsigned char*)ws, 0, olds, counts_only ? kFlagCountsOnly : 0, s, false, false,
+                      !validate);
 }
 
 kq_status kq_codebook_grad_step(const float* G, int64_t n, int32_t dim, const int32_t* idx, int32_t k,
@@ -740,7 +747,7 @@ kq_status kq_fit_layer_yinyang(const float* X, int64_t n, int32_t dim, int32_t k
     for (int32_t r = 0; r < iters; ++r) {
         kq_layer lu = {X, n, k, nxt, idx, nullptr, counts, distortion};
         const float* olds[1] = {cur};
-        if ((st = run_update(&lu, 0, 1, w, r, olds, 0, s, true)) != KQ_OK) return st;
+        if ((st = run_update(&lu, 0, 1, w, r, olds, 0, s, true, false, r == 0)) != KQ_OK) return st;
         const YyParams p = yy_params(w, L, X, n, k, t, nxt, cur, idx, nullptr, stats ? (long long*)stats + 3 * (size_t)r : nullptr);
         if (launch_yy_round(p, s) != hipSuccess) return KQ_ERR_HIP;
         if (launch_yy_partials(p, s) != hipSuccess) return KQ_ERR_HIP;
@@ -774,7 +781,8 @@ kq_status kq_assign_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
     }
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
-        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, s, fused);
+        st = run_assign(layers, l0, l1, (unsigned char*)ws, dist_slot, s, fused, nullptr, nullptr,
+                        fused && !reuse && !validate);
         if (st != KQ_OK) return st;
     }
     return KQ_OK;
@@ -804,7 +812,8 @@ kq_status kq_update_stack(const kq_layer* layers, int32_t n_layers, int32_t dist
     for (int32_t l0 = 0; l0 < n_layers; l0 += KQ_MAX_STACK) {
         const int32_t l1 = (n_layers - l0 < KQ_MAX_STACK) ? n_layers : l0 + KQ_MAX_STACK;
         st = run_update(layers, l0, l1, (unsigned char*)ws, dist_slot, nullptr, counts_only ? kFlagCountsOnly : 0, s,
-                        (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0, from_sums);
+                        (flags & KQ_F_DISTORTION_FROM_ASSIGN) != 0, from_sums,
+                        !validate && !from_sums && !counts_only && !reuse);
         if (st != KQ_OK) return st;
     }
     return KQ_OK;

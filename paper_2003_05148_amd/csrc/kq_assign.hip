@@ -207,6 +207,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     __shared__ unsigned long long s_sum[FUSED ? kFuseMaxK * kDim : 1];  // fused: member sums
     __shared__ unsigned s_cnt[FUSED ? kFuseMaxK : 1];                   // fused: member counts
     __shared__ int s_next;                                              // fused: the next unit to hand out
+    __shared__ unsigned s_mx;                                           // fused: the layer's largest magnitude
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
@@ -301,8 +302,19 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
         for (int e = tid; e < kFuseMaxK * kDim; e += kAssignWaves * kWave) s_sum[e] = 0ull;
         for (int e = tid; e < kFuseMaxK; e += kAssignWaves * kWave) s_cnt[e] = 0u;
     }
-    // fused: the scale of the layer's fixed-point sums, read once
-    const double fsc = FUSED ? fixed_scale((int)L.xmax[L.nxmax]) : 0.0;
+    // fused: the scale of the layer's fixed-point sums, read once (or formed from the block
+    // maxima, and then stored by the layer's first workgroup for the launches after)
+    double fsc = 0.0;
+    if (FUSED) {
+        int shift;
+        if (p.derive_shift) {
+            shift = derive_shift<kAssignWaves * kWave>(L, &s_mx);
+            if (j == 0 && tid == 0) L.xmax[L.nxmax] = (unsigned)shift;
+        } else {
+            shift = (int)L.xmax[L.nxmax];
+        }
+        fsc = fixed_scale(shift);
+    }
     __syncthreads();
 
     // fused: this wave's unit (uniform over the wave); plain: the round's first unit
@@ -583,7 +595,6 @@ __global__ __launch_bounds__(kSumThreads) void assign_finish_kernel(const StackP
     if (threadIdx.x == 0) *L.dist = v;
 }
 
-int assign_grid(int total_units) { return total_units < kAssignGridMax ? total_units : kAssignGridMax; }
 
 int assign_partition(const int* units, int nlayers, int* g) {
     long long T = 0;

@@ -94,6 +94,16 @@ inline int base_shift(int64_t n) {
 // Two full-rate instructions per value (a conversion and an fma in fp64).
 constexpr unsigned long long kFixedBias = 0x4338000000000000ull;  // the bits of 1.5 * 2^52
 __device__ __forceinline__ double fixed_scale(int shift) { return __builtin_ldexp(1.0, shift); }
+
+// the layer's shift from its largest magnitude (fp32 bits, sign cleared):
+// s = base + 5 - e with max < 2^e, where base = min(57 - ceil(log2 n), 46) (e = -126 for a subnormal
+// maximum, e = 0 for an all-zero layer; a non-finite maximum gives e >= 129 and a shift
+// that keeps the sums finite but meaningless, which KQ_F_VALIDATE reports)
+__device__ __forceinline__ int layer_shift(unsigned maxbits, int base) {
+    const int be = (int)(maxbits >> 23);                          // biased exponent (255: inf or NaN)
+    const int e = maxbits == 0u ? 0 : (be == 0 ? -126 : be - 126);  // max < 2^e
+    return base + 5 - e;
+}
 __device__ __forceinline__ unsigned long long fixed_bits(float x, double scale) {
     return __builtin_bit_cast(unsigned long long, __builtin_fma((double)x, scale, 0x1.8p52));
 }
@@ -175,12 +185,28 @@ struct StackParams {
     int unit_begin[KQ_MAX_STACK];
     int wg_begin[KQ_MAX_STACK];  // assignment: first workgroup of each layer (0x7fffffff past the last)
     int assign_grid;             // assignment: the number of workgroups
+    int derive_shift;            // 1: the shift pass left only the block maxima; a launch that
+                                 // needs a layer's shift forms it from them, and one of the
+                                 // layer's workgroups stores it at xmax[nxmax] for the launches after
     DevLayer L[KQ_MAX_STACK];
 };
 
 // host-side: fill the table from the layer records
 inline void set_unit_table(StackParams& p) {
     for (int l = 0; l < KQ_MAX_STACK; ++l) p.unit_begin[l] = l < p.nlayers ? p.L[l].unit_begin : 0x7fffffff;
+}
+
+// device-side: the layer's shift from its block maxima (what shift_kernel stores at
+// xmax[nxmax]), called by every thread of a workgroup of THREADS threads (two barriers)
+template <int THREADS>
+__device__ __forceinline__ int derive_shift(const DevLayer& L, unsigned* s_mx) {
+    if (threadIdx.x == 0) *s_mx = 0u;
+    __syncthreads();
+    unsigned m = 0u;
+    for (int q = threadIdx.x; q < L.nxmax; q += THREADS) m = max(m, L.xmax[q]);
+    if (m != 0u) atomicMax(s_mx, m);  // LDS
+    __syncthreads();
+    return layer_shift(*s_mx, L.shift);
 }
 
 // device-side: the layer a unit (tile or workgroup) belongs to (layers are in order)
@@ -255,12 +281,13 @@ constexpr int kSumThreads = 640;
 int assign_partition(const int* units, int nlayers, int* g);
 hipError_t launch_assign(const StackParams& p, hipStream_t s, bool fused = false, hipEvent_t start = nullptr,
                          hipEvent_t stop = nullptr);
-int assign_grid(int total_units);
 hipError_t launch_assign_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_update(const StackParams& p, hipStream_t s);
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s);
 hipError_t launch_fill_zero(void* ws, size_t bytes, hipStream_t s);
-hipError_t launch_absmax(const StackParams& p, hipStream_t s);
+// the block maxima of |x| (or |g|) and, with `with_shift`, each layer's shift and non-finite
+// flag; without it the next launch that forms sums derives the shift (StackParams::derive_shift)
+hipError_t launch_absmax(const StackParams& p, hipStream_t s, bool with_shift);
 
 struct CbqLayer {
     const float* C;

@@ -8,8 +8,10 @@
 // takes count * kFixedBias back off).
 // Integer addition is associative, so the sums, and with them the new codebook, do not
 // depend on the order in which blocks or lanes add.  absmax_kernel takes the maxima of |x|
-// per block of 8192 values and shift_kernel turns them into each layer's s (and flags
-// non-finite values); both run once per call, or once per fit, before any sum is formed.
+// per block of 8192 values, once per call or once per fit, before any sum is formed; with a
+// range check shift_kernel turns them into each layer's s (and flags non-finite values),
+// otherwise the first launch that forms sums does (derive_shift: every workgroup takes the
+// layer's largest block maximum, one of them stores s for the launches after).
 //
 // update_kernel: one launch covers every layer of a stack.  A layer's kernels are cut
 // into chunks and its codebook into ranges of at most 768 entries; a workgroup of 1024
@@ -46,16 +48,6 @@ __device__ __forceinline__ float sqdist9u(const float* x, const float* __restric
         acc = __fmaf_rn(t, t, acc);
     }
     return acc;
-}
-
-// the layer's shift from its largest magnitude (fp32 bits, sign cleared):
-// s = base + 5 - e with max < 2^e, where base = min(57 - ceil(log2 n), 46) (e = -126 for a subnormal
-// maximum, e = 0 for an all-zero layer; a non-finite maximum gives e >= 129 and a shift
-// that keeps the sums finite but meaningless, which KQ_F_VALIDATE reports)
-__device__ __forceinline__ int layer_shift(unsigned maxbits, int base) {
-    const int be = (int)(maxbits >> 23);                          // biased exponent (255: inf or NaN)
-    const int e = maxbits == 0u ? 0 : (be == 0 ? -126 : be - 126);  // max < 2^e
-    return base + 5 - e;
 }
 
 struct UpdateCtx {
@@ -113,6 +105,7 @@ __device__ __forceinline__ void add_rows(const UpdateCtx& c, const float* __rest
 __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParams p) {
     extern __shared__ unsigned long long s_dyn[];  // [krange][9] sums, then [krange] u32 counts
     __shared__ double s_wd[kUpdateThreads / kWave];
+    __shared__ unsigned s_mx;
 
     const int li = find_layer(p, blockIdx.x);
     const DevLayer& L = p.L[li];
@@ -127,7 +120,16 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     c.s_cnt = (unsigned*)(s_dyn + (size_t)c.kr * kDim);
     c.C_old = L.C_old;
     c.sums = (L.flags & kFlagCountsOnly) == 0;
-    c.scale = fixed_scale(c.sums ? (int)L.xmax[L.nxmax] : 0);  // set by shift_kernel before this launch
+    int shift = 0;
+    if (c.sums) {  // set by shift_kernel before this launch, or formed here from the block maxima
+        if (p.derive_shift) {
+            shift = derive_shift<kUpdateThreads>(L, &s_mx);
+            if (u == 0 && tid == 0) L.xmax[L.nxmax] = (unsigned)shift;  // for the launches after
+        } else {
+            shift = (int)L.xmax[L.nxmax];
+        }
+    }
+    c.scale = fixed_scale(shift);
     c.want_dist = L.part != nullptr;
     const bool need_x = c.sums || c.want_dist;
 
@@ -305,7 +307,7 @@ __global__ __launch_bounds__(256) void shift_kernel(const StackParams p) {
     }
 }
 
-hipError_t launch_absmax(const StackParams& p, hipStream_t s) {
+hipError_t launch_absmax(const StackParams& p, hipStream_t s, bool with_shift) {
     StackParams q = p;
     int blk = 0;
     for (int l = 0; l < q.nlayers; ++l) {
@@ -316,7 +318,7 @@ hipError_t launch_absmax(const StackParams& p, hipStream_t s) {
     set_unit_table(q);
     hipLaunchKernelGGL(absmax_kernel, dim3(blk), dim3(256), 0, s, q);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || !with_shift) return e;
     hipLaunchKernelGGL(shift_kernel, dim3(q.nlayers), dim3(256), 0, s, q);
     return hipGetLastError();
 }

@@ -37,7 +37,7 @@ constexpr int kUpdateThreads = 1024;
 constexpr int kUpdateMinKernelsPerBlock = 1024;
 constexpr int kUpdateTargetBlocks = 256;
 constexpr int kUpdateLdsMaxK = 768;     // LDS histogram [768][9] int64 + [768] u32
-constexpr int kFinishEntries = 8;  // codebook entries per finishing workgroup
+constexpr int kFinishEntries = 16;  // codebook entries per finishing workgroup
 constexpr size_t kUpdatePartialBudget = size_t(1) << 24;  // bytes of partials per layer above 768 entries
 
 inline int update_ranges(int32_t k) { return (k + kUpdateLdsMaxK - 1) / kUpdateLdsMaxK; }
@@ -255,9 +255,10 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // workgroup must call it; the result is valid in thread 0.
 template <int NT>
 __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src, int m, double* s_w) {
+    // (threads NT and up of a larger workgroup take part in the barrier only)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     double a = 0.0;
-    for (int q = tid; q < m; q += 8 * NT) {  // eight loads in flight, added in order
+    for (int q = tid; tid < NT && q < m; q += 8 * NT) {  // eight loads in flight, added in order
         double v[8];
 #pragma unroll
         for (int r = 0; r < 8; ++r) v[r] = q + r * NT < m ? src[q + r * NT] : 0.0;
@@ -266,7 +267,7 @@ __device__ __forceinline__ double block_fixed_sum(const double* __restrict__ src
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) a += __shfl_xor(a, off);
-    if (lane == 0) s_w[wave] = a;
+    if (lane == 0 && tid < NT) s_w[wave] = a;
     __syncthreads();
     double r = 0.0;
     if (tid == 0)

@@ -28,12 +28,14 @@
 // Codebook gradient step (Eq. 2): the same sums over a gradient tensor G instead of the
 // kernels, with the same shift rule applied to max |g|; the finish then writes
 // c - gamma * mean instead of the mean.
-// update_finish_kernel: a workgroup of 640 threads owns 8 entries of one layer; eight
-// groups of 80 threads add an eighth of the partials each, eight loads in flight per
-// thread (any order gives the same integers; 12, 16, 24 or 32 in flight measured slower), then it divides and writes the codebook
-// and the counts (fewer, fuller workgroups measured faster than 2 or 4 entries each:
-// the launch is short and its cost is mostly per workgroup).  One more workgroup
-// per layer adds the distortion partials in a fixed order (those of the assignment kernel
+// update_finish_kernel: a workgroup of 960 threads owns 16 entries of one layer; six
+// groups of 160 threads add a sixth of the partials each, nine loads in flight per thread
+// (one batch for the 54 partials of the largest ResNet-18 layers; any order gives the same
+// integers), then it divides and writes the codebook and the counts.  Fewer, fuller
+// workgroups measured faster: the launch is short, and the workgroups dispatched last
+// start up to 2 us after the first (528 workgroups of 640 threads at 8 entries each; 2
+// or 4 entries each were slower still).  One more workgroup per layer adds the distortion
+// partials in a fixed order with its first 640 threads (those of the assignment kernel
 // when the distortion comes from there).  The kernel boundary orders every partial before
 // its use, so no fence or atomic counter is needed.
 #include "kq_internal.h"
@@ -166,10 +168,10 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
     }
 }
 
-constexpr int kFinishGroups = kSumThreads / (10 * kFinishEntries);
-constexpr int kFinishBatch = 8;
+constexpr int kFinishGroups = 6;
+constexpr int kFinishBatch = 9;
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
-static_assert(kFinishThreads == kSumThreads, "the distortion sum reuses the finishing workgroup");
+static_assert(kFinishThreads >= kSumThreads, "the distortion sum uses the first kSumThreads threads");
 
 __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const StackParams p) {
     __shared__ unsigned long long s_S[kFinishGroups][kFinishEntries * 10];
@@ -192,7 +194,7 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         if (threadIdx.x == 0) *dist = a;
         return;
     }
-    // layer and entry range of this workgroup: each layer owns ceil(k / 8) workgroups
+    // layer and entry range of this workgroup: each layer owns ceil(k / kFinishEntries) workgroups
     const DevLayer& L = p.L[li];
     const int k = L.k, nb = L.nchunks, flags = L.flags, nx = L.nxmax, ub = L.unit_begin;
     const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;

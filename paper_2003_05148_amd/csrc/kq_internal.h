@@ -133,10 +133,11 @@ inline size_t ws_hist(int64_t n, int32_t k) {
     return align256(sizeof(int64_t) * 10 * (size_t)k * parts);
 }
 // Largest magnitudes of the values whose fixed-point sums a call forms (the kernels, or the
-// gradients of Eq. 2): one maximum of |v| per block of 8192 values (fp32 bits with the sign
+// gradients of Eq. 2): one maximum of |v| per block of 32768 values (fp32 bits with the sign
 // cleared, so a NaN orders above +inf and every finite value), then the layer's shift, then
 // -- used in the first layer's region of a call -- one non-finite flag per layer of the call.
-constexpr int kAbsMaxPerBlock = 8192;
+constexpr int kAbsMaxThreads = 1024;
+constexpr int kAbsMaxPerBlock = 32 * kAbsMaxThreads;  // eight 16-byte loads per thread
 inline int absmax_blocks(int64_t n) { return (int)((n * kDim + kAbsMaxPerBlock - 1) / kAbsMaxPerBlock); }
 inline size_t ws_xmax(int64_t n) {
     return align256(sizeof(unsigned) * ((size_t)absmax_blocks(n) + 1 + KQ_MAX_STACK));

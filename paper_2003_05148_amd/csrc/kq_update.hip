@@ -8,7 +8,7 @@
 // takes count * kFixedBias back off).
 // Integer addition is associative, so the sums, and with them the new codebook, do not
 // depend on the order in which blocks or lanes add.  absmax_kernel takes the maxima of |x|
-// per block of 8192 values, once per call or once per fit, before any sum is formed; with a
+// per block of 32768 values, once per call or once per fit, before any sum is formed; with a
 // range check shift_kernel turns them into each layer's s (and flags non-finite values),
 // otherwise the first launch that forms sums does (derive_shift: every workgroup takes the
 // layer's largest block maximum, one of them stores s for the launches after).
@@ -255,10 +255,11 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
     }
 }
 
-// per-block maximum of |v| over 8192 values of a layer (the kernels, or the gradients of
+// per-block maximum of |v| over 32768 values of a layer (the kernels, or the gradients of
 // Eq. 2) as fp32 bits with the sign cleared: an integer maximum, so a NaN counts as the
-// largest value and shift_kernel can flag it
-__global__ __launch_bounds__(256) void absmax_kernel(const StackParams p) {
+// largest value and shift_kernel can flag it.  Blocks of 1024 threads: a grid of many small
+// workgroups is slow to dispatch (the last start microseconds after the first)
+__global__ __launch_bounds__(kAbsMaxThreads) void absmax_kernel(const StackParams p) {
     __shared__ unsigned s_mx;
     const int li = find_layer(p, blockIdx.x);
     const DevLayer& L = p.L[li];
@@ -272,15 +273,16 @@ __global__ __launch_bounds__(256) void absmax_kernel(const StackParams p) {
     if ((reinterpret_cast<uintptr_t>(L.X) & 15u) == 0 && base + kAbsMaxPerBlock <= count) {
         // a whole block from a 16-byte aligned tensor: eight 16-byte loads per thread in flight
         const uint4* __restrict__ V4 = reinterpret_cast<const uint4*>(V + base);
-        uint4 v[kAbsMaxPerBlock / 1024];
+        constexpr int kPer = kAbsMaxPerBlock / (4 * kAbsMaxThreads);
+        uint4 v[kPer];
 #pragma unroll
-        for (int u = 0; u < kAbsMaxPerBlock / 1024; ++u) v[u] = V4[threadIdx.x + 256 * u];
+        for (int u = 0; u < kPer; ++u) v[u] = V4[threadIdx.x + kAbsMaxThreads * u];
 #pragma unroll
-        for (int u = 0; u < kAbsMaxPerBlock / 1024; ++u)
+        for (int u = 0; u < kPer; ++u)
             m = max(m, max(max(v[u].x & 0x7fffffffu, v[u].y & 0x7fffffffu), max(v[u].z & 0x7fffffffu, v[u].w & 0x7fffffffu)));
     } else {
 #pragma unroll 4
-        for (int q = threadIdx.x; q < kAbsMaxPerBlock; q += 256) {
+        for (int q = threadIdx.x; q < kAbsMaxPerBlock; q += kAbsMaxThreads) {
             const long long e = base + q;
             if (e < count) m = max(m, V[e] & 0x7fffffffu);
         }
@@ -318,7 +320,7 @@ hipError_t launch_absmax(const StackParams& p, hipStream_t s, bool with_shift) {
     }
     q.total_units = blk;
     set_unit_table(q);
-    hipLaunchKernelGGL(absmax_kernel, dim3(blk), dim3(256), 0, s, q);
+    hipLaunchKernelGGL(absmax_kernel, dim3(blk), dim3(kAbsMaxThreads), 0, s, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !with_shift) return e;
     hipLaunchKernelGGL(shift_kernel, dim3(q.nlayers), dim3(256), 0, s, q);

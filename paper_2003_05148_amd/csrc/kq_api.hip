@@ -261,13 +261,22 @@ kq_status run_fit(const kq_layer* layers, int32_t n_layers, int32_t iters, unsig
             init = nullptr;
         }
         const bool fused = fusable(layers, l0, l1);  // the member sums come with the assignment
+        // with fused sums nothing reads a round's indices but the last round's: the rounds
+        // before it store none (nor best distances)
+        kq_layer inner[KQ_MAX_STACK];
+        for (int32_t l = 0; l < l1 - l0; ++l) {
+            inner[l] = quiet[l];
+            inner[l].idx = nullptr;
+            inner[l].best_d = nullptr;
+        }
         for (int32_t t = 0; t <= iters; ++t) {
             const bool last = (t == iters);
             const float* const* from = t == 0 ? init : nullptr;
             void* const* ev = (round_events && l0 == 0) ? round_events + 2 * t : nullptr;
             // round 0 forms the shifts (from the block maxima) unless the range check did
             const bool derive = t == 0 && !validate;
-            kq_status st = run_assign(quiet, 0, l1 - l0, w, 0, s, fused && !(last && !need_last), from, ev, derive);
+            const bool fuse_t = fused && !(last && !need_last);
+            kq_status st = run_assign(fuse_t && !last ? inner : quiet, 0, l1 - l0, w, 0, s, fuse_t, from, ev, derive);
             if (st != KQ_OK) return st;
             if (last && !need_last) break;
             st = run_update(layers + l0, 0, l1 - l0, w, t, from, last ? kFlagCountsOnly : 0, s, true, fused, derive);

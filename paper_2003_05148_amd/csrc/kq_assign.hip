@@ -496,7 +496,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
             int myj = rj;  // the entry this lane's kernel ends with
             if (sure) {
                 dist = rd;
-                L.idx[i] = rj;
+                if (L.idx) L.idx[i] = rj;  // (a fit's rounds before the last keep no indices)
                 if (L.best_d) L.best_d[i] = rd;
             }
 
@@ -560,7 +560,7 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
                 wave_argmin(fd, fj);
                 if (lane == f) {
                     if (fj == 0x7fffffff) fj = 0;  // every distance NaN or +inf: entry 0, as a plain scan gives
-                    L.idx[i] = fj;
+                    if (L.idx) L.idx[i] = fj;
                     if (L.best_d) L.best_d[i] = fd;
                     dist = fd;
                     myj = fj;

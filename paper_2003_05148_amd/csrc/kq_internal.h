@@ -186,6 +186,7 @@ struct StackParams {
     int unit_begin[KQ_MAX_STACK];
     int wg_begin[KQ_MAX_STACK];  // assignment: first workgroup of each layer (0x7fffffff past the last)
     int assign_grid;             // assignment: the number of workgroups
+    int finish_direct;           // update finish: layer l owns a fixed block of workgroups
     int derive_shift;            // 1: the shift pass left only the block maxima; a launch that
                                  // needs a layer's shift forms it from them, and one of the
                                  // layer's workgroups stores it at xmax[nxmax] for the launches after

@@ -170,6 +170,8 @@ __global__ __launch_bounds__(kUpdateThreads) void update_kernel(const StackParam
 
 constexpr int kFinishGroups = 6;
 constexpr int kFinishBatch = 9;
+constexpr int kFinishDirectWgs = 16;  // workgroups per layer in the direct form
+constexpr int kFinishDirectK = kFinishDirectWgs * kFinishEntries;  // 256
 constexpr int kFinishThreads = kFinishEntries * 10 * kFinishGroups;  // 640
 static_assert(kFinishThreads >= kSumThreads, "the distortion sum uses the first kSumThreads threads");
 
@@ -177,10 +179,20 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
     __shared__ unsigned long long s_S[kFinishGroups][kFinishEntries * 10];
     __shared__ double s_w[kSumThreads / kWave];
     const int b = blockIdx.x;
-    // (the launch is short: the unit table and then the layer's fields are read in one batch
-    // each, since every dependent load of the arguments is a memory round trip)
-    const int total = p.total_units, li = find_layer(p, b);
-    asm volatile("" ::"s"(total), "s"(li));
+    // The launch is short, and every dependent load of the arguments is a memory round trip.
+    // With every codebook of at most kFinishDirectK entries (p.finish_direct) layer l owns
+    // workgroups kFinishDirectWgs l .., so the fields of layer b / kFinishDirectWgs are read in
+    // the first batch; otherwise the table of first workgroups gives the layer and its fields
+    // come in later batches.
+    const int ld = min(b / kFinishDirectWgs, KQ_MAX_STACK - 1);
+    const DevLayer& Ld = p.L[ld];
+    int k = Ld.k, nb = Ld.nchunks, flags = Ld.flags, nx = Ld.nxmax, ub = Ld.unit_begin;
+    const unsigned long long* __restrict__ h = (const unsigned long long*)Ld.hist;
+    const unsigned* xm = Ld.xmax;
+    const float* C_old = Ld.C_old;
+    const int total = p.total_units, direct = p.finish_direct;
+    asm volatile("" ::"s"(k), "s"(nb), "s"(flags), "s"(nx), "s"(ub), "s"(h), "s"(xm), "s"(C_old), "s"(total),
+                 "s"(direct));
     if (b >= total) {  // the last nlayers workgroups: the distortion of layer b - total
         const DevLayer& L = p.L[b - total];
         double* const dist = L.dist;
@@ -194,13 +206,20 @@ __global__ __launch_bounds__(kFinishThreads) void update_finish_kernel(const Sta
         if (threadIdx.x == 0) *dist = a;
         return;
     }
-    // layer and entry range of this workgroup: each layer owns ceil(k / kFinishEntries) workgroups
+    const int lt = direct ? ld : find_layer(p, b);  // the layer
+    const int li = lt;
+    if (!direct) {  // layer and entry range from the table: each layer owns ceil(k / kFinishEntries) workgroups
+        const DevLayer& Lt = p.L[lt];
+        k = Lt.k;
+        nb = Lt.nchunks;
+        flags = Lt.flags;
+        nx = Lt.nxmax;
+        ub = Lt.unit_begin;
+        h = (const unsigned long long*)Lt.hist;
+        xm = Lt.xmax;
+        C_old = Lt.C_old;
+    }
     const DevLayer& L = p.L[li];
-    const int k = L.k, nb = L.nchunks, flags = L.flags, nx = L.nxmax, ub = L.unit_begin;
-    const unsigned long long* __restrict__ h = (const unsigned long long*)L.hist;
-    const unsigned* const xm = L.xmax;
-    const float* const C_old = L.C_old;
-    asm volatile("" ::"s"(k), "s"(nb), "s"(flags), "s"(nx), "s"(ub), "s"(h), "s"(xm), "s"(C_old));
     const int j0 = (b - ub) * kFinishEntries;
     const int tid = threadIdx.x;
     const int g = tid / (kFinishEntries * 10), v = tid - g * (kFinishEntries * 10);
@@ -347,10 +366,13 @@ hipError_t launch_update(const StackParams& p, hipStream_t s) {
 // the finishing launch numbers its workgroups per layer: ceil(k / 4) each
 hipError_t launch_update_finish(const StackParams& p, hipStream_t s) {
     StackParams q = p;
+    bool direct = true;  // every codebook fits kFinishDirectWgs workgroups
+    for (int l = 0; l < q.nlayers; ++l) direct &= q.L[l].k <= kFinishDirectK;
+    q.finish_direct = direct ? 1 : 0;
     int blk = 0;
     for (int l = 0; l < q.nlayers; ++l) {
         q.L[l].unit_begin = blk;
-        blk += (q.L[l].k + kFinishEntries - 1) / kFinishEntries;
+        blk += direct ? kFinishDirectWgs : (q.L[l].k + kFinishEntries - 1) / kFinishEntries;
     }
     q.total_units = blk;  // followed by one workgroup per layer for the distortion
     set_unit_table(q);

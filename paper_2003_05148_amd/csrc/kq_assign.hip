@@ -227,7 +227,9 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     const int n = L.n, k = L.k, U = L.nunits, j = (int)blockIdx.x - g0;
     const float* __restrict__ C = L.C;
     const float* const Xl = L.X;
-    asm volatile("" ::"s"(n), "s"(k), "s"(U), "s"(C), "s"(Xl));
+    const unsigned* const xmax = L.xmax;
+    const int nxmax = L.nxmax, derive = p.derive_shift;
+    asm volatile("" ::"s"(n), "s"(k), "s"(U), "s"(C), "s"(Xl), "s"(xmax), "s"(nxmax), "s"(derive));
     const int q = U / gl, r = U - q * gl;  // workgroup j: q units, one more for the first r
     int ub = j * q + min(j, r);            // units of the layer, [ub, u_end)
     const int u_end = ub + q + (j < r ? 1 : 0);
@@ -240,6 +242,9 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     // unit from an LDS counter, so that a wave its SIMD serves less often takes fewer units.
     float xo[kDim];  // this lane's kernel of the current round
     load_kernel(L, ub + wave, lane, xo);
+    // fused: the layer's shift, loaded with the first kernels (a later load would be one more
+    // round trip before the first unit)
+    const unsigned shift_word = FUSED && !derive ? xmax[nxmax] : 0u;
     const float* s_cf = reinterpret_cast<const float*>(s_c);
     // entries c0 .. c0 + cn - 1 of layer L into LDS: A operands [w_h | w_h | w_m] of w = (-2c, |c|^2)
     // and the fp32 rows (padding entries: screened far away, never taken by the rescoring)
@@ -307,11 +312,11 @@ __global__ __launch_bounds__(kAssignWaves * kWave, 1) void assign_kernel(const S
     double fsc = 0.0;
     if (FUSED) {
         int shift;
-        if (p.derive_shift) {
+        if (derive) {
             shift = derive_shift<kAssignWaves * kWave>(L, &s_mx);
             if (j == 0 && tid == 0) L.xmax[L.nxmax] = (unsigned)shift;
         } else {
-            shift = (int)L.xmax[L.nxmax];
+            shift = (int)shift_word;
         }
         fsc = fixed_scale(shift);
     }

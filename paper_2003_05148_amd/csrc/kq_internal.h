@@ -22,8 +22,10 @@ constexpr int kWave = 64;
 // contiguous run of the stack's units, one unit per wave at a time.
 constexpr int kAssignWaves = 12;
 constexpr int kAssignTilesPerWave = 2;
-// codebook entries staged in LDS at a time (64 B of operands + 48 B of fp32 row each)
-constexpr int kAssignChunk = 384;
+// codebook entries staged in LDS at a time by the plain assignment (64 B of operands + 48 B
+// of fp32 row each: 112 KB of the CU's 160 KB; codebooks up to this size stay resident, and
+// a larger one takes fewer chunks, each costing a staging pass between two barriers)
+constexpr int kAssignChunk = 1024;
 constexpr int kAssignGridMax = 256;  // the persistent grid: one workgroup per CU
 
 // ---- update kernel geometry ---------------------------------------------------------
